@@ -1,0 +1,201 @@
+/*
+ * locks.h -- C ABI of the Locks per-step sparse decode attention for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The method (arXiv 2607.24555): every 16-token KV page keeps a resident rank-r
+ * spectral summary of its keys (Sec. 4 "Build"); every decode step rebuilds each
+ * page's 16 logits from its summary and takes their log-sum-exp (Sec. 4 "Score",
+ * Eq. (1)), averages the normalised page shares over the GQA group, keeps the
+ * sink page, the most recent page and the top (k-2) other pages (Sec. 4, Cor.
+ * "Group-shared selection"), and runs exact attention over those pages only
+ * (Sec. 2 "Decode-time attention"; App. E).
+ *
+ * Conventions shared by every call
+ *  - All tensor arguments are DEVICE pointers owned by the caller; the library
+ *    never allocates, frees, synchronises or throws.  Every call enqueues its
+ *    kernels on `stream` (a hipStream_t; NULL = the default stream) and returns a
+ *    status immediately.
+ *  - Host-side checks (configuration, null pointers, workspace size) run before
+ *    any launch; a failing check returns an error and launches nothing.
+ *    Device-resident values (page-table entries, sequence lengths) are trusted:
+ *    page_table[s][j] must be a valid block for every j < ceil(seq_lens[s]/16),
+ *    and seq_lens[s] <= 16 * max_pages_per_seq.  Entries past a sequence's last
+ *    page are never read.
+ *  - Layouts (row-major, innermost last):
+ *      q           [num_seqs][num_q_heads][128]          (q_dtype)
+ *      k/v cache   [num_blocks][num_kv_heads][16][128]   (kv_dtype)
+ *      page_table  int32 [num_seqs][max_pages_per_seq]   logical page -> block
+ *      seq_lens    int32 [num_seqs]                      tokens per sequence
+ *      summaries   uint8 [num_blocks][num_kv_heads][locks_summary_stride(rank)]
+ *    Query head h belongs to KV head h / (num_q_heads / num_kv_heads).
+ *  - Page ids returned and accepted by this API are LOGICAL page indices within
+ *    their sequence.  Page j holds tokens [16j, 16j+16); page 0 is the sink and
+ *    page ceil(L/16)-1 is the most recent page.  A page has a summary only once
+ *    it is complete (16 tokens).
+ *  - The workspace `ws` (caller-allocated, >= locks_workspace_bytes(cfg) bytes,
+ *    256-byte aligned) holds per-call scratch; its content need not be
+ *    initialised and is meaningless after the call.  Calls that share one
+ *    workspace must be ordered on one stream.
+ *  - Calls with no launches (num_seqs == 0) return LOCKS_OK.
+ */
+#ifndef LOCKS_H
+#define LOCKS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum {
+  LOCKS_OK = 0,
+  LOCKS_E_INVAL = -1,        /* bad configuration value or null pointer          */
+  LOCKS_E_UNSUPPORTED = -2,  /* head_dim != 128, page_size != 16, dtype unknown */
+  LOCKS_E_WORKSPACE = -3,    /* ws null or smaller than locks_workspace_bytes    */
+  LOCKS_E_HIP = -4           /* a HIP launch failed; see locks_last_hip_error    */
+};
+
+/* Element types of q and of the KV cache. */
+enum { LOCKS_BF16 = 0, LOCKS_FP32 = 1 };
+
+/* Fixed-shape configuration of one decode step (Sec. 4 "Implementation": r, B and
+ * b fixed, hence fixed shapes). */
+typedef struct locks_cfg {
+  int32_t num_seqs;          /* S >= 0                                          */
+  int32_t num_q_heads;       /* H_q, a multiple of H_kv; G = H_q / H_kv <= 64   */
+  int32_t num_kv_heads;      /* H_kv >= 1                                       */
+  int32_t head_dim;          /* d, must be 128                                  */
+  int32_t page_size;         /* B, must be 16                                   */
+  int32_t rank;              /* r in [1, 15]                                    */
+  int32_t budget_tokens;     /* b; the page budget k = ceil(b / 16) must be >= 2
+                                (sink and most recent page take two slots,
+                                Sec. 2 and App. C.1 "Budget counting")          */
+  int32_t max_pages_per_seq; /* row stride of page_table, >= 1                  */
+  int32_t num_blocks;        /* physical blocks in the caches, >= 1             */
+  int32_t kv_dtype;          /* LOCKS_BF16 or LOCKS_FP32                        */
+  int32_t q_dtype;           /* LOCKS_BF16 or LOCKS_FP32                        */
+} locks_cfg_t;
+
+/* Stored payload of one page summary (Sec. 4 "Build"; App. C.1 table):
+ * d*r/2 int4 basis bytes + B*r int8 coefficient bytes + d int8 centroid bytes +
+ * 2*(r + B + 1) bytes of float16 scales = 818 / 490 / 326 bytes at r = 8 / 4 / 2.
+ * Returns 0 for r outside [1, 15]. */
+size_t locks_summary_payload_bytes(int32_t rank);
+
+/* Record stride in the summary store: the payload rounded up to 16 bytes
+ * (832 / 496 / 336 at r = 8 / 4 / 2).  Record layout, byte offsets:
+ *   [0, 64r)          basis V (d x r): column l at 64*l, 128 excess-8 nibbles,
+ *                     element c in byte c/2, low nibble for even c; code in [-7, 7]
+ *   [64r, 80r)        coefficients C (16 x r) row-major, excess-128 bytes
+ *   [80r, 80r+128)    centroid mu, excess-128 bytes
+ *   [80r+128, +2(r+17)) float16 scales: r basis columns, 16 coefficient rows,
+ *                     1 centroid; value = code * scale
+ *   rest              zero padding
+ * Returns 0 for r outside [1, 15]. */
+size_t locks_summary_stride(int32_t rank);
+
+/* Bytes of workspace the select / attend / decode-step calls need for cfg
+ * (0 if cfg is invalid). */
+size_t locks_workspace_bytes(const locks_cfg_t* cfg);
+
+/* Build the summaries of complete pages (Sec. 4 "Build"): per (page, KV head)
+ * centre the 16 keys, eigendecompose the 16 x 16 Gram of the deviations, keep the
+ * r leading nonzero modes (a mode counts as zero when its eigenvalue is at most
+ * max(1e-6 * leading eigenvalue, 1e-10 * mean squared key norm)), form the
+ * orthonormal basis V = D^T U_r S_r^{-1} and coefficients C = U_r S_r, make each
+ * basis column's largest-magnitude entry positive, quantise (basis int4 per
+ * column, coefficients int8 per row, centroid int8; scale = f16(max|x|/qmax),
+ * code = round-half-even(x / scale)) and write the record of every KV head of
+ * that page into summaries[block].
+ *   build_list  NULL: every complete page of every sequence.  Otherwise n_build
+ *               int32 pairs (seq, logical page) in device memory; pairs that do
+ *               not name a complete page are skipped.
+ * Returns LOCKS_E_INVAL for n_build < 0 or a null k_cache / page_table /
+ * seq_lens / summaries. */
+int locks_build_summaries(const locks_cfg_t* cfg, const void* k_cache,
+                          const int32_t* page_table, const int32_t* seq_lens,
+                          const int32_t* build_list, int32_t n_build,
+                          void* summaries, void* stream);
+
+/* The same build without quantisation (the float basis variant): for each of the
+ * n_build listed (seq, page) pairs (build_list required) and each KV head, write
+ *   mu     float [n_build][H_kv][128]
+ *   basis  float [n_build][H_kv][128][r]   (sign convention as above)
+ *   coef   float [n_build][H_kv][16][r]
+ *   sigma2 float [n_build][H_kv][16]       all Gram eigenvalues, descending, >= 0
+ * Dropped modes have zero basis and coefficient columns.  Listed pairs that are
+ * not complete pages leave their rows untouched. */
+int locks_build_factors(const locks_cfg_t* cfg, const void* k_cache,
+                        const int32_t* page_table, const int32_t* seq_lens,
+                        const int32_t* build_list, int32_t n_build,
+                        float* mu, float* basis, float* coef, float* sigma2,
+                        void* stream);
+
+/* Score every complete page from its summary and select the shared page table
+ * (Sec. 4 "Score", Eq. (1) and the share-average combine; Cor. "Group-shared
+ * selection"; App. E "union table"):
+ *   hat s_j(q_g) = log sum_i exp[(q_g^T mu_j + (V_j^T q_g)^T c_i) / sqrt(128)],
+ *   mbar_j = (1/G) sum_g exp(hat s_j(q_g)) / sum_{j'} exp(hat s_j'(q_g)),
+ * the normaliser summing every complete page of the sequence.  The table of each
+ * (seq, KV head) holds page 0, the most recent page and the k-2 other pages of
+ * largest mbar (lower index first on ties), in ascending order; a sequence with at
+ * most k pages selects all of them.
+ *   out_page_ids  int32 [S][H_kv][k], ascending, padded with -1
+ *   out_sel_lse   float [S][H_q][k], hat s of each selected page (natural log,
+ *                 1/sqrt(d) included); NaN for padding and for a page without
+ *                 summary (the partial last page)
+ *   out_all_lse   nullable float [S][H_q][max_pages_per_seq]: hat s of every
+ *                 complete page (entries of other pages are not written). */
+int locks_select(const locks_cfg_t* cfg, const void* q, const void* summaries,
+                 const int32_t* page_table, const int32_t* seq_lens,
+                 int32_t* out_page_ids, float* out_sel_lse, float* out_all_lse,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/* Exact attention of every query head over the tokens of its KV head's selected
+ * pages, softmax renormalised over that set (Sec. 2; App. E "sparse decode"):
+ *   o_g = sum_{i in S} softmax_S(q_g^T k_i / sqrt(128)) v_i.
+ * The partial last page contributes its valid tokens only; -1 entries of
+ * page_ids are skipped; ids must be < ceil(seq_lens[s]/16).
+ *   page_ids  int32 [S][H_kv][k] (k from cfg->budget_tokens)
+ *   out       float [S][H_q][128]
+ *   out_lse   nullable float [S][H_q], log of the softmax denominator
+ * A query with no token to attend gets out = 0 and out_lse = -inf. */
+int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                        const void* v_cache, const int32_t* page_table,
+                        const int32_t* seq_lens, const int32_t* page_ids,
+                        float* out, float* out_lse, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/* Dense paged decode attention over every token of each sequence (Sec. 2,
+ * decode-time attention): the same-GPU baseline, with locks_sparse_attend's
+ * arguments minus page_ids. */
+int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                       const void* v_cache, const int32_t* page_table,
+                       const int32_t* seq_lens, float* out, float* out_lse,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* One fused decode step (App. E critical path, allocation-free and fixed-shape):
+ * first the summaries of the n_build listed (seq, page) pairs are built (pages
+ * that completed this step; n_build = 0 builds nothing, build_list may then be
+ * NULL), then locks_select, then locks_sparse_attend over the selected table, all
+ * on `stream`.  Outputs as in those calls. */
+int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                      const void* v_cache, const int32_t* page_table,
+                      const int32_t* seq_lens, void* summaries,
+                      const int32_t* build_list, int32_t n_build,
+                      int32_t* out_page_ids, float* out_sel_lse, float* out,
+                      float* out_lse, void* ws, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* locks_strerror(int status);
+
+/* The hipError_t of the last failed launch on the calling thread (0 if none). */
+int locks_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOCKS_H */

@@ -1,0 +1,239 @@
+// Host side of the C ABI declared in include/locks.h: argument validation,
+// workspace planning and stream-ordered launches.  No allocation, no
+// synchronisation, no exceptions.
+#include "locks_internal.h"
+
+namespace locks {
+
+namespace {
+thread_local int g_last_hip_error = 0;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int validate(const locks_cfg_t* c) {
+  if (!c) return LOCKS_E_INVAL;
+  if (c->head_dim != kDim || c->page_size != kPage) return LOCKS_E_UNSUPPORTED;
+  if ((c->kv_dtype != LOCKS_BF16 && c->kv_dtype != LOCKS_FP32) ||
+      (c->q_dtype != LOCKS_BF16 && c->q_dtype != LOCKS_FP32))
+    return LOCKS_E_UNSUPPORTED;
+  if (c->num_seqs < 0 || c->num_kv_heads < 1 || c->num_q_heads < 1) return LOCKS_E_INVAL;
+  if (c->num_q_heads % c->num_kv_heads) return LOCKS_E_INVAL;
+  if (c->num_q_heads / c->num_kv_heads > kMaxGroup) return LOCKS_E_UNSUPPORTED;
+  if (c->rank < 1 || c->rank > kMaxRank) return LOCKS_E_INVAL;
+  if (c->budget_tokens < 1 || (c->budget_tokens + kPage - 1) / kPage < 2) return LOCKS_E_INVAL;
+  if (c->max_pages_per_seq < 1 || c->num_blocks < 1) return LOCKS_E_INVAL;
+  if ((long)c->num_seqs * c->num_q_heads > 0x7fffffffL / kDim) return LOCKS_E_INVAL;
+  return LOCKS_OK;
+}
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return LOCKS_OK;
+  g_last_hip_error = (int)e;
+  return LOCKS_E_HIP;
+}
+
+struct Ws {
+  float* s_hat;
+  float2* part;
+  float* lz;
+  uint32_t* keys;
+  float* attn;
+};
+
+Ws carve(void* ws, const WsPlan& p) {
+  char* b = static_cast<char*>(ws);
+  return Ws{reinterpret_cast<float*>(b + p.s_hat_off), reinterpret_cast<float2*>(b + p.part_off),
+            reinterpret_cast<float*>(b + p.lz_off), reinterpret_cast<uint32_t*>(b + p.key_off),
+            reinterpret_cast<float*>(b + p.attn_off)};
+}
+
+int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
+  const WsPlan p = plan_workspace(*c);
+  if (!ws || ws_bytes < p.total) return LOCKS_E_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return LOCKS_E_WORKSPACE;
+  return LOCKS_OK;
+}
+
+int dense_splits(const locks_cfg_t& c) {
+  return (c.max_pages_per_seq + kDensePagesPerSplit - 1) / kDensePagesPerSplit;
+}
+
+}  // namespace
+
+int page_budget(const locks_cfg_t& c) { return (c.budget_tokens + kPage - 1) / kPage; }
+
+WsPlan plan_workspace(const locks_cfg_t& c) {
+  WsPlan p{};
+  const size_t S = (size_t)c.num_seqs, Hq = (size_t)c.num_q_heads, Hkv = (size_t)c.num_kv_heads;
+  const size_t mp = (size_t)c.max_pages_per_seq;
+  p.n_tiles = (int)((mp + kScanTile - 1) / kScanTile);
+  const int k = page_budget(c);
+  const int sparse_splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
+  p.n_splits = sparse_splits > dense_splits(c) ? sparse_splits : dense_splits(c);
+  size_t off = 0;
+  p.s_hat_off = off;
+  p.s_hat_bytes = S * Hq * mp * sizeof(float);
+  off = align256(off + p.s_hat_bytes);
+  p.part_off = off;
+  p.part_bytes = S * Hq * (size_t)p.n_tiles * sizeof(float2);
+  off = align256(off + p.part_bytes);
+  p.lz_off = off;
+  p.lz_bytes = S * Hq * sizeof(float);
+  off = align256(off + p.lz_bytes);
+  p.key_off = off;
+  p.key_bytes = S * Hkv * mp * sizeof(uint32_t);
+  off = align256(off + p.key_bytes);
+  p.attn_off = off;
+  p.attn_bytes = S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float);
+  off = align256(off + p.attn_bytes);
+  p.total = off;
+  return p;
+}
+
+static int select_impl(const locks_cfg_t* c, const void* q, const void* summaries,
+                       const int32_t* page_table, const int32_t* seq_lens, int32_t* out_page_ids,
+                       float* out_sel_lse, float* out_all_lse, void* ws, hipStream_t st) {
+  const WsPlan p = plan_workspace(*c);
+  Ws w = carve(ws, p);
+  float* s_hat = out_all_lse ? out_all_lse : w.s_hat;
+  hipError_t e = launch_scan(*c, q, summaries, page_table, seq_lens, s_hat, c->max_pages_per_seq,
+                             w.part, p.n_tiles, st);
+  if (e != hipSuccess) return hip_status(e);
+  e = launch_select(*c, s_hat, c->max_pages_per_seq, w.part, p.n_tiles, seq_lens, w.lz, w.keys,
+                    out_page_ids, out_sel_lse, st);
+  return hip_status(e);
+}
+
+}  // namespace locks
+
+using namespace locks;
+
+extern "C" {
+
+size_t locks_summary_payload_bytes(int32_t rank) {
+  return (rank < 1 || rank > kMaxRank) ? 0 : (size_t)rec_payload(rank);
+}
+
+size_t locks_summary_stride(int32_t rank) {
+  return (rank < 1 || rank > kMaxRank) ? 0 : (size_t)rec_stride(rank);
+}
+
+size_t locks_workspace_bytes(const locks_cfg_t* cfg) {
+  if (validate(cfg) != LOCKS_OK) return 0;
+  return plan_workspace(*cfg).total;
+}
+
+int locks_build_summaries(const locks_cfg_t* cfg, const void* k_cache, const int32_t* page_table,
+                          const int32_t* seq_lens, const int32_t* build_list, int32_t n_build,
+                          void* summaries, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!k_cache || !page_table || !seq_lens || !summaries || n_build < 0) return LOCKS_E_INVAL;
+  if (build_list == nullptr && n_build > 0) return LOCKS_E_INVAL;
+  if (cfg->num_seqs == 0) return LOCKS_OK;
+  const bool all = build_list == nullptr;
+  return hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, all,
+                                 summaries, nullptr, nullptr, nullptr, nullptr,
+                                 static_cast<hipStream_t>(stream)));
+}
+
+int locks_build_factors(const locks_cfg_t* cfg, const void* k_cache, const int32_t* page_table,
+                        const int32_t* seq_lens, const int32_t* build_list, int32_t n_build,
+                        float* mu, float* basis, float* coef, float* sigma2, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!k_cache || !page_table || !seq_lens || !build_list || n_build < 0 || !mu || !basis ||
+      !coef || !sigma2)
+    return LOCKS_E_INVAL;
+  if (cfg->num_seqs == 0 || n_build == 0) return LOCKS_OK;
+  return hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
+                                 nullptr, mu, basis, coef, sigma2, static_cast<hipStream_t>(stream)));
+}
+
+int locks_select(const locks_cfg_t* cfg, const void* q, const void* summaries,
+                 const int32_t* page_table, const int32_t* seq_lens, int32_t* out_page_ids,
+                 float* out_sel_lse, float* out_all_lse, void* ws, size_t ws_bytes, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!q || !summaries || !page_table || !seq_lens || !out_page_ids || !out_sel_lse)
+    return LOCKS_E_INVAL;
+  if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
+  if (cfg->num_seqs == 0) return LOCKS_OK;
+  return select_impl(cfg, q, summaries, page_table, seq_lens, out_page_ids, out_sel_lse,
+                     out_all_lse, ws, static_cast<hipStream_t>(stream));
+}
+
+int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                        const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
+                        const int32_t* page_ids, float* out, float* out_lse, void* ws,
+                        size_t ws_bytes, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !page_ids || !out)
+    return LOCKS_E_INVAL;
+  if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
+  if (cfg->num_seqs == 0) return LOCKS_OK;
+  const WsPlan p = plan_workspace(*cfg);
+  const int k = page_budget(*cfg);
+  const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
+  return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, page_ids,
+                                  kSparsePagesPerSplit, splits, carve(ws, p).attn, out, out_lse,
+                                  static_cast<hipStream_t>(stream)));
+}
+
+int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                       const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
+                       float* out, float* out_lse, void* ws, size_t ws_bytes, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !out) return LOCKS_E_INVAL;
+  if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
+  if (cfg->num_seqs == 0) return LOCKS_OK;
+  const WsPlan p = plan_workspace(*cfg);
+  return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, nullptr,
+                                  kDensePagesPerSplit, dense_splits(*cfg), carve(ws, p).attn, out,
+                                  out_lse, static_cast<hipStream_t>(stream)));
+}
+
+int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                      const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
+                      void* summaries, const int32_t* build_list, int32_t n_build,
+                      int32_t* out_page_ids, float* out_sel_lse, float* out, float* out_lse,
+                      void* ws, size_t ws_bytes, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !summaries || !out_page_ids ||
+      !out_sel_lse || !out || n_build < 0 || (n_build > 0 && !build_list))
+    return LOCKS_E_INVAL;
+  if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
+  if (cfg->num_seqs == 0) return LOCKS_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n_build > 0) {
+    rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
+                                 summaries, nullptr, nullptr, nullptr, nullptr, st));
+    if (rc) return rc;
+  }
+  rc = select_impl(cfg, q, summaries, page_table, seq_lens, out_page_ids, out_sel_lse, nullptr, ws,
+                   st);
+  if (rc) return rc;
+  const WsPlan p = plan_workspace(*cfg);
+  const int k = page_budget(*cfg);
+  const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
+  return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, out_page_ids,
+                                  kSparsePagesPerSplit, splits, carve(ws, p).attn, out, out_lse, st));
+}
+
+const char* locks_strerror(int status) {
+  switch (status) {
+    case LOCKS_OK: return "ok";
+    case LOCKS_E_INVAL: return "invalid argument";
+    case LOCKS_E_UNSUPPORTED: return "unsupported configuration";
+    case LOCKS_E_WORKSPACE: return "workspace missing, misaligned or too small";
+    case LOCKS_E_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+int locks_last_hip_error(void) { return g_last_hip_error; }
+
+}  // extern "C"

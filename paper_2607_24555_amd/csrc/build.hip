@@ -1,0 +1,334 @@
+// Per-page summary construction (Sec. 4 "Build"): centre the page's 16 keys,
+// eigendecompose the 16 x 16 Gram of the deviations, keep the r leading nonzero
+// modes, form V = D^T U_r S_r^{-1} and C = U_r S_r, quantise and pack.
+//
+// Mapping: one 64-lane wave per block, four (page, KV head) items per wave, 16
+// lanes per item with lane i owning row i of the page.  The symmetric 16 x 16
+// eigenproblem is solved by cyclic Jacobi in round-robin (tournament) order: each
+// of the 15 rounds of a sweep rotates 8 disjoint index pairs at once, so the 16
+// lanes of an item update their own rows in parallel.  Everything is fp32; the
+// Gram is formed with the same summation order for (i, j) and (j, i), so it is
+// exactly symmetric.
+#include "locks_internal.h"
+
+namespace locks {
+namespace {
+
+constexpr int kItems = 4;         // items per block
+constexpr int kMaxSweeps = 12;
+constexpr float kZeroRel = 1e-6f;
+constexpr float kZeroAbs = 1e-10f;
+
+// Tournament pairing of 16 indices (circle method): index 15 meets t in round t,
+// the others meet (2t - i) mod 15.  Over the 15 rounds every pair meets once.
+__device__ __forceinline__ int partner(int t, int i) {
+  if (i == 15) return t;
+  if (i == t) return 15;
+  int p = 2 * t - i;
+  p %= 15;
+  if (p < 0) p += 15;
+  return p;
+}
+
+__device__ __forceinline__ float group16_sum(float v) {
+  for (int o = 8; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float group16_max(float v) {
+  for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float f16_scale(float amax, float qmax) {
+  float s = fminf(amax / qmax, 65504.0f);
+  return (float)(_Float16)s;
+}
+
+__device__ __forceinline__ int quant(float x, float s, int qmax) {
+  if (!(s > 0.0f)) return 0;
+  float c = rintf(x / s);
+  c = fminf(fmaxf(c, (float)-qmax), (float)qmax);
+  return (int)c;
+}
+
+__device__ __forceinline__ uint16_t f16_bits(float s) {
+  _Float16 h = (_Float16)s;
+  return *reinterpret_cast<uint16_t*>(&h);
+}
+
+template <typename KT, bool kFactors>
+__global__ __launch_bounds__(64) void build_kernel(
+    int S, int H_kv, int max_pages, int r, const KT* __restrict__ k_cache,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
+    const int32_t* __restrict__ build_list, int n_items, int all_pages,
+    uint8_t* __restrict__ summaries, float* __restrict__ mu_out, float* __restrict__ basis_out,
+    float* __restrict__ coef_out, float* __restrict__ sigma2_out) {
+  __shared__ float sD[kItems][kPage][kDim + 1];
+  __shared__ float sA[kItems][kPage][kPage + 1];
+  __shared__ float sU[kItems][kPage][kPage + 1];
+  __shared__ float sC[kItems][kPage][kPage];
+  __shared__ float sMu[kItems][kDim];
+  __shared__ float2 sCS[kItems][kPage];
+  __shared__ float sLam[kItems][kPage];
+  __shared__ int sOrd[kItems][kPage];
+
+  const int grp = threadIdx.x >> 4;
+  const int li = threadIdx.x & 15;
+  const long item = (long)blockIdx.x * kItems + grp;
+
+  // ---- which (seq, page, KV head) this group builds
+  bool active = false;
+  int s = 0, j = 0, h = 0, e = 0;
+  if (all_pages) {
+    h = (int)(item % H_kv);
+    long t = item / H_kv;
+    j = (int)(t % max_pages);
+    s = (int)(t / max_pages);
+    active = s < S && j < seq_lens[s] / kPage;
+  } else {
+    h = (int)(item % H_kv);
+    e = (int)(item / H_kv);
+    if (e < n_items) {
+      s = build_list[2 * e];
+      j = build_list[2 * e + 1];
+      active = s >= 0 && s < S && j >= 0 && j < max_pages && j < seq_lens[s] / kPage;
+    }
+  }
+  const long blk = active ? (long)page_table[(long)s * max_pages + j] : 0;
+
+  // ---- load row li of the page, track its squared norm
+  float energy = 0.0f;
+  {
+    const KT* src = k_cache + ((blk * H_kv + h) * kPage + li) * kDim;
+    for (int c = 0; c < kDim; ++c) {
+      float x = active ? load_elem(src, c) : 0.0f;
+      sD[grp][li][c] = x;
+      energy = fmaf(x, x, energy);
+    }
+  }
+  energy = group16_sum(energy) * (1.0f / kPage);
+  __syncthreads();
+
+  // ---- centroid: pairwise sum over the 16 rows (exact for equal rows)
+  for (int cc = 0; cc < 8; ++cc) {
+    const int c = 8 * li + cc;
+    float v[kPage];
+#pragma unroll
+    for (int i = 0; i < kPage; ++i) v[i] = sD[grp][i][c];
+#pragma unroll
+    for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+      for (int i = 0; i < w; ++i) v[i] = v[i] + v[i + w];
+    sMu[grp][c] = v[0] * (1.0f / kPage);
+  }
+  __syncthreads();
+  for (int c = 0; c < kDim; ++c) sD[grp][li][c] -= sMu[grp][c];
+  __syncthreads();
+
+  // ---- Gram of the deviations (same summation order for (i,j) and (j,i))
+  for (int jj = 0; jj < kPage; ++jj) {
+    float g = 0.0f;
+    for (int c = 0; c < kDim; ++c) g = fmaf(sD[grp][li][c], sD[grp][jj][c], g);
+    sA[grp][li][jj] = g;
+    sU[grp][li][jj] = (li == jj) ? 1.0f : 0.0f;
+  }
+  __syncthreads();
+
+  // ---- cyclic Jacobi, tournament order
+  for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
+    float off = 0.0f, dia = 0.0f;
+    for (int jj = 0; jj < kPage; ++jj) {
+      const float a = sA[grp][li][jj];
+      if (jj == li) dia = a * a; else off = fmaf(a, a, off);
+    }
+    off = group16_sum(off);
+    dia = group16_sum(dia);
+    const int done = off <= 1e-12f * dia;
+    if (__all(done)) break;
+    for (int t = 0; t < 15; ++t) {
+      const int p = partner(t, li);
+      const int P = min(li, p), Q = max(li, p);
+      const float app = sA[grp][P][P], aqq = sA[grp][Q][Q], apq = sA[grp][P][Q];
+      float c = 1.0f, sn = 0.0f;
+      if (apq != 0.0f) {
+        const float theta = (aqq - app) / (2.0f * apq);
+        const float tt = copysignf(1.0f, theta) / (fabsf(theta) + sqrtf(fmaf(theta, theta, 1.0f)));
+        c = 1.0f / sqrtf(fmaf(tt, tt, 1.0f));
+        sn = tt * c;
+      }
+      sCS[grp][li] = make_float2(c, sn);
+      __syncthreads();
+      // columns: (A J) and (U J) on this lane's row
+      for (int m = 0; m < kPage; ++m) {
+        const int pm = partner(t, m);
+        if (m < pm) {
+          const float2 cs = sCS[grp][m];
+          const float x = sA[grp][li][m], y = sA[grp][li][pm];
+          sA[grp][li][m] = cs.x * x - cs.y * y;
+          sA[grp][li][pm] = cs.y * x + cs.x * y;
+          const float u = sU[grp][li][m], w = sU[grp][li][pm];
+          sU[grp][li][m] = cs.x * u - cs.y * w;
+          sU[grp][li][pm] = cs.y * u + cs.x * w;
+        }
+      }
+      __syncthreads();
+      // rows: J^T (A J); lane P gets c*row_P - s*row_Q, lane Q gets s*row_P + c*row_Q
+      float nr[kPage];
+#pragma unroll
+      for (int m = 0; m < kPage; ++m) {
+        const float xp = sA[grp][P][m], xq = sA[grp][Q][m];
+        nr[m] = (li == P) ? (c * xp - sn * xq) : (sn * xp + c * xq);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int m = 0; m < kPage; ++m) sA[grp][li][m] = nr[m];
+      __syncthreads();
+    }
+  }
+
+  // ---- eigenvalues descending (ties by index), zero-mode floor
+  {
+    const float lam = sA[grp][li][li];
+    int rank = 0;
+    for (int m = 0; m < kPage; ++m) {
+      const float o = sA[grp][m][m];
+      rank += (o > lam) || (o == lam && m < li);
+    }
+    sOrd[grp][rank] = li;
+    sLam[grp][rank] = fmaxf(lam, 0.0f);
+  }
+  __syncthreads();
+  const float top = sLam[grp][0];
+  const float floor_ = fmaxf(kZeroRel * top, kZeroAbs * energy);
+
+  const long out_item = all_pages ? 0 : (long)e * H_kv + h;
+  uint8_t* rec = summaries + (blk * H_kv + h) * (long)rec_stride(r);
+
+  // ---- basis columns, one at a time: V[:, l] = D^T u_l / sigma_l
+  float cabs = 0.0f;  // running max |C[li][:]| for the row scale
+  for (int l = 0; l < r; ++l) {
+    const float lam = sLam[grp][l];
+    const bool kept = lam > floor_ && lam > 0.0f;
+    const float sig = kept ? sqrtf(lam) : 1.0f;
+    const int mode = sOrd[grp][l];
+    float v[8];
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) {
+      const int c = 8 * li + cc;
+      float acc = 0.0f;
+      for (int i = 0; i < kPage; ++i) acc = fmaf(sD[grp][i][c], sU[grp][i][mode], acc);
+      v[cc] = kept ? acc / sig : 0.0f;
+    }
+    // sign convention: largest |v| (first index on ties) made positive
+    float best = -1.0f;
+    int bidx = 0;
+    float bval = 0.0f;
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) {
+      const float a = fabsf(v[cc]);
+      if (a > best) { best = a; bidx = 8 * li + cc; bval = v[cc]; }
+    }
+    for (int o = 8; o > 0; o >>= 1) {
+      const float ob = __shfl_xor(best, o, 64);
+      const int oi = __shfl_xor(bidx, o, 64);
+      const float ov = __shfl_xor(bval, o, 64);
+      if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; bval = ov; }
+    }
+    const float flip = (bval < 0.0f) ? -1.0f : 1.0f;
+    const float cval = kept ? flip * sU[grp][li][mode] * sig : 0.0f;
+    sC[grp][li][l] = cval;
+    cabs = fmaxf(cabs, fabsf(cval));
+    if (!active) continue;
+    if (kFactors) {
+      float* bo = basis_out + out_item * (kDim * (long)r);
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) bo[(8 * li + cc) * r + l] = flip * v[cc];
+    } else {
+      const float vs = f16_scale(best, 7.0f);
+      uint32_t word = 0;
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+        const int code = quant(flip * v[cc], vs, 7);
+        word |= (uint32_t)(code + 8) << (4 * cc);
+      }
+      *reinterpret_cast<uint32_t*>(rec + 64 * l + 4 * li) = word;
+      if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * l) = f16_bits(vs);
+    }
+  }
+  if (!active) return;
+
+  if (kFactors) {
+    float* mo = mu_out + out_item * kDim;
+    for (int cc = 0; cc < 8; ++cc) mo[8 * li + cc] = sMu[grp][8 * li + cc];
+    float* co = coef_out + out_item * (kPage * (long)r);
+    for (int l = 0; l < r; ++l) co[li * r + l] = sC[grp][li][l];
+    sigma2_out[out_item * kPage + li] = sLam[grp][li];
+    return;
+  }
+
+  // ---- coefficient row li: int8 with its own scale
+  {
+    const float cs = f16_scale(cabs, 127.0f);
+    for (int l = 0; l < r; ++l)
+      rec[rec_coef_off(r) + li * r + l] = (uint8_t)(quant(sC[grp][li][l], cs, 127) + 128);
+    *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * (r + li)) = f16_bits(cs);
+  }
+  // ---- centroid: int8 with one scale
+  {
+    float m = 0.0f;
+    for (int cc = 0; cc < 8; ++cc) m = fmaxf(m, fabsf(sMu[grp][8 * li + cc]));
+    m = group16_max(m);
+    const float ms = f16_scale(m, 127.0f);
+    for (int cc = 0; cc < 8; ++cc)
+      rec[rec_mu_off(r) + 8 * li + cc] = (uint8_t)(quant(sMu[grp][8 * li + cc], ms, 127) + 128);
+    if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * (r + kPage)) = f16_bits(ms);
+  }
+  // ---- zero padding up to the record stride
+  {
+    const int pad0 = rec_payload(r);
+    if (pad0 + li < rec_stride(r)) rec[pad0 + li] = 0;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_build(const locks_cfg_t& c, const void* k_cache, const int32_t* page_table,
+                        const int32_t* seq_lens, const int32_t* build_list, int32_t n_items,
+                        bool all_pages, void* summaries, float* mu, float* basis, float* coef,
+                        float* sigma2, hipStream_t st) {
+  const long items = all_pages ? (long)c.num_seqs * c.max_pages_per_seq * c.num_kv_heads
+                               : (long)n_items * c.num_kv_heads;
+  if (items == 0) return hipSuccess;
+  const long blocks = (items + kItems - 1) / kItems;
+  if (blocks > 0x7fffffffL) return hipErrorInvalidConfiguration;
+  const bool factors = mu != nullptr;
+  const dim3 grid((unsigned)blocks), block(64);
+  if (c.kv_dtype == LOCKS_BF16) {
+    auto* k = static_cast<const uint16_t*>(k_cache);
+    if (factors)
+      hipLaunchKernelGGL((build_kernel<uint16_t, true>), grid, block, 0, st, c.num_seqs,
+                         c.num_kv_heads, c.max_pages_per_seq, c.rank, k, page_table, seq_lens,
+                         build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu, basis,
+                         coef, sigma2);
+    else
+      hipLaunchKernelGGL((build_kernel<uint16_t, false>), grid, block, 0, st, c.num_seqs,
+                         c.num_kv_heads, c.max_pages_per_seq, c.rank, k, page_table, seq_lens,
+                         build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu, basis,
+                         coef, sigma2);
+  } else {
+    auto* k = static_cast<const float*>(k_cache);
+    if (factors)
+      hipLaunchKernelGGL((build_kernel<float, true>), grid, block, 0, st, c.num_seqs,
+                         c.num_kv_heads, c.max_pages_per_seq, c.rank, k, page_table, seq_lens,
+                         build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu, basis,
+                         coef, sigma2);
+    else
+      hipLaunchKernelGGL((build_kernel<float, false>), grid, block, 0, st, c.num_seqs,
+                         c.num_kv_heads, c.max_pages_per_seq, c.rank, k, page_table, seq_lens,
+                         build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu, basis,
+                         coef, sigma2);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace locks

@@ -1,0 +1,102 @@
+// Internal declarations shared by the HIP translation units of liblocks.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/locks.h"
+
+namespace locks {
+
+constexpr int kPage = 16;    // B
+constexpr int kDim = 128;    // d
+constexpr int kMaxRank = 15; // r <= B - 1 (rank of centred page deviations)
+constexpr int kMaxGroup = 64;
+
+// Byte offsets inside one summary record for rank r (see locks_summary_stride).
+__host__ __device__ constexpr int rec_coef_off(int r) { return 64 * r; }
+__host__ __device__ constexpr int rec_mu_off(int r) { return 80 * r; }
+__host__ __device__ constexpr int rec_scale_off(int r) { return 80 * r + kDim; }
+__host__ __device__ constexpr int rec_payload(int r) { return 82 * r + 162; }
+__host__ __device__ constexpr int rec_stride(int r) { return (rec_payload(r) + 15) / 16 * 16; }
+
+// ---------------------------------------------------------------- device helpers
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b16) {
+  return __uint_as_float(b16 << 16);
+}
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T* p, size_t i);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p, size_t i) {
+  return p[i];
+}
+template <>
+__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, size_t i) {
+  return bf16_bits_to_f32(p[i]);
+}
+
+// Float -> uint32 whose unsigned order matches the float order (NaN excluded).
+__device__ __forceinline__ uint32_t f32_order_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float order_key_f32(uint32_t k) {
+  uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+  return __uint_as_float(u);
+}
+
+__device__ __forceinline__ float warp_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float warp_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// ---------------------------------------------------------------- workspace plan
+
+struct WsPlan {
+  size_t s_hat_off, s_hat_bytes;      // float [S][H_q][max_pages]
+  size_t part_off, part_bytes;        // float2 [S][H_q][n_tiles]  (max, sum exp)
+  size_t lz_off, lz_bytes;            // float [S][H_q]
+  size_t key_off, key_bytes;          // uint32 [S][H_kv][max_pages]  order keys
+  size_t attn_off, attn_bytes;        // float [S][H_q][n_splits][d + 2]
+  size_t total;
+  int n_tiles;                        // scan tiles per sequence
+  int n_splits;                       // attention splits per (seq, KV head)
+};
+
+constexpr int kScanTile = 64;         // pages per scan block
+constexpr int kSparsePagesPerSplit = 8;
+constexpr int kDensePagesPerSplit = 64;
+
+WsPlan plan_workspace(const locks_cfg_t& c);
+int page_budget(const locks_cfg_t& c);  // k = ceil(b / 16)
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipError_t of the launch (hipSuccess on success).
+
+hipError_t launch_build(const locks_cfg_t& c, const void* k_cache, const int32_t* page_table,
+                        const int32_t* seq_lens, const int32_t* build_list, int32_t n_items,
+                        bool all_pages, void* summaries, float* mu, float* basis, float* coef,
+                        float* sigma2, hipStream_t st);
+
+hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,
+                       const int32_t* page_table, const int32_t* seq_lens, float* s_hat,
+                       int s_hat_stride, float2* partials, int n_tiles, hipStream_t st);
+
+hipError_t launch_select(const locks_cfg_t& c, const float* s_hat, int s_hat_stride,
+                         const float2* partials, int n_tiles, const int32_t* seq_lens,
+                         float* lz, uint32_t* keys, int32_t* out_page_ids, float* out_sel_lse,
+                         hipStream_t st);
+
+hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cache,
+                         const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
+                         const int32_t* page_ids, int pages_per_split, int n_splits,
+                         float* partial, float* out, float* out_lse, hipStream_t st);
+
+}  // namespace locks

@@ -1,0 +1,246 @@
+"""Thin ctypes binding of liblocks (include/locks.h).
+
+Argument marshalling only: every step of the decode path runs in the HIP
+kernels of liblocks.so.  Tensors are torch device tensors (PyTorch provides the
+device memory and the stream); the binding passes their data pointers and the
+current HIP stream.  If the library is not built, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblocks.so")
+
+LOCKS_BF16 = 0
+LOCKS_FP32 = 1
+PAGE = 16
+HEAD_DIM = 128
+
+
+class LocksError(RuntimeError):
+    pass
+
+
+class _Cfg(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "num_seqs", "num_q_heads", "num_kv_heads", "head_dim", "page_size", "rank",
+        "budget_tokens", "max_pages_per_seq", "num_blocks", "kv_dtype", "q_dtype")]
+
+
+@dataclass
+class Config:
+    num_seqs: int
+    num_q_heads: int
+    num_kv_heads: int
+    rank: int
+    budget_tokens: int
+    max_pages_per_seq: int
+    num_blocks: int
+    kv_dtype: int = LOCKS_BF16
+    q_dtype: int = LOCKS_BF16
+    head_dim: int = HEAD_DIM
+    page_size: int = PAGE
+
+    @property
+    def group(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+    @property
+    def k(self) -> int:
+        return (self.budget_tokens + PAGE - 1) // PAGE
+
+    def c(self) -> _Cfg:
+        return _Cfg(self.num_seqs, self.num_q_heads, self.num_kv_heads, self.head_dim,
+                    self.page_size, self.rank, self.budget_tokens, self.max_pages_per_seq,
+                    self.num_blocks, self.kv_dtype, self.q_dtype)
+
+
+_lib = None
+_P = ctypes.c_void_p
+_SZ = ctypes.c_size_t
+_I = ctypes.c_int32
+
+_SIGS = {
+    "locks_summary_payload_bytes": (_SZ, [_I]),
+    "locks_summary_stride": (_SZ, [_I]),
+    "locks_workspace_bytes": (_SZ, [ctypes.POINTER(_Cfg)]),
+    "locks_build_summaries": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _I, _P, _P]),
+    "locks_build_factors": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _I, _P, _P, _P,
+                                           _P, _P]),
+    "locks_select": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                                    _P]),
+    "locks_sparse_attend": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P, _P,
+                                           _P, _SZ, _P]),
+    "locks_dense_attend": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P, _P,
+                                          _SZ, _P]),
+    "locks_decode_step": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P, _I,
+                                         _P, _P, _P, _P, _P, _SZ, _P]),
+    "locks_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "locks_last_hip_error": (ctypes.c_int, []),
+}
+
+
+def lib():
+    """Load liblocks.so (raises LocksError when it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise LocksError(f"{LIB_PATH} is missing: build it with "
+                             "`python -m paper_2607_24555_amd.build_lib`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise LocksError("liblocks takes device tensors")
+    if not t.is_contiguous():
+        raise LocksError("liblocks takes contiguous tensors")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> Optional[ctypes.c_void_p]:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(rc: int):
+    if rc != 0:
+        L = lib()
+        msg = L.locks_strerror(rc).decode()
+        raise LocksError(f"liblocks status {rc}: {msg} (hip error {L.locks_last_hip_error()})")
+
+
+def summary_payload_bytes(rank: int) -> int:
+    return int(lib().locks_summary_payload_bytes(rank))
+
+
+def summary_stride(rank: int) -> int:
+    return int(lib().locks_summary_stride(rank))
+
+
+def workspace_bytes(cfg: Config) -> int:
+    c = cfg.c()
+    return int(lib().locks_workspace_bytes(ctypes.byref(c)))
+
+
+def alloc_workspace(cfg: Config, device="cuda") -> torch.Tensor:
+    n = workspace_bytes(cfg)
+    if n == 0:
+        raise LocksError("invalid configuration")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def alloc_summaries(cfg: Config, device="cuda") -> torch.Tensor:
+    return torch.zeros(cfg.num_blocks, cfg.num_kv_heads, summary_stride(cfg.rank),
+                       dtype=torch.uint8, device=device)
+
+
+def build_summaries(cfg: Config, k_cache, page_table, seq_lens, summaries,
+                    build_list: Optional[torch.Tensor] = None, stream=None):
+    c = cfg.c()
+    n = 0 if build_list is None else int(build_list.shape[0])
+    _check(lib().locks_build_summaries(ctypes.byref(c), _ptr(k_cache), _ptr(page_table),
+                                       _ptr(seq_lens), _ptr(build_list), n, _ptr(summaries),
+                                       _stream(stream)))
+
+
+def build_factors(cfg: Config, k_cache, page_table, seq_lens, build_list: torch.Tensor,
+                  stream=None):
+    n = int(build_list.shape[0])
+    dev = k_cache.device
+    mu = torch.zeros(n, cfg.num_kv_heads, HEAD_DIM, device=dev)
+    basis = torch.zeros(n, cfg.num_kv_heads, HEAD_DIM, cfg.rank, device=dev)
+    coef = torch.zeros(n, cfg.num_kv_heads, PAGE, cfg.rank, device=dev)
+    sigma2 = torch.zeros(n, cfg.num_kv_heads, PAGE, device=dev)
+    c = cfg.c()
+    _check(lib().locks_build_factors(ctypes.byref(c), _ptr(k_cache), _ptr(page_table),
+                                     _ptr(seq_lens), _ptr(build_list), n, _ptr(mu), _ptr(basis),
+                                     _ptr(coef), _ptr(sigma2), _stream(stream)))
+    return mu, basis, coef, sigma2
+
+
+def alloc_select_outputs(cfg: Config, device="cuda"):
+    ids = torch.empty(cfg.num_seqs, cfg.num_kv_heads, cfg.k, dtype=torch.int32, device=device)
+    sel = torch.empty(cfg.num_seqs, cfg.num_q_heads, cfg.k, dtype=torch.float32, device=device)
+    return ids, sel
+
+
+def select(cfg: Config, q, summaries, page_table, seq_lens, ws, out_ids=None, out_sel_lse=None,
+           out_all_lse=None, stream=None):
+    if out_ids is None:
+        out_ids, out_sel_lse = alloc_select_outputs(cfg, q.device)
+    c = cfg.c()
+    _check(lib().locks_select(ctypes.byref(c), _ptr(q), _ptr(summaries), _ptr(page_table),
+                              _ptr(seq_lens), _ptr(out_ids), _ptr(out_sel_lse), _ptr(out_all_lse),
+                              _ptr(ws), ws.numel(), _stream(stream)))
+    return out_ids, out_sel_lse
+
+
+def alloc_attend_outputs(cfg: Config, device="cuda"):
+    out = torch.empty(cfg.num_seqs, cfg.num_q_heads, HEAD_DIM, dtype=torch.float32, device=device)
+    lse = torch.empty(cfg.num_seqs, cfg.num_q_heads, dtype=torch.float32, device=device)
+    return out, lse
+
+
+def sparse_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, page_ids, ws,
+                  out=None, out_lse=None, stream=None):
+    if out is None:
+        out, out_lse = alloc_attend_outputs(cfg, q.device)
+    c = cfg.c()
+    _check(lib().locks_sparse_attend(ctypes.byref(c), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                     _ptr(page_table), _ptr(seq_lens), _ptr(page_ids), _ptr(out),
+                                     _ptr(out_lse), _ptr(ws), ws.numel(), _stream(stream)))
+    return out, out_lse
+
+
+def dense_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, ws, out=None,
+                 out_lse=None, stream=None):
+    if out is None:
+        out, out_lse = alloc_attend_outputs(cfg, q.device)
+    c = cfg.c()
+    _check(lib().locks_dense_attend(ctypes.byref(c), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                    _ptr(page_table), _ptr(seq_lens), _ptr(out), _ptr(out_lse),
+                                    _ptr(ws), ws.numel(), _stream(stream)))
+    return out, out_lse
+
+
+def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summaries, ws,
+                build_list: Optional[torch.Tensor] = None, out_ids=None, out_sel_lse=None,
+                out=None, out_lse=None, stream=None):
+    if out_ids is None:
+        out_ids, out_sel_lse = alloc_select_outputs(cfg, q.device)
+    if out is None:
+        out, out_lse = alloc_attend_outputs(cfg, q.device)
+    n = 0 if build_list is None else int(build_list.shape[0])
+    c = cfg.c()
+    _check(lib().locks_decode_step(ctypes.byref(c), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                   _ptr(page_table), _ptr(seq_lens), _ptr(summaries),
+                                   _ptr(build_list), n, _ptr(out_ids), _ptr(out_sel_lse),
+                                   _ptr(out), _ptr(out_lse), _ptr(ws), ws.numel(), _stream(stream)))
+    return out_ids, out_sel_lse, out, out_lse
+
+
+def config_for(spec, num_blocks: int, max_pages: int) -> Config:
+    """Config of a workloads.WorkloadSpec laid out with num_blocks / max_pages."""
+    dt = {"bf16": LOCKS_BF16, "fp32": LOCKS_FP32}
+    return Config(spec.num_seqs, spec.num_q_heads, spec.num_kv_heads, spec.rank,
+                  spec.budget_tokens, max_pages, num_blocks, dt[spec.kv_dtype], dt[spec.q_dtype])
+
+
+def page_count(seq_len: int) -> int:
+    return math.ceil(seq_len / PAGE)

@@ -1,0 +1,106 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before any launch (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_24555_amd import locks as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "locks.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(locks_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return B.lib()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) == 11
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B._SIGS), "binding and header disagree"
+
+
+def cfg(**kw):
+    c = B.Config(num_seqs=2, num_q_heads=8, num_kv_heads=2, rank=8, budget_tokens=256,
+                 max_pages_per_seq=64, num_blocks=128)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def test_payload_and_stride(lib):
+    assert [B.summary_payload_bytes(r) for r in (8, 4, 2)] == [818, 490, 326]
+    assert [B.summary_stride(r) for r in (8, 4, 2)] == [832, 496, 336]
+    assert B.summary_payload_bytes(0) == 0 and B.summary_stride(16) == 0
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(head_dim=64), -2), (dict(page_size=32), -2), (dict(kv_dtype=7), -2),
+    (dict(rank=0), -1), (dict(rank=16), -1), (dict(num_q_heads=7), -1),
+    (dict(budget_tokens=16), -1), (dict(budget_tokens=0), -1), (dict(max_pages_per_seq=0), -1),
+    (dict(num_blocks=0), -1), (dict(num_kv_heads=0), -1), (dict(num_seqs=-1), -1),
+    (dict(num_q_heads=130, num_kv_heads=2), -2),
+])
+def test_bad_config_is_rejected_before_launch(lib, bad, code):
+    c = cfg(**bad).c()
+    assert lib.locks_workspace_bytes(ctypes.byref(c)) == 0
+    fake = ctypes.c_void_p(0x1000)
+    rc = lib.locks_select(ctypes.byref(c), fake, fake, fake, fake, fake, fake, None, fake, 1 << 30, None)
+    assert rc == code
+    rc = lib.locks_build_summaries(ctypes.byref(c), fake, fake, fake, None, 0, fake, None)
+    assert rc == code
+
+
+def test_null_pointers_and_workspace(lib):
+    c = cfg().c()
+    need = lib.locks_workspace_bytes(ctypes.byref(c))
+    assert need > 0
+    fake = ctypes.c_void_p(0x1000)
+    # null query
+    assert lib.locks_select(ctypes.byref(c), None, fake, fake, fake, fake, fake, None, fake, need, None) == -1
+    # workspace too small / missing / misaligned
+    assert lib.locks_select(ctypes.byref(c), fake, fake, fake, fake, fake, fake, None, fake, need - 1, None) == -3
+    assert lib.locks_select(ctypes.byref(c), fake, fake, fake, fake, fake, fake, None, None, need, None) == -3
+    assert lib.locks_select(ctypes.byref(c), fake, fake, fake, fake, fake, fake, None,
+                            ctypes.c_void_p(0x1010), need, None) == -3
+    assert lib.locks_sparse_attend(ctypes.byref(c), fake, fake, fake, fake, fake, None, fake, None,
+                                   fake, need, None) == -1
+    assert lib.locks_dense_attend(ctypes.byref(c), fake, None, fake, fake, fake, fake, None, fake,
+                                  need, None) == -1
+    assert lib.locks_decode_step(ctypes.byref(c), fake, fake, fake, fake, fake, fake, None, 3, fake,
+                                 fake, fake, None, fake, need, None) == -1
+    assert lib.locks_build_summaries(ctypes.byref(c), fake, fake, fake, None, -1, fake, None) == -1
+    assert lib.locks_build_factors(ctypes.byref(c), fake, fake, fake, None, 4, fake, fake, fake,
+                                   fake, None) == -1
+    assert lib.locks_strerror(-3).decode().startswith("workspace")
+    assert lib.locks_last_hip_error() == 0
+
+
+def test_empty_batch_is_a_no_op(lib):
+    c = cfg(num_seqs=0).c()
+    need = lib.locks_workspace_bytes(ctypes.byref(c))
+    fake = ctypes.c_void_p(0x1000)
+    ws = ctypes.c_void_p(0x10000)
+    assert lib.locks_select(ctypes.byref(c), fake, fake, fake, fake, fake, fake, None, ws, need, None) == 0
+    assert lib.locks_decode_step(ctypes.byref(c), fake, fake, fake, fake, fake, fake, None, 0, fake,
+                                 fake, fake, None, ws, need, None) == 0
+
+
+def test_workspace_grows_with_shape(lib):
+    small = cfg().c()
+    big = cfg(max_pages_per_seq=4096).c()
+    assert lib.locks_workspace_bytes(ctypes.byref(big)) > lib.locks_workspace_bytes(ctypes.byref(small))
