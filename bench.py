@@ -1,0 +1,218 @@
+#!/usr/bin/env python
+"""Decode-step benchmark of the Locks sparse decode attention on one MI355X.
+
+One step = the fused locks_decode_step (summary scan -> share-average combine and
+top-k table -> sparse attention over the table) on the 1,048,576-token GLM-4-9B-
+shaped workload (1 sequence, 32 query heads over 2 KV heads, d = 128, page 16,
+r = 8, budget 2048 tokens, bf16 KV, synthetic inputs).  Inputs are resident in HBM
+before timing; the step rotates over --copies independent copies of the KV cache
+and summary store so that the 256 MB last-level cache cannot serve repeats.
+
+Prints ONE JSON line.  `value` is the per-step latency in microseconds.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-step latency (µs) + achieved HBM GB/s vs peak at 128K/1M ctx, r=8"
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--copies", type=int, default=3)
+    ap.add_argument("--workload", choices=["1m", "128k", "128k-r2", "32k"], default="1m")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-build", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+WORKLOADS = {
+    # name: (workload id, overrides, description)
+    "1m": (3, {}, "glm4-9b-1m: 1 seq x 1,048,576 tokens, 32 q / 2 kv heads, d 128, "
+                  "page 16, r 8, b 2048, bf16 KV"),
+    "128k": (2, {}, "llama3.1-8b-128k: 8 seq x 131,072 tokens, 32 q / 8 kv heads, d 128, "
+                    "page 16, r 8, b 2048, bf16 KV"),
+    "128k-r2": (2, {"rank": 2}, "llama3.1-8b-128k: 8 seq x 131,072 tokens, 32 q / 8 kv heads, "
+                                "d 128, page 16, r 2, b 2048, bf16 KV"),
+    "32k": (1, {}, "llama3.1-8b-32k: 1 seq x 32,768 tokens, 32 q / 8 kv heads, d 128, page 16, "
+                   "r 8, b 2048, bf16 KV"),
+}
+
+
+def timed(fn, n, sync):
+    """Wall time and summed event time of n calls of fn(i) on torch's current stream."""
+    import torch
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    sync()
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(n):
+        fn(i)
+    end.record()
+    sync()
+    t1 = time.perf_counter()
+    return (t1 - t0) / n * 1e6, start.elapsed_time(end) / n * 1e3
+
+
+def cpu_baseline(w, cfg, sample_pages):
+    """The CPU oracle's decode step (score + select + attend) on a prefix of one
+    (sequence, KV head) holding `sample_pages` complete pages, scaled to the whole
+    step by page-heads.  BLAS limited to one thread."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import locks_oracle as O
+    from workloads import gather_unit
+
+    k, v, q = gather_unit(w, 0, 0)
+    L = min(k.shape[0], sample_pages * 16)
+    k, v = k[:L], v[:L]
+    rec = O.unit_summaries(k, cfg.rank)                  # build: not part of the step
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            O.decode_step(q, k, v, rec, cfg.rank, cfg.budget_tokens)
+            reps += 1
+            if time.perf_counter() - t0 > 10.0 or reps >= 20:
+                break
+        dt = (time.perf_counter() - t0) / reps
+    total_page_heads = sum(math.ceil(L_ / 16) for L_ in w.spec.seq_lens) * cfg.num_kv_heads
+    scale = total_page_heads / (L // 16)
+    return {"value": round(dt * scale * 1e6, 1), "unit": "us", "cores": 1, "kind": "oracle",
+            "sample": f"oracle decode step on seq 0 / KV head 0 truncated to {L // 16} pages "
+                      f"({L} tokens, G={cfg.group} heads), {reps} reps, {dt:.3f} s each, "
+                      f"scaled x{scale:.1f} to the step's {total_page_heads} page-heads"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is "
+                                   "described in DESIGN.md and not implemented",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+
+    from paper_2607_24555_amd import locks as B
+    from workloads import make_workload
+
+    dev = torch.device("cuda:0")
+    wid, ov, desc = WORKLOADS[args.workload]
+    t_gen = time.perf_counter()
+    w = make_workload(wid, seed=args.seed, device=dev, **ov)
+    t_gen = time.perf_counter() - t_gen
+    cfg = B.config_for(w.spec, w.num_blocks, w.max_pages)
+    q, pt, sl = w.q, w.page_table, w.seq_lens
+    R = max(1, args.copies)
+    ks = [w.k_cache] + [w.k_cache.clone() for _ in range(R - 1)]
+    vs = [w.v_cache] + [w.v_cache.clone() for _ in range(R - 1)]
+    summ = [B.alloc_summaries(cfg, dev) for _ in range(R)]
+    ws = B.alloc_workspace(cfg, dev)
+    sync = torch.cuda.synchronize
+
+    n_pages = sum(math.ceil(L / 16) for L in w.spec.seq_lens)
+    page_heads = n_pages * cfg.num_kv_heads
+    complete_heads = sum(L // 16 for L in w.spec.seq_lens) * cfg.num_kv_heads
+    payload = B.summary_payload_bytes(cfg.rank)
+    stride = B.summary_stride(cfg.rank)
+    k_sel = min(cfg.k, n_pages)
+    kv_page = 2 * 16 * 128 * 2
+    alg_scan = complete_heads * payload
+    alg_attend = cfg.num_seqs * cfg.num_kv_heads * k_sel * kv_page
+    alg_step = alg_scan + alg_attend
+
+    # ---- summary build (separately timed): every complete page, every copy
+    build_us = None
+    for i in range(R):
+        B.build_summaries(cfg, ks[i], pt, sl, summ[i])
+    sync()
+    if not args.no_build:
+        _, build_us = timed(lambda i: B.build_summaries(cfg, ks[i % R], pt, sl, summ[i % R]),
+                            R, sync)
+
+    # ---- scan alone (dominant kernel): roofline on its algorithmic bytes
+    all_lse = torch.empty(cfg.num_seqs, cfg.num_q_heads, cfg.max_pages_per_seq, device=dev)
+    for i in range(args.warmup):
+        B.score_pages(cfg, q, summ[i % R], pt, sl, ws, all_lse)
+    _, scan_us = timed(lambda i: B.score_pages(cfg, q, summ[i % R], pt, sl, ws, all_lse),
+                       args.steps, sync)
+
+    # ---- fused decode step
+    ids, sel = B.alloc_select_outputs(cfg, dev)
+    out, lse = B.alloc_attend_outputs(cfg, dev)
+
+    def step(i):
+        B.decode_step(cfg, q, ks[i % R], vs[i % R], pt, sl, summ[i % R], ws, out_ids=ids,
+                      out_sel_lse=sel, out=out, out_lse=lse)
+
+    for i in range(args.warmup):
+        step(i)
+    step_wall_us, step_ev_us = timed(step, args.steps, sync)
+
+    # ---- dense baseline on identical inputs
+    dense_us = None
+    if not args.no_dense:
+        dout, dlse = B.alloc_attend_outputs(cfg, dev)
+
+        def dstep(i):
+            B.dense_attend(cfg, q, ks[i % R], vs[i % R], pt, sl, ws, out=dout, out_lse=dlse)
+
+        for i in range(max(2, args.warmup // 2)):
+            dstep(i)
+        dense_us, _ = timed(dstep, max(4, args.steps // 4), sync)
+
+    scan_gbps = alg_scan / (scan_us * 1e-6) / 1e9
+    res = {
+        "metric": METRIC,
+        "value": round(step_wall_us, 2),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_wall_us / 1e3, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": desc, "global_batch": cfg.num_seqs,
+                   "seq_len": int(max(w.spec.seq_lens)), "parallelism": "single-gpu",
+                   "copies_rotated": R},
+        "roofline": {"bound": "hbm", "kernel": "scan_kernel (locks_score_pages)",
+                     "achieved": round(scan_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(scan_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "alg_bytes_per_launch": alg_scan, "unit_bytes": payload,
+                     "units_per_launch": complete_heads, "avg_launch_us": round(scan_us, 2)},
+        "step": {"alg_bytes": alg_step, "alg_GBps": round(alg_step / (step_wall_us * 1e-6) / 1e9, 1),
+                 "frac_of_peak": round(alg_step / (step_wall_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                 "event_us": round(step_ev_us, 2), "summary_stride_bytes": stride,
+                 "selected_pages_per_kv_head": k_sel},
+        "dense": None if dense_us is None else {
+            "us": round(dense_us, 2), "bytes": n_pages * cfg.num_kv_heads * kv_page,
+            "GBps": round(n_pages * cfg.num_kv_heads * kv_page / (dense_us * 1e-6) / 1e9, 1),
+            "speedup_sparse_vs_dense": round(dense_us / step_wall_us, 3)},
+        "build": None if build_us is None else {
+            "us": round(build_us, 1), "pages": complete_heads,
+            "read_GBps": round(complete_heads * 16 * 128 * 2 / (build_us * 1e-6) / 1e9, 1)},
+        "gen_s": round(t_gen, 1),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, cfg, sample_pages=8192)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -133,6 +133,14 @@ int locks_build_factors(const locks_cfg_t* cfg, const void* k_cache,
                         float* mu, float* basis, float* coef, float* sigma2,
                         void* stream);
 
+/* Score every complete page from its summary (Sec. 4 "Score", Eq. (1)):
+ *   out_all_lse[s][h][j] = hat s_j(q_h) for every complete page j of sequence s
+ *   (float [S][H_q][max_pages_per_seq]; entries of other pages are not written).
+ * This is the scan that locks_select runs first, exposed on its own. */
+int locks_score_pages(const locks_cfg_t* cfg, const void* q, const void* summaries,
+                      const int32_t* page_table, const int32_t* seq_lens, float* out_all_lse,
+                      void* ws, size_t ws_bytes, void* stream);
+
 /* Score every complete page from its summary and select the shared page table
  * (Sec. 4 "Score", Eq. (1) and the share-average combine; Cor. "Group-shared
  * selection"; App. E "union table"):

@@ -163,6 +163,20 @@ int locks_select(const locks_cfg_t* cfg, const void* q, const void* summaries,
                      out_all_lse, ws, static_cast<hipStream_t>(stream));
 }
 
+int locks_score_pages(const locks_cfg_t* cfg, const void* q, const void* summaries,
+                      const int32_t* page_table, const int32_t* seq_lens, float* out_all_lse,
+                      void* ws, size_t ws_bytes, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!q || !summaries || !page_table || !seq_lens || !out_all_lse) return LOCKS_E_INVAL;
+  if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
+  if (cfg->num_seqs == 0) return LOCKS_OK;
+  const WsPlan p = plan_workspace(*cfg);
+  return hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, out_all_lse,
+                                cfg->max_pages_per_seq, carve(ws, p).part, p.n_tiles,
+                                static_cast<hipStream_t>(stream)));
+}
+
 int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
                         const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
                         const int32_t* page_ids, float* out, float* out_lse, void* ws,

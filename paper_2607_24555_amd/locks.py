@@ -76,6 +76,7 @@ _SIGS = {
                                            _P, _P]),
     "locks_select": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                     _P]),
+    "locks_score_pages": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "locks_sparse_attend": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P, _P,
                                            _P, _SZ, _P]),
     "locks_dense_attend": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P, _P,
@@ -189,6 +190,18 @@ def select(cfg: Config, q, summaries, page_table, seq_lens, ws, out_ids=None, ou
                               _ptr(seq_lens), _ptr(out_ids), _ptr(out_sel_lse), _ptr(out_all_lse),
                               _ptr(ws), ws.numel(), _stream(stream)))
     return out_ids, out_sel_lse
+
+
+def score_pages(cfg: Config, q, summaries, page_table, seq_lens, ws, out_all_lse=None,
+                stream=None):
+    if out_all_lse is None:
+        out_all_lse = torch.empty(cfg.num_seqs, cfg.num_q_heads, cfg.max_pages_per_seq,
+                                  dtype=torch.float32, device=q.device)
+    c = cfg.c()
+    _check(lib().locks_score_pages(ctypes.byref(c), _ptr(q), _ptr(summaries), _ptr(page_table),
+                                   _ptr(seq_lens), _ptr(out_all_lse), _ptr(ws), ws.numel(),
+                                   _stream(stream)))
+    return out_all_lse
 
 
 def alloc_attend_outputs(cfg: Config, device="cuda"):
