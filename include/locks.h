@@ -33,9 +33,11 @@
  *    page ceil(L/16)-1 is the most recent page.  A page has a summary only once
  *    it is complete (16 tokens).
  *  - The workspace `ws` (caller-allocated, >= locks_workspace_bytes(cfg) bytes,
- *    256-byte aligned) holds per-call scratch; its content need not be
- *    initialised and is meaningless after the call.  Calls that share one
- *    workspace must be ordered on one stream.
+ *    256-byte aligned) holds per-call scratch and a few completion counters.  It
+ *    must be zero-filled once before its first use; every call leaves the
+ *    counters at zero again, so no clearing is needed between calls (the step is
+ *    graph-capturable).  Calls that share one workspace must be ordered on one
+ *    stream.
  *  - Calls with no launches (num_seqs == 0) return LOCKS_OK.
  */
 #ifndef LOCKS_H
@@ -52,7 +54,8 @@ extern "C" {
 enum {
   LOCKS_OK = 0,
   LOCKS_E_INVAL = -1,        /* bad configuration value or null pointer          */
-  LOCKS_E_UNSUPPORTED = -2,  /* head_dim != 128, page_size != 16, dtype unknown */
+  LOCKS_E_UNSUPPORTED = -2,  /* head_dim != 128, page_size != 16, G > 16,
+                                dtype unknown                                    */
   LOCKS_E_WORKSPACE = -3,    /* ws null or smaller than locks_workspace_bytes    */
   LOCKS_E_HIP = -4           /* a HIP launch failed; see locks_last_hip_error    */
 };
@@ -64,7 +67,7 @@ enum { LOCKS_BF16 = 0, LOCKS_FP32 = 1 };
  * b fixed, hence fixed shapes). */
 typedef struct locks_cfg {
   int32_t num_seqs;          /* S >= 0                                          */
-  int32_t num_q_heads;       /* H_q, a multiple of H_kv; G = H_q / H_kv <= 64   */
+  int32_t num_q_heads;       /* H_q, a multiple of H_kv; G = H_q / H_kv <= 16   */
   int32_t num_kv_heads;      /* H_kv >= 1                                       */
   int32_t head_dim;          /* d, must be 128                                  */
   int32_t page_size;         /* B, must be 16                                   */

@@ -35,16 +35,20 @@ int hip_status(hipError_t e) {
 struct Ws {
   float* s_hat;
   float2* part;
-  float* lz;
-  uint32_t* keys;
+  uint32_t* ckey;
+  int32_t* cidx;
   float* attn;
+  int* ctr_sel;
+  int* ctr_attn;
 };
 
-Ws carve(void* ws, const WsPlan& p) {
+Ws carve(void* ws, const WsPlan& p, const locks_cfg_t& c) {
   char* b = static_cast<char*>(ws);
+  int* ctr = reinterpret_cast<int*>(b + p.ctr_off);
+  const size_t nc = (size_t)c.num_seqs * c.num_kv_heads;
   return Ws{reinterpret_cast<float*>(b + p.s_hat_off), reinterpret_cast<float2*>(b + p.part_off),
-            reinterpret_cast<float*>(b + p.lz_off), reinterpret_cast<uint32_t*>(b + p.key_off),
-            reinterpret_cast<float*>(b + p.attn_off)};
+            reinterpret_cast<uint32_t*>(b + p.ckey_off), reinterpret_cast<int32_t*>(b + p.cidx_off),
+            reinterpret_cast<float*>(b + p.attn_off), ctr, ctr + nc};
 }
 
 int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
@@ -66,26 +70,19 @@ WsPlan plan_workspace(const locks_cfg_t& c) {
   WsPlan p{};
   const size_t S = (size_t)c.num_seqs, Hq = (size_t)c.num_q_heads, Hkv = (size_t)c.num_kv_heads;
   const size_t mp = (size_t)c.max_pages_per_seq;
-  p.n_tiles = (int)((mp + kScanTile - 1) / kScanTile);
   const int k = page_budget(c);
+  const size_t K = k > 2 ? (size_t)(k - 2) : 1;
+  p.n_chunks = (int)((mp + kSelChunk - 1) / kSelChunk);
   const int sparse_splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
   p.n_splits = sparse_splits > dense_splits(c) ? sparse_splits : dense_splits(c);
   size_t off = 0;
-  p.s_hat_off = off;
-  p.s_hat_bytes = S * Hq * mp * sizeof(float);
-  off = align256(off + p.s_hat_bytes);
-  p.part_off = off;
-  p.part_bytes = S * Hq * (size_t)p.n_tiles * sizeof(float2);
-  off = align256(off + p.part_bytes);
-  p.lz_off = off;
-  p.lz_bytes = S * Hq * sizeof(float);
-  off = align256(off + p.lz_bytes);
-  p.key_off = off;
-  p.key_bytes = S * Hkv * mp * sizeof(uint32_t);
-  off = align256(off + p.key_bytes);
-  p.attn_off = off;
-  p.attn_bytes = S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float);
-  off = align256(off + p.attn_bytes);
+  auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
+  p.s_hat_off = take(S * Hq * mp * sizeof(float));
+  p.part_off = take(S * Hq * (size_t)scan_blocks(c) * sizeof(float2));
+  p.ckey_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(uint32_t));
+  p.cidx_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(int32_t));
+  p.attn_off = take(S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float));
+  p.ctr_off = take(2 * S * Hkv * sizeof(int));
   p.total = off;
   return p;
 }
@@ -94,13 +91,13 @@ static int select_impl(const locks_cfg_t* c, const void* q, const void* summarie
                        const int32_t* page_table, const int32_t* seq_lens, int32_t* out_page_ids,
                        float* out_sel_lse, float* out_all_lse, void* ws, hipStream_t st) {
   const WsPlan p = plan_workspace(*c);
-  Ws w = carve(ws, p);
+  Ws w = carve(ws, p, *c);
   float* s_hat = out_all_lse ? out_all_lse : w.s_hat;
   hipError_t e = launch_scan(*c, q, summaries, page_table, seq_lens, s_hat, c->max_pages_per_seq,
-                             w.part, p.n_tiles, st);
+                             w.part, st);
   if (e != hipSuccess) return hip_status(e);
-  e = launch_select(*c, s_hat, c->max_pages_per_seq, w.part, p.n_tiles, seq_lens, w.lz, w.keys,
-                    out_page_ids, out_sel_lse, st);
+  e = launch_select(*c, seq_lens, s_hat, c->max_pages_per_seq, w.part, w.ckey, w.cidx, p.n_chunks,
+                    w.ctr_sel, out_page_ids, out_sel_lse, st);
   return hip_status(e);
 }
 
@@ -172,9 +169,9 @@ int locks_score_pages(const locks_cfg_t* cfg, const void* q, const void* summari
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
   const WsPlan p = plan_workspace(*cfg);
+  const Ws w = carve(ws, p, *cfg);
   return hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, out_all_lse,
-                                cfg->max_pages_per_seq, carve(ws, p).part, p.n_tiles,
-                                static_cast<hipStream_t>(stream)));
+                                cfg->max_pages_per_seq, w.part, static_cast<hipStream_t>(stream)));
 }
 
 int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
@@ -191,7 +188,7 @@ int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cac
   const int k = page_budget(*cfg);
   const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, page_ids,
-                                  kSparsePagesPerSplit, splits, carve(ws, p).attn, out, out_lse,
+                                  kSparsePagesPerSplit, splits, carve(ws, p, *cfg).attn, out, out_lse,
                                   static_cast<hipStream_t>(stream)));
 }
 
@@ -205,7 +202,7 @@ int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cach
   if (cfg->num_seqs == 0) return LOCKS_OK;
   const WsPlan p = plan_workspace(*cfg);
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, nullptr,
-                                  kDensePagesPerSplit, dense_splits(*cfg), carve(ws, p).attn, out,
+                                  kDensePagesPerSplit, dense_splits(*cfg), carve(ws, p, *cfg).attn, out,
                                   out_lse, static_cast<hipStream_t>(stream)));
 }
 
@@ -234,7 +231,7 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
   const int k = page_budget(*cfg);
   const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, out_page_ids,
-                                  kSparsePagesPerSplit, splits, carve(ws, p).attn, out, out_lse, st));
+                                  kSparsePagesPerSplit, splits, carve(ws, p, *cfg).attn, out, out_lse, st));
 }
 
 const char* locks_strerror(int status) {

@@ -12,7 +12,7 @@ namespace locks {
 constexpr int kPage = 16;    // B
 constexpr int kDim = 128;    // d
 constexpr int kMaxRank = 15; // r <= B - 1 (rank of centred page deviations)
-constexpr int kMaxGroup = 64;
+constexpr int kMaxGroup = 16;   // G = H_q / H_kv
 
 // Byte offsets inside one summary record for rank r (see locks_summary_stride).
 __host__ __device__ constexpr int rec_coef_off(int r) { return 64 * r; }
@@ -60,22 +60,27 @@ __device__ __forceinline__ float warp_sum(float v) {
 // ---------------------------------------------------------------- workspace plan
 
 struct WsPlan {
-  size_t s_hat_off, s_hat_bytes;      // float [S][H_q][max_pages]
-  size_t part_off, part_bytes;        // float2 [S][H_q][n_tiles]  (max, sum exp)
-  size_t lz_off, lz_bytes;            // float [S][H_q]
-  size_t key_off, key_bytes;          // uint32 [S][H_kv][max_pages]  order keys
-  size_t attn_off, attn_bytes;        // float [S][H_q][n_splits][d + 2]
+  size_t s_hat_off;   // float [S][H_q][max_pages]        page scores
+  size_t part_off;    // float2 [S][H_q][scan blocks]     (max, sum exp), log2 domain
+  size_t ckey_off;    // uint32 [S][H_kv][chunks][k-2]    per-chunk survivors (keys)
+  size_t cidx_off;    // int32  [S][H_kv][chunks][k-2]    per-chunk survivors (pages)
+  size_t attn_off;    // float [S][H_q][splits][d + 2]    split-K partials
+  size_t ctr_off;     // int [2][S][H_kv]                 last-block counters (kept zero)
   size_t total;
-  int n_tiles;                        // scan tiles per sequence
-  int n_splits;                       // attention splits per (seq, KV head)
+  int n_chunks;       // select chunks per sequence
+  int n_splits;       // attention splits per (seq, KV head)
 };
 
-constexpr int kScanTile = 64;         // pages per scan block
+constexpr int kScanPagesPerBlock = 256;  // 4 waves x 64 pages
+constexpr int kSelChunk = 1024;          // pages per select block
 constexpr int kSparsePagesPerSplit = 8;
 constexpr int kDensePagesPerSplit = 64;
 
 WsPlan plan_workspace(const locks_cfg_t& c);
 int page_budget(const locks_cfg_t& c);  // k = ceil(b / 16)
+inline int scan_blocks(const locks_cfg_t& c) {
+  return (c.max_pages_per_seq + kScanPagesPerBlock - 1) / kScanPagesPerBlock;
+}
 
 // ---------------------------------------------------------------- launchers
 // Each returns hipError_t of the launch (hipSuccess on success).
@@ -87,12 +92,12 @@ hipError_t launch_build(const locks_cfg_t& c, const void* k_cache, const int32_t
 
 hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,
                        const int32_t* page_table, const int32_t* seq_lens, float* s_hat,
-                       int s_hat_stride, float2* partials, int n_tiles, hipStream_t st);
+                       int s_hat_stride, float2* partials, hipStream_t st);
 
-hipError_t launch_select(const locks_cfg_t& c, const float* s_hat, int s_hat_stride,
-                         const float2* partials, int n_tiles, const int32_t* seq_lens,
-                         float* lz, uint32_t* keys, int32_t* out_page_ids, float* out_sel_lse,
-                         hipStream_t st);
+hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
+                         int s_hat_stride, const float2* partials, uint32_t* cand_key,
+                         int32_t* cand_idx, int n_chunks, int* counters, int32_t* out_page_ids,
+                         float* out_sel_lse, hipStream_t st);
 
 hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cache,
                          const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,

@@ -2,12 +2,9 @@
 // (sequence, KV head) and every query head g of its group,
 //   hat s_j(q_g) = log sum_i exp[(q_g^T mu_j + (V_j^T q_g)^T c_i) / sqrt(d)],
 // read from the page's stored record (int4 basis, int8 coefficients and centroid,
-// float16 scales).  Also writes, per block of kScanTile pages and per query head,
-// the partial (max, sum exp) that the combine step needs for the share normaliser.
-//
-// Mapping: one 64-lane wave per block, one page per lane, the group's queries in
-// LDS (broadcast reads).  Integer codes are accumulated against q in fp32 and the
-// scale is applied once per dot product, so the dequantisation is exact.
+// float16 scales).  Every block also writes, per query head, the partial
+// (max, sum 2^x) of its pages' scores in the log2 domain; the select kernel
+// reduces them into log Z_g = log sum_j exp(hat s_j(q_g)).
 #include "locks_internal.h"
 
 namespace locks {
@@ -20,108 +17,6 @@ __device__ __forceinline__ float load_q<float>(const float* q, size_t i) { retur
 template <>
 __device__ __forceinline__ float load_q<uint16_t>(const uint16_t* q, size_t i) {
   return bf16_bits_to_f32(q[i]);
-}
-
-__device__ __forceinline__ float f16_bits_to_f32(uint16_t b) {
-  _Float16 h;
-  __builtin_memcpy(&h, &b, 2);
-  return (float)h;
-}
-
-template <typename QT, int R>
-__global__ __launch_bounds__(64) void scan_kernel(
-    int H_q, int H_kv, int max_pages, const QT* __restrict__ q,
-    const uint8_t* __restrict__ summaries, const int32_t* __restrict__ page_table,
-    const int32_t* __restrict__ seq_lens, float* __restrict__ s_hat, int s_hat_stride,
-    float2* __restrict__ partials, int n_tiles) {
-  constexpr int stride = rec_stride(R);
-  __shared__ float sq[kMaxGroup][kDim];
-  const int tile = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
-  const int lane = threadIdx.x;
-  const int G = H_q / H_kv;
-  const int n_c = seq_lens[s] / kPage;
-  if (tile * kScanTile >= n_c) {
-    // no complete page in this tile: an empty partial keeps the combine exact
-    if (tile < n_tiles)
-      for (int g = lane; g < G; g += 64)
-        partials[((long)s * H_q + h * G + g) * n_tiles + tile] = make_float2(-INFINITY, 0.0f);
-    return;
-  }
-  for (int e = lane; e < G * kDim; e += 64)
-    sq[e / kDim][e % kDim] = load_q(q, ((long)s * H_q + h * G) * kDim + e);
-  __syncthreads();
-
-  const int j = tile * kScanTile + lane;
-  const bool valid = j < n_c;
-  const long blk = valid ? (long)page_table[(long)s * max_pages + j] : 0;
-  const uint8_t* rec = summaries + (blk * H_kv + h) * (long)stride;
-
-  // scales and coefficient codes of this lane's page
-  const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + rec_scale_off(R));
-  float vs[R];
-#pragma unroll
-  for (int l = 0; l < R; ++l) vs[l] = f16_bits_to_f32(sc[l]);
-  const float ms = f16_bits_to_f32(sc[R + kPage]);
-  constexpr float kLog2e = 1.4426950408889634f;
-  const float zscale = kLog2e / sqrtf((float)kDim);
-
-  for (int g = 0; g < G; ++g) {
-    float a = 0.0f;
-    float p[R];
-#pragma unroll
-    for (int l = 0; l < R; ++l) p[l] = 0.0f;
-    for (int c0 = 0; c0 < kDim; c0 += 8) {
-      const uint2 mb = *reinterpret_cast<const uint2*>(rec + rec_mu_off(R) + c0);
-      float qq[8];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) qq[t] = sq[g][c0 + t];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const uint32_t w = t < 4 ? mb.x : mb.y;
-        const int code = (int)((w >> (8 * (t & 3))) & 0xffu) - 128;
-        a = fmaf((float)code, qq[t], a);
-      }
-#pragma unroll
-      for (int l = 0; l < R; ++l) {
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(rec + 64 * l + c0 / 2);
-        float acc = p[l];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          const int code = (int)((w >> (4 * t)) & 0xfu) - 8;
-          acc = fmaf((float)code, qq[t], acc);
-        }
-        p[l] = acc;
-      }
-    }
-    a *= ms;
-#pragma unroll
-    for (int l = 0; l < R; ++l) p[l] *= vs[l];
-    // 16 reconstructed logits (log2 domain) and their log-sum-exp
-    float z[kPage];
-    float zmax = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < kPage; ++i) {
-      float dot = 0.0f;
-#pragma unroll
-      for (int l = 0; l < R; ++l) {
-        const int code = (int)rec[rec_coef_off(R) + i * R + l] - 128;
-        dot = fmaf((float)code, p[l], dot);
-      }
-      const float cs = f16_bits_to_f32(sc[R + i]);
-      z[i] = fmaf(cs, dot, a) * zscale;
-      zmax = fmaxf(zmax, z[i]);
-    }
-    float sum = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kPage; ++i) sum += exp2f(z[i] - zmax);
-    const float shat = (zmax + log2f(sum)) * 0.69314718055994531f;
-    const long row = (long)s * H_q + h * G + g;
-    if (valid) s_hat[row * s_hat_stride + j] = shat;
-    // tile partial of the normaliser sum_j exp(hat s_j)
-    const float m = warp_max(valid ? shat : -INFINITY);
-    const float l = warp_sum(valid ? __expf(shat - m) : 0.0f);
-    if (lane == 0) partials[row * n_tiles + tile] = make_float2(m, l);
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -191,12 +86,62 @@ __device__ __forceinline__ float lds_f16(const uint8_t* p) {
   return (float)*reinterpret_cast<const _Float16*>(p);
 }
 
+// Reduction over the four lanes {l, l^16, l^32, l^48} with two VALU lane swaps.
+__device__ __forceinline__ float red4_max(float v) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float red4_sum(float v) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int R>
+struct TileRegs {
+  uint4 vb[Geom<R>::kSets];       // basis slices, MFMA A layout
+  uint4 tl[Geom<R>::kTailLoads];  // record tails, 16-byte chunks
+};
+
+// Issue the loads of one 16-page tile (no wait).
+template <int R>
+__device__ __forceinline__ void issue_tile(TileRegs<R>& T, const uint8_t* __restrict__ summaries,
+                                           const int32_t* __restrict__ pt_row, int page0, int n_c,
+                                           int H_kv, int h, int lane) {
+  using Gm = Geom<R>;
+  const int col = lane & 15, grp = lane >> 4;
+  const int my_blk = (lane < 16 && page0 + lane < n_c) ? pt_row[page0 + lane] : -1;
+#pragma unroll
+  for (int st = 0; st < Gm::kSets; ++st) {
+    const int pp = col / R, l = col % R;
+    const int page = st * Gm::kPPS + pp;
+    const int blk = __shfl(my_blk, page < 16 ? page : 0, 64);
+    const bool ok = col < Gm::kPPS * R && page < 16 && blk >= 0;
+    T.vb[st] = ok ? *reinterpret_cast<const uint4*>(summaries + ((long)blk * H_kv + h) * Gm::kStride +
+                                                    64 * l + 16 * grp)
+                  : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < Gm::kTailLoads; ++u) {
+    const int c = lane + 64 * u;
+    const int page = c / Gm::kTailCh, off = (c % Gm::kTailCh) * 16;
+    const int blk = __shfl(my_blk, page < 16 ? page : 0, 64);
+    T.tl[u] = (c < 16 * Gm::kTailCh && blk >= 0)
+                  ? *reinterpret_cast<const uint4*>(summaries + ((long)blk * H_kv + h) * Gm::kStride +
+                                                    64 * R + off)
+                  : make_uint4(0, 0, 0, 0);
+  }
+}
+
 template <typename QT, int R>
 __global__ __launch_bounds__(256) void scan_mfma_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q,
     const uint8_t* __restrict__ summaries, const int32_t* __restrict__ page_table,
     const int32_t* __restrict__ seq_lens, float* __restrict__ s_hat, int s_hat_stride,
-    float2* __restrict__ partials, int n_parts) {
+    float2* __restrict__ partials) {
   using Gm = Geom<R>;
   constexpr bool kSplitQ = sizeof(QT) == 4;  // fp32 queries: f16 hi + lo
   __shared__ __align__(16) uint8_t sTail[4][16][Gm::kTail];
@@ -211,10 +156,13 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
   const int n_c = seq_lens[s] / kPage;
   const int pg = blockIdx.x * 4 + wave;  // 64-page group of this wave
   const long row0 = (long)s * H_q + (long)h * G;
-  if (pg * 64 >= n_c) {
-    if (pg < n_parts && lane < G) partials[(row0 + lane) * n_parts + pg] = make_float2(-INFINITY, 0.0f);
-    return;
-  }
+  const int32_t* pt_row = page_table + (long)s * max_pages;
+  const int n_parts = gridDim.x;
+  float run_m = -INFINITY, run_s = 0.0f;  // running normaliser, log2 domain
+  const int npack = 16 / G;                // pages per stage-2 pass
+  if (pg * 64 < n_c) {
+  TileRegs<R> buf[2];
+  issue_tile<R>(buf[0], summaries, pt_row, pg * 64, n_c, H_kv, h, lane);
 
   // ---- B operands: column = query head, K permuted to match the decoders
   constexpr int kPerm[8] = {0, 4, 1, 5, 2, 6, 3, 7};
@@ -249,151 +197,416 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
       bml[ks][j] = (_Float16)(b - (float)bh);
     }
 
-  constexpr float kLog2e = 1.4426950408889634f;
-  const float c0 = kLog2e * 0.08838834764831845f;  // log2(e) / sqrt(128)
-  const int npack = 16 / G;                         // pages per stage-2 pass
+  constexpr float kLn2 = 0.69314718055994531f;
+  const float c0 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
   const int kpass = npack * R;
   const int ksteps = (kpass + 3) / 4;
   const int pcol = col / G, gcol = col % G;
   const bool colvalid = pcol < npack;
-  float run_m = -INFINITY, run_s = 0.0f;
 
+#pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int page0 = (pg * 4 + t) * 16;
-    if (page0 >= n_c) break;
-    const int my_blk = (lane < 16 && page0 + lane < n_c)
-                           ? page_table[(long)s * max_pages + page0 + lane] : -1;
-    // ---- issue the loads: basis slices into registers, record tails into LDS
-    uint4 vb[Gm::kSets];
+    if (page0 < n_c) {
+      TileRegs<R>& cur = buf[t & 1];
+      if (t + 1 < 4 && page0 + 16 < n_c)
+        issue_tile<R>(buf[(t + 1) & 1], summaries, pt_row, page0 + 16, n_c, H_kv, h, lane);
 #pragma unroll
-    for (int st = 0; st < Gm::kSets; ++st) {
-      const int pp = col / R, l = col % R;
-      const int page = st * Gm::kPPS + pp;
-      const int blk = __shfl(my_blk, page < 16 ? page : 0, 64);
-      const bool ok = col < Gm::kPPS * R && page < 16 && blk >= 0;
-      vb[st] = ok ? *reinterpret_cast<const uint4*>(summaries + ((long)blk * H_kv + h) * Gm::kStride +
-                                                    64 * l + 16 * grp)
-                  : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int u = 0; u < Gm::kTailLoads; ++u) {
-      const int c = lane + 64 * u;
-      const int page = c / Gm::kTailCh, off = (c % Gm::kTailCh) * 16;
-      const int blk = __shfl(my_blk, page < 16 ? page : 0, 64);
-      if (c < 16 * Gm::kTailCh) {
-        const uint4 v = blk >= 0 ? *reinterpret_cast<const uint4*>(
-                                       summaries + ((long)blk * H_kv + h) * Gm::kStride + 64 * R + off)
-                                 : make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4*>(&sTail[wave][page][off]) = v;
+      for (int u = 0; u < Gm::kTailLoads; ++u) {
+        const int c = lane + 64 * u;
+        if (c < 16 * Gm::kTailCh)
+          *reinterpret_cast<uint4*>(&sTail[wave][c / Gm::kTailCh][(c % Gm::kTailCh) * 16]) = cur.tl[u];
       }
-    }
-    __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_wave_barrier();
 
-    // ---- stage 1: p = V^T q (scaled by the basis column scales)
+      // ---- stage 1: p = V^T q (scaled by the basis column scales)
 #pragma unroll
-    for (int st = 0; st < Gm::kSets; ++st) {
-      f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-      const uint32_t w[4] = {vb[st].x, vb[st].y, vb[st].z, vb[st].w};
+      for (int st = 0; st < Gm::kSets; ++st) {
+        f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        const uint32_t w[4] = {cur.vb[st].x, cur.vb[st].y, cur.vb[st].z, cur.vb[st].w};
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const h8 a = nib8_to_h8(w[ks]);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bv[ks], acc, 0, 0, 0);
-        if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bvl[ks], acc, 0, 0, 0);
+        for (int ks = 0; ks < 4; ++ks) {
+          const h8 a = nib8_to_h8(w[ks]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bv[ks], acc, 0, 0, 0);
+          if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bvl[ks], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int m = 4 * grp + j;
+          const int pp = m / R, l = m % R;
+          const int page = st * Gm::kPPS + pp;
+          if (m < Gm::kPPS * R && page < 16 && col < G)
+            sP[wave][page][l][col] = acc[j] * inv_qs * lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
+        }
       }
+      // ---- centroid term a = mu^T q, one page per row
+      {
+        const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][col][Gm::kMu + 32 * grp]);
+        const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][col][Gm::kMu + 32 * grp + 16]);
+        const uint32_t w[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+        f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int m = 4 * grp + j;
-        const int pp = m / R, l = m % R;
-        const int page = st * Gm::kPPS + pp;
-        if (m < Gm::kPPS * R && page < 16 && col < G)
-          sP[wave][page][l][col] = acc[j] * inv_qs * lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
-      }
-    }
-    // ---- centroid term a = mu^T q, one page per row
-    {
-      const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][col][Gm::kMu + 32 * grp]);
-      const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][col][Gm::kMu + 32 * grp + 16]);
-      const uint32_t w[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
-      f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int ks = 0; ks < 4; ++ks) {
+          const h8 a = byte8_to_h8(w[2 * ks], w[2 * ks + 1]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bm[ks], acc, 0, 0, 0);
+          if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bml[ks], acc, 0, 0, 0);
+        }
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const h8 a = byte8_to_h8(w[2 * ks], w[2 * ks + 1]);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bm[ks], acc, 0, 0, 0);
-        if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bml[ks], acc, 0, 0, 0);
+        for (int j = 0; j < 4; ++j) {
+          const int page = 4 * grp + j;
+          if (col < G)
+            sA[wave][page][col] =
+                acc[j] * inv_qs * c0 * lds_f16(&sTail[wave][page][Gm::kSc + 2 * (R + 16)]);
+        }
       }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int page = 4 * grp + j;
-        if (col < G)
-          sA[wave][page][col] = acc[j] * inv_qs * lds_f16(&sTail[wave][page][Gm::kSc + 2 * (R + 16)]);
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_wave_barrier();
 
-    // ---- stage 2: 16 logits per (page, head), npack pages per pass
-    for (int p0 = 0; p0 < 16; p0 += npack) {
-      f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-      for (int kstep = 0; kstep < ksteps; ++kstep) {
-        const int k = 4 * kstep + grp;
-        const int ppk = k / R, l = k % R;
-        const int pk = p0 + ppk;
-        const bool kv = k < kpass && pk < 16;
-        const float a = kv ? (float)((int)sTail[wave][pk][col * R + l] - 128) : 0.0f;
-        const float b = (kv && colvalid && ppk == pcol) ? sP[wave][pk][l][gcol] : 0.0f;
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+      // ---- stage 2: 16 logits per (page, head), npack pages per pass
+      for (int p0 = 0; p0 < 16; p0 += npack) {
+        f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int kstep = 0; kstep < ksteps; ++kstep) {
+          const int k = 4 * kstep + grp;
+          const int ppk = k / R, l = k % R;
+          const int pk = p0 + ppk;
+          const bool kv = k < kpass && pk < 16;
+          const float a = kv ? (float)((int)sTail[wave][pk][col * R + l] - 128) : 0.0f;
+          const float b = (kv && colvalid && ppk == pcol) ? sP[wave][pk][l][gcol] : 0.0f;
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+        }
+        const int page = p0 + pcol;
+        const bool live = colvalid && page < 16 && page0 + page < n_c;
+        const int pl = page < 16 ? page : 15;
+        const float av = sA[wave][pl][gcol];
+        const uint2 csw = *reinterpret_cast<const uint2*>(&sTail[wave][pl][Gm::kSc + 2 * (R + 4 * grp)]);
+        const h2 cs01 = as_h2(csw.x), cs23 = as_h2(csw.y);
+        float z[4];
+        z[0] = fmaf((float)cs01.x * c0, acc[0], av);
+        z[1] = fmaf((float)cs01.y * c0, acc[1], av);
+        z[2] = fmaf((float)cs23.x * c0, acc[2], av);
+        z[3] = fmaf((float)cs23.y * c0, acc[3], av);
+        float mx = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+        mx = red4_max(mx);
+        float sm = __builtin_amdgcn_exp2f(z[0] - mx) + __builtin_amdgcn_exp2f(z[1] - mx) +
+                   __builtin_amdgcn_exp2f(z[2] - mx) + __builtin_amdgcn_exp2f(z[3] - mx);
+        sm = red4_sum(sm);
+        const float s2 = mx + __builtin_amdgcn_logf(sm);  // log2-domain page score
+        if (live) {
+          if (grp == 0) s_hat[(row0 + gcol) * s_hat_stride + page0 + page] = s2 * kLn2;
+          const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+          if (s2 > run_m) { run_s = fmaf(run_s, e, 1.0f); run_m = s2; }
+          else run_s += e;
+        }
       }
-      const int page = p0 + pcol;
-      const bool live = colvalid && page < 16 && page0 + page < n_c;
-      const int pl = page < 16 ? page : 15;
-      const float av = sA[wave][pl][gcol] * c0;
-      float z[4];
-      float mx = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float cs = lds_f16(&sTail[wave][pl][Gm::kSc + 2 * (R + 4 * grp + j)]);
-        z[j] = fmaf(cs * c0, acc[j], av);
-        mx = fmaxf(mx, z[j]);
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      float sm = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sm += exp2f(z[j] - mx);
-      sm += __shfl_xor(sm, 16, 64);
-      sm += __shfl_xor(sm, 32, 64);
-      const float shat = (mx + log2f(sm)) * 0.69314718055994531f;
-      if (live) {
-        if (grp == 0) s_hat[(row0 + gcol) * s_hat_stride + page0 + page] = shat;
-        const float nm = fmaxf(run_m, shat);
-        run_s = run_s * exp2f((run_m - nm) * kLog2e) + exp2f((shat - nm) * kLog2e);
-        run_m = nm;
-      }
+      __builtin_amdgcn_wave_barrier();
     }
-    __builtin_amdgcn_wave_barrier();
   }
-  // ---- per-head partial (max, sum exp) of this wave's 64 pages
+  }  // pages of this wave
+  // ---- block partial (max, sum exp) per head over its 256 pages (log2 domain)
   if (lane < 16) sRun[wave][lane] = make_float2(run_m, run_s);
-  __builtin_amdgcn_wave_barrier();
-  if (lane < G) {
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int g = threadIdx.x;
     float m = -INFINITY, l = 0.0f;
-    for (int c = lane; c < npack * G; c += G) m = fmaxf(m, sRun[wave][c].x);
+    for (int w = 0; w < 4; ++w)
+      for (int c = g; c < npack * G; c += G) m = fmaxf(m, sRun[w][c].x);
     if (m > -INFINITY)
-      for (int c = lane; c < npack * G; c += G) {
-        const float2 v = sRun[wave][c];
-        if (v.y > 0.0f) l += v.y * exp2f((v.x - m) * kLog2e);
+      for (int w = 0; w < 4; ++w)
+        for (int c = g; c < npack * G; c += G) {
+          const float2 v = sRun[w][c];
+          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+        }
+    partials[(row0 + g) * n_parts + blockIdx.x] = make_float2(m, l);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fast path for r in {2, 4, 8} and G in {4, 16} (G = 16 / NPACK).
+//
+// Differences from the generic kernel above:
+//  * stage 1 runs on 16x16x64 int8 MFMA.  A basis nibble becomes an int8 with
+//    three ops per eight codes; each query head is written as a 22-bit fixed-point
+//    integer (power-of-two scale per head) split into three signed 8-bit digits,
+//    one MFMA chain per digit.  The excess-8 bias of the codes is removed exactly
+//    by starting each integer accumulator at -8 * sum(digit).  Dot products of
+//    codes and queries are therefore exact integers.
+//  * stage-1 rows are assigned so that output register j of lane group grp holds
+//    slot 4j + grp = (page, basis column); those registers are directly the B
+//    operand of stage 2 (block-diagonal over the pages of a pass), so the
+//    projections never go through LDS.
+//  * every load is unconditional (clamped to a valid record) and 32-bit offset.
+// ---------------------------------------------------------------------------
+
+typedef int i4v __attribute__((ext_vector_type(4)));
+
+template <int R>
+struct FastGeom {
+  static constexpr int kPPS = 16 / R;                 // pages per stage-1 set
+  static constexpr int kSets = R;                     // 16 pages x R slots / 16 rows
+  static constexpr int kStride = rec_stride(R);
+  static constexpr int kTail = kStride - 64 * R;
+  static constexpr int kTailCh = kTail / 16;
+  static constexpr int kTailLoads = (16 * kTailCh + 63) / 64;
+  static constexpr int kMu = 16 * R;
+  static constexpr int kSc = 16 * R + kDim;
+};
+
+template <int R>
+struct FastRegs {
+  uint4 vb[FastGeom<R>::kSets];
+  uint4 tl[FastGeom<R>::kTailLoads];
+};
+
+template <int R>
+__device__ __forceinline__ void fast_issue(FastRegs<R>& T, const uint8_t* __restrict__ summ,
+                                           const int32_t* __restrict__ pt_row, int page0, int n_c,
+                                           int H_kv, int h, int lane) {
+  using Gm = FastGeom<R>;
+  const int col = lane & 15, grp = lane >> 4;
+  const int qs = 4 * (col & 3) + (col >> 2);  // stage-1 slot of A row `col`
+  const int a_pp = qs / R, a_l = qs % R;
+  // block of page0 + lane (lanes >= 16 and pages past the end reuse page0's block)
+  const int pl = page0 + (lane & 15);
+  const int my_blk = pt_row[pl < n_c ? pl : page0];
+#pragma unroll
+  for (int st = 0; st < Gm::kSets; ++st) {
+    const int blk = __shfl(my_blk, st * Gm::kPPS + a_pp, 64);
+    const uint32_t off = (uint32_t)(blk * H_kv + h) * (uint32_t)Gm::kStride + 64u * a_l + 16u * grp;
+    T.vb[st] = *reinterpret_cast<const uint4*>(summ + off);
+  }
+#pragma unroll
+  for (int u = 0; u < Gm::kTailLoads; ++u) {
+    int c = lane + 64 * u;
+    c = c < 16 * Gm::kTailCh ? c : 16 * Gm::kTailCh - 1;
+    const int page = c / Gm::kTailCh, o = (c % Gm::kTailCh) * 16;
+    const int blk = __shfl(my_blk, page, 64);
+    const uint32_t off = (uint32_t)(blk * H_kv + h) * (uint32_t)Gm::kStride + 64u * R + o;
+    T.tl[u] = *reinterpret_cast<const uint4*>(summ + off);
+  }
+}
+
+__device__ __forceinline__ int sbyte(int x) { return (int)(int8_t)(x & 0xff); }
+
+template <typename QT, int R, int NPACK>
+__global__ __launch_bounds__(256) void scan_fast_kernel(
+    int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
+    float* __restrict__ s_hat, int s_hat_stride, float2* __restrict__ partials) {
+  using Gm = FastGeom<R>;
+  constexpr int G = 16 / NPACK;
+  constexpr int kPasses = 16 / NPACK;
+  constexpr int kKS = (NPACK * R) / 4 > 0 ? (NPACK * R) / 4 : 1;  // k-steps per pass
+  __shared__ __align__(16) uint8_t sTail[4][16][Gm::kTail];
+  __shared__ float sA[4][16][16];
+  __shared__ float2 sRun[4][16];
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int h = blockIdx.y, s = blockIdx.z;
+  const int n_c = seq_lens[s] / kPage;
+  const int pg = blockIdx.x * 4 + wave;
+  const long row0 = (long)s * H_q + (long)h * G;
+  const int32_t* pt_row = page_table + (long)s * max_pages;
+  const int gcol = col % G, pcol = col / G;
+  constexpr float c0 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
+  float run_m = -INFINITY, run_s = 0.0f;
+
+  if (pg * 64 < n_c) {
+    FastRegs<R> buf[2];
+    fast_issue<R>(buf[0], summ, pt_row, pg * 64, n_c, H_kv, h, lane);
+
+    // ---- query digits: lane (head gcol, K slice grp); K order matches the decoders
+    // element e of MFMA half hh <-> d = 32 grp + 16 hh + perm16[e]
+    constexpr int kPerm16[16] = {0, 2, 4, 6, 1, 3, 5, 7, 8, 10, 12, 14, 9, 11, 13, 15};
+    float qf[32];
+    float qmax = 0.0f;
+    {
+      const QT* qrow = q + (row0 + gcol) * kDim + 32 * grp;
+#pragma unroll
+      for (int c = 0; c < 32; ++c) {
+        qf[c] = load_q(qrow, c);
+        qmax = fmaxf(qmax, fabsf(qf[c]));
       }
-    partials[(row0 + lane) * n_parts + pg] = make_float2(m, l);
+    }
+    qmax = red4_max(qmax);
+    int ex = 0;
+    (void)frexpf(qmax, &ex);                 // qmax < 2^ex
+    const float qscale = ldexpf(1.0f, 22 - ex);
+    const float inv_scale = ldexpf(1.0f, ex - 22) * c0;
+    i4v bd[3][2];
+    float bsum[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int dw = 0; dw < 4; ++dw) {
+        uint32_t w0 = 0, w1 = 0, w2 = 0;
+#pragma unroll
+        for (int bb = 0; bb < 4; ++bb) {
+          const int e = 4 * dw + bb;
+          const int Q = (qmax > 0.0f) ? (int)rintf(qf[16 * hh + kPerm16[e]] * qscale) : 0;
+          const int d2 = sbyte(Q);
+          const int q1 = (Q - d2) >> 8;
+          const int d1 = sbyte(q1);
+          const int d0 = (q1 - d1) >> 8;
+          bsum[0] += (float)d0;
+          bsum[1] += (float)d1;
+          bsum[2] += (float)d2;
+          w0 |= (uint32_t)(d0 & 0xff) << (8 * bb);
+          w1 |= (uint32_t)(d1 & 0xff) << (8 * bb);
+          w2 |= (uint32_t)(d2 & 0xff) << (8 * bb);
+        }
+        bd[0][hh][dw] = (int)w0;
+        bd[1][hh][dw] = (int)w1;
+        bd[2][hh][dw] = (int)w2;
+      }
+    int bias[3];
+#pragma unroll
+    for (int t = 0; t < 3; ++t) bias[t] = -8 * (int)red4_sum(bsum[t]);
+
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int page0 = (pg * 4 + t) * 16;
+      if (page0 < n_c) {
+        FastRegs<R>& cur = buf[t & 1];
+        if (t + 1 < 4 && page0 + 16 < n_c)
+          fast_issue<R>(buf[(t + 1) & 1], summ, pt_row, page0 + 16, n_c, H_kv, h, lane);
+#pragma unroll
+        for (int u = 0; u < Gm::kTailLoads; ++u) {
+          const int c = lane + 64 * u;
+          if (c < 16 * Gm::kTailCh)
+            *reinterpret_cast<uint4*>(&sTail[wave][c / Gm::kTailCh][(c % Gm::kTailCh) * 16]) = cur.tl[u];
+        }
+        __builtin_amdgcn_wave_barrier();
+
+        // ---- stage 1 (int8 MFMA): projections of every (page, basis column) slot
+        float vals[4 * Gm::kSets];
+#pragma unroll
+        for (int st = 0; st < Gm::kSets; ++st) {
+          const uint32_t w[4] = {cur.vb[st].x, cur.vb[st].y, cur.vb[st].z, cur.vb[st].w};
+          i4v acc[3];
+#pragma unroll
+          for (int d = 0; d < 3; ++d) acc[d] = i4v{bias[d], bias[d], bias[d], bias[d]};
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
+            const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
+                           (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+#pragma unroll
+            for (int d = 0; d < 3; ++d)
+              acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bd[d][hh], acc[d], 0, 0, 0);
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int slot = 4 * j + grp;
+            const int page = st * Gm::kPPS + slot / R, l = slot % R;
+            const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
+            const float v = fmaf((float)acc[0][j], 65536.0f, fmaf((float)acc[1][j], 256.0f, (float)acc[2][j]));
+            vals[4 * st + j] = v * (vs * inv_scale);
+          }
+        }
+        // ---- centroid term (int8 MFMA, one page per row): sA[page][col]
+        {
+          const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][col][Gm::kMu + 32 * grp]);
+          const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][col][Gm::kMu + 32 * grp + 16]);
+          const uint32_t mw[8] = {m0.x ^ 0x80808080u, m0.y ^ 0x80808080u, m0.z ^ 0x80808080u,
+                                  m0.w ^ 0x80808080u, m1.x ^ 0x80808080u, m1.y ^ 0x80808080u,
+                                  m1.z ^ 0x80808080u, m1.w ^ 0x80808080u};
+          i4v acc[3];
+#pragma unroll
+          for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
+            const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
+                           (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
+                           (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
+                           (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
+#pragma unroll
+            for (int d = 0; d < 3; ++d)
+              acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bd[d][hh], acc[d], 0, 0, 0);
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int page = 4 * grp + j;
+            const float ms = lds_f16(&sTail[wave][page][Gm::kSc + 2 * (R + 16)]);
+            const float v = fmaf((float)acc[0][j], 65536.0f, fmaf((float)acc[1][j], 256.0f, (float)acc[2][j]));
+            sA[wave][page][col] = v * (ms * inv_scale);
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+
+        // ---- stage 2 (fp32 MFMA): 16 logits per (page, head), NPACK pages per pass
+#pragma unroll
+        for (int ps = 0; ps < kPasses; ++ps) {
+          const int pcpage = ps * NPACK + pcol;  // page of this lane's column
+          f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int kk = 0; kk < kKS; ++kk) {
+            const int rho = (NPACK * R >= 4) ? ps * kKS + kk : (ps * NPACK * R) / 4;
+            const int st = rho / 4, j = rho % 4;
+            const int slot = 4 * j + grp;
+            const int pk = st * Gm::kPPS + slot / R, l = slot % R;
+            const float a = (float)((int)sTail[wave][pk][col * R + l] - 128);
+            const float b = (pk == pcpage) ? vals[rho] : 0.0f;
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+          }
+          const float av = sA[wave][pcpage][col];
+          const uint2 csw = *reinterpret_cast<const uint2*>(&sTail[wave][pcpage][Gm::kSc + 2 * (R + 4 * grp)]);
+          const h2 cs01 = as_h2(csw.x), cs23 = as_h2(csw.y);
+          float z0 = fmaf((float)cs01.x, acc[0], av), z1 = fmaf((float)cs01.y, acc[1], av);
+          float z2 = fmaf((float)cs23.x, acc[2], av), z3 = fmaf((float)cs23.y, acc[3], av);
+          float mx = fmaxf(fmaxf(z0, z1), fmaxf(z2, z3));
+          mx = red4_max(mx);
+          float sm = __builtin_amdgcn_exp2f(z0 - mx) + __builtin_amdgcn_exp2f(z1 - mx) +
+                     __builtin_amdgcn_exp2f(z2 - mx) + __builtin_amdgcn_exp2f(z3 - mx);
+          sm = red4_sum(sm);
+          const float s2 = mx + __builtin_amdgcn_logf(sm);
+          const bool live = page0 + pcpage < n_c;
+          if (live && grp == 0) s_hat[(row0 + gcol) * s_hat_stride + page0 + pcpage] = s2 * 0.69314718055994531f;
+          const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+          const bool up = s2 > run_m;
+          const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
+          run_s = live ? ns : run_s;
+          run_m = (live && up) ? s2 : run_m;
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
+  }
+  // ---- block partial (max, sum exp) per head over its 256 pages, log2 domain
+  if (lane < 16) sRun[wave][lane] = make_float2(run_m, run_s);
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int g = threadIdx.x;
+    float m = -INFINITY, l = 0.0f;
+    for (int w = 0; w < 4; ++w)
+      for (int c = g; c < 16; c += G) m = fmaxf(m, sRun[w][c].x);
+    if (m > -INFINITY)
+      for (int w = 0; w < 4; ++w)
+        for (int c = g; c < 16; c += G) {
+          const float2 v = sRun[w][c];
+          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+        }
+    partials[(row0 + g) * gridDim.x + blockIdx.x] = make_float2(m, l);
   }
 }
 
 template <typename QT>
-hipError_t dispatch_mfma(int r, dim3 grid, hipStream_t st, int H_q, int H_kv, int max_pages,
+hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H_kv, int max_pages,
                          const QT* q, const uint8_t* sum, const int32_t* pt, const int32_t* sl,
-                         float* s_hat, int s_hat_stride, float2* part, int n_parts) {
+                         float* s_hat, int s_hat_stride, float2* part) {
+#define LOCKS_SCAN_FAST(RR, NP)                                                              \
+  if (r == RR && G == 16 / NP) {                                                            \
+    hipLaunchKernelGGL((scan_fast_kernel<QT, RR, NP>), grid, dim3(256), 0, st, H_q, H_kv,   \
+                       max_pages, q, sum, pt, sl, s_hat, s_hat_stride, part);               \
+    return hipGetLastError();                                                               \
+  }
+  LOCKS_SCAN_FAST(8, 1) LOCKS_SCAN_FAST(8, 4) LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(4, 4)
+  LOCKS_SCAN_FAST(2, 1) LOCKS_SCAN_FAST(2, 4)
+#undef LOCKS_SCAN_FAST
 #define LOCKS_SCAN_MFMA_CASE(RR)                                                             \
   case RR:                                                                                  \
     hipLaunchKernelGGL((scan_mfma_kernel<QT, RR>), grid, dim3(256), 0, st, H_q, H_kv,       \
-                       max_pages, q, sum, pt, sl, s_hat, s_hat_stride, part, n_parts);      \
+                       max_pages, q, sum, pt, sl, s_hat, s_hat_stride, part);               \
     break;
   switch (r) {
     LOCKS_SCAN_MFMA_CASE(1) LOCKS_SCAN_MFMA_CASE(2) LOCKS_SCAN_MFMA_CASE(3)
@@ -408,51 +621,20 @@ hipError_t dispatch_mfma(int r, dim3 grid, hipStream_t st, int H_q, int H_kv, in
   return hipGetLastError();
 }
 
-template <typename QT>
-hipError_t dispatch(int r, dim3 grid, hipStream_t st, int H_q, int H_kv, int max_pages,
-                    const QT* q, const uint8_t* sum, const int32_t* pt, const int32_t* sl,
-                    float* s_hat, int s_hat_stride, float2* part, int n_tiles) {
-#define LOCKS_SCAN_CASE(RR)                                                                   \
-  case RR:                                                                                    \
-    hipLaunchKernelGGL((scan_kernel<QT, RR>), grid, dim3(64), 0, st, H_q, H_kv, max_pages, q, \
-                       sum, pt, sl, s_hat, s_hat_stride, part, n_tiles);                      \
-    break;
-  switch (r) {
-    LOCKS_SCAN_CASE(1) LOCKS_SCAN_CASE(2) LOCKS_SCAN_CASE(3) LOCKS_SCAN_CASE(4)
-    LOCKS_SCAN_CASE(5) LOCKS_SCAN_CASE(6) LOCKS_SCAN_CASE(7) LOCKS_SCAN_CASE(8)
-    LOCKS_SCAN_CASE(9) LOCKS_SCAN_CASE(10) LOCKS_SCAN_CASE(11) LOCKS_SCAN_CASE(12)
-    LOCKS_SCAN_CASE(13) LOCKS_SCAN_CASE(14) LOCKS_SCAN_CASE(15)
-    default:
-      return hipErrorInvalidValue;
-  }
-#undef LOCKS_SCAN_CASE
-  return hipGetLastError();
-}
-
 }  // namespace
 
 hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,
                        const int32_t* page_table, const int32_t* seq_lens, float* s_hat,
-                       int s_hat_stride, float2* partials, int n_tiles, hipStream_t st) {
+                       int s_hat_stride, float2* partials, hipStream_t st) {
+  const dim3 grid(scan_blocks(c), c.num_kv_heads, c.num_seqs);
   const int G = c.num_q_heads / c.num_kv_heads;
-  if (G <= 16) {
-    const dim3 grid((n_tiles + 3) / 4, c.num_kv_heads, c.num_seqs);
-    if (c.q_dtype == LOCKS_BF16)
-      return dispatch_mfma(c.rank, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                           static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(summaries),
-                           page_table, seq_lens, s_hat, s_hat_stride, partials, n_tiles);
-    return dispatch_mfma(c.rank, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                         static_cast<const float*>(q), static_cast<const uint8_t*>(summaries),
-                         page_table, seq_lens, s_hat, s_hat_stride, partials, n_tiles);
-  }
-  const dim3 grid(n_tiles, c.num_kv_heads, c.num_seqs);
   if (c.q_dtype == LOCKS_BF16)
-    return dispatch(c.rank, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                    static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(summaries),
-                    page_table, seq_lens, s_hat, s_hat_stride, partials, n_tiles);
-  return dispatch(c.rank, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                  static_cast<const float*>(q), static_cast<const uint8_t*>(summaries),
-                  page_table, seq_lens, s_hat, s_hat_stride, partials, n_tiles);
+    return dispatch_scan(c.rank, G, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
+                         static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(summaries),
+                         page_table, seq_lens, s_hat, s_hat_stride, partials);
+  return dispatch_scan(c.rank, G, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
+                       static_cast<const float*>(q), static_cast<const uint8_t*>(summaries),
+                       page_table, seq_lens, s_hat, s_hat_stride, partials);
 }
 
 }  // namespace locks

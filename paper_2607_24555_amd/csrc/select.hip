@@ -1,187 +1,261 @@
 // Share-average combine and shared top-k table (Sec. 4 "Score"; Cor.
 // "Group-shared selection"; App. E "union table").
 //
-//  1. lz_kernel     log Z_g = log sum_j exp(hat s_j(q_g)) over every complete page,
-//                   from the scan's per-tile (max, sum exp) partials.
-//  2. key_kernel    per candidate page (neither page 0 nor the most recent page):
-//                   log mbar_j + log G = log sum_g exp(hat s_j(q_g) - log Z_g),
-//                   stored as an order-preserving uint32 key.
-//  3. topk_kernel   one block per (sequence, KV head): radix select of the
-//                   (k-2)-th largest key (4 passes of 8 bits), then an ordered
-//                   compaction that keeps every larger key and the lowest-index
-//                   equal keys, so ties go to the lower page index and the table
-//                   comes out ascending; adds page 0 and the most recent page and
-//                   gathers the selected pages' hat s for every head of the group.
+// One kernel, grid (chunk of kSelChunk pages, KV head, sequence):
+//  1. every block reduces the scan blocks' partials into lz2_g = log2 Z_g, then
+//     scores the candidate pages of its chunk (neither page 0 nor the most recent
+//     page):  log2 mbar_j + log2 G = log2 sum_g 2^(s2_j(q_g) - lz2_g); the score
+//     becomes an order-preserving uint32 key (key 0 marks "no candidate");
+//  2. the block keeps its chunk's top (k-2) keys: a bisection over the key space
+//     finds T, the (k-2)-th largest key, then an ordered compaction keeps every key
+//     above T and the lowest-index keys equal to T, so ties go to the lower page
+//     index and the survivors come out in ascending page order;
+//  3. the last block of the (sequence, KV head) to finish (device-scope counter)
+//     runs the same selection over all chunks' survivors, adds page 0 and the most
+//     recent page, writes the ascending table, gathers hat s of the selected pages
+//     for every head of the group and leaves the counter at zero.
 #include "locks_internal.h"
 
 namespace locks {
 namespace {
 
-constexpr int kKeyBlock = 256;
-constexpr int kTopkBlock = 1024;
-constexpr int kTopkWaves = kTopkBlock / 64;
+constexpr int kSelThreads = 256;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kPerThread = kSelChunk / kSelThreads;
+constexpr int kLdsCand = 8192;  // survivors the merge keeps in LDS
 
-__global__ __launch_bounds__(256) void lz_kernel(int H_q, const int32_t* __restrict__ seq_lens,
-                                                 const float2* __restrict__ partials, int n_tiles,
-                                                 float* __restrict__ lz) {
-  const int hq = blockIdx.x, s = blockIdx.y;
-  const int n_c = seq_lens[s] / kPage;
-  const int used = (n_c + kScanTile - 1) / kScanTile;
-  const float2* p = partials + ((long)s * H_q + hq) * n_tiles;
-  __shared__ float red[4];
-  float m = -INFINITY;
-  for (int t = threadIdx.x; t < used; t += 256) m = fmaxf(m, p[t].x);
-  m = warp_max(m);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
-  __syncthreads();
-  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  __syncthreads();
-  float l = 0.0f;
-  if (m > -INFINITY)
-    for (int t = threadIdx.x; t < used; t += 256) {
-      const float2 v = p[t];
-      if (v.y > 0.0f) l += v.y * __expf(v.x - m);
-    }
-  l = warp_sum(l);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = l;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const float tot = red[0] + red[1] + red[2] + red[3];
-    lz[(long)s * H_q + hq] = (m > -INFINITY) ? m + logf(tot) : -INFINITY;
-  }
+struct Red {
+  int v[2][kSelWaves];
+  uint32_t mx[kSelWaves], mn[kSelWaves];
+  int flag;
+};
+
+__device__ __forceinline__ int wave_sum_i(int v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
 }
 
-__global__ __launch_bounds__(kKeyBlock) void key_kernel(int H_q, int H_kv, int max_pages,
-                                                        const int32_t* __restrict__ seq_lens,
-                                                        const float* __restrict__ s_hat,
-                                                        int s_hat_stride, const float* __restrict__ lz,
-                                                        uint32_t* __restrict__ keys) {
-  const int h = blockIdx.y, s = blockIdx.z;
-  const int j = blockIdx.x * kKeyBlock + threadIdx.x;
-  const int L = seq_lens[s];
-  const int n = (L + kPage - 1) / kPage;
-  if (j < 1 || j > n - 2) return;  // only candidates get a key
-  const int G = H_q / H_kv;
-  const long row0 = (long)s * H_q + h * G;
-  float m = -INFINITY;
-  for (int g = 0; g < G; ++g) m = fmaxf(m, s_hat[(row0 + g) * s_hat_stride + j] - lz[row0 + g]);
-  float sum = 0.0f;
-  for (int g = 0; g < G; ++g) sum += __expf(s_hat[(row0 + g) * s_hat_stride + j] - lz[row0 + g] - m);
-  const float score = m + __logf(sum);
-  keys[((long)s * H_kv + h) * max_pages + j] = f32_order_key(score);
+// Sum over the block (all threads must call; alternate `par` between calls).
+__device__ __forceinline__ int block_sum(int v, Red& r, int par) {
+  v = wave_sum_i(v);
+  if ((threadIdx.x & 63) == 0) r.v[par][threadIdx.x >> 6] = v;
+  __syncthreads();
+  int t = 0;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) t += r.v[par][w];
+  return t;
 }
 
-// Exclusive prefix count of a per-thread flag over the whole block, in thread
-// order.  Returns the count before this thread; *total gets the block total.
-__device__ __forceinline__ int block_excl_count(bool flag, int* wave_tot, int* total) {
-  const uint64_t ballot = __ballot(flag);
+// Exclusive prefix count of a flag in thread order, and the block total.
+__device__ __forceinline__ int block_excl(bool p, Red& r, int par, int* total) {
+  const uint64_t b = __ballot(p);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint64_t below = lane ? (ballot & ((~0ull) >> (64 - lane))) : 0ull;
-  const int in_wave = __popcll(below);
-  if (lane == 0) wave_tot[wave] = __popcll(ballot);
+  const int in_wave = __popcll(lane ? (b & (~0ull >> (64 - lane))) : 0ull);
+  if (lane == 0) r.v[par][wave] = __popcll(b);
   __syncthreads();
   int before = 0, tot = 0;
-  for (int w = 0; w < kTopkWaves; ++w) {
-    const int v = wave_tot[w];
-    before += (w < wave) ? v : 0;
-    tot += v;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    before += w < wave ? r.v[par][w] : 0;
+    tot += r.v[par][w];
   }
-  __syncthreads();
   *total = tot;
   return before + in_wave;
 }
 
-__global__ __launch_bounds__(kTopkBlock) void topk_kernel(
-    int H_q, int H_kv, int max_pages, int k, const int32_t* __restrict__ seq_lens,
-    const uint32_t* __restrict__ keys_all, const float* __restrict__ s_hat, int s_hat_stride,
+__device__ __forceinline__ void block_minmax(uint32_t& mn, uint32_t& mx, Red& r) {
+  for (int o = 32; o > 0; o >>= 1) {
+    mx = max(mx, (uint32_t)__shfl_xor((int)mx, o, 64));
+    mn = min(mn, (uint32_t)__shfl_xor((int)mn, o, 64));
+  }
+  if ((threadIdx.x & 63) == 0) { r.mx[threadIdx.x >> 6] = mx; r.mn[threadIdx.x >> 6] = mn; }
+  __syncthreads();
+  mx = 0u;
+  mn = 0xffffffffu;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) { mx = max(mx, r.mx[w]); mn = min(mn, r.mn[w]); }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(
+    int H_q, int H_kv, int max_pages, int k, int n_chunks, const int32_t* __restrict__ seq_lens,
+    const float* __restrict__ s_hat, int s_hat_stride, const float2* __restrict__ partials,
+    int n_parts, uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx, int* __restrict__ counters,
     int32_t* __restrict__ out_ids, float* __restrict__ out_sel_lse) {
-  const int h = blockIdx.x, s = blockIdx.y;
+  __shared__ Red red;
+  __shared__ float s_lz2[16];
+  __shared__ uint32_t s_key[kLdsCand];
+  __shared__ int32_t s_idx[kLdsCand];
+  const int chunk = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
   const int tid = threadIdx.x;
   const int L = seq_lens[s];
   const int n = (L + kPage - 1) / kPage;
   const int n_c = L / kPage;
   const int G = H_q / H_kv;
-  int32_t* ids = out_ids + ((long)s * H_kv + h) * k;
-  const uint32_t* keys = keys_all + ((long)s * H_kv + h) * max_pages;
+  const int K = k - 2;
+  const long row0 = (long)s * H_q + (long)h * G;
+  const long ch_base = ((long)s * H_kv + h) * n_chunks;
+  constexpr float kLog2e = 1.4426950408889634f;
+  int par = 0;
+  const int p0 = chunk * kSelChunk;
 
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t sh_prefix, sh_mask, sh_remaining;
-  __shared__ int wave_tot[kTopkWaves];
-
-  if (n <= k) {
-    for (int t = tid; t < k; t += kTopkBlock) ids[t] = t < n ? t : -1;
-  } else {
-    const int K = k - 2;
-    if (tid == 0) { sh_prefix = 0; sh_mask = 0; sh_remaining = (uint32_t)K; }
+  // ---- log2 Z_g from the scan blocks' (max, sum 2^x) partials; 16 threads per head
+  if (n > k && p0 <= n - 2) {
+    const int g = tid >> 4, sub = tid & 15;
+    const float2* pp = partials + (row0 + (g < G ? g : 0)) * n_parts;
+    float m = -INFINITY, l = 0.0f;
+    if (g < G)
+      for (int t = sub; t < n_parts; t += 16) m = fmaxf(m, pp[t].x);
+    for (int o = 8; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if (g < G && m > -INFINITY)
+      for (int t = sub; t < n_parts; t += 16) {
+        const float2 v = pp[t];
+        if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+      }
+    for (int o = 8; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
+    if (g < G && sub == 0) s_lz2[g] = m + __builtin_amdgcn_logf(l);
     __syncthreads();
-    for (int pass = 0; pass < 4; ++pass) {
-      const int shift = 24 - 8 * pass;
-      for (int t = tid; t < 256; t += kTopkBlock) hist[t] = 0;
-      __syncthreads();
-      const uint32_t prefix = sh_prefix, mask = sh_mask;
-      for (int j = 1 + tid; j <= n - 2; j += kTopkBlock) {
-        const uint32_t key = keys[j];
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+  }
+
+  // ---- 1+2: chunk-local top K of the candidate pages
+  if (n > k && p0 <= n - 2) {
+    uint32_t key[kPerThread];
+    uint32_t kmx = 0u, kmn = 0xffffffffu;
+    int local = 0;
+#pragma unroll
+    for (int u = 0; u < kPerThread; ++u) {
+      const int j = p0 + tid + kSelThreads * u;
+      key[u] = 0u;
+      if (j >= 1 && j <= n - 2) {
+        float m = -INFINITY;
+        for (int g = 0; g < G; ++g)
+          m = fmaxf(m, s_hat[(row0 + g) * s_hat_stride + j] * kLog2e - s_lz2[g]);
+        float sum = 0.0f;
+        for (int g = 0; g < G; ++g)
+          sum += __builtin_amdgcn_exp2f(s_hat[(row0 + g) * s_hat_stride + j] * kLog2e - s_lz2[g] - m);
+        key[u] = max(1u, f32_order_key(m + __builtin_amdgcn_logf(sum)));
+        kmx = max(kmx, key[u]);
+        kmn = min(kmn, key[u]);
+        ++local;
       }
-      __syncthreads();
-      if (tid == 0) {
-        uint32_t rem = sh_remaining, cum = 0;
-        int dsel = 0;
-        for (int dgt = 255; dgt >= 0; --dgt) {
-          if (cum + hist[dgt] >= rem) { dsel = dgt; break; }
-          cum += hist[dgt];
-        }
-        sh_remaining = rem - cum;
-        sh_prefix = prefix | ((uint32_t)dsel << shift);
-        sh_mask = mask | (255u << shift);
+    }
+    const int n_cand = block_sum(local, red, par); par ^= 1;
+    uint32_t T = 1u;
+    int take_eq = 1 << 30;
+    if (n_cand > K) {
+      block_minmax(kmn, kmx, red);
+      uint32_t lo = kmn, hi = kmx;  // invariant: #{key >= lo} >= K
+      while (lo < hi) {
+        const uint32_t mid = lo + (uint32_t)((((uint64_t)hi - lo) + 1) >> 1);
+        int c = 0;
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) c += key[u] >= mid;
+        if (block_sum(c, red, par) >= K) lo = mid; else hi = mid - 1;
+        par ^= 1;
       }
+      T = lo;
+      int c = 0;
+#pragma unroll
+      for (int u = 0; u < kPerThread; ++u) c += key[u] > T;
+      take_eq = K - block_sum(c, red, par); par ^= 1;
+    }
+    int run_eq = 0, run_sel = 0;
+#pragma unroll
+    for (int u = 0; u < kPerThread; ++u) {
+      int tot_eq, tot_sel;
+      const bool eq = key[u] != 0u && key[u] == T;
+      const int before_eq = block_excl(eq, red, par, &tot_eq); par ^= 1;
+      const bool sel = (key[u] != 0u && key[u] > T) || (eq && run_eq + before_eq < take_eq);
+      const int before_sel = block_excl(sel, red, par, &tot_sel); par ^= 1;
+      if (sel) {
+        cand_key[(ch_base + chunk) * K + run_sel + before_sel] = key[u];
+        cand_idx[(ch_base + chunk) * K + run_sel + before_sel] = p0 + tid + kSelThreads * u;
+      }
+      run_eq += tot_eq;
+      run_sel += tot_sel;
+    }
+    for (int t = run_sel + tid; t < K; t += kSelThreads) {
+      cand_key[(ch_base + chunk) * K + t] = 0u;
+      cand_idx[(ch_base + chunk) * K + t] = -1;
+    }
+  }
+
+  // ---- 3: the last block of this (sequence, KV head) merges
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) red.flag = atomicAdd(&counters[s * H_kv + h], 1) == n_chunks - 1;
+  __syncthreads();
+  if (!red.flag) return;
+  __threadfence();
+  int32_t* ids = out_ids + ((long)s * H_kv + h) * k;
+  if (n <= k) {
+    for (int t = tid; t < k; t += kSelThreads) ids[t] = t < n ? t : -1;
+  } else {
+    const int used = (n - 2) / kSelChunk + 1;  // chunks that hold candidates (pages 1..n-2)
+    const int N = used * K;
+    const bool in_lds = N <= kLdsCand;
+    const uint32_t* gk = cand_key + ch_base * K;
+    const int32_t* gi = cand_idx + ch_base * K;
+    if (in_lds) {
+      for (int e = tid; e < N; e += kSelThreads) { s_key[e] = gk[e]; s_idx[e] = gi[e]; }
       __syncthreads();
     }
-    const uint32_t T = sh_prefix;
-    const int take_eq = (int)sh_remaining;  // equal keys to keep, lowest index first
+    uint32_t kmx = 0u, kmn = 0xffffffffu;
+    for (int e = tid; e < N; e += kSelThreads) {
+      const uint32_t v = in_lds ? s_key[e] : gk[e];
+      if (v) { kmx = max(kmx, v); kmn = min(kmn, v); }
+    }
+    block_minmax(kmn, kmx, red);
+    uint32_t lo = kmn, hi = kmx;
+    while (lo < hi) {
+      const uint32_t mid = lo + (uint32_t)((((uint64_t)hi - lo) + 1) >> 1);
+      int c = 0;
+      for (int e = tid; e < N; e += kSelThreads) c += (in_lds ? s_key[e] : gk[e]) >= mid;
+      if (block_sum(c, red, par) >= K) lo = mid; else hi = mid - 1;
+      par ^= 1;
+    }
+    const uint32_t T = lo;
+    int c = 0;
+    for (int e = tid; e < N; e += kSelThreads) c += (in_lds ? s_key[e] : gk[e]) > T;
+    const int take_eq = K - block_sum(c, red, par);
+    par ^= 1;
+    // survivors are ascending in page index (chunk order, ascending inside a chunk)
     int run_eq = 0, run_sel = 0;
-    for (int base = 1; base <= n - 2; base += kTopkBlock) {
-      const int j = base + tid;
-      const bool in = j <= n - 2;
-      const uint32_t key = in ? keys[j] : 0u;
-      const bool gt = in && key > T;
-      const bool eq = in && key == T;
+    for (int base = 0; base < N; base += kSelThreads) {
+      const int e = base + tid;
+      const uint32_t v = e < N ? (in_lds ? s_key[e] : gk[e]) : 0u;
       int tot_eq, tot_sel;
-      const int before_eq = block_excl_count(eq, wave_tot, &tot_eq);
-      const bool sel = gt || (eq && run_eq + before_eq < take_eq);
-      const int before_sel = block_excl_count(sel, wave_tot, &tot_sel);
-      if (sel) ids[1 + run_sel + before_sel] = j;
+      const bool eq = v != 0u && v == T;
+      const int before_eq = block_excl(eq, red, par, &tot_eq); par ^= 1;
+      const bool sel = (v != 0u && v > T) || (eq && run_eq + before_eq < take_eq);
+      const int before_sel = block_excl(sel, red, par, &tot_sel); par ^= 1;
+      if (sel) ids[1 + run_sel + before_sel] = in_lds ? s_idx[e] : gi[e];
       run_eq += tot_eq;
       run_sel += tot_sel;
     }
     if (tid == 0) { ids[0] = 0; ids[k - 1] = n - 1; }
   }
   __syncthreads();
-  // hat s of the selected pages for every head of the group (NaN without summary)
-  for (int e = tid; e < G * k; e += kTopkBlock) {
+  for (int e = tid; e < G * k; e += kSelThreads) {
     const int g = e / k, t = e % k;
     const int id = ids[t];
-    const long row = (long)s * H_q + h * G + g;
-    out_sel_lse[row * k + t] = (id >= 0 && id < n_c) ? s_hat[row * s_hat_stride + id] : __int_as_float(0x7fc00000);
+    out_sel_lse[(row0 + g) * k + t] =
+        (id >= 0 && id < n_c) ? s_hat[(row0 + g) * s_hat_stride + id] : __int_as_float(0x7fc00000);
   }
+  if (tid == 0) counters[s * H_kv + h] = 0;
 }
 
 }  // namespace
 
-hipError_t launch_select(const locks_cfg_t& c, const float* s_hat, int s_hat_stride,
-                         const float2* partials, int n_tiles, const int32_t* seq_lens, float* lz,
-                         uint32_t* keys, int32_t* out_page_ids, float* out_sel_lse,
-                         hipStream_t st) {
+hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
+                         int s_hat_stride, const float2* partials, uint32_t* cand_key,
+                         int32_t* cand_idx, int n_chunks, int* counters, int32_t* out_page_ids,
+                         float* out_sel_lse, hipStream_t st) {
   const int k = page_budget(c);
-  hipLaunchKernelGGL(lz_kernel, dim3(c.num_q_heads, c.num_seqs), dim3(256), 0, st, c.num_q_heads,
-                     seq_lens, partials, n_tiles, lz);
-  hipLaunchKernelGGL(key_kernel,
-                     dim3((c.max_pages_per_seq + kKeyBlock - 1) / kKeyBlock, c.num_kv_heads, c.num_seqs),
-                     dim3(kKeyBlock), 0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                     seq_lens, s_hat, s_hat_stride, lz, keys);
-  hipLaunchKernelGGL(topk_kernel, dim3(c.num_kv_heads, c.num_seqs), dim3(kTopkBlock), 0, st,
-                     c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq, k, seq_lens, keys, s_hat,
-                     s_hat_stride, out_page_ids, out_sel_lse);
+  hipLaunchKernelGGL(select_kernel, dim3(n_chunks, c.num_kv_heads, c.num_seqs), dim3(kSelThreads),
+                     0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq, k, n_chunks,
+                     seq_lens, s_hat, s_hat_stride, partials, scan_blocks(c), cand_key, cand_idx,
+                     counters, out_page_ids, out_sel_lse);
   return hipGetLastError();
 }
 

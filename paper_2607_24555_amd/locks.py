@@ -143,7 +143,8 @@ def alloc_workspace(cfg: Config, device="cuda") -> torch.Tensor:
     n = workspace_bytes(cfg)
     if n == 0:
         raise LocksError("invalid configuration")
-    return torch.empty(n, dtype=torch.uint8, device=device)
+    # zero-filled once: the kernels' completion counters start (and end) at zero
+    return torch.zeros(n, dtype=torch.uint8, device=device)
 
 
 def alloc_summaries(cfg: Config, device="cuda") -> torch.Tensor:

@@ -53,7 +53,7 @@ def test_payload_and_stride(lib):
     (dict(rank=0), -1), (dict(rank=16), -1), (dict(num_q_heads=7), -1),
     (dict(budget_tokens=16), -1), (dict(budget_tokens=0), -1), (dict(max_pages_per_seq=0), -1),
     (dict(num_blocks=0), -1), (dict(num_kv_heads=0), -1), (dict(num_seqs=-1), -1),
-    (dict(num_q_heads=130, num_kv_heads=2), -2),
+    (dict(num_q_heads=34, num_kv_heads=2), -2),
 ])
 def test_bad_config_is_rejected_before_launch(lib, bad, code):
     c = cfg(**bad).c()
