@@ -33,11 +33,10 @@
  *    page ceil(L/16)-1 is the most recent page.  A page has a summary only once
  *    it is complete (16 tokens).
  *  - The workspace `ws` (caller-allocated, >= locks_workspace_bytes(cfg) bytes,
- *    256-byte aligned) holds per-call scratch and a few completion counters.  It
- *    must be zero-filled once before its first use; every call leaves the
- *    counters at zero again, so no clearing is needed between calls (the step is
- *    graph-capturable).  Calls that share one workspace must be ordered on one
- *    stream.
+ *    256-byte aligned) holds per-call scratch; its content need not be
+ *    initialised and is meaningless after the call.  No call clears memory, so a
+ *    captured step replays without extra nodes.  Calls that share one workspace
+ *    must be ordered on one stream.
  *  - Calls with no launches (num_seqs == 0) return LOCKS_OK.
  */
 #ifndef LOCKS_H

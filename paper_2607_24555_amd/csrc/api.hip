@@ -38,17 +38,13 @@ struct Ws {
   uint32_t* ckey;
   int32_t* cidx;
   float* attn;
-  int* ctr_sel;
-  int* ctr_attn;
 };
 
-Ws carve(void* ws, const WsPlan& p, const locks_cfg_t& c) {
+Ws carve(void* ws, const WsPlan& p) {
   char* b = static_cast<char*>(ws);
-  int* ctr = reinterpret_cast<int*>(b + p.ctr_off);
-  const size_t nc = (size_t)c.num_seqs * c.num_kv_heads;
   return Ws{reinterpret_cast<float*>(b + p.s_hat_off), reinterpret_cast<float2*>(b + p.part_off),
             reinterpret_cast<uint32_t*>(b + p.ckey_off), reinterpret_cast<int32_t*>(b + p.cidx_off),
-            reinterpret_cast<float*>(b + p.attn_off), ctr, ctr + nc};
+            reinterpret_cast<float*>(b + p.attn_off)};
 }
 
 int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
@@ -82,7 +78,6 @@ WsPlan plan_workspace(const locks_cfg_t& c) {
   p.ckey_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(uint32_t));
   p.cidx_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(int32_t));
   p.attn_off = take(S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float));
-  p.ctr_off = take(2 * S * Hkv * sizeof(int));
   p.total = off;
   return p;
 }
@@ -91,13 +86,13 @@ static int select_impl(const locks_cfg_t* c, const void* q, const void* summarie
                        const int32_t* page_table, const int32_t* seq_lens, int32_t* out_page_ids,
                        float* out_sel_lse, float* out_all_lse, void* ws, hipStream_t st) {
   const WsPlan p = plan_workspace(*c);
-  Ws w = carve(ws, p, *c);
+  Ws w = carve(ws, p);
   float* s_hat = out_all_lse ? out_all_lse : w.s_hat;
-  hipError_t e = launch_scan(*c, q, summaries, page_table, seq_lens, s_hat, c->max_pages_per_seq,
-                             w.part, st);
+  const SHatLayout lay = out_all_lse ? shat_head_major(*c) : shat_head_minor(*c);
+  hipError_t e = launch_scan(*c, q, summaries, page_table, seq_lens, s_hat, lay, w.part, st);
   if (e != hipSuccess) return hip_status(e);
-  e = launch_select(*c, seq_lens, s_hat, c->max_pages_per_seq, w.part, w.ckey, w.cidx, p.n_chunks,
-                    w.ctr_sel, out_page_ids, out_sel_lse, st);
+  e = launch_select(*c, seq_lens, s_hat, lay, w.part, w.ckey, w.cidx, p.n_chunks, out_page_ids,
+                    out_sel_lse, st);
   return hip_status(e);
 }
 
@@ -169,9 +164,9 @@ int locks_score_pages(const locks_cfg_t* cfg, const void* q, const void* summari
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
   const WsPlan p = plan_workspace(*cfg);
-  const Ws w = carve(ws, p, *cfg);
+  const Ws w = carve(ws, p);
   return hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, out_all_lse,
-                                cfg->max_pages_per_seq, w.part, static_cast<hipStream_t>(stream)));
+                                shat_head_major(*cfg), w.part, static_cast<hipStream_t>(stream)));
 }
 
 int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
@@ -188,7 +183,7 @@ int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cac
   const int k = page_budget(*cfg);
   const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, page_ids,
-                                  kSparsePagesPerSplit, splits, carve(ws, p, *cfg).attn, out, out_lse,
+                                  kSparsePagesPerSplit, splits, carve(ws, p).attn, out, out_lse,
                                   static_cast<hipStream_t>(stream)));
 }
 
@@ -202,7 +197,7 @@ int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cach
   if (cfg->num_seqs == 0) return LOCKS_OK;
   const WsPlan p = plan_workspace(*cfg);
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, nullptr,
-                                  kDensePagesPerSplit, dense_splits(*cfg), carve(ws, p, *cfg).attn, out,
+                                  kDensePagesPerSplit, dense_splits(*cfg), carve(ws, p).attn, out,
                                   out_lse, static_cast<hipStream_t>(stream)));
 }
 
@@ -231,7 +226,7 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
   const int k = page_budget(*cfg);
   const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, out_page_ids,
-                                  kSparsePagesPerSplit, splits, carve(ws, p, *cfg).attn, out, out_lse, st));
+                                  kSparsePagesPerSplit, splits, carve(ws, p).attn, out, out_lse, st));
 }
 
 const char* locks_strerror(int status) {

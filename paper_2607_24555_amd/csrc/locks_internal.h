@@ -57,15 +57,33 @@ __device__ __forceinline__ float warp_sum(float v) {
   return v;
 }
 
+// ---------------------------------------------------------------- page-score layout
+
+// Page scores hat s: element (seq s, KV head h, group head g, page j) lives at
+// s * seq + h * kvh + g * head + j * page.  The API's out_all_lse is head-major
+// ([S][H_q][max_pages]); the internal workspace copy is head-minor
+// ([S][H_kv][max_pages][G]) so that one page's G scores are contiguous.
+struct SHatLayout {
+  long seq, kvh, head, page;
+  __host__ __device__ long base(int s, int h) const { return s * seq + h * kvh; }
+};
+inline SHatLayout shat_head_major(const locks_cfg_t& c) {
+  const long mp = c.max_pages_per_seq, G = c.num_q_heads / c.num_kv_heads;
+  return SHatLayout{c.num_q_heads * mp, G * mp, mp, 1};
+}
+inline SHatLayout shat_head_minor(const locks_cfg_t& c) {
+  const long mp = c.max_pages_per_seq, G = c.num_q_heads / c.num_kv_heads;
+  return SHatLayout{c.num_kv_heads * mp * G, mp * G, 1, G};
+}
+
 // ---------------------------------------------------------------- workspace plan
 
 struct WsPlan {
-  size_t s_hat_off;   // float [S][H_q][max_pages]        page scores
+  size_t s_hat_off;   // float [S][H_kv][max_pages][G]    page scores (head-minor)
   size_t part_off;    // float2 [S][H_q][scan blocks]     (max, sum exp), log2 domain
   size_t ckey_off;    // uint32 [S][H_kv][chunks][k-2]    per-chunk survivors (keys)
   size_t cidx_off;    // int32  [S][H_kv][chunks][k-2]    per-chunk survivors (pages)
   size_t attn_off;    // float [S][H_q][splits][d + 2]    split-K partials
-  size_t ctr_off;     // int [2][S][H_kv]                 last-block counters (kept zero)
   size_t total;
   int n_chunks;       // select chunks per sequence
   int n_splits;       // attention splits per (seq, KV head)
@@ -92,11 +110,11 @@ hipError_t launch_build(const locks_cfg_t& c, const void* k_cache, const int32_t
 
 hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,
                        const int32_t* page_table, const int32_t* seq_lens, float* s_hat,
-                       int s_hat_stride, float2* partials, hipStream_t st);
+                       SHatLayout lay, float2* partials, hipStream_t st);
 
 hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
-                         int s_hat_stride, const float2* partials, uint32_t* cand_key,
-                         int32_t* cand_idx, int n_chunks, int* counters, int32_t* out_page_ids,
+                         SHatLayout lay, const float2* partials, uint32_t* cand_key,
+                         int32_t* cand_idx, int n_chunks, int32_t* out_page_ids,
                          float* out_sel_lse, hipStream_t st);
 
 hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cache,

@@ -140,7 +140,7 @@ template <typename QT, int R>
 __global__ __launch_bounds__(256) void scan_mfma_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q,
     const uint8_t* __restrict__ summaries, const int32_t* __restrict__ page_table,
-    const int32_t* __restrict__ seq_lens, float* __restrict__ s_hat, int s_hat_stride,
+    const int32_t* __restrict__ seq_lens, float* __restrict__ s_hat, SHatLayout lay,
     float2* __restrict__ partials) {
   using Gm = Geom<R>;
   constexpr bool kSplitQ = sizeof(QT) == 4;  // fp32 queries: f16 hi + lo
@@ -291,7 +291,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
         sm = red4_sum(sm);
         const float s2 = mx + __builtin_amdgcn_logf(sm);  // log2-domain page score
         if (live) {
-          if (grp == 0) s_hat[(row0 + gcol) * s_hat_stride + page0 + page] = s2 * kLn2;
+          if (grp == 0) s_hat[lay.base(s, h) + gcol * lay.head + (long)(page0 + page) * lay.page] = s2 * kLn2;
           const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
           if (s2 > run_m) { run_s = fmaf(run_s, e, 1.0f); run_m = s2; }
           else run_s += e;
@@ -390,7 +390,7 @@ template <typename QT, int R, int NPACK>
 __global__ __launch_bounds__(256) void scan_fast_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
-    float* __restrict__ s_hat, int s_hat_stride, float2* __restrict__ partials) {
+    float* __restrict__ s_hat, SHatLayout lay, float2* __restrict__ partials) {
   using Gm = FastGeom<R>;
   constexpr int G = 16 / NPACK;
   constexpr int kPasses = 16 / NPACK;
@@ -561,7 +561,8 @@ __global__ __launch_bounds__(256) void scan_fast_kernel(
           sm = red4_sum(sm);
           const float s2 = mx + __builtin_amdgcn_logf(sm);
           const bool live = page0 + pcpage < n_c;
-          if (live && grp == 0) s_hat[(row0 + gcol) * s_hat_stride + page0 + pcpage] = s2 * 0.69314718055994531f;
+          if (live && grp == 0)
+            s_hat[lay.base(s, h) + gcol * lay.head + (long)(page0 + pcpage) * lay.page] = s2 * 0.69314718055994531f;
           const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
           const bool up = s2 > run_m;
           const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
@@ -593,11 +594,11 @@ __global__ __launch_bounds__(256) void scan_fast_kernel(
 template <typename QT>
 hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H_kv, int max_pages,
                          const QT* q, const uint8_t* sum, const int32_t* pt, const int32_t* sl,
-                         float* s_hat, int s_hat_stride, float2* part) {
+                         float* s_hat, SHatLayout lay, float2* part) {
 #define LOCKS_SCAN_FAST(RR, NP)                                                              \
   if (r == RR && G == 16 / NP) {                                                            \
     hipLaunchKernelGGL((scan_fast_kernel<QT, RR, NP>), grid, dim3(256), 0, st, H_q, H_kv,   \
-                       max_pages, q, sum, pt, sl, s_hat, s_hat_stride, part);               \
+                       max_pages, q, sum, pt, sl, s_hat, lay, part);               \
     return hipGetLastError();                                                               \
   }
   LOCKS_SCAN_FAST(8, 1) LOCKS_SCAN_FAST(8, 4) LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(4, 4)
@@ -606,7 +607,7 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
 #define LOCKS_SCAN_MFMA_CASE(RR)                                                             \
   case RR:                                                                                  \
     hipLaunchKernelGGL((scan_mfma_kernel<QT, RR>), grid, dim3(256), 0, st, H_q, H_kv,       \
-                       max_pages, q, sum, pt, sl, s_hat, s_hat_stride, part);               \
+                       max_pages, q, sum, pt, sl, s_hat, lay, part);               \
     break;
   switch (r) {
     LOCKS_SCAN_MFMA_CASE(1) LOCKS_SCAN_MFMA_CASE(2) LOCKS_SCAN_MFMA_CASE(3)
@@ -625,16 +626,16 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
 
 hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,
                        const int32_t* page_table, const int32_t* seq_lens, float* s_hat,
-                       int s_hat_stride, float2* partials, hipStream_t st) {
+                       SHatLayout lay, float2* partials, hipStream_t st) {
   const dim3 grid(scan_blocks(c), c.num_kv_heads, c.num_seqs);
   const int G = c.num_q_heads / c.num_kv_heads;
   if (c.q_dtype == LOCKS_BF16)
     return dispatch_scan(c.rank, G, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
                          static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(summaries),
-                         page_table, seq_lens, s_hat, s_hat_stride, partials);
+                         page_table, seq_lens, s_hat, lay, partials);
   return dispatch_scan(c.rank, G, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
                        static_cast<const float*>(q), static_cast<const uint8_t*>(summaries),
-                       page_table, seq_lens, s_hat, s_hat_stride, partials);
+                       page_table, seq_lens, s_hat, lay, partials);
 }
 
 }  // namespace locks

@@ -1,19 +1,21 @@
 // Share-average combine and shared top-k table (Sec. 4 "Score"; Cor.
 // "Group-shared selection"; App. E "union table").
 //
-// One kernel, grid (chunk of kSelChunk pages, KV head, sequence):
-//  1. every block reduces the scan blocks' partials into lz2_g = log2 Z_g, then
-//     scores the candidate pages of its chunk (neither page 0 nor the most recent
-//     page):  log2 mbar_j + log2 G = log2 sum_g 2^(s2_j(q_g) - lz2_g); the score
-//     becomes an order-preserving uint32 key (key 0 marks "no candidate");
-//  2. the block keeps its chunk's top (k-2) keys: a bisection over the key space
-//     finds T, the (k-2)-th largest key, then an ordered compaction keeps every key
-//     above T and the lowest-index keys equal to T, so ties go to the lower page
-//     index and the survivors come out in ascending page order;
-//  3. the last block of the (sequence, KV head) to finish (device-scope counter)
-//     runs the same selection over all chunks' survivors, adds page 0 and the most
-//     recent page, writes the ascending table, gathers hat s of the selected pages
-//     for every head of the group and leaves the counter at zero.
+// Two kernels:
+//  select_chunk_kernel, grid (chunk of kSelChunk pages, KV head, sequence):
+//   * reduces the scan blocks' partials into lz2_g = log2 Z_g;
+//   * scores the candidate pages of its chunk (neither page 0 nor the most recent
+//     page):  log2 mbar_j + log2 G = log2 sum_g 2^(s2_j(q_g) - lz2_g), as an
+//     order-preserving uint32 key (key 0 marks "no candidate");
+//   * keeps the chunk's top (k-2) keys: a bisection over the key space finds T,
+//     the (k-2)-th largest key; an ordered compaction keeps every key above T and
+//     the lowest-index keys equal to T (ties go to the lower page index), so the
+//     survivors come out in ascending page order.
+//  select_merge_kernel, one block per (sequence, KV head): the same selection over
+//   all chunks' survivors, plus page 0 and the most recent page, written as the
+//   ascending table, and the selected pages' hat s gathered for every head.
+// Each thread owns a contiguous run of pages (or survivors) held in registers;
+// block counts use wave ballots and the ordered compaction two exclusive scans.
 #include "locks_internal.h"
 
 namespace locks {
@@ -21,46 +23,46 @@ namespace {
 
 constexpr int kSelThreads = 256;
 constexpr int kSelWaves = kSelThreads / 64;
-constexpr int kPerThread = kSelChunk / kSelThreads;
-constexpr int kLdsCand = 8192;  // survivors the merge keeps in LDS
+constexpr int kPerThread = kSelChunk / kSelThreads;  // contiguous pages per thread
+constexpr int kMergeRegs = 32;                       // survivors per thread in registers
+constexpr float kLog2e = 1.4426950408889634f;
 
 struct Red {
   int v[2][kSelWaves];
+  int sc[2][kSelWaves];
   uint32_t mx[kSelWaves], mn[kSelWaves];
-  int flag;
 };
 
-__device__ __forceinline__ int wave_sum_i(int v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
-// Sum over the block (all threads must call; alternate `par` between calls).
-__device__ __forceinline__ int block_sum(int v, Red& r, int par) {
-  v = wave_sum_i(v);
-  if ((threadIdx.x & 63) == 0) r.v[par][threadIdx.x >> 6] = v;
+// Block sum of small non-negative per-thread counts (< 2^bits), via wave ballots.
+__device__ __forceinline__ int block_count(int v, int bits, Red& r, int par) {
+  int w = 0;
+  for (int b = 0; b < bits; ++b) w += __popcll(__ballot((v >> b) & 1)) << b;
+  if ((threadIdx.x & 63) == 0) r.v[par][threadIdx.x >> 6] = w;
   __syncthreads();
   int t = 0;
 #pragma unroll
-  for (int w = 0; w < kSelWaves; ++w) t += r.v[par][w];
+  for (int i = 0; i < kSelWaves; ++i) t += r.v[par][i];
   return t;
 }
 
-// Exclusive prefix count of a flag in thread order, and the block total.
-__device__ __forceinline__ int block_excl(bool p, Red& r, int par, int* total) {
-  const uint64_t b = __ballot(p);
+// Exclusive block scan of per-thread ints in thread order, and the total.
+__device__ __forceinline__ int block_excl_scan(int v, Red& r, int par, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int in_wave = __popcll(lane ? (b & (~0ull >> (64 - lane))) : 0ull);
-  if (lane == 0) r.v[par][wave] = __popcll(b);
+  int x = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) r.sc[par][wave] = x;
   __syncthreads();
   int before = 0, tot = 0;
 #pragma unroll
-  for (int w = 0; w < kSelWaves; ++w) {
-    before += w < wave ? r.v[par][w] : 0;
-    tot += r.v[par][w];
+  for (int i = 0; i < kSelWaves; ++i) {
+    before += i < wave ? r.sc[par][i] : 0;
+    tot += r.sc[par][i];
   }
   *total = tot;
-  return before + in_wave;
+  return before + x - v;
 }
 
 __device__ __forceinline__ void block_minmax(uint32_t& mn, uint32_t& mx, Red& r) {
@@ -77,16 +79,233 @@ __device__ __forceinline__ void block_minmax(uint32_t& mn, uint32_t& mx, Red& r)
   __syncthreads();
 }
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(
-    int H_q, int H_kv, int max_pages, int k, int n_chunks, const int32_t* __restrict__ seq_lens,
-    const float* __restrict__ s_hat, int s_hat_stride, const float2* __restrict__ partials,
-    int n_parts, uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx, int* __restrict__ counters,
-    int32_t* __restrict__ out_ids, float* __restrict__ out_sel_lse) {
+__device__ __forceinline__ int bit_length(int x) { return x > 0 ? 32 - __clz(x) : 0; }
+
+// Flags in sel[] the K largest of the keys held by the block (NK per thread,
+// key 0 = empty, thread-major order = ascending page order).  Ties at the
+// threshold keep the lowest positions.  Returns this thread's kept count.
+template <int NK>
+__device__ __forceinline__ int select_top(const uint32_t (&key)[NK], int K, bool (&sel)[NK],
+                                          Red& red) {
+  int local = 0;
+  uint32_t kmx = 0u, kmn = 0xffffffffu;
+#pragma unroll
+  for (int u = 0; u < NK; ++u)
+    if (key[u]) { ++local; kmx = max(kmx, key[u]); kmn = min(kmn, key[u]); }
+  const int bits = bit_length(NK);
+  int par = 0;
+  const int n_cand = block_count(local, bits, red, par);
+  par ^= 1;
+  uint32_t T = 1u;
+  int take_eq = 1 << 30;
+  if (n_cand > K) {
+    block_minmax(kmn, kmx, red);
+    uint32_t lo = kmn, hi = kmx;  // invariant: #{key >= lo} >= K
+    while (lo < hi) {
+      const uint32_t mid = lo + (uint32_t)((((uint64_t)hi - lo) + 1) >> 1);
+      int c = 0;
+#pragma unroll
+      for (int u = 0; u < NK; ++u) c += key[u] >= mid;
+      if (block_count(c, bits, red, par) >= K) lo = mid; else hi = mid - 1;
+      par ^= 1;
+    }
+    T = lo;
+    int c = 0;
+#pragma unroll
+    for (int u = 0; u < NK; ++u) c += key[u] > T;
+    take_eq = K - block_count(c, bits, red, par);
+  }
+  int eq_l = 0;
+#pragma unroll
+  for (int u = 0; u < NK; ++u) eq_l += key[u] != 0u && key[u] == T;
+  int tot;
+  int eq_rank = block_excl_scan(eq_l, red, 0, &tot);
+  int kept = 0;
+#pragma unroll
+  for (int u = 0; u < NK; ++u) {
+    const bool eq = key[u] != 0u && key[u] == T;
+    sel[u] = (key[u] != 0u && key[u] > T) || (eq && eq_rank < take_eq);
+    eq_rank += eq;
+    kept += sel[u];
+  }
+  return kept;
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_chunk_kernel(
+    int H_q, int H_kv, int k, int n_chunks, const int32_t* __restrict__ seq_lens,
+    const float* __restrict__ s_hat, SHatLayout lay, const float2* __restrict__ partials,
+    int n_parts, uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx) {
   __shared__ Red red;
   __shared__ float s_lz2[16];
-  __shared__ uint32_t s_key[kLdsCand];
-  __shared__ int32_t s_idx[kLdsCand];
   const int chunk = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int L = seq_lens[s];
+  const int n = (L + kPage - 1) / kPage;
+  const int G = H_q / H_kv;
+  const int K = k - 2;
+  const int p0 = chunk * kSelChunk;
+  if (K <= 0 || n <= k || p0 > n - 2) return;  // uniform: nothing to rank in this chunk
+  const long row0 = (long)s * H_q + (long)h * G;
+
+  // ---- log2 Z_g from the scan blocks' (max, sum 2^x) partials, 16 threads per head
+  {
+    const int g = tid >> 4, sub = tid & 15;
+    const float2* pp = partials + (row0 + (g < G ? g : 0)) * n_parts;
+    float m = -INFINITY, l = 0.0f;
+    for (int base = 0; base < n_parts; base += 16 * 8) {
+      float2 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int t = base + sub + 16 * u;
+        v[u] = pp[t < n_parts ? t : 0];
+        if (!(g < G && t < n_parts)) v[u] = make_float2(-INFINITY, 0.0f);
+      }
+      float mm = m;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) mm = fmaxf(mm, v[u].x);
+      float ll = (m > -INFINITY) ? l * __builtin_amdgcn_exp2f(m - mm) : 0.0f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        ll += (v[u].y > 0.0f) ? v[u].y * __builtin_amdgcn_exp2f(v[u].x - mm) : 0.0f;
+      m = mm;
+      l = ll;
+    }
+    for (int o = 8; o > 0; o >>= 1) {
+      const float om = __shfl_xor(m, o, 64), ol = __shfl_xor(l, o, 64);
+      const float mm = fmaxf(m, om);
+      l = (mm > -INFINITY) ? l * __builtin_amdgcn_exp2f(m - mm) + ol * __builtin_amdgcn_exp2f(om - mm)
+                           : 0.0f;
+      m = mm;
+    }
+    if (g < G && sub == 0) s_lz2[g] = m + __builtin_amdgcn_logf(l);
+    __syncthreads();
+  }
+
+  // ---- keys of this thread's kPerThread consecutive pages (unconditional loads)
+  uint32_t key[kPerThread];
+  {
+    const int j0 = p0 + kPerThread * tid;
+    const float* base = s_hat + lay.base(s, h);
+    float sv[kPerThread][kMaxGroup];
+#pragma unroll
+    for (int u = 0; u < kPerThread; ++u) {
+      const long j = min(max(j0 + u, 1), n - 2);
+#pragma unroll
+      for (int g = 0; g < kMaxGroup; ++g) sv[u][g] = base[j * lay.page + (long)(g < G ? g : 0) * lay.head];
+    }
+#pragma unroll
+    for (int u = 0; u < kPerThread; ++u) {
+      float m = -INFINITY;
+#pragma unroll
+      for (int g = 0; g < kMaxGroup; ++g)
+        if (g < G) m = fmaxf(m, sv[u][g] * kLog2e - s_lz2[g]);
+      float sum = 0.0f;
+#pragma unroll
+      for (int g = 0; g < kMaxGroup; ++g)
+        if (g < G) sum += __builtin_amdgcn_exp2f(sv[u][g] * kLog2e - s_lz2[g] - m);
+      const int j = j0 + u;
+      key[u] = (j >= 1 && j <= n - 2) ? max(1u, f32_order_key(m + __builtin_amdgcn_logf(sum))) : 0u;
+    }
+  }
+  bool sel[kPerThread];
+  const int kept = select_top<kPerThread>(key, K, sel, red);
+  int tot;
+  int pos = block_excl_scan(kept, red, 1, &tot);
+  const long row = (((long)s * H_kv + h) * n_chunks + chunk) * K;
+#pragma unroll
+  for (int u = 0; u < kPerThread; ++u)
+    if (sel[u]) {
+      cand_key[row + pos] = key[u];
+      cand_idx[row + pos] = p0 + kPerThread * tid + u;
+      ++pos;
+    }
+  for (int t = tot + tid; t < K; t += kSelThreads) {
+    cand_key[row + t] = 0u;
+    cand_idx[row + t] = -1;
+  }
+}
+
+// Final selection for one (sequence, KV head).  kRegs: every thread holds its
+// run of survivors in registers (at most kMergeRegs each); otherwise the run is
+// re-read from global memory in every pass.
+template <bool kRegs>
+__device__ void merge_select(int N, int K, const uint32_t* __restrict__ gk,
+                             const int32_t* __restrict__ gi, int32_t* ids, Red& red) {
+  const int tid = threadIdx.x;
+  if (kRegs) {
+    const int P = (N + kSelThreads - 1) / kSelThreads;  // <= kMergeRegs
+    const int e0 = min(N, tid * P);
+    uint32_t key[kMergeRegs];
+#pragma unroll
+    for (int u = 0; u < kMergeRegs; ++u) {
+      const int e = e0 + u;
+      const uint32_t v = gk[min(e, N - 1)];
+      key[u] = (u < P && e < N) ? v : 0u;
+    }
+    bool sel[kMergeRegs];
+    const int kept = select_top<kMergeRegs>(key, K, sel, red);
+    int tot;
+    int pos = 1 + block_excl_scan(kept, red, 1, &tot);
+#pragma unroll
+    for (int u = 0; u < kMergeRegs; ++u)
+      if (sel[u]) ids[pos++] = gi[e0 + u];
+  } else {
+    // survivors in groups of kSelThreads * 4, each pass re-reading global memory
+    const int P = (N + kSelThreads - 1) / kSelThreads;
+    const int e0 = min(N, tid * P), e1 = min(N, e0 + P);
+    uint32_t kmx = 0u, kmn = 0xffffffffu;
+    for (int e = e0; e < e1; ++e) {
+      const uint32_t v = gk[e];
+      if (v) { kmx = max(kmx, v); kmn = min(kmn, v); }
+    }
+    block_minmax(kmn, kmx, red);
+    const int bits = bit_length(P);
+    int par = 0;
+    uint32_t lo = kmn, hi = kmx;
+    while (lo < hi) {
+      const uint32_t mid = lo + (uint32_t)((((uint64_t)hi - lo) + 1) >> 1);
+      int c = 0;
+      for (int e = e0; e < e1; ++e) c += gk[e] >= mid;
+      if (block_count(c, bits, red, par) >= K) lo = mid; else hi = mid - 1;
+      par ^= 1;
+    }
+    const uint32_t T = lo;
+    int c = 0, eq_l = 0;
+    for (int e = e0; e < e1; ++e) {
+      const uint32_t v = gk[e];
+      c += v > T;
+      eq_l += v != 0u && v == T;
+    }
+    const int take_eq = K - block_count(c, bits, red, par);
+    int tot;
+    int eq_rank = block_excl_scan(eq_l, red, 0, &tot);
+    int kept = 0;
+    {
+      int r = eq_rank;
+      for (int e = e0; e < e1; ++e) {
+        const uint32_t v = gk[e];
+        const bool eq = v != 0u && v == T;
+        kept += (v != 0u && v > T) || (eq && r < take_eq);
+        r += eq;
+      }
+    }
+    int pos = 1 + block_excl_scan(kept, red, 1, &tot);
+    for (int e = e0; e < e1; ++e) {
+      const uint32_t v = gk[e];
+      const bool eq = v != 0u && v == T;
+      if ((v != 0u && v > T) || (eq && eq_rank < take_eq)) ids[pos++] = gi[e];
+      eq_rank += eq;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_merge_kernel(
+    int H_q, int H_kv, int k, int n_chunks, const int32_t* __restrict__ seq_lens,
+    const float* __restrict__ s_hat, SHatLayout lay, const uint32_t* __restrict__ cand_key,
+    const int32_t* __restrict__ cand_idx, int32_t* __restrict__ out_ids,
+    float* __restrict__ out_sel_lse) {
+  __shared__ Red red;
+  const int h = blockIdx.x, s = blockIdx.y;
   const int tid = threadIdx.x;
   const int L = seq_lens[s];
   const int n = (L + kPage - 1) / kPage;
@@ -94,168 +313,42 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   const int G = H_q / H_kv;
   const int K = k - 2;
   const long row0 = (long)s * H_q + (long)h * G;
-  const long ch_base = ((long)s * H_kv + h) * n_chunks;
-  constexpr float kLog2e = 1.4426950408889634f;
-  int par = 0;
-  const int p0 = chunk * kSelChunk;
-
-  // ---- log2 Z_g from the scan blocks' (max, sum 2^x) partials; 16 threads per head
-  if (n > k && p0 <= n - 2) {
-    const int g = tid >> 4, sub = tid & 15;
-    const float2* pp = partials + (row0 + (g < G ? g : 0)) * n_parts;
-    float m = -INFINITY, l = 0.0f;
-    if (g < G)
-      for (int t = sub; t < n_parts; t += 16) m = fmaxf(m, pp[t].x);
-    for (int o = 8; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-    if (g < G && m > -INFINITY)
-      for (int t = sub; t < n_parts; t += 16) {
-        const float2 v = pp[t];
-        if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
-      }
-    for (int o = 8; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
-    if (g < G && sub == 0) s_lz2[g] = m + __builtin_amdgcn_logf(l);
-    __syncthreads();
-  }
-
-  // ---- 1+2: chunk-local top K of the candidate pages
-  if (n > k && p0 <= n - 2) {
-    uint32_t key[kPerThread];
-    uint32_t kmx = 0u, kmn = 0xffffffffu;
-    int local = 0;
-#pragma unroll
-    for (int u = 0; u < kPerThread; ++u) {
-      const int j = p0 + tid + kSelThreads * u;
-      key[u] = 0u;
-      if (j >= 1 && j <= n - 2) {
-        float m = -INFINITY;
-        for (int g = 0; g < G; ++g)
-          m = fmaxf(m, s_hat[(row0 + g) * s_hat_stride + j] * kLog2e - s_lz2[g]);
-        float sum = 0.0f;
-        for (int g = 0; g < G; ++g)
-          sum += __builtin_amdgcn_exp2f(s_hat[(row0 + g) * s_hat_stride + j] * kLog2e - s_lz2[g] - m);
-        key[u] = max(1u, f32_order_key(m + __builtin_amdgcn_logf(sum)));
-        kmx = max(kmx, key[u]);
-        kmn = min(kmn, key[u]);
-        ++local;
-      }
-    }
-    const int n_cand = block_sum(local, red, par); par ^= 1;
-    uint32_t T = 1u;
-    int take_eq = 1 << 30;
-    if (n_cand > K) {
-      block_minmax(kmn, kmx, red);
-      uint32_t lo = kmn, hi = kmx;  // invariant: #{key >= lo} >= K
-      while (lo < hi) {
-        const uint32_t mid = lo + (uint32_t)((((uint64_t)hi - lo) + 1) >> 1);
-        int c = 0;
-#pragma unroll
-        for (int u = 0; u < kPerThread; ++u) c += key[u] >= mid;
-        if (block_sum(c, red, par) >= K) lo = mid; else hi = mid - 1;
-        par ^= 1;
-      }
-      T = lo;
-      int c = 0;
-#pragma unroll
-      for (int u = 0; u < kPerThread; ++u) c += key[u] > T;
-      take_eq = K - block_sum(c, red, par); par ^= 1;
-    }
-    int run_eq = 0, run_sel = 0;
-#pragma unroll
-    for (int u = 0; u < kPerThread; ++u) {
-      int tot_eq, tot_sel;
-      const bool eq = key[u] != 0u && key[u] == T;
-      const int before_eq = block_excl(eq, red, par, &tot_eq); par ^= 1;
-      const bool sel = (key[u] != 0u && key[u] > T) || (eq && run_eq + before_eq < take_eq);
-      const int before_sel = block_excl(sel, red, par, &tot_sel); par ^= 1;
-      if (sel) {
-        cand_key[(ch_base + chunk) * K + run_sel + before_sel] = key[u];
-        cand_idx[(ch_base + chunk) * K + run_sel + before_sel] = p0 + tid + kSelThreads * u;
-      }
-      run_eq += tot_eq;
-      run_sel += tot_sel;
-    }
-    for (int t = run_sel + tid; t < K; t += kSelThreads) {
-      cand_key[(ch_base + chunk) * K + t] = 0u;
-      cand_idx[(ch_base + chunk) * K + t] = -1;
-    }
-  }
-
-  // ---- 3: the last block of this (sequence, KV head) merges
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) red.flag = atomicAdd(&counters[s * H_kv + h], 1) == n_chunks - 1;
-  __syncthreads();
-  if (!red.flag) return;
-  __threadfence();
   int32_t* ids = out_ids + ((long)s * H_kv + h) * k;
   if (n <= k) {
     for (int t = tid; t < k; t += kSelThreads) ids[t] = t < n ? t : -1;
   } else {
     const int used = (n - 2) / kSelChunk + 1;  // chunks that hold candidates (pages 1..n-2)
     const int N = used * K;
-    const bool in_lds = N <= kLdsCand;
-    const uint32_t* gk = cand_key + ch_base * K;
-    const int32_t* gi = cand_idx + ch_base * K;
-    if (in_lds) {
-      for (int e = tid; e < N; e += kSelThreads) { s_key[e] = gk[e]; s_idx[e] = gi[e]; }
-      __syncthreads();
-    }
-    uint32_t kmx = 0u, kmn = 0xffffffffu;
-    for (int e = tid; e < N; e += kSelThreads) {
-      const uint32_t v = in_lds ? s_key[e] : gk[e];
-      if (v) { kmx = max(kmx, v); kmn = min(kmn, v); }
-    }
-    block_minmax(kmn, kmx, red);
-    uint32_t lo = kmn, hi = kmx;
-    while (lo < hi) {
-      const uint32_t mid = lo + (uint32_t)((((uint64_t)hi - lo) + 1) >> 1);
-      int c = 0;
-      for (int e = tid; e < N; e += kSelThreads) c += (in_lds ? s_key[e] : gk[e]) >= mid;
-      if (block_sum(c, red, par) >= K) lo = mid; else hi = mid - 1;
-      par ^= 1;
-    }
-    const uint32_t T = lo;
-    int c = 0;
-    for (int e = tid; e < N; e += kSelThreads) c += (in_lds ? s_key[e] : gk[e]) > T;
-    const int take_eq = K - block_sum(c, red, par);
-    par ^= 1;
-    // survivors are ascending in page index (chunk order, ascending inside a chunk)
-    int run_eq = 0, run_sel = 0;
-    for (int base = 0; base < N; base += kSelThreads) {
-      const int e = base + tid;
-      const uint32_t v = e < N ? (in_lds ? s_key[e] : gk[e]) : 0u;
-      int tot_eq, tot_sel;
-      const bool eq = v != 0u && v == T;
-      const int before_eq = block_excl(eq, red, par, &tot_eq); par ^= 1;
-      const bool sel = (v != 0u && v > T) || (eq && run_eq + before_eq < take_eq);
-      const int before_sel = block_excl(sel, red, par, &tot_sel); par ^= 1;
-      if (sel) ids[1 + run_sel + before_sel] = in_lds ? s_idx[e] : gi[e];
-      run_eq += tot_eq;
-      run_sel += tot_sel;
-    }
+    const long base = ((long)s * H_kv + h) * n_chunks * K;
+    if (K > 0 && N <= kSelThreads * kMergeRegs)
+      merge_select<true>(N, K, cand_key + base, cand_idx + base, ids, red);
+    else if (K > 0)
+      merge_select<false>(N, K, cand_key + base, cand_idx + base, ids, red);
     if (tid == 0) { ids[0] = 0; ids[k - 1] = n - 1; }
   }
   __syncthreads();
+  const float* sb = s_hat + lay.base(s, h);
   for (int e = tid; e < G * k; e += kSelThreads) {
     const int g = e / k, t = e % k;
     const int id = ids[t];
     out_sel_lse[(row0 + g) * k + t] =
-        (id >= 0 && id < n_c) ? s_hat[(row0 + g) * s_hat_stride + id] : __int_as_float(0x7fc00000);
+        (id >= 0 && id < n_c) ? sb[(long)id * lay.page + (long)g * lay.head] : __int_as_float(0x7fc00000);
   }
-  if (tid == 0) counters[s * H_kv + h] = 0;
 }
 
 }  // namespace
 
 hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
-                         int s_hat_stride, const float2* partials, uint32_t* cand_key,
-                         int32_t* cand_idx, int n_chunks, int* counters, int32_t* out_page_ids,
+                         SHatLayout lay, const float2* partials, uint32_t* cand_key,
+                         int32_t* cand_idx, int n_chunks, int32_t* out_page_ids,
                          float* out_sel_lse, hipStream_t st) {
   const int k = page_budget(c);
-  hipLaunchKernelGGL(select_kernel, dim3(n_chunks, c.num_kv_heads, c.num_seqs), dim3(kSelThreads),
-                     0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq, k, n_chunks,
-                     seq_lens, s_hat, s_hat_stride, partials, scan_blocks(c), cand_key, cand_idx,
-                     counters, out_page_ids, out_sel_lse);
+  hipLaunchKernelGGL(select_chunk_kernel, dim3(n_chunks, c.num_kv_heads, c.num_seqs),
+                     dim3(kSelThreads), 0, st, c.num_q_heads, c.num_kv_heads, k, n_chunks, seq_lens,
+                     s_hat, lay, partials, scan_blocks(c), cand_key, cand_idx);
+  hipLaunchKernelGGL(select_merge_kernel, dim3(c.num_kv_heads, c.num_seqs), dim3(kSelThreads), 0,
+                     st, c.num_q_heads, c.num_kv_heads, k, n_chunks, seq_lens, s_hat, lay,
+                     cand_key, cand_idx, out_page_ids, out_sel_lse);
   return hipGetLastError();
 }
 

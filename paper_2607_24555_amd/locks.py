@@ -143,8 +143,7 @@ def alloc_workspace(cfg: Config, device="cuda") -> torch.Tensor:
     n = workspace_bytes(cfg)
     if n == 0:
         raise LocksError("invalid configuration")
-    # zero-filled once: the kernels' completion counters start (and end) at zero
-    return torch.zeros(n, dtype=torch.uint8, device=device)
+    return torch.empty(n, dtype=torch.uint8, device=device)
 
 
 def alloc_summaries(cfg: Config, device="cuda") -> torch.Tensor:
