@@ -37,6 +37,8 @@ struct Ws {
   float2* part;
   uint32_t* ckey;
   int32_t* cidx;
+  uint32_t* keys;
+  uint32_t* thr;
   float* attn;
 };
 
@@ -44,6 +46,7 @@ Ws carve(void* ws, const WsPlan& p) {
   char* b = static_cast<char*>(ws);
   return Ws{reinterpret_cast<float*>(b + p.s_hat_off), reinterpret_cast<float2*>(b + p.part_off),
             reinterpret_cast<uint32_t*>(b + p.ckey_off), reinterpret_cast<int32_t*>(b + p.cidx_off),
+            reinterpret_cast<uint32_t*>(b + p.keys_off), reinterpret_cast<uint32_t*>(b + p.thr_off),
             reinterpret_cast<float*>(b + p.attn_off)};
 }
 
@@ -77,6 +80,8 @@ WsPlan plan_workspace(const locks_cfg_t& c) {
   p.part_off = take(S * Hq * (size_t)scan_blocks(c) * sizeof(float2));
   p.ckey_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(uint32_t));
   p.cidx_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(int32_t));
+  p.keys_off = take(S * Hkv * mp * sizeof(uint32_t));
+  p.thr_off = take(S * Hkv * (size_t)p.n_chunks * sizeof(uint32_t));
   p.attn_off = take(S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float));
   p.total = off;
   return p;
@@ -91,8 +96,8 @@ static int select_impl(const locks_cfg_t* c, const void* q, const void* summarie
   const SHatLayout lay = out_all_lse ? shat_head_major(*c) : shat_head_minor(*c);
   hipError_t e = launch_scan(*c, q, summaries, page_table, seq_lens, s_hat, lay, w.part, st);
   if (e != hipSuccess) return hip_status(e);
-  e = launch_select(*c, seq_lens, s_hat, lay, w.part, w.ckey, w.cidx, p.n_chunks, out_page_ids,
-                    out_sel_lse, st);
+  const SelectBufs sb{w.ckey, w.cidx, w.keys, w.thr, p.n_chunks};
+  e = launch_select(*c, seq_lens, s_hat, lay, w.part, sb, out_page_ids, out_sel_lse, st);
   return hip_status(e);
 }
 

@@ -83,6 +83,8 @@ struct WsPlan {
   size_t part_off;    // float2 [S][H_q][scan blocks]     (max, sum exp), log2 domain
   size_t ckey_off;    // uint32 [S][H_kv][chunks][k-2]    per-chunk survivors (keys)
   size_t cidx_off;    // int32  [S][H_kv][chunks][k-2]    per-chunk survivors (pages)
+  size_t keys_off;    // uint32 [S][H_kv][max_pages]      share-averaged page keys
+  size_t thr_off;     // uint32 [S][H_kv][chunks]         per-chunk cut (lower bound)
   size_t attn_off;    // float [S][H_q][splits][d + 2]    split-K partials
   size_t total;
   int n_chunks;       // select chunks per sequence
@@ -90,7 +92,8 @@ struct WsPlan {
 };
 
 constexpr int kScanPagesPerBlock = 256;  // 4 waves x 64 pages
-constexpr int kSelChunk = 1024;          // pages per select block
+constexpr int kSelChunk = 1024;          // pages per select block (generic path)
+constexpr int kFastChunk = 4096;         // pages per select block (wave-level path)
 constexpr int kSparsePagesPerSplit = 8;
 constexpr int kDensePagesPerSplit = 64;
 
@@ -112,10 +115,17 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
                        const int32_t* page_table, const int32_t* seq_lens, float* s_hat,
                        SHatLayout lay, float2* partials, hipStream_t st);
 
+struct SelectBufs {
+  uint32_t* cand_key;
+  int32_t* cand_idx;
+  uint32_t* keys;
+  uint32_t* thr;
+  int n_chunks;
+};
+bool select_fast_path(const locks_cfg_t& c);
 hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
-                         SHatLayout lay, const float2* partials, uint32_t* cand_key,
-                         int32_t* cand_idx, int n_chunks, int32_t* out_page_ids,
-                         float* out_sel_lse, hipStream_t st);
+                         SHatLayout lay, const float2* partials, const SelectBufs& sb,
+                         int32_t* out_page_ids, float* out_sel_lse, hipStream_t st);
 
 hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cache,
                          const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,

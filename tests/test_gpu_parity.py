@@ -277,6 +277,10 @@ def test_build_factors_reconstruct_like_oracle(case):
     (8, [0, 15, 16, 33, 160, 161, 2000], 1, 48, "bf16"),
     (4, [2048, 1, 999, 32], 15, 512, "fp32"),
     (2, [4096 * 4 + 3, 64], 8, 2048, "bf16"),
+    # budget above 2080 tokens: the block-level (generic) selection path
+    (4, [16 * 700 + 7, 16 * 300, 5000, 16 * 257], 8, 4096, "bf16"),
+    # more than 4096 pages per sequence: several wave-level selection chunks
+    (2, [4096 * 16 * 2 + 37, 4096 * 16 + 80], 2, 256, "bf16"),
 ])
 def test_edge_batches(G, lens, rank, budget, kv):
     """Empty, sub-page, exact-page, tiny-budget and n <= k sequences in one batch."""
@@ -291,3 +295,22 @@ def test_edge_batches(G, lens, rank, budget, kv):
     ids2, sel2, out2, lse2 = B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws)
     torch.cuda.synchronize()
     assert torch.equal(ids, ids2) and torch.equal(out, out2)
+
+
+def test_identical_pages_tie_break():
+    """Every page holds the same keys, so all page scores tie exactly: the table
+    is the sink, the k - 2 lowest candidate pages and the recent page (ties go
+    to the lower page), across two selection chunks."""
+    n = 5001
+    spec = WorkloadSpec("ties", 1, 8, 2, [16 * (n - 1) + 3], 4, 1024, "bf16", "bf16")
+    w = build_workload(spec, 5)
+    w.k_cache[:] = w.k_cache[:1].clone()
+    d = Dev(w)
+    cfg = d.cfg
+    store, recs = d.oracle_summaries()
+    ids, sel, out, lse = B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws)
+    torch.cuda.synchronize()
+    want = [0] + list(range(1, cfg.k - 1)) + [n - 1]
+    for h in range(cfg.num_kv_heads):
+        assert ids_of(ids[0, h].tolist()) == want
+    _check_step_against_oracle("ties", d, recs, ids, out, lse, min_same_frac=1.0)
