@@ -9,6 +9,11 @@
 // page load), then writes an unnormalised partial (o, max, sum).  merge_kernel
 // combines the splits exactly: m = max m_s, l = sum l_s e^{m_s - m},
 // o = sum o_s e^{m_s - m} / l, lse = m + log l.
+//
+// bf16 Q and KV take attend_mfma_kernel: each wave owns pages_per_split / 4
+// consecutive list entries and handles one page (16 tokens) per step on the
+// matrix cores; the block's four waves combine in LDS before the partial is
+// written.  Other dtypes take the VALU kernel attend_kernel.
 #include "locks_internal.h"
 
 namespace locks {
@@ -106,6 +111,188 @@ __global__ __launch_bounds__(kAttnBlock) void attend_kernel(
   }
 }
 
+
+// ---------------------------------------------------------------- MFMA path
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+typedef short s4v __attribute__((ext_vector_type(4)));
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ bf8v as_bf8(uint4 v) { return __builtin_bit_cast(bf8v, v); }
+
+// Round-to-nearest-even float -> bf16 bits (finite inputs).
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Sum / max over the lanes {l, l^16, l^32, l^48} (the four 16-lane rows).
+__device__ __forceinline__ float rows_max(float v) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float rows_sum(float v) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// 16-bit element e (0..7) of a uint4.
+__device__ __forceinline__ uint32_t half_of(const uint4& v, int e) {
+  const uint32_t w = e < 2 ? v.x : (e < 4 ? v.y : (e < 6 ? v.z : v.w));
+  return (e & 1) ? (w >> 16) : (w & 0xffffu);
+}
+
+// One page of K (16 tokens x 128) and V in the operand layouts below.
+struct PageRegs {
+  uint4 k[4];  // lane (t = l % 16, r = l / 16): K[t][32 r + 8 kb .. + 7], kb = 0..3
+  uint4 v[4];  // lane (c = l % 16, r): V[4 r + j][8 c .. 8 c + 7], j = 0..3
+};
+
+__device__ __forceinline__ void load_page(PageRegs& P, const uint16_t* kp, const uint16_t* vp,
+                                          int c16, int r4) {
+  const uint4* k4 = reinterpret_cast<const uint4*>(kp + c16 * kDim + 32 * r4);
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) P.k[kb] = k4[kb];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) P.v[j] = *reinterpret_cast<const uint4*>(vp + (4 * r4 + j) * kDim + 8 * c16);
+}
+
+// Lane layout (l = 16 r + c):
+//   S^T = K Q^T  (mfma 16x16x32, M = token, N = head, K = dim with dim order
+//                 32 r + 8 kb + e): lane holds S^T[4 r + j][c], j = 0..3, so head
+//                 c's 16 logits are the j values of lanes c, c+16, c+32, c+48;
+//   O^T += V^T P (mfma 16x16x16, M = dim, N = head, K = token; tile n covers
+//                 dims 8 m + n, m = 0..15): P is the B operand exactly as S^T
+//                 left it, and lane holds O^T for head c, dims 32 r + 8 j + n.
+// P enters as bf16 hi + lo (two MFMAs) so the weights keep ~16 bits.
+__global__ __launch_bounds__(256) void attend_mfma_kernel(
+    int H_q, int H_kv, int max_pages, int k_list, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
+    const int32_t* __restrict__ page_ids, int pages_per_split, int n_splits,
+    float* __restrict__ partial) {
+  __shared__ float sO[4][kMaxGroup][kDim];
+  __shared__ float sM[4][kMaxGroup], sL[4][kMaxGroup];
+  const int split = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c16 = lane & 15, r4 = lane >> 4;
+  const int G = H_q / H_kv;
+  const int L = seq_lens[s];
+  const int n = (L + kPage - 1) / kPage;
+  const float zs = kLog2e / sqrtf((float)kDim);
+
+  uint4 qb[4];
+  {
+    const int g = c16 < G ? c16 : 0;
+    const uint4* q4 = reinterpret_cast<const uint4*>(q + ((long)s * H_q + h * G + g) * kDim + 32 * r4);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) qb[kb] = c16 < G ? q4[kb] : make_uint4(0, 0, 0, 0);
+  }
+  const int ppw = pages_per_split / 4;
+  const int t_begin = split * pages_per_split + wave * ppw, t_end = t_begin + ppw;
+  const int32_t* ids = page_ids ? page_ids + ((long)s * H_kv + h) * k_list : nullptr;
+  auto page_at = [&](int t) -> int {
+    int id = -1;
+    if (t < t_end) id = ids ? (t < k_list ? ids[t] : -1) : t;
+    return (id >= 0 && id < n) ? id : -1;
+  };
+  const long kv_head = (long)h * kPage * kDim;
+  const long kv_blk = (long)H_kv * kPage * kDim;
+  auto page_ptr = [&](int id, const uint16_t* base) {
+    const long blk = page_table[(long)s * max_pages + (id >= 0 ? id : 0)];
+    return base + blk * kv_blk + kv_head;
+  };
+
+  float m = -INFINITY, l = 0.0f;
+  f4v o[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) o[t] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+
+  if (n > 0) {
+    int id = page_at(t_begin);
+    PageRegs cur;
+    load_page(cur, page_ptr(id, k_cache), page_ptr(id, v_cache), c16, r4);
+    for (int t = t_begin; t < t_end; ++t) {
+      // prefetch the next entry (a valid page stands in for an empty one)
+      const int id_next = page_at(t + 1);
+      PageRegs nxt;
+      if (t + 1 < t_end)
+        load_page(nxt, page_ptr(id_next, k_cache), page_ptr(id_next, v_cache), c16, r4);
+      if (id >= 0) {
+        const int valid = min(kPage, L - id * kPage);
+        f4v st = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+          st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(cur.k[kb]), as_bf8(qb[kb]), st, 0, 0, 0);
+        float z[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) z[j] = (4 * r4 + j < valid) ? st[j] * zs : -INFINITY;
+        const float pm = rows_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
+        const float mn = fmaxf(m, pm);
+        const float sc = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - mn);
+        float p[4], ps = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          p[j] = (z[j] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(z[j] - mn);
+          ps += p[j];
+        }
+        l = l * sc + rows_sum(ps);
+        m = mn;
+        uint32_t hi[4], lo[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          hi[j] = bf16_rne(p[j]);
+          lo[j] = bf16_rne(p[j] - __uint_as_float(hi[j] << 16));
+        }
+        const s4v bh = __builtin_bit_cast(s4v, make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16)));
+        const s4v bl = __builtin_bit_cast(s4v, make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)));
+#pragma unroll
+        for (int t8 = 0; t8 < 8; ++t8) {
+          o[t8] *= sc;
+          const uint32_t a01 = half_of(cur.v[0], t8) | (half_of(cur.v[1], t8) << 16);
+          const uint32_t a23 = half_of(cur.v[2], t8) | (half_of(cur.v[3], t8) << 16);
+          const s4v a = __builtin_bit_cast(s4v, make_uint2(a01, a23));
+          o[t8] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bh, o[t8], 0, 0, 0);
+          o[t8] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bl, o[t8], 0, 0, 0);
+        }
+      }
+      id = id_next;
+      cur = nxt;
+    }
+  }
+  // combine the block's four waves; m is kept in log2 units until here
+  if (r4 == 0) { sM[wave][c16] = m; sL[wave][c16] = l; }
+#pragma unroll
+  for (int t8 = 0; t8 < 8; ++t8)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sO[wave][c16][32 * r4 + 8 * j + t8] = o[t8][j];
+  __syncthreads();
+  for (int e = tid; e < G * (kDim + 2); e += 256) {
+    const int g = e / (kDim + 2), c = e % (kDim + 2);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, sM[w][g]);
+    float acc = 0.0f, ls = 0.0f;
+    if (mx > -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float wt = sM[w][g] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(sM[w][g] - mx);
+        ls += sL[w][g] * wt;
+        if (c < kDim) acc += sO[w][g][c] * wt;
+      }
+    }
+    const float v = c < kDim ? acc : (c == kDim ? (mx == -INFINITY ? mx : mx * kLn2) : ls);
+    const long row = (long)s * H_q + h * G + g;
+    partial[(row * n_splits + split) * (kDim + 2) + c] = v;
+  }
+}
+
 __global__ __launch_bounds__(kDim) void merge_kernel(int H_q, int n_splits,
                                                      const float* __restrict__ partial,
                                                      float* __restrict__ out,
@@ -113,17 +300,35 @@ __global__ __launch_bounds__(kDim) void merge_kernel(int H_q, int n_splits,
   const int hq = blockIdx.x, s = blockIdx.y, c = threadIdx.x;
   const long row = (long)s * H_q + hq;
   const float* p = partial + row * n_splits * (kDim + 2);
-  float m = -INFINITY;
-  for (int t = 0; t < n_splits; ++t) m = fmaxf(m, p[t * (kDim + 2) + kDim]);
-  float l = 0.0f, o = 0.0f;
-  if (m > -INFINITY) {
-    for (int t = 0; t < n_splits; ++t) {
-      const float mt = p[t * (kDim + 2) + kDim];
-      if (mt == -INFINITY) continue;
-      const float w = __expf(mt - m);
-      l += p[t * (kDim + 2) + kDim + 1] * w;
-      o += p[t * (kDim + 2) + c] * w;
+  constexpr int kB = 8;
+  float m = -INFINITY, l = 0.0f, o = 0.0f;
+  for (int t0 = 0; t0 < n_splits; t0 += kB) {
+    float mt[kB], lt[kB], ot[kB];
+#pragma unroll
+    for (int u = 0; u < kB; ++u) {
+      const float* pt = p + (long)min(t0 + u, n_splits - 1) * (kDim + 2);
+      mt[u] = pt[kDim];
+      lt[u] = pt[kDim + 1];
+      ot[u] = pt[c];
     }
+#pragma unroll
+    for (int u = 0; u < kB; ++u) asm volatile("" : "+v"(mt[u]), "+v"(lt[u]), "+v"(ot[u]));
+#pragma unroll
+    for (int u = 0; u < kB; ++u) mt[u] = t0 + u < n_splits ? mt[u] : -INFINITY;
+    float mm = m;
+#pragma unroll
+    for (int u = 0; u < kB; ++u) mm = fmaxf(mm, mt[u]);
+    if (mm == -INFINITY) continue;
+    const float sc = (m == -INFINITY) ? 0.0f : __expf(m - mm);
+    l *= sc;
+    o *= sc;
+#pragma unroll
+    for (int u = 0; u < kB; ++u) {
+      const float w = (mt[u] == -INFINITY) ? 0.0f : __expf(mt[u] - mm);
+      l += lt[u] * w;
+      o += ot[u] * w;
+    }
+    m = mm;
   }
   out[row * kDim + c] = (l > 0.0f) ? o / l : 0.0f;
   if (out_lse && c == 0) out_lse[row] = (l > 0.0f) ? m + logf(l) : -INFINITY;
@@ -148,8 +353,11 @@ hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cach
                          float* partial, float* out, float* out_lse, hipStream_t st) {
   const bool qb = c.q_dtype == LOCKS_BF16, kb = c.kv_dtype == LOCKS_BF16;
   if (qb && kb)
-    launch_typed<uint16_t, uint16_t>(c, q, k_cache, v_cache, page_table, seq_lens, page_ids,
-                                     pages_per_split, n_splits, partial, st);
+    hipLaunchKernelGGL(attend_mfma_kernel, dim3(n_splits, c.num_kv_heads, c.num_seqs), dim3(256), 0,
+                       st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq, page_budget(c),
+                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
+                       static_cast<const uint16_t*>(v_cache), page_table, seq_lens, page_ids,
+                       pages_per_split, n_splits, partial);
   else if (qb)
     launch_typed<uint16_t, float>(c, q, k_cache, v_cache, page_table, seq_lens, page_ids,
                                   pages_per_split, n_splits, partial, st);

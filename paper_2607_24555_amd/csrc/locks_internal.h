@@ -94,8 +94,8 @@ struct WsPlan {
 constexpr int kScanPagesPerBlock = 256;  // 4 waves x 64 pages
 constexpr int kSelChunk = 1024;          // pages per select block (generic path)
 constexpr int kFastChunk = 4096;         // pages per select block (wave-level path)
-constexpr int kSparsePagesPerSplit = 8;
-constexpr int kDensePagesPerSplit = 64;
+constexpr int kSparsePagesPerSplit = 4;   // one page per wave of a 4-wave block
+constexpr int kDensePagesPerSplit = 256;
 
 WsPlan plan_workspace(const locks_cfg_t& c);
 int page_budget(const locks_cfg_t& c);  // k = ceil(b / 16)
