@@ -387,7 +387,7 @@ __device__ __forceinline__ void fast_issue(FastRegs<R>& T, const uint8_t* __rest
 __device__ __forceinline__ int sbyte(int x) { return (int)(int8_t)(x & 0xff); }
 
 template <typename QT, int R, int NPACK>
-__global__ __launch_bounds__(256) void scan_fast_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_fast_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     float* __restrict__ s_hat, SHatLayout lay, float2* __restrict__ partials) {
@@ -411,8 +411,8 @@ __global__ __launch_bounds__(256) void scan_fast_kernel(
   float run_m = -INFINITY, run_s = 0.0f;
 
   if (pg * 64 < n_c) {
-    FastRegs<R> buf[2];
-    fast_issue<R>(buf[0], summ, pt_row, pg * 64, n_c, H_kv, h, lane);
+    FastRegs<R> cur;
+    fast_issue<R>(cur, summ, pt_row, pg * 64, n_c, H_kv, h, lane);
 
     // ---- query digits: lane (head gcol, K slice grp); K order matches the decoders
     // element e of MFMA half hh <-> d = 32 grp + 16 hh + perm16[e]
@@ -466,9 +466,6 @@ __global__ __launch_bounds__(256) void scan_fast_kernel(
     for (int t = 0; t < 4; ++t) {
       const int page0 = (pg * 4 + t) * 16;
       if (page0 < n_c) {
-        FastRegs<R>& cur = buf[t & 1];
-        if (t + 1 < 4 && page0 + 16 < n_c)
-          fast_issue<R>(buf[(t + 1) & 1], summ, pt_row, page0 + 16, n_c, H_kv, h, lane);
 #pragma unroll
         for (int u = 0; u < Gm::kTailLoads; ++u) {
           const int c = lane + 64 * u;
@@ -481,6 +478,7 @@ __global__ __launch_bounds__(256) void scan_fast_kernel(
         float vals[4 * Gm::kSets];
 #pragma unroll
         for (int st = 0; st < Gm::kSets; ++st) {
+          if (st % 4 == 0) __builtin_amdgcn_sched_barrier(0);
           const uint32_t w[4] = {cur.vb[st].x, cur.vb[st].y, cur.vb[st].z, cur.vb[st].w};
           i4v acc[3];
 #pragma unroll
@@ -503,6 +501,12 @@ __global__ __launch_bounds__(256) void scan_fast_kernel(
             vals[4 * st + j] = v * (vs * inv_scale);
           }
         }
+        // the record registers are consumed: fetch the next 16 pages into them while
+        // the rest of this step runs from LDS and registers
+        __builtin_amdgcn_sched_barrier(0);
+        if (t + 1 < 4 && page0 + 16 < n_c)
+          fast_issue<R>(cur, summ, pt_row, page0 + 16, n_c, H_kv, h, lane);
+        __builtin_amdgcn_sched_barrier(0);
         // ---- centroid term (int8 MFMA, one page per row): sA[page][col]
         {
           const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][col][Gm::kMu + 32 * grp]);
@@ -537,6 +541,7 @@ __global__ __launch_bounds__(256) void scan_fast_kernel(
         // ---- stage 2 (fp32 MFMA): 16 logits per (page, head), NPACK pages per pass
 #pragma unroll
         for (int ps = 0; ps < kPasses; ++ps) {
+          if (ps % 4 == 0) __builtin_amdgcn_sched_barrier(0);
           const int pcpage = ps * NPACK + pcol;  // page of this lane's column
           f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
