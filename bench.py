@@ -100,8 +100,8 @@ def cpu_baseline(w, cfg, sample_pages):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is "
-                                   "described in DESIGN.md and not implemented",
+        print(json.dumps({"error": "the Locks decode step runs on one GPU; sharding across "
+                                   "GPUs is not implemented",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch

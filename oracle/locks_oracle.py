@@ -19,7 +19,7 @@ the paper states it:
   recent page always kept (Sec. 4 "Score"; Cor. "Group-shared selection");
 * exact attention restricted to the selected pages (Sec. 2; App. E).
 
-Readings of points the paper leaves open (each also listed in the design doc):
+Readings of points the paper leaves open:
 
 * scale 1/sqrt(d) in both the score and attention;
 * a mode is dropped when sigma^2 <= max(ZERO_MODE_REL * sigma_1^2,
