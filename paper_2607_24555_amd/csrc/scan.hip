@@ -386,6 +386,64 @@ __device__ __forceinline__ void fast_issue(FastRegs<R>& T, const uint8_t* __rest
 
 __device__ __forceinline__ int sbyte(int x) { return (int)(int8_t)(x & 0xff); }
 
+// Query digits of head gcol for the int8 projection: q is scaled by a power of
+// two to a 22-bit fixed-point integer and split into three signed 8-bit digits
+// (most significant first).  Element e of MFMA half hh <-> d = 32 grp + 16 hh +
+// perm16[e], the order in which the decoders expand the packed codes.  bias[t]
+// = -8 * sum(digit t) removes the excess-8 offset of the int4 codes.
+struct QDigits {
+  i4v bd[3][2];
+  int bias[3];
+  float inv_scale;  // fixed-point unit * log2(e) / sqrt(d)
+};
+
+template <typename QT>
+__device__ __forceinline__ QDigits q_digits(const QT* __restrict__ qrow, int grp) {
+  constexpr int kPerm16[16] = {0, 2, 4, 6, 1, 3, 5, 7, 8, 10, 12, 14, 9, 11, 13, 15};
+  constexpr float c0 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
+  QDigits D;
+  float qf[32];
+  float qmax = 0.0f;
+#pragma unroll
+  for (int c = 0; c < 32; ++c) {
+    qf[c] = load_q(qrow + 32 * grp, c);
+    qmax = fmaxf(qmax, fabsf(qf[c]));
+  }
+  qmax = red4_max(qmax);
+  int ex = 0;
+  (void)frexpf(qmax, &ex);  // qmax < 2^ex
+  const float qscale = ldexpf(1.0f, 22 - ex);
+  D.inv_scale = ldexpf(1.0f, ex - 22) * c0;
+  float bsum[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int dw = 0; dw < 4; ++dw) {
+      uint32_t w0 = 0, w1 = 0, w2 = 0;
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) {
+        const int e = 4 * dw + bb;
+        const int Q = (qmax > 0.0f) ? (int)rintf(qf[16 * hh + kPerm16[e]] * qscale) : 0;
+        const int d2 = sbyte(Q);
+        const int q1 = (Q - d2) >> 8;
+        const int d1 = sbyte(q1);
+        const int d0 = (q1 - d1) >> 8;
+        bsum[0] += (float)d0;
+        bsum[1] += (float)d1;
+        bsum[2] += (float)d2;
+        w0 |= (uint32_t)(d0 & 0xff) << (8 * bb);
+        w1 |= (uint32_t)(d1 & 0xff) << (8 * bb);
+        w2 |= (uint32_t)(d2 & 0xff) << (8 * bb);
+      }
+      D.bd[0][hh][dw] = (int)w0;
+      D.bd[1][hh][dw] = (int)w1;
+      D.bd[2][hh][dw] = (int)w2;
+    }
+#pragma unroll
+  for (int t = 0; t < 3; ++t) D.bias[t] = -8 * (int)red4_sum(bsum[t]);
+  return D;
+}
+
 template <typename QT, int R, int NPACK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_fast_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
@@ -414,53 +472,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     FastRegs<R> cur;
     fast_issue<R>(cur, summ, pt_row, pg * 64, n_c, H_kv, h, lane);
 
-    // ---- query digits: lane (head gcol, K slice grp); K order matches the decoders
-    // element e of MFMA half hh <-> d = 32 grp + 16 hh + perm16[e]
-    constexpr int kPerm16[16] = {0, 2, 4, 6, 1, 3, 5, 7, 8, 10, 12, 14, 9, 11, 13, 15};
-    float qf[32];
-    float qmax = 0.0f;
-    {
-      const QT* qrow = q + (row0 + gcol) * kDim + 32 * grp;
-#pragma unroll
-      for (int c = 0; c < 32; ++c) {
-        qf[c] = load_q(qrow, c);
-        qmax = fmaxf(qmax, fabsf(qf[c]));
-      }
-    }
-    qmax = red4_max(qmax);
-    int ex = 0;
-    (void)frexpf(qmax, &ex);                 // qmax < 2^ex
-    const float qscale = ldexpf(1.0f, 22 - ex);
-    const float inv_scale = ldexpf(1.0f, ex - 22) * c0;
-    i4v bd[3][2];
-    float bsum[3] = {0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-      for (int dw = 0; dw < 4; ++dw) {
-        uint32_t w0 = 0, w1 = 0, w2 = 0;
-#pragma unroll
-        for (int bb = 0; bb < 4; ++bb) {
-          const int e = 4 * dw + bb;
-          const int Q = (qmax > 0.0f) ? (int)rintf(qf[16 * hh + kPerm16[e]] * qscale) : 0;
-          const int d2 = sbyte(Q);
-          const int q1 = (Q - d2) >> 8;
-          const int d1 = sbyte(q1);
-          const int d0 = (q1 - d1) >> 8;
-          bsum[0] += (float)d0;
-          bsum[1] += (float)d1;
-          bsum[2] += (float)d2;
-          w0 |= (uint32_t)(d0 & 0xff) << (8 * bb);
-          w1 |= (uint32_t)(d1 & 0xff) << (8 * bb);
-          w2 |= (uint32_t)(d2 & 0xff) << (8 * bb);
-        }
-        bd[0][hh][dw] = (int)w0;
-        bd[1][hh][dw] = (int)w1;
-        bd[2][hh][dw] = (int)w2;
-      }
-    int bias[3];
-#pragma unroll
-    for (int t = 0; t < 3; ++t) bias[t] = -8 * (int)red4_sum(bsum[t]);
+    const QDigits QD = q_digits(q + (row0 + gcol) * kDim, grp);
+    const float inv_scale = QD.inv_scale;
+    const i4v(&bd)[3][2] = QD.bd;
+    const int(&bias)[3] = QD.bias;
 
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -596,6 +611,204 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
 }
 
+// ---------------------------------------------------------------------------
+// r = 8, G = 16: stage 2 with (page, token) rows.
+//
+// Stage 1 is the int8 projection above.  Stage 2 reconstructs the logits of
+// four pages at a time with one f16 MFMA 16x16x32 (B as hi + lo): rows m are
+// (page a = m / 4 of the quad, token 4 ps + m % 4), K index 8 kg + e is (page
+// e / 2 of the quad, basis column 4 (e % 2) + kg), so A is block diagonal and B
+// is exactly stage-1 registers vals[8 Q + e] of lane group kg.  After the four
+// passes of a quad each lane holds all 16 logits of (page 4 Q + grp, head col)
+// and takes the page LSE in registers.  The centroid MFMA reads its rows in the
+// order page 4 (row & 3) + (row >> 2), which leaves a(page 4 j + grp, head col)
+// in register j of the same lanes.  Coefficient rows are copied to LDS with
+// their bytes reordered to l = 0, 4, 1, 5, 2, 6, 3, 7, so that the two codes a
+// lane needs (l = grp, 4 + grp) are one 16-bit read.
+// ---------------------------------------------------------------------------
+template <typename QT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8_kernel(
+    int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
+    float* __restrict__ s_hat, SHatLayout lay, float2* __restrict__ partials) {
+  constexpr int R = 8;
+  using Gm = FastGeom<R>;
+  constexpr int G = 16;
+  __shared__ __align__(16) uint8_t sTail[4][16][Gm::kTail];
+  __shared__ float2 sRun[4][64];
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int h = blockIdx.y, s = blockIdx.z;
+  const int n_c = seq_lens[s] / kPage;
+  const int pg = blockIdx.x * 4 + wave;
+  const long row0 = (long)s * H_q + (long)h * G;
+  const int32_t* pt_row = page_table + (long)s * max_pages;
+  float run_m = -INFINITY, run_s = 0.0f;
+
+  if (pg * 64 < n_c) {
+    FastRegs<R> cur;
+    fast_issue<R>(cur, summ, pt_row, pg * 64, n_c, H_kv, h, lane);
+    const QDigits QD = q_digits(q + (row0 + col) * kDim, grp);
+    const int a_row = col >> 2, t_row = col & 3;  // A row of this lane: (page, token)
+    float* shat_base = s_hat + lay.base(s, h) + (long)col * lay.head;
+
+#pragma unroll 1
+    for (int t = 0; t < 4; ++t) {
+      const int page0 = (pg * 4 + t) * 16;
+      if (page0 >= n_c) break;
+      // ---- record tails to LDS; coefficient rows reordered to l = 0,4,1,5,2,6,3,7
+#pragma unroll
+      for (int u = 0; u < Gm::kTailLoads; ++u) {
+        const int c = lane + 64 * u;
+        if (c < 16 * Gm::kTailCh) {
+          const int o = c % Gm::kTailCh;
+          uint4 v = cur.tl[u];
+          if (o < 8) {
+            v = make_uint4(__builtin_amdgcn_perm(v.y, v.x, 0x05010400u),
+                           __builtin_amdgcn_perm(v.y, v.x, 0x07030602u),
+                           __builtin_amdgcn_perm(v.w, v.z, 0x05010400u),
+                           __builtin_amdgcn_perm(v.w, v.z, 0x07030602u));
+          }
+          *reinterpret_cast<uint4*>(&sTail[wave][c / Gm::kTailCh][o * 16]) = v;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+
+      // ---- stage 1 (int8 MFMA): vals[4 st + j] = p(page 2 st + j / 2, l = 4 (j % 2) + grp)
+      float vals[4 * Gm::kSets];
+#pragma unroll
+      for (int st = 0; st < Gm::kSets; ++st) {
+        if (st % 4 == 0) __builtin_amdgcn_sched_barrier(0);
+        const uint32_t w[4] = {cur.vb[st].x, cur.vb[st].y, cur.vb[st].z, cur.vb[st].w};
+        i4v acc[3];
+#pragma unroll
+        for (int d = 0; d < 3; ++d) acc[d] = i4v{QD.bias[d], QD.bias[d], QD.bias[d], QD.bias[d]};
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
+          const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
+                         (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+#pragma unroll
+          for (int d = 0; d < 3; ++d)
+            acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
+          const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
+          const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
+          vals[4 * st + j] = v * (vs * QD.inv_scale);
+        }
+      }
+      // the record registers are consumed: fetch the next 16 pages into them
+      __builtin_amdgcn_sched_barrier(0);
+      if (t + 1 < 4 && page0 + 16 < n_c)
+        fast_issue<R>(cur, summ, pt_row, page0 + 16, n_c, H_kv, h, lane);
+      __builtin_amdgcn_sched_barrier(0);
+
+      // ---- centroid term: areg[j] = a(page 4 j + grp, head col)
+      float areg[4];
+      {
+        const int cp = 4 * (col & 3) + (col >> 2);
+        const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][cp][Gm::kMu + 32 * grp]);
+        const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][cp][Gm::kMu + 32 * grp + 16]);
+        const uint32_t mw[8] = {m0.x ^ 0x80808080u, m0.y ^ 0x80808080u, m0.z ^ 0x80808080u,
+                                m0.w ^ 0x80808080u, m1.x ^ 0x80808080u, m1.y ^ 0x80808080u,
+                                m1.z ^ 0x80808080u, m1.w ^ 0x80808080u};
+        i4v acc[3];
+#pragma unroll
+        for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
+          const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
+                         (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
+                         (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
+                         (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
+#pragma unroll
+          for (int d = 0; d < 3; ++d)
+            acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float ms = lds_f16(&sTail[wave][4 * j + grp][Gm::kSc + 2 * (R + 16)]);
+          const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
+          areg[j] = v * (ms * QD.inv_scale);
+        }
+      }
+
+      // ---- stage 2 per quad of pages, then the page LSE in registers
+#pragma unroll
+      for (int Q = 0; Q < 4; ++Q) {
+        __builtin_amdgcn_sched_barrier(0);
+        h8 bh, bl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = vals[8 * Q + e];
+          const _Float16 hi = (_Float16)v;
+          bh[e] = hi;
+          bl[e] = (_Float16)(v - (float)hi);
+        }
+        float z[16];
+#pragma unroll
+        for (int ps = 0; ps < 4; ++ps) {
+          const uint32_t pr = *reinterpret_cast<const uint16_t*>(
+              &sTail[wave][4 * Q + a_row][(4 * ps + t_row) * R + 2 * grp]);
+          const h2 pair = as_h2(__builtin_amdgcn_perm(0x64646464u, pr, 0x05010400u)) -
+                          h2{(_Float16)1152.0f, (_Float16)1152.0f};
+          const uint32_t pw = __builtin_bit_cast(uint32_t, pair);
+          const uint4 aw = make_uint4(a_row == 0 ? pw : 0u, a_row == 1 ? pw : 0u,
+                                      a_row == 2 ? pw : 0u, a_row == 3 ? pw : 0u);
+          const h8 A = __builtin_bit_cast(h8, aw);
+          f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bh, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bl, acc, 0, 0, 0);
+          const uint2 csw = *reinterpret_cast<const uint2*>(
+              &sTail[wave][4 * Q + grp][Gm::kSc + 2 * (R + 4 * ps)]);
+          const h2 c01 = as_h2(csw.x), c23 = as_h2(csw.y);
+          z[4 * ps + 0] = fmaf((float)c01.x, acc[0], areg[Q]);
+          z[4 * ps + 1] = fmaf((float)c01.y, acc[1], areg[Q]);
+          z[4 * ps + 2] = fmaf((float)c23.x, acc[2], areg[Q]);
+          z[4 * ps + 3] = fmaf((float)c23.y, acc[3], areg[Q]);
+        }
+        float mx = z[0];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, z[i]);
+        float sm = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i] - mx);
+        const float s2 = mx + __builtin_amdgcn_logf(sm);
+        const int page = page0 + 4 * Q + grp;
+        const bool live = page < n_c;
+        if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
+        const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+        const bool up = s2 > run_m;
+        const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
+        run_s = live ? ns : run_s;
+        run_m = (live && up) ? s2 : run_m;
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  // ---- block partial (max, sum exp) per head over its 256 pages, log2 domain
+  sRun[wave][lane] = make_float2(run_m, run_s);
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int g = threadIdx.x;
+    float m = -INFINITY, l = 0.0f;
+    for (int w = 0; w < 4; ++w)
+      for (int r = 0; r < 4; ++r) m = fmaxf(m, sRun[w][g + 16 * r].x);
+    if (m > -INFINITY)
+      for (int w = 0; w < 4; ++w)
+        for (int r = 0; r < 4; ++r) {
+          const float2 v = sRun[w][g + 16 * r];
+          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+        }
+    partials[(row0 + g) * gridDim.x + blockIdx.x] = make_float2(m, l);
+  }
+}
+
 template <typename QT>
 hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H_kv, int max_pages,
                          const QT* q, const uint8_t* sum, const int32_t* pt, const int32_t* sl,
@@ -606,7 +819,12 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
                        max_pages, q, sum, pt, sl, s_hat, lay, part);               \
     return hipGetLastError();                                                               \
   }
-  LOCKS_SCAN_FAST(8, 1) LOCKS_SCAN_FAST(8, 4) LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(4, 4)
+  if (r == 8 && G == 16) {
+    hipLaunchKernelGGL((scan_r8_kernel<QT>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
+                       sum, pt, sl, s_hat, lay, part);
+    return hipGetLastError();
+  }
+  LOCKS_SCAN_FAST(8, 4) LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(4, 4)
   LOCKS_SCAN_FAST(2, 1) LOCKS_SCAN_FAST(2, 4)
 #undef LOCKS_SCAN_FAST
 #define LOCKS_SCAN_MFMA_CASE(RR)                                                             \
