@@ -91,7 +91,7 @@ struct WsPlan {
   int n_splits;       // attention splits per (seq, KV head)
 };
 
-constexpr int kScanPagesPerBlock = 256;  // 4 waves x 64 pages
+constexpr int kScanPagesPerBlock = 256;  // 4 waves x 64 pages (generic scan kernels)
 constexpr int kSelChunk = 1024;          // pages per select block (generic path)
 constexpr int kFastChunk = 4096;         // pages per select block (wave-level path)
 constexpr int kSparsePagesPerSplit = 4;   // one page per wave of a 4-wave block
@@ -99,8 +99,10 @@ constexpr int kDensePagesPerSplit = 256;
 
 WsPlan plan_workspace(const locks_cfg_t& c);
 int page_budget(const locks_cfg_t& c);  // k = ceil(b / 16)
+int scan_pages_per_block(const locks_cfg_t& c);  // pages covered by one scan block
 inline int scan_blocks(const locks_cfg_t& c) {
-  return (c.max_pages_per_seq + kScanPagesPerBlock - 1) / kScanPagesPerBlock;
+  const int ppb = scan_pages_per_block(c);
+  return (c.max_pages_per_seq + ppb - 1) / ppb;
 }
 
 // ---------------------------------------------------------------- launchers

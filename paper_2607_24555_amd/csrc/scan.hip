@@ -626,6 +626,60 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // their bytes reordered to l = 0, 4, 1, 5, 2, 6, 3, 7, so that the two codes a
 // lane needs (l = grp, 4 + grp) are one 16-bit read.
 // ---------------------------------------------------------------------------
+// Physical block of page page0 + (lane & 15); lanes past the end of the
+// sequence take page0's block (a valid record that is loaded but not used).
+__device__ __forceinline__ int lane_block(const int32_t* __restrict__ pt_row, int page0, int n_c,
+                                          int lane) {
+  const int pl = page0 + (lane & 15);
+  return pt_row[pl < n_c ? pl : page0];
+}
+
+// Basis set st of the 16 pages whose blocks lanes 0..15 hold in `blk`.
+template <int R>
+__device__ __forceinline__ uint4 load_basis(const uint8_t* __restrict__ summ, int blk, int st,
+                                            int H_kv, int h, int lane) {
+  using Gm = FastGeom<R>;
+  const int col = lane & 15, grp = lane >> 4;
+  const int qs = 4 * (col & 3) + (col >> 2);
+  const int b = __shfl(blk, st * Gm::kPPS + qs / R, 64);
+  const uint32_t off = (uint32_t)(b * H_kv + h) * (uint32_t)Gm::kStride + 64u * (qs % R) + 16u * grp;
+  return *reinterpret_cast<const uint4*>(summ + off);
+}
+
+template <int R>
+__device__ __forceinline__ void load_tail(uint4 (&tl)[FastGeom<R>::kTailLoads],
+                                          const uint8_t* __restrict__ summ, int blk, int H_kv,
+                                          int h, int lane) {
+  using Gm = FastGeom<R>;
+#pragma unroll
+  for (int u = 0; u < Gm::kTailLoads; ++u) {
+    int c = lane + 64 * u;
+    c = c < 16 * Gm::kTailCh ? c : 16 * Gm::kTailCh - 1;
+    const int b = __shfl(blk, c / Gm::kTailCh, 64);
+    const uint32_t off = (uint32_t)(b * H_kv + h) * (uint32_t)Gm::kStride + 64u * R + (c % Gm::kTailCh) * 16;
+    tl[u] = *reinterpret_cast<const uint4*>(summ + off);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// r = 8, G = 16: stage 2 with (page, token) rows.
+//
+// Stage 1 is the int8 projection above.  Stage 2 reconstructs the logits of
+// four pages at a time with one f16 MFMA 16x16x32 (B as hi + lo): rows m are
+// (page a = m / 4 of the quad, token 4 ps + m % 4), K index 8 kg + e is (page
+// e / 2 of the quad, basis column 4 (e % 2) + kg), so A is block diagonal and B
+// is exactly stage-1 registers vals[8 Q + e] of lane group kg.  After the four
+// passes of a quad each lane holds all 16 logits of (page 4 Q + grp, head col)
+// and takes the page LSE in registers.  The centroid MFMA reads its rows in the
+// order page 4 (row & 3) + (row >> 2), which leaves a(page 4 j + grp, head col)
+// in register j of the same lanes.  Coefficient rows are copied to LDS with
+// their bytes reordered to l = 0, 4, 1, 5, 2, 6, 3, 7, so that the two codes a
+// lane needs (l = grp, 4 + grp) are one 16-bit read.  Stage 1 runs per quad
+// (basis sets 2 Q, 2 Q + 1), and each consumed register set is refilled at once
+// with the next 16 pages' records.
+// ---------------------------------------------------------------------------
+constexpr int kR8Steps = 4;  // 16-page steps per wave: a block covers 4 x 16 x kR8Steps pages
+
 template <typename QT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
@@ -646,24 +700,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int32_t* pt_row = page_table + (long)s * max_pages;
   float run_m = -INFINITY, run_s = 0.0f;
 
-  if (pg * 64 < n_c) {
-    FastRegs<R> cur;
-    fast_issue<R>(cur, summ, pt_row, pg * 64, n_c, H_kv, h, lane);
+  constexpr int kWavePages = 16 * kR8Steps;
+  if (pg * kWavePages < n_c) {
+    uint4 vb[Gm::kSets];
+    uint4 tl[Gm::kTailLoads];
+    {
+      const int blk0 = lane_block(pt_row, pg * kWavePages, n_c, lane);
+#pragma unroll
+      for (int st = 0; st < Gm::kSets; ++st) vb[st] = load_basis<R>(summ, blk0, st, H_kv, h, lane);
+      load_tail<R>(tl, summ, blk0, H_kv, h, lane);
+    }
+    int blk_n1 = pg * kWavePages + 16 < n_c ? lane_block(pt_row, pg * kWavePages + 16, n_c, lane) : 0;
     const QDigits QD = q_digits(q + (row0 + col) * kDim, grp);
     const int a_row = col >> 2, t_row = col & 3;  // A row of this lane: (page, token)
     float* shat_base = s_hat + lay.base(s, h) + (long)col * lay.head;
 
 #pragma unroll 1
-    for (int t = 0; t < 4; ++t) {
-      const int page0 = (pg * 4 + t) * 16;
+    for (int t = 0; t < kR8Steps; ++t) {
+      const int page0 = (pg * kR8Steps + t) * 16;
       if (page0 >= n_c) break;
+      const bool more = t + 1 < kR8Steps && page0 + 16 < n_c;
+      const int blk_n2 = (t + 2 < kR8Steps && page0 + 32 < n_c) ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
       // ---- record tails to LDS; coefficient rows reordered to l = 0,4,1,5,2,6,3,7
 #pragma unroll
       for (int u = 0; u < Gm::kTailLoads; ++u) {
         const int c = lane + 64 * u;
         if (c < 16 * Gm::kTailCh) {
           const int o = c % Gm::kTailCh;
-          uint4 v = cur.tl[u];
+          uint4 v = tl[u];
           if (o < 8) {
             v = make_uint4(__builtin_amdgcn_perm(v.y, v.x, 0x05010400u),
                            __builtin_amdgcn_perm(v.y, v.x, 0x07030602u),
@@ -674,38 +738,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         }
       }
       __builtin_amdgcn_wave_barrier();
-
-      // ---- stage 1 (int8 MFMA): vals[4 st + j] = p(page 2 st + j / 2, l = 4 (j % 2) + grp)
-      float vals[4 * Gm::kSets];
-#pragma unroll
-      for (int st = 0; st < Gm::kSets; ++st) {
-        if (st % 4 == 0) __builtin_amdgcn_sched_barrier(0);
-        const uint32_t w[4] = {cur.vb[st].x, cur.vb[st].y, cur.vb[st].z, cur.vb[st].w};
-        i4v acc[3];
-#pragma unroll
-        for (int d = 0; d < 3; ++d) acc[d] = i4v{QD.bias[d], QD.bias[d], QD.bias[d], QD.bias[d]};
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
-          const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
-                         (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
-#pragma unroll
-          for (int d = 0; d < 3; ++d)
-            acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
-          const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
-          const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
-          vals[4 * st + j] = v * (vs * QD.inv_scale);
-        }
-      }
-      // the record registers are consumed: fetch the next 16 pages into them
-      __builtin_amdgcn_sched_barrier(0);
-      if (t + 1 < 4 && page0 + 16 < n_c)
-        fast_issue<R>(cur, summ, pt_row, page0 + 16, n_c, H_kv, h, lane);
-      __builtin_amdgcn_sched_barrier(0);
+      if (more) load_tail<R>(tl, summ, blk_n1, H_kv, h, lane);
 
       // ---- centroid term: areg[j] = a(page 4 j + grp, head col)
       float areg[4];
@@ -738,17 +771,47 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         }
       }
 
-      // ---- stage 2 per quad of pages, then the page LSE in registers
 #pragma unroll
       for (int Q = 0; Q < 4; ++Q) {
         __builtin_amdgcn_sched_barrier(0);
+        // ---- stage 1 (int8 MFMA) for basis sets 2Q, 2Q+1:
+        //      vals[4 i + j] = p(page 4 Q + 2 i + j / 2, l = 4 (j % 2) + grp)
+        float vals[8];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const int st = 2 * Q + i;
+          const uint32_t w[4] = {vb[st].x, vb[st].y, vb[st].z, vb[st].w};
+          i4v acc[3];
+#pragma unroll
+          for (int d = 0; d < 3; ++d) acc[d] = i4v{QD.bias[d], QD.bias[d], QD.bias[d], QD.bias[d]};
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
+            const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
+                           (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+#pragma unroll
+            for (int d = 0; d < 3; ++d)
+              acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
+          }
+          if (more) vb[st] = load_basis<R>(summ, blk_n1, st, H_kv, h, lane);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
+            const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
+            const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
+            vals[4 * i + j] = v * (vs * QD.inv_scale);
+          }
+        }
+        // ---- stage 2 for the quad, then the page LSE in registers
         h8 bh, bl;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float v = vals[8 * Q + e];
-          const _Float16 hi = (_Float16)v;
-          bh[e] = hi;
-          bl[e] = (_Float16)(v - (float)hi);
+        for (int e = 0; e < 8; e += 2) {
+          const auto hi = __builtin_amdgcn_cvt_pkrtz(vals[e], vals[e + 1]);
+          const auto lo = __builtin_amdgcn_cvt_pkrtz(vals[e] - (float)hi[0], vals[e + 1] - (float)hi[1]);
+          bh[e] = hi[0];
+          bh[e + 1] = hi[1];
+          bl[e] = lo[0];
+          bl[e + 1] = lo[1];
         }
         float z[16];
 #pragma unroll
@@ -767,18 +830,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           const uint2 csw = *reinterpret_cast<const uint2*>(
               &sTail[wave][4 * Q + grp][Gm::kSc + 2 * (R + 4 * ps)]);
           const h2 c01 = as_h2(csw.x), c23 = as_h2(csw.y);
-          z[4 * ps + 0] = fmaf((float)c01.x, acc[0], areg[Q]);
-          z[4 * ps + 1] = fmaf((float)c01.y, acc[1], areg[Q]);
-          z[4 * ps + 2] = fmaf((float)c23.x, acc[2], areg[Q]);
-          z[4 * ps + 3] = fmaf((float)c23.y, acc[3], areg[Q]);
+          z[4 * ps + 0] = (float)c01.x * acc[0];
+          z[4 * ps + 1] = (float)c01.y * acc[1];
+          z[4 * ps + 2] = (float)c23.x * acc[2];
+          z[4 * ps + 3] = (float)c23.y * acc[3];
         }
-        float mx = z[0];
-#pragma unroll
-        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, z[i]);
+        // z are the logits minus the centroid logit a.  The deviations of a
+        // page's tokens sum to ~0 (the coefficient columns are orthogonal to
+        // the all-ones vector), so the largest is >= ~0 and sum 2^z is safe
+        // without a max; a max-shifted sum is taken only if it is not finite.
         float sm = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i] - mx);
-        const float s2 = mx + __builtin_amdgcn_logf(sm);
+        for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i]);
+        float shift = 0.0f;
+        if (!(sm > 0.0f && sm < INFINITY)) {
+          shift = z[0];
+#pragma unroll
+          for (int i = 1; i < 16; ++i) shift = fmaxf(shift, z[i]);
+          sm = 0.0f;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i] - shift);
+        }
+        const float s2 = areg[Q] + shift + __builtin_amdgcn_logf(sm);
         const int page = page0 + 4 * Q + grp;
         const bool live = page < n_c;
         if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
@@ -788,10 +861,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         run_s = live ? ns : run_s;
         run_m = (live && up) ? s2 : run_m;
       }
+      blk_n1 = blk_n2;
       __builtin_amdgcn_wave_barrier();
     }
   }
-  // ---- block partial (max, sum exp) per head over its 256 pages, log2 domain
+  // ---- block partial (max, sum exp) per head over its pages, log2 domain
   sRun[wave][lane] = make_float2(run_m, run_s);
   __syncthreads();
   if (threadIdx.x < G) {
@@ -846,6 +920,14 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
 }
 
 }  // namespace
+
+static bool use_r8_kernel(const locks_cfg_t& c) {
+  return c.rank == 8 && c.num_q_heads == 16 * c.num_kv_heads;
+}
+
+int scan_pages_per_block(const locks_cfg_t& c) {
+  return use_r8_kernel(c) ? 64 * kR8Steps : kScanPagesPerBlock;
+}
 
 hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,
                        const int32_t* page_table, const int32_t* seq_lens, float* s_hat,
