@@ -34,6 +34,8 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-build", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the step from captured HIP graphs instead of launching it")
     ap.add_argument("--seed", type=int, default=0)
     return ap.parse_args()
 
@@ -49,6 +51,27 @@ WORKLOADS = {
     "32k": (1, {}, "llama3.1-8b-32k: 1 seq x 32,768 tokens, 32 q / 8 kv heads, d 128, page 16, "
                    "r 8, b 2048, bf16 KV"),
 }
+
+
+def as_graphs(fn, n_copies):
+    """Capture fn(i) for every rotated copy into its own HIP graph (the library
+    allocates nothing and only enqueues on the current stream); returns a
+    replay function with fn's signature."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(n_copies):
+            fn(i)
+    torch.cuda.current_stream().wait_stream(side)
+    graphs = []
+    for i in range(n_copies):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn(i)
+        graphs.append(g)
+    torch.cuda.synchronize()
+    return lambda i: graphs[i % n_copies].replay()
 
 
 def timed(fn, n, sync):
@@ -158,9 +181,10 @@ def main():
         B.decode_step(cfg, q, ks[i % R], vs[i % R], pt, sl, summ[i % R], ws, out_ids=ids,
                       out_sel_lse=sel, out=out, out_lse=lse)
 
+    run = as_graphs(step, R) if args.graph else step
     for i in range(args.warmup):
-        step(i)
-    step_wall_us, step_ev_us = timed(step, args.steps, sync)
+        run(i)
+    step_wall_us, step_ev_us = timed(run, args.steps, sync)
 
     # ---- dense baseline on identical inputs
     dense_us = None
@@ -170,9 +194,10 @@ def main():
         def dstep(i):
             B.dense_attend(cfg, q, ks[i % R], vs[i % R], pt, sl, ws, out=dout, out_lse=dlse)
 
+        drun = as_graphs(dstep, R) if args.graph else dstep
         for i in range(max(2, args.warmup // 2)):
-            dstep(i)
-        dense_us, _ = timed(dstep, max(4, args.steps // 4), sync)
+            drun(i)
+        dense_us, _ = timed(drun, max(4, args.steps // 4), sync)
 
     scan_gbps = alg_scan / (scan_us * 1e-6) / 1e9
     res = {
@@ -199,6 +224,7 @@ def main():
         "step": {"alg_bytes": alg_step, "alg_GBps": round(alg_step / (step_wall_us * 1e-6) / 1e9, 1),
                  "frac_of_peak": round(alg_step / (step_wall_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
                  "event_us": round(step_ev_us, 2), "summary_stride_bytes": stride,
+                 "launch": "hip-graph replay" if args.graph else "eager",
                  "selected_pages_per_kv_head": k_sel},
         "dense": None if dense_us is None else {
             "us": round(dense_us, 2), "bytes": n_pages * cfg.num_kv_heads * kv_page,

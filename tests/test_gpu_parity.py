@@ -314,3 +314,47 @@ def test_identical_pages_tie_break():
     for h in range(cfg.num_kv_heads):
         assert ids_of(ids[0, h].tolist()) == want
     _check_step_against_oracle("ties", d, recs, ids, out, lse, min_same_frac=1.0)
+
+
+@pytest.mark.parametrize("name", ["G16", "r4-G4"])
+def test_decode_step_graph_replay(name):
+    """The fused step captured in a HIP graph gives the eager result on every
+    replay, with eager library work and host synchronisation between replays."""
+    d = _mk(name)
+    cfg, dev = d.cfg, d.device
+    store = B.alloc_summaries(cfg, dev)
+    B.build_summaries(cfg, d.k, d.pt, d.sl, store)
+    ids, sel = B.alloc_select_outputs(cfg, dev)
+    out, lse = B.alloc_attend_outputs(cfg, dev)
+    B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws, out_ids=ids, out_sel_lse=sel,
+                  out=out, out_lse=lse)
+    torch.cuda.synchronize()
+    ws2 = B.alloc_workspace(cfg, dev)
+    gids, gsel = B.alloc_select_outputs(cfg, dev)
+    gout, glse = B.alloc_attend_outputs(cfg, dev)
+
+    def call():
+        B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, ws2, out_ids=gids, out_sel_lse=gsel,
+                      out=gout, out_lse=glse)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (gids, gsel, gout, glse):
+            t.zero_()
+        # eager work of the program between replays (another step, another workspace)
+        B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(gids, ids), rep
+        assert torch.equal(gout, out) and torch.equal(glse, lse), rep
+        assert torch.equal(torch.nan_to_num(gsel, nan=-7.0), torch.nan_to_num(sel, nan=-7.0)), rep
+    print(f"[{name}] graph replay matches the eager step on 3 replays")
