@@ -37,7 +37,6 @@ struct Ws {
   float2* part;
   uint32_t* ckey;
   int32_t* cidx;
-  uint32_t* keys;
   uint32_t* thr;
   float* attn;
 };
@@ -46,7 +45,7 @@ Ws carve(void* ws, const WsPlan& p) {
   char* b = static_cast<char*>(ws);
   return Ws{reinterpret_cast<float*>(b + p.s_hat_off), reinterpret_cast<float2*>(b + p.part_off),
             reinterpret_cast<uint32_t*>(b + p.ckey_off), reinterpret_cast<int32_t*>(b + p.cidx_off),
-            reinterpret_cast<uint32_t*>(b + p.keys_off), reinterpret_cast<uint32_t*>(b + p.thr_off),
+            reinterpret_cast<uint32_t*>(b + p.thr_off),
             reinterpret_cast<float*>(b + p.attn_off)};
 }
 
@@ -80,7 +79,6 @@ WsPlan plan_workspace(const locks_cfg_t& c) {
   p.part_off = take(S * Hq * (size_t)scan_blocks(c) * sizeof(float2));
   p.ckey_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(uint32_t));
   p.cidx_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(int32_t));
-  p.keys_off = take(S * Hkv * mp * sizeof(uint32_t));
   p.thr_off = take(S * Hkv * (size_t)p.n_chunks * sizeof(uint32_t));
   p.attn_off = take(S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float));
   p.total = off;
@@ -96,7 +94,7 @@ static int select_impl(const locks_cfg_t* c, const void* q, const void* summarie
   const SHatLayout lay = out_all_lse ? shat_head_major(*c) : shat_head_minor(*c);
   hipError_t e = launch_scan(*c, q, summaries, page_table, seq_lens, s_hat, lay, w.part, st);
   if (e != hipSuccess) return hip_status(e);
-  const SelectBufs sb{w.ckey, w.cidx, w.keys, w.thr, p.n_chunks};
+  const SelectBufs sb{w.ckey, w.cidx, w.thr, p.n_chunks};
   e = launch_select(*c, seq_lens, s_hat, lay, w.part, sb, out_page_ids, out_sel_lse, st);
   return hip_status(e);
 }
@@ -224,14 +222,27 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
                                  summaries, nullptr, nullptr, nullptr, nullptr, st));
     if (rc) return rc;
   }
+  const WsPlan p = plan_workspace(*cfg);
+  const Ws w = carve(ws, p);
+  const int k = page_budget(*cfg);
+  const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
+  if (attend_select_fused(*cfg)) {
+    // scan -> per-chunk selection -> attention whose blocks merge the table
+    const SHatLayout lay = shat_head_minor(*cfg);
+    const SelectBufs sb{w.ckey, w.cidx, w.thr, p.n_chunks};
+    rc = hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, w.s_hat, lay, w.part, st));
+    if (rc) return rc;
+    rc = hip_status(launch_select_chunks(*cfg, seq_lens, w.s_hat, lay, w.part, sb, st));
+    if (rc) return rc;
+    return hip_status(launch_attend_select(*cfg, q, k_cache, v_cache, page_table, seq_lens, sb,
+                                           w.s_hat, lay, out_page_ids, out_sel_lse,
+                                           kSparsePagesPerSplit, splits, w.attn, out, out_lse, st));
+  }
   rc = select_impl(cfg, q, summaries, page_table, seq_lens, out_page_ids, out_sel_lse, nullptr, ws,
                    st);
   if (rc) return rc;
-  const WsPlan p = plan_workspace(*cfg);
-  const int k = page_budget(*cfg);
-  const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, out_page_ids,
-                                  kSparsePagesPerSplit, splits, carve(ws, p).attn, out, out_lse, st));
+                                  kSparsePagesPerSplit, splits, w.attn, out, out_lse, st));
 }
 
 const char* locks_strerror(int status) {

@@ -13,8 +13,13 @@
 // bf16 Q and KV take attend_mfma_kernel: each wave owns pages_per_split / 4
 // consecutive list entries and handles one page (16 tokens) per step on the
 // matrix cores; the block's four waves combine in LDS before the partial is
-// written.  Other dtypes take the VALU kernel attend_kernel.
+// written.  Other dtypes take the VALU kernel attend_kernel.  In the fused
+// decode step (kSelect) every block first derives its (sequence, KV head)'s
+// page table from the selection chunks' survivors -- all blocks of the unit
+// compute the same table -- and writes the table entries it attends together
+// with their estimated page LSEs.
 #include "locks_internal.h"
+#include "topk.h"
 
 namespace locks {
 namespace {
@@ -171,14 +176,29 @@ __device__ __forceinline__ void load_page(PageRegs& P, const uint16_t* kp, const
 //                 dims 8 m + n, m = 0..15): P is the B operand exactly as S^T
 //                 left it, and lane holds O^T for head c, dims 32 r + 8 j + n.
 // P enters as bf16 hi + lo (two MFMAs) so the weights keep ~16 bits.
+// Chunk survivors and outputs of the selection merged into the attention kernel.
+struct SelTable {
+  const uint32_t* cand_key;
+  const int32_t* cand_idx;
+  const uint32_t* thr;
+  int n_rows;
+  const float* s_hat;
+  SHatLayout lay;
+  int32_t* out_ids;
+  float* out_sel_lse;
+};
+
+template <bool kSelect, int kNK = 8>
 __global__ __launch_bounds__(256) void attend_mfma_kernel(
     int H_q, int H_kv, int max_pages, int k_list, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ page_ids, int pages_per_split, int n_splits,
-    float* __restrict__ partial) {
+    float* __restrict__ partial, SelTable tb) {
   __shared__ float sO[4][kMaxGroup][kDim];
   __shared__ float sM[4][kMaxGroup], sL[4][kMaxGroup];
+  __shared__ int32_t s_tab[kSelect ? kFastK + 2 : 1];
+  __shared__ MergeLds<4> mergeL;
   const int split = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c16 = lane & 15, r4 = lane >> 4;
@@ -197,6 +217,30 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
   const int ppw = pages_per_split / 4;
   const int t_begin = split * pages_per_split + wave * ppw, t_end = t_begin + ppw;
   const int32_t* ids = page_ids ? page_ids + ((long)s * H_kv + h) * k_list : nullptr;
+  if constexpr (kSelect) {
+    const long unit = (long)s * H_kv + h;
+    const int K = k_list - 2 > 0 ? k_list - 2 : 0;
+    const int used = n > k_list ? (n - 2) / kFastChunk + 1 : 0;
+    merge_table<kNK, 4>(k_list, n, used, tb.cand_key + unit * tb.n_rows * K,
+                       tb.cand_idx + unit * tb.n_rows * K, tb.thr + unit * tb.n_rows, s_tab,
+                       mergeL);
+    ids = s_tab;
+    // this block's table entries and their estimated page LSEs (NaN without a summary)
+    const int t0 = split * pages_per_split, n_c = L / kPage;
+    const float* sb = tb.s_hat + tb.lay.base(s, h);
+    for (int e = tid; e < pages_per_split * (G + 1); e += 256) {
+      const int t = t0 + e % pages_per_split, g = e / pages_per_split;
+      if (t >= k_list) continue;
+      const int id = s_tab[t];
+      if (g == G) {
+        tb.out_ids[unit * k_list + t] = id;
+      } else {
+        const bool ok = id >= 0 && id < n_c;
+        const float v = sb[(long)(ok ? id : 0) * tb.lay.page + (long)(ok ? g : 0) * tb.lay.head];
+        tb.out_sel_lse[((long)s * H_q + h * G + g) * k_list + t] = ok ? v : __int_as_float(0x7fc00000);
+      }
+    }
+  }
   auto page_at = [&](int t) -> int {
     int id = -1;
     if (t < t_end) id = ids ? (t < k_list ? ids[t] : -1) : t;
@@ -353,11 +397,12 @@ hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cach
                          float* partial, float* out, float* out_lse, hipStream_t st) {
   const bool qb = c.q_dtype == LOCKS_BF16, kb = c.kv_dtype == LOCKS_BF16;
   if (qb && kb)
-    hipLaunchKernelGGL(attend_mfma_kernel, dim3(n_splits, c.num_kv_heads, c.num_seqs), dim3(256), 0,
-                       st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq, page_budget(c),
-                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
-                       static_cast<const uint16_t*>(v_cache), page_table, seq_lens, page_ids,
-                       pages_per_split, n_splits, partial);
+    hipLaunchKernelGGL(attend_mfma_kernel<false>, dim3(n_splits, c.num_kv_heads, c.num_seqs),
+                       dim3(256), 0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
+                       page_budget(c), static_cast<const uint16_t*>(q),
+                       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache),
+                       page_table, seq_lens, page_ids, pages_per_split, n_splits, partial,
+                       SelTable{});
   else if (qb)
     launch_typed<uint16_t, float>(c, q, k_cache, v_cache, page_table, seq_lens, page_ids,
                                   pages_per_split, n_splits, partial, st);
@@ -367,6 +412,29 @@ hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cach
   else
     launch_typed<float, float>(c, q, k_cache, v_cache, page_table, seq_lens, page_ids,
                                pages_per_split, n_splits, partial, st);
+  hipLaunchKernelGGL(merge_kernel, dim3(c.num_q_heads, c.num_seqs), dim3(kDim), 0, st,
+                     c.num_q_heads, n_splits, partial, out, out_lse);
+  return hipGetLastError();
+}
+
+bool attend_select_fused(const locks_cfg_t& c) {
+  return c.q_dtype == LOCKS_BF16 && c.kv_dtype == LOCKS_BF16 && select_fast_path(c) &&
+         select_fast_merge_nk(c) == 8;
+}
+
+hipError_t launch_attend_select(const locks_cfg_t& c, const void* q, const void* k_cache,
+                                const void* v_cache, const int32_t* page_table,
+                                const int32_t* seq_lens, const SelectBufs& sb, const float* s_hat,
+                                SHatLayout lay, int32_t* out_ids, float* out_sel_lse,
+                                int pages_per_split, int n_splits, float* partial, float* out,
+                                float* out_lse, hipStream_t st) {
+  const int rows = (c.max_pages_per_seq + kFastChunk - 1) / kFastChunk;
+  const SelTable tb{sb.cand_key, sb.cand_idx, sb.thr, rows, s_hat, lay, out_ids, out_sel_lse};
+  hipLaunchKernelGGL((attend_mfma_kernel<true, 8>), dim3(n_splits, c.num_kv_heads, c.num_seqs), dim3(256),
+                     0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq, page_budget(c),
+                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
+                     static_cast<const uint16_t*>(v_cache), page_table, seq_lens, nullptr,
+                     pages_per_split, n_splits, partial, tb);
   hipLaunchKernelGGL(merge_kernel, dim3(c.num_q_heads, c.num_seqs), dim3(kDim), 0, st,
                      c.num_q_heads, n_splits, partial, out, out_lse);
   return hipGetLastError();

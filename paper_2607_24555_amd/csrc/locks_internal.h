@@ -83,7 +83,6 @@ struct WsPlan {
   size_t part_off;    // float2 [S][H_q][scan blocks]     (max, sum exp), log2 domain
   size_t ckey_off;    // uint32 [S][H_kv][chunks][k-2]    per-chunk survivors (keys)
   size_t cidx_off;    // int32  [S][H_kv][chunks][k-2]    per-chunk survivors (pages)
-  size_t keys_off;    // uint32 [S][H_kv][max_pages]      share-averaged page keys
   size_t thr_off;     // uint32 [S][H_kv][chunks]         per-chunk cut (lower bound)
   size_t attn_off;    // float [S][H_q][splits][d + 2]    split-K partials
   size_t total;
@@ -92,8 +91,8 @@ struct WsPlan {
 };
 
 constexpr int kScanPagesPerBlock = 256;  // 4 waves x 64 pages (generic scan kernels)
-constexpr int kSelChunk = 1024;          // pages per select block (generic path)
-constexpr int kFastChunk = 4096;         // pages per select block (wave-level path)
+constexpr int kSelChunk = 1024;          // pages per selection chunk (block-level path)
+constexpr int kFastChunk = 4096;         // pages per selection chunk (fast path)
 constexpr int kSparsePagesPerSplit = 4;   // one page per wave of a 4-wave block
 constexpr int kDensePagesPerSplit = 256;
 
@@ -120,11 +119,17 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
 struct SelectBufs {
   uint32_t* cand_key;
   int32_t* cand_idx;
-  uint32_t* keys;
   uint32_t* thr;
   int n_chunks;
 };
+// Fast selection: k - 2 <= 128 and every chunk survivor fits one merge block;
+// the merge holds 8 (small) or 32 survivors per lane.
 bool select_fast_path(const locks_cfg_t& c);
+int select_fast_merge_nk(const locks_cfg_t& c);
+// Fast path, first half: per-chunk keys and top k - 2 (survivors + cuts in sb).
+hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
+                                SHatLayout lay, const float2* partials, const SelectBufs& sb,
+                                hipStream_t st);
 hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
                          SHatLayout lay, const float2* partials, const SelectBufs& sb,
                          int32_t* out_page_ids, float* out_sel_lse, hipStream_t st);
@@ -133,5 +138,15 @@ hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cach
                          const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
                          const int32_t* page_ids, int pages_per_split, int n_splits,
                          float* partial, float* out, float* out_lse, hipStream_t st);
+
+// Fused decode-step tail: the selection merge inside the attention kernel
+// (bf16 Q and KV, fast selection path), then the split merge.
+bool attend_select_fused(const locks_cfg_t& c);
+hipError_t launch_attend_select(const locks_cfg_t& c, const void* q, const void* k_cache,
+                                const void* v_cache, const int32_t* page_table,
+                                const int32_t* seq_lens, const SelectBufs& sb, const float* s_hat,
+                                SHatLayout lay, int32_t* out_ids, float* out_sel_lse,
+                                int pages_per_split, int n_splits, float* partial, float* out,
+                                float* out_lse, hipStream_t st);
 
 }  // namespace locks

@@ -17,6 +17,7 @@
 // Each thread owns a contiguous run of pages (or survivors) held in registers;
 // block counts use wave ballots and the ordered compaction two exclusive scans.
 #include "locks_internal.h"
+#include "topk.h"
 
 namespace locks {
 namespace {
@@ -337,82 +338,21 @@ __global__ __launch_bounds__(kSelThreads) void select_merge_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Fast path, used when k - 2 <= kFastK and all chunk survivors fit one block's
-// registers.  Three kernels:
-//   keys  - one block per 512 pages of a (sequence, KV head): Z_g and the
-//           share-averaged key of every page, written as one uint32 per page;
-//   chunk - one 4-wave block per 4096 pages: their top K (block-wide cut);
-//   merge - one 4-wave block per (sequence, KV head): top K of all chunk
-//           survivors, sink + recent, estimated page LSEs of the table.
+// Fast path, used when k - 2 <= kFastK and all chunk survivors fit one 4-wave
+// block's registers.  Two kernels:
+//   chunk - one 16-wave block per 4096 pages of a (sequence, KV head): Z_g from the scan
+//           partials, the share-averaged key of every page (staged in LDS), and
+//           the chunk's top K by a histogram cut;
+//   merge - one block per (sequence, KV head): top K of all chunk survivors,
+//           sink + recent, estimated page LSEs of the table.
+// The fused decode step runs the merge inside the attention kernel instead.
 // Keys live in registers wave-major, then register-major: element u of lane l
 // in wave w has position (w * NK + u) * 64 + l, which is page order, so ties
 // resolve to lower pages.
 // ---------------------------------------------------------------------------
 
-constexpr int kFastK = 128;
-constexpr int kKeyPages = 512;        // pages per key block
-
-template <int C>
-__device__ __forceinline__ int dpp(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, C, 0xF, 0xF, false);
-}
-// All-lane sums / extrema over the wave: quad xor, half-row and row mirrors,
-// then the 16- and 32-lane swaps.
-__device__ __forceinline__ int wave_sum_i(int v) {
-  v += dpp<0xB1>(v);
-  v += dpp<0x4E>(v);
-  v += dpp<0x141>(v);
-  v += dpp<0x140>(v);
-  auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  v = (int)p[0] + (int)p[1];
-  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-  return __builtin_amdgcn_readfirstlane((int)r[0] + (int)r[1]);
-}
-__device__ __forceinline__ uint32_t wave_max_u(uint32_t v) {
-  v = max(v, (uint32_t)dpp<0xB1>((int)v));
-  v = max(v, (uint32_t)dpp<0x4E>((int)v));
-  v = max(v, (uint32_t)dpp<0x141>((int)v));
-  v = max(v, (uint32_t)dpp<0x140>((int)v));
-  auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  v = max((uint32_t)p[0], (uint32_t)p[1]);
-  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-  return __builtin_amdgcn_readfirstlane(max((uint32_t)r[0], (uint32_t)r[1]));
-}
-__device__ __forceinline__ uint32_t wave_min_u(uint32_t v) {
-  v = min(v, (uint32_t)dpp<0xB1>((int)v));
-  v = min(v, (uint32_t)dpp<0x4E>((int)v));
-  v = min(v, (uint32_t)dpp<0x141>((int)v));
-  v = min(v, (uint32_t)dpp<0x140>((int)v));
-  auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  v = min((uint32_t)p[0], (uint32_t)p[1]);
-  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-  return __builtin_amdgcn_readfirstlane(min((uint32_t)r[0], (uint32_t)r[1]));
-}
-// Inclusive prefix sum over the wave: shifts inside 16-lane rows, then the
-// last lane of row 0 / row 2 is added to row 1 / row 3 and lane 31 to rows 2-3.
-__device__ __forceinline__ int wave_incl_scan(int x) {
-  x += dpp<0x111>(x);
-  x += dpp<0x112>(x);
-  x += dpp<0x114>(x);
-  x += dpp<0x118>(x);
-  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
-  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
-  return x;
-}
-
-__device__ __forceinline__ uint64_t lanes_below() {
-  const int l = threadIdx.x & 63;
-  return l ? (~0ull >> (64 - l)) : 0ull;
-}
-
-// Cut of a top K: keep keys > T, and the first take_eq keys == T in position
-// order.  Key 0 marks an empty slot.  lo_hint must satisfy
-// count(key >= lo_hint) >= K (1 is always valid).  The bisection stops as soon
-// as some threshold has exactly K keys at or above it.
-struct WaveCut {
-  uint32_t T;
-  int take_eq;
-};
+constexpr int kChunkWaves = 16;                           // 1024-thread chunk blocks
+constexpr int kChunkNK = kFastChunk / (64 * kChunkWaves);  // keys per lane in a chunk (4)
 
 // xor-shuffle inside groups of four lanes (DPP quad permutation).
 template <int O>
@@ -420,48 +360,45 @@ __device__ __forceinline__ float quad_xor(float v) {
   return __int_as_float(dpp<O == 1 ? 0xB1 : 0x4E>(__float_as_int(v)));
 }
 
-// An empty asm that consumes v: the load producing v can no longer be moved
-// under a branch, where it would be waited for before the next one is issued.
-template <typename T>
-__device__ __forceinline__ void pin(T& v) {
-  asm volatile("" : "+v"(v));
-}
-
 __device__ __forceinline__ uint32_t page_key(float m, float sum) {
   return max(1u, f32_order_key(m + __builtin_amdgcn_logf(sum)));
 }
 
-// keys[s][h][j] for the 512 pages of this block (0 for pages that are not
-// candidates); log2 Z_g from the scan blocks' (max, sum 2^x) partials.
 template <int kG>  // G when one page's G scores are contiguous (4, 8, 16), else 0
-__global__ __launch_bounds__(256) void select_keys_kernel(
-    int H_q, int H_kv, int k, int mp, const int32_t* __restrict__ seq_lens,
+__global__ __launch_bounds__(64 * kChunkWaves) void select_chunk_keys_kernel(
+    int H_q, int H_kv, int k, const int32_t* __restrict__ seq_lens,
     const float* __restrict__ s_hat, SHatLayout lay, const float2* __restrict__ partials,
-    int n_parts, uint32_t* __restrict__ keys) {
+    int n_parts, uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx,
+    uint32_t* __restrict__ thr, int n_rows) {
+  constexpr int kT = 64 * kChunkWaves;
   __shared__ float s_lz2[kMaxGroup];
-  const int h = blockIdx.y, s = blockIdx.z, tid = threadIdx.x;
-  const int L = seq_lens[s];
-  const int n = (L + kPage - 1) / kPage;
+  __shared__ __align__(16) uint32_t sk[kFastChunk];
+  __shared__ CutLds<kChunkWaves> L;
+  __shared__ HistLds<kChunkWaves> HL;
+  const int chunk = blockIdx.x, h = blockIdx.y, s = blockIdx.z, tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int Ls = seq_lens[s];
+  const int n = (Ls + kPage - 1) / kPage;
   const int G = H_q / H_kv;
-  const int p0 = blockIdx.x * kKeyPages;
-  if (k - 2 <= 0 || n <= k || p0 > n - 2) return;
+  const int K = k - 2;
+  const int p0 = chunk * kFastChunk;
+  if (K <= 0 || n <= k || p0 > n - 2) return;
   const long row0 = (long)s * H_q + (long)h * G;
   const float* base = s_hat + lay.base(s, h);
-  uint32_t* kout = keys + ((long)s * H_kv + h) * mp;
-  // contiguous layout: float4 number f = 256 i + tid of the block's span holds
+  // contiguous layout: float4 number f = kT i + tid of the chunk's span holds
   // heads 4 (f % LP) .. +3 of page p0 + f / LP; the LP lanes of a page are
   // adjacent.  These loads are issued before Z_g is reduced.
-  constexpr int LP = kG ? kG / 4 : 1, per = kG ? kG / 2 : 1;
+  constexpr int LP = kG ? kG / 4 : 1, per = kG ? kFastChunk * kG / 4 / kT : 1;
   float4 v[per];
   if constexpr (kG != 0) {
 #pragma unroll
     for (int i = 0; i < per; ++i) {
-      const int po = (i * 256 + tid) / LP;
+      const int po = (i * kT + tid) / LP;
       const long j = min(max(p0 + po, 1), n - 2);
       v[i] = *reinterpret_cast<const float4*>(base + j * kG + 4 * (tid % LP));
     }
   }
-  {
+  if (tid < 256) {
     constexpr int kPer = 16;  // partials per thread and pass (16 threads per head)
     const int g = tid >> 4, sub = tid & 15;
     const float2* pp = partials + (row0 + (g < G ? g : 0)) * n_parts;
@@ -493,8 +430,8 @@ __global__ __launch_bounds__(256) void select_keys_kernel(
       m = mm;
     }
     if (g < G && sub == 0) s_lz2[g] = m + __builtin_amdgcn_logf(l);
-    __syncthreads();
   }
+  __syncthreads();
   if constexpr (kG != 0) {
     const int q = tid % LP;
     float lzq[4];
@@ -502,28 +439,26 @@ __global__ __launch_bounds__(256) void select_keys_kernel(
     for (int c = 0; c < 4; ++c) lzq[c] = s_lz2[4 * q + c];
 #pragma unroll
     for (int i = 0; i < per; ++i) {
-      {
-        const int po = (i * 256 + tid) / LP;
-        const float a0 = v[i].x * kLog2e - lzq[0], a1 = v[i].y * kLog2e - lzq[1];
-        const float a2 = v[i].z * kLog2e - lzq[2], a3 = v[i].w * kLog2e - lzq[3];
-        float m = fmaxf(fmaxf(a0, a1), fmaxf(a2, a3));
-        if (LP >= 2) m = fmaxf(m, quad_xor<1>(m));
-        if (LP >= 4) m = fmaxf(m, quad_xor<2>(m));
-        float sum = __builtin_amdgcn_exp2f(a0 - m) + __builtin_amdgcn_exp2f(a1 - m) +
-                    __builtin_amdgcn_exp2f(a2 - m) + __builtin_amdgcn_exp2f(a3 - m);
-        if (LP >= 2) sum += quad_xor<1>(sum);
-        if (LP >= 4) sum += quad_xor<2>(sum);
-        const int j = p0 + po;
-        if (q == 0 && j < mp) kout[j] = (j >= 1 && j <= n - 2) ? page_key(m, sum) : 0u;
-      }
+      const int po = (i * kT + tid) / LP;
+      const float a0 = v[i].x * kLog2e - lzq[0], a1 = v[i].y * kLog2e - lzq[1];
+      const float a2 = v[i].z * kLog2e - lzq[2], a3 = v[i].w * kLog2e - lzq[3];
+      float m = fmaxf(fmaxf(a0, a1), fmaxf(a2, a3));
+      if (LP >= 2) m = fmaxf(m, quad_xor<1>(m));
+      if (LP >= 4) m = fmaxf(m, quad_xor<2>(m));
+      float sum = __builtin_amdgcn_exp2f(a0 - m) + __builtin_amdgcn_exp2f(a1 - m) +
+                  __builtin_amdgcn_exp2f(a2 - m) + __builtin_amdgcn_exp2f(a3 - m);
+      if (LP >= 2) sum += quad_xor<1>(sum);
+      if (LP >= 4) sum += quad_xor<2>(sum);
+      const int j = p0 + po;
+      if (q == 0) sk[po] = (j >= 1 && j <= n - 2) ? page_key(m, sum) : 0u;
     }
   } else {
     float lz[kMaxGroup];
 #pragma unroll
     for (int g = 0; g < kMaxGroup; ++g) lz[g] = g < G ? s_lz2[g] : 0.0f;
 #pragma unroll
-    for (int half = 0; half < kKeyPages / 256; ++half) {
-      const int j = p0 + half * 256 + tid;
+    for (int part = 0; part < kFastChunk / kT; ++part) {
+      const int j = p0 + part * kT + tid;
       const long jj = min(max(j, 1), n - 2);
       float sv[kMaxGroup];
 #pragma unroll
@@ -537,374 +472,107 @@ __global__ __launch_bounds__(256) void select_keys_kernel(
 #pragma unroll
       for (int g = 0; g < kMaxGroup; ++g)
         if (g < G) sum += __builtin_amdgcn_exp2f(sv[g] * kLog2e - lz[g] - m);
-      if (j < mp) kout[j] = (j >= 1 && j <= n - 2) ? page_key(m, sum) : 0u;
-    }
-  }
-}
-
-// Block-cooperative cut over NW waves holding NK keys per lane.  Every wave
-// takes the same decisions from per-wave ballot counts exchanged through LDS,
-// one barrier per bisection step (the count slots are double-buffered).
-template <int NW>
-struct CutLds {
-  int cnt[2][NW];
-  uint32_t mn[NW], mx[NW];
-  int eq[NW], gt[NW];
-};
-
-template <int NK>
-__device__ __forceinline__ int wave_count_ge(const uint32_t (&key)[NK], uint32_t t) {
-  int c = 0;
-#pragma unroll
-  for (int u = 0; u < NK; ++u) c += __popcll(__ballot(key[u] >= t));
-  return c;
-}
-
-template <int NK, int NW>
-__device__ __forceinline__ WaveCut block_cut(const uint32_t (&key)[NK], int K, uint32_t lo_hint,
-                                             CutLds<NW>& L) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  uint32_t kmx = 0u, kmn = 0xffffffffu;
-#pragma unroll
-  for (int u = 0; u < NK; ++u) {
-    kmx = max(kmx, key[u]);
-    kmn = min(kmn, key[u] ? key[u] : 0xffffffffu);
-  }
-  const int nz = wave_count_ge(key, 1u);
-  kmx = wave_max_u(kmx);
-  kmn = wave_min_u(kmn);
-  if (lane == 0) { L.cnt[0][wave] = nz; L.mn[wave] = kmn; L.mx[wave] = kmx; }
-  __syncthreads();
-  int total = 0;
-  uint32_t lo = 0xffffffffu, hi = 0u;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) { total += L.cnt[0][w]; lo = min(lo, L.mn[w]); hi = max(hi, L.mx[w]); }
-  if (total <= K) return WaveCut{1u, 1 << 30};
-  lo = max(lo, lo_hint);
-  int par = 1;
-  while (lo < hi) {
-    const uint32_t mid = lo + (uint32_t)((((uint64_t)hi - lo) + 1) >> 1);
-    const int cw = wave_count_ge(key, mid);
-    if (lane == 0) L.cnt[par][wave] = cw;
-    __syncthreads();
-    int c = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) c += L.cnt[par][w];
-    par ^= 1;
-    if (c == K) { lo = mid; break; }
-    if (c > K) lo = mid; else hi = mid - 1;
-  }
-  const int gw = lo == 0xffffffffu ? 0 : wave_count_ge(key, lo + 1);
-  if (lane == 0) L.cnt[par][wave] = gw;
-  __syncthreads();
-  int c = 0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) c += L.cnt[par][w];
-  return WaveCut{lo, K - c};
-}
-
-// Calls f(u, slot) for every kept element (slot = rank in block position
-// order); returns the number kept.  Contains one barrier.
-template <int NK, int NW, typename F>
-__device__ __forceinline__ int block_emit(const uint32_t (&key)[NK], WaveCut cut, CutLds<NW>& L,
-                                          F f) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  int eq_w = 0, gt_w = 0;
-#pragma unroll
-  for (int u = 0; u < NK; ++u) {
-    eq_w += __popcll(__ballot(key[u] != 0u && key[u] == cut.T));
-    gt_w += __popcll(__ballot(key[u] != 0u && key[u] > cut.T));
-  }
-  if (lane == 0) { L.eq[wave] = eq_w; L.gt[wave] = gt_w; }
-  __syncthreads();
-  int eq_base = 0, base = 0, total = 0;
-  // kept by each wave: its keys > T plus its share of the first take_eq keys == T
-  int eq_seen = 0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    const int e = L.eq[w];
-    const int kept = L.gt[w] + min(max(cut.take_eq - eq_seen, 0), e);
-    if (w < wave) { base += kept; eq_base += e; }
-    total += kept;
-    eq_seen += e;
-  }
-  const uint64_t lt = lanes_below();
-#pragma unroll
-  for (int u = 0; u < NK; ++u) {
-    const bool nz = key[u] != 0u;
-    const bool eq = nz && key[u] == cut.T;
-    const uint64_t em = __ballot(eq);
-    const int er = eq_base + __popcll(em & lt);
-    eq_base += __popcll(em);
-    const bool keep = (nz && key[u] > cut.T) || (eq && er < cut.take_eq);
-    const uint64_t km = __ballot(keep);
-    if (keep) f(u, base + __popcll(km & lt));
-    base += __popcll(km);
-  }
-  return total;
-}
-
-// Histogram cut.  Bins measure how far a key lies below the block maximum M,
-// in 1/32 of a log2 unit (bin 0 holds M; the last bin also takes everything
-// further down).  The prefix over bins locates the boundary bin b*: every key
-// in a lower bin is kept, and only the few keys of b* are ranked exactly.  When
-// b* holds more than kBoundaryMax keys, bisection over b*'s key range decides.
-constexpr int kBins = 1024;
-constexpr float kBinsPerUnit = 32.0f;
-constexpr int kBoundaryMax = 64;
-
-template <int NW>
-struct HistLds {
-  int hist[kBins];
-  uint32_t mx[NW];
-  int wtot[NW];
-  int nb;                      // keys in the boundary bin
-  uint32_t bmin;               // smallest key in the boundary bin
-  int bstar, need;             // boundary bin, keys to take from it
-  uint32_t bkey[kBoundaryMax];
-  int bpos[kBoundaryMax];
-  WaveCut cut;
-};
-
-__device__ __forceinline__ int key_bin(uint32_t key, float Mf) {
-  const float d = (Mf - order_key_f32(key)) * kBinsPerUnit;
-  return (int)fminf(fmaxf(d, 0.0f), (float)(kBins - 1));
-}
-
-template <int NK, int NW>
-__device__ __forceinline__ WaveCut block_hist_cut(const uint32_t (&key)[NK], int K, HistLds<NW>& H,
-                                                  CutLds<NW>& L) {
-  constexpr int kT = 64 * NW, kPer = kBins / kT;
-  static_assert(kBins % kT == 0, "bins per thread");
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  // 1. block maximum and candidate count; clear the histogram
-#pragma unroll
-  for (int b = 0; b < kPer; ++b) H.hist[tid * kPer + b] = 0;
-  if (tid == 0) { H.nb = 0; H.bmin = 0xffffffffu; H.bstar = kBins - 1; H.need = 1; }
-  uint32_t kmx = 0u;
-#pragma unroll
-  for (int u = 0; u < NK; ++u) kmx = max(kmx, key[u]);
-  const int nz = wave_count_ge(key, 1u);
-  kmx = wave_max_u(kmx);
-  if (lane == 0) { H.mx[wave] = kmx; H.wtot[wave] = nz; }
-  __syncthreads();
-  uint32_t M = 0u;
-  int total = 0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) { M = max(M, H.mx[w]); total += H.wtot[w]; }
-  if (total <= K) return WaveCut{1u, 1 << 30};
-  const float Mf = order_key_f32(M);
-  // 2. histogram
-  int bin[NK];
-#pragma unroll
-  for (int u = 0; u < NK; ++u) {
-    bin[u] = key[u] ? key_bin(key[u], Mf) : -1;
-    if (key[u]) atomicAdd(&H.hist[bin[u]], 1);
-  }
-  __syncthreads();
-  // 3. boundary bin: first bin where the running count reaches K
-  int c = 0;
-#pragma unroll
-  for (int b = 0; b < kPer; ++b) c += H.hist[tid * kPer + b];
-  int incl = wave_incl_scan(c);
-  if (lane == 63) H.wtot[wave] = incl;
-  __syncthreads();
-  int before = 0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) before += w < wave ? H.wtot[w] : 0;
-  incl += before;
-  if (incl >= K && incl - c < K) {
-    int run = incl - c, b = 0;
-    while (b < kPer - 1 && run + H.hist[tid * kPer + b] < K) run += H.hist[tid * kPer + b++];
-    H.bstar = tid * kPer + b;
-    H.need = K - run;
-  }
-  __syncthreads();
-  // 4. collect the boundary bin (position order is rebuilt by ranking)
-  const int bstar = H.bstar;
-#pragma unroll
-  for (int u = 0; u < NK; ++u) {
-    if (bin[u] == bstar) {
-      const int slot = atomicAdd(&H.nb, 1);
-      atomicMin(&H.bmin, key[u]);
-      if (slot < kBoundaryMax) {
-        H.bkey[slot] = key[u];
-        H.bpos[slot] = (wave * NK + u) * 64 + lane;
-      }
+      sk[part * kT + tid] = (j >= 1 && j <= n - 2) ? page_key(m, sum) : 0u;
     }
   }
   __syncthreads();
-  const int nb = H.nb;
-  if (nb > kBoundaryMax) return block_cut<NK, NW>(key, K, H.bmin, L);
-  // 5. wave 0 ranks the boundary keys: (key desc, position asc)
-  if (wave == 0) {
-    const bool have = lane < nb;
-    const uint32_t mk = have ? H.bkey[lane] : 0u;
-    const int mp_ = have ? H.bpos[lane] : 0x7fffffff;
-    int rank = 0;
-    for (int j = 0; j < nb; ++j) {
-      const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)mk, j);
-      const int pj = __builtin_amdgcn_readlane(mp_, j);
-      rank += (kj > mk) || (kj == mk && pj < mp_);
-    }
-    const int need = H.need;
-    const uint64_t at = __ballot(have && rank == need - 1);
-    const uint32_t T = __shfl(mk, (int)__builtin_ctzll(at), 64);
-    const int gt = __popcll(__ballot(have && mk > T));
-    if (lane == 0) H.cut = WaveCut{T, need - gt};
-  }
-  __syncthreads();
-  return H.cut;
-}
-
-constexpr int kChunkWaves = 4;
-constexpr int kChunkRegs = kFastChunk / (64 * kChunkWaves);  // 16 keys per lane
-constexpr int kMergeWaves = 4;
-constexpr int kMergeRegsFast = 8;                     // 2048 survivors max
-
-// Top K of 4096 pages' keys -> cand rows; thr = the chunk's cut when it kept K
-// keys (a lower bound of the sequence-wide cut), else 1.
-__global__ __launch_bounds__(64 * kChunkWaves) void select_chunk_fast_kernel(
-    int H_kv, int k, int mp, const int32_t* __restrict__ seq_lens,
-    const uint32_t* __restrict__ keys, uint32_t* __restrict__ cand_key,
-    int32_t* __restrict__ cand_idx, uint32_t* __restrict__ thr, int n_rows) {
-  __shared__ CutLds<kChunkWaves> L;
-  __shared__ HistLds<kChunkWaves> HL;
-  const int chunk = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int Ls = seq_lens[s];
-  const int n = (Ls + kPage - 1) / kPage;
-  const int K = k - 2;
-  const int p0 = chunk * kFastChunk;
-  if (K <= 0 || n <= k || p0 > n - 2) return;
-  const uint32_t* kb = keys + ((long)s * H_kv + h) * mp;
-  const int P0 = p0 + wave * (64 * kChunkRegs);
-  uint32_t key[kChunkRegs];
+  uint32_t key[kChunkNK];
 #pragma unroll
-  for (int u = 0; u < kChunkRegs; ++u) key[u] = kb[min(max(P0 + u * 64 + lane, 1), n - 2)];
-#pragma unroll
-  for (int u = 0; u < kChunkRegs; ++u) pin(key[u]);
-#pragma unroll
-  for (int u = 0; u < kChunkRegs; ++u) {
-    const int j = P0 + u * 64 + lane;
-    key[u] = (j >= 1 && j <= n - 2) ? key[u] : 0u;
-  }
-  const WaveCut cut = block_hist_cut<kChunkRegs, kChunkWaves>(key, K, HL, L);
+  for (int u = 0; u < kChunkNK; ++u) key[u] = sk[(wave * kChunkNK + u) * 64 + lane];
+  const WaveCut cut = block_hist_cut<kChunkNK, kChunkWaves>(key, K, HL, L);
   const long row = (((long)s * H_kv + h) * n_rows + chunk) * K;
-  const int tot = block_emit<kChunkRegs, kChunkWaves>(key, cut, L, [&](int u, int slot) {
+  const int tot = block_emit<kChunkNK, kChunkWaves>(key, cut, L, [&](int u, int slot) {
     cand_key[row + slot] = key[u];
-    cand_idx[row + slot] = P0 + u * 64 + lane;
+    cand_idx[row + slot] = p0 + (wave * kChunkNK + u) * 64 + lane;
   });
-  for (int t = tot + tid; t < K; t += 64 * kChunkWaves) { cand_key[row + t] = 0u; cand_idx[row + t] = -1; }
+  for (int t = tot + tid; t < K; t += kT) { cand_key[row + t] = 0u; cand_idx[row + t] = -1; }
   if (tid == 0) thr[((long)s * H_kv + h) * n_rows + chunk] = tot == K ? cut.T : 1u;
 }
 
-__global__ __launch_bounds__(64 * kMergeWaves) void select_merge_fast_kernel(
+template <int NK>
+__global__ __launch_bounds__(256) void select_merge_fast_kernel(
     int H_q, int H_kv, int k, int n_rows, const int32_t* __restrict__ seq_lens,
     const float* __restrict__ s_hat, SHatLayout lay, const uint32_t* __restrict__ cand_key,
     const int32_t* __restrict__ cand_idx, const uint32_t* __restrict__ thr,
     int32_t* __restrict__ out_ids, float* __restrict__ out_sel_lse) {
-  __shared__ CutLds<kMergeWaves> L;
-  __shared__ HistLds<kMergeWaves> HL;
-  __shared__ int32_t s_ids[kFastK + 2];
-  __shared__ uint32_t s_lo;
-  const int h = blockIdx.x, s = blockIdx.y;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  __shared__ MergeLds<4> ML;
+  __shared__ int32_t s_tab[kFastK + 2];
+  const int h = blockIdx.x, s = blockIdx.y, tid = threadIdx.x;
   const int Ls = seq_lens[s];
   const int n = (Ls + kPage - 1) / kPage;
   const int n_c = Ls / kPage;
   const int G = H_q / H_kv;
-  const int K = k - 2;
+  const int K = k - 2 > 0 ? k - 2 : 0;
   const long row0 = (long)s * H_q + (long)h * G;
-  int32_t* ids = out_ids + ((long)s * H_kv + h) * k;
-  if (n <= k) {
-    if (tid < k) s_ids[tid] = tid < n ? tid : -1;
-  } else if (K > 0) {
-    const int used = (n - 2) / kFastChunk + 1;
-    const int N = used * K;  // <= 64 * kMergeWaves * kMergeRegsFast (checked on the host)
-    const long base = ((long)s * H_kv + h) * n_rows * K;
-    const int e0 = wave * (64 * kMergeRegsFast) + lane;
-    uint32_t key[kMergeRegsFast];
-    int32_t idx[kMergeRegsFast];
-#pragma unroll
-    for (int u = 0; u < kMergeRegsFast; ++u) {
-      const int e = min(e0 + u * 64, N - 1);
-      key[u] = cand_key[base + e];
-      idx[u] = cand_idx[base + e];
-    }
-    if (wave == 0) {
-      const uint32_t* tr = thr + ((long)s * H_kv + h) * n_rows;
-      const uint32_t lo = wave_max_u(lane < used ? tr[lane] : 1u);
-      if (lane == 0) s_lo = lo;
-    }
-#pragma unroll
-    for (int u = 0; u < kMergeRegsFast; ++u) pin(key[u]);
-#pragma unroll
-    for (int u = 0; u < kMergeRegsFast; ++u) key[u] = e0 + u * 64 < N ? key[u] : 0u;
-    __syncthreads();
-    // keys below the best chunk cut cannot reach the sequence-wide top K
-    const uint32_t lo = s_lo;
-#pragma unroll
-    for (int u = 0; u < kMergeRegsFast; ++u) key[u] = key[u] >= lo ? key[u] : 0u;
-    const WaveCut cut = block_hist_cut<kMergeRegsFast, kMergeWaves>(key, K, HL, L);
-    block_emit<kMergeRegsFast, kMergeWaves>(key, cut, L,
-                                            [&](int u, int slot) { s_ids[1 + slot] = idx[u]; });
-    if (tid == 0) { s_ids[0] = 0; s_ids[k - 1] = n - 1; }
-  }
-  __syncthreads();
-  if (tid < k) ids[tid] = s_ids[tid];
+  const long unit = (long)s * H_kv + h;
+  const int used = n > k ? (n - 2) / kFastChunk + 1 : 0;
+  merge_table<NK, 4>(k, n, used, cand_key + unit * n_rows * K, cand_idx + unit * n_rows * K,
+                           thr + unit * n_rows, s_tab, ML);
+  if (tid < k) out_ids[unit * k + tid] = s_tab[tid];
   // estimated page LSE of every table entry (NaN for a partial page or padding)
   const float* sb = s_hat + lay.base(s, h);
-  constexpr int kT = 64 * kMergeWaves;
-  constexpr int kPer = (kMaxGroup * (kFastK + 2) + kT - 1) / kT;
+  constexpr int kPer = (kMaxGroup * (kFastK + 2) + 255) / 256;
   float val[kPer];
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int e = tid + kT * u;
+    const int e = tid + 256 * u;
     const int g = e / k, t = e - g * k;
-    const int id = e < G * k ? s_ids[t] : -1;
+    const int id = e < G * k ? s_tab[t] : -1;
     const bool ok = id >= 0 && id < n_c;
     const float v = sb[(long)(ok ? id : 0) * lay.page + (long)(ok ? g : 0) * lay.head];
     val[u] = ok ? v : __int_as_float(0x7fc00000);
   }
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int e = tid + kT * u;
+    const int e = tid + 256 * u;
     if (e < G * k) out_sel_lse[row0 * k + e] = val[u];
   }
 }
 
 }  // namespace
 
+static long fast_rows(const locks_cfg_t& c) {
+  return (c.max_pages_per_seq + kFastChunk - 1) / kFastChunk;
+}
+
+int select_fast_merge_nk(const locks_cfg_t& c) {
+  const long n = fast_rows(c) * (page_budget(c) - 2);
+  return n <= 64L * 4 * 8 ? 8 : 32;
+}
+
 bool select_fast_path(const locks_cfg_t& c) {
   const int K = page_budget(c) - 2;
-  const long rows = (c.max_pages_per_seq + kFastChunk - 1) / kFastChunk;
-  return K <= kFastK && rows * K <= 64L * kMergeWaves * kMergeRegsFast && rows <= 64;
+  return K <= kFastK && fast_rows(c) * K <= 64L * 4 * 32;
+}
+
+hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
+                                SHatLayout lay, const float2* partials, const SelectBufs& sb,
+                                hipStream_t st) {
+  const int k = page_budget(c);
+  const int G = c.num_q_heads / c.num_kv_heads;
+  const bool contiguous = lay.head == 1 && lay.page == G;
+  auto* kern = select_chunk_keys_kernel<0>;
+  if (contiguous && G == 16) kern = select_chunk_keys_kernel<16>;
+  if (contiguous && G == 8) kern = select_chunk_keys_kernel<8>;
+  if (contiguous && G == 4) kern = select_chunk_keys_kernel<4>;
+  const int rows = (int)fast_rows(c);
+  hipLaunchKernelGGL(kern, dim3(rows, c.num_kv_heads, c.num_seqs), dim3(64 * kChunkWaves), 0, st,
+                     c.num_q_heads, c.num_kv_heads, k, seq_lens, s_hat, lay, partials,
+                     scan_blocks(c), sb.cand_key, sb.cand_idx, sb.thr, rows);
+  return hipGetLastError();
 }
 
 hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
                          SHatLayout lay, const float2* partials, const SelectBufs& sb,
                          int32_t* out_page_ids, float* out_sel_lse, hipStream_t st) {
   const int k = page_budget(c);
-  const int mp = c.max_pages_per_seq;
   if (select_fast_path(c)) {
-    const int rows = (mp + kFastChunk - 1) / kFastChunk;
-    const int G = c.num_q_heads / c.num_kv_heads;
-    const bool contiguous = lay.head == 1 && lay.page == G;
-    auto* kern = select_keys_kernel<0>;
-    if (contiguous && G == 16) kern = select_keys_kernel<16>;
-    if (contiguous && G == 8) kern = select_keys_kernel<8>;
-    if (contiguous && G == 4) kern = select_keys_kernel<4>;
-    hipLaunchKernelGGL(kern, dim3((mp + kKeyPages - 1) / kKeyPages, c.num_kv_heads, c.num_seqs),
-                       dim3(256), 0, st, c.num_q_heads, c.num_kv_heads, k, mp, seq_lens, s_hat,
-                       lay, partials, scan_blocks(c), sb.keys);
-    hipLaunchKernelGGL(select_chunk_fast_kernel, dim3(rows, c.num_kv_heads, c.num_seqs),
-                       dim3(64 * kChunkWaves), 0, st, c.num_kv_heads, k, mp, seq_lens, sb.keys, sb.cand_key,
-                       sb.cand_idx, sb.thr, rows);
-    hipLaunchKernelGGL(select_merge_fast_kernel, dim3(c.num_kv_heads, c.num_seqs),
-                       dim3(64 * kMergeWaves), 0,
-                       st, c.num_q_heads, c.num_kv_heads, k, rows, seq_lens, s_hat, lay,
-                       sb.cand_key, sb.cand_idx, sb.thr, out_page_ids, out_sel_lse);
+    hipError_t e = launch_select_chunks(c, seq_lens, s_hat, lay, partials, sb, st);
+    if (e != hipSuccess) return e;
+    auto* kern = select_fast_merge_nk(c) == 8 ? select_merge_fast_kernel<8> : select_merge_fast_kernel<32>;
+    hipLaunchKernelGGL(kern, dim3(c.num_kv_heads, c.num_seqs), dim3(256), 0, st, c.num_q_heads,
+                       c.num_kv_heads, k, (int)fast_rows(c), seq_lens, s_hat, lay, sb.cand_key,
+                       sb.cand_idx, sb.thr, out_page_ids, out_sel_lse);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(select_chunk_kernel, dim3(sb.n_chunks, c.num_kv_heads, c.num_seqs),

@@ -297,12 +297,14 @@ def test_edge_batches(G, lens, rank, budget, kv):
     assert torch.equal(ids, ids2) and torch.equal(out, out2)
 
 
-def test_identical_pages_tie_break():
+@pytest.mark.parametrize("n,budget,rank", [(5001, 1024, 4), (16389, 2048, 2)])
+def test_identical_pages_tie_break(n, budget, rank):
     """Every page holds the same keys, so all page scores tie exactly: the table
     is the sink, the k - 2 lowest candidate pages and the recent page (ties go
-    to the lower page), across two selection chunks."""
-    n = 5001
-    spec = WorkloadSpec("ties", 1, 8, 2, [16 * (n - 1) + 3], 4, 1024, "bf16", "bf16")
+    to the lower page), across several selection chunks (the larger case keeps
+    more tied survivors than the compacted final cut holds)."""
+    print(f"[ties] n={n} b={budget} r={rank}", flush=True)
+    spec = WorkloadSpec("ties", 1, 8, 2, [16 * (n - 1) + 3], rank, budget, "bf16", "bf16")
     w = build_workload(spec, 5)
     w.k_cache[:] = w.k_cache[:1].clone()
     d = Dev(w)
@@ -313,6 +315,9 @@ def test_identical_pages_tie_break():
     want = [0] + list(range(1, cfg.k - 1)) + [n - 1]
     for h in range(cfg.num_kv_heads):
         assert ids_of(ids[0, h].tolist()) == want
+    ids2, sel2 = B.select(cfg, d.q, store, d.pt, d.sl, d.ws)
+    torch.cuda.synchronize()
+    assert torch.equal(ids2, ids)
     _check_step_against_oracle("ties", d, recs, ids, out, lse, min_same_frac=1.0)
 
 
