@@ -56,6 +56,17 @@ int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
   return LOCKS_OK;
 }
 
+// Table entries per attention block: 4 (one page per wave), doubled while the
+// grid would exceed ~512 blocks, so large batches stream several pages per
+// wave instead of paying per-block latency many times over.
+int sparse_pages_per_split(const locks_cfg_t& c) {
+  const long units = (long)c.num_seqs * c.num_kv_heads;
+  const int k = page_budget(c);
+  int pps = kSparsePagesPerSplit;
+  while (pps < 32 && units * ((k + pps - 1) / pps) > 512) pps *= 2;
+  return pps;
+}
+
 int dense_splits(const locks_cfg_t& c) {
   return (c.max_pages_per_seq + kDensePagesPerSplit - 1) / kDensePagesPerSplit;
 }
@@ -184,9 +195,10 @@ int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cac
   if (cfg->num_seqs == 0) return LOCKS_OK;
   const WsPlan p = plan_workspace(*cfg);
   const int k = page_budget(*cfg);
-  const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
+  const int pps = sparse_pages_per_split(*cfg);
+  const int splits = (k + pps - 1) / pps;
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, page_ids,
-                                  kSparsePagesPerSplit, splits, carve(ws, p).attn, out, out_lse,
+                                  pps, splits, carve(ws, p).attn, out, out_lse,
                                   static_cast<hipStream_t>(stream)));
 }
 
@@ -225,7 +237,8 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
   const WsPlan p = plan_workspace(*cfg);
   const Ws w = carve(ws, p);
   const int k = page_budget(*cfg);
-  const int splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
+  const int pps = sparse_pages_per_split(*cfg);
+  const int splits = (k + pps - 1) / pps;
   if (attend_select_fused(*cfg)) {
     // scan -> per-chunk selection -> attention whose blocks merge the table
     const SHatLayout lay = shat_head_minor(*cfg);
@@ -236,13 +249,13 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
     if (rc) return rc;
     return hip_status(launch_attend_select(*cfg, q, k_cache, v_cache, page_table, seq_lens, sb,
                                            w.s_hat, lay, out_page_ids, out_sel_lse,
-                                           kSparsePagesPerSplit, splits, w.attn, out, out_lse, st));
+                                           pps, splits, w.attn, out, out_lse, st));
   }
   rc = select_impl(cfg, q, summaries, page_table, seq_lens, out_page_ids, out_sel_lse, nullptr, ws,
                    st);
   if (rc) return rc;
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, out_page_ids,
-                                  kSparsePagesPerSplit, splits, w.attn, out, out_lse, st));
+                                  pps, splits, w.attn, out, out_lse, st));
 }
 
 const char* locks_strerror(int status) {
