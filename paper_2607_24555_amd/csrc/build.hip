@@ -63,7 +63,9 @@ __global__ __launch_bounds__(64) void build_kernel(
     const int32_t* __restrict__ build_list, int n_items, int all_pages,
     uint8_t* __restrict__ summaries, float* __restrict__ mu_out, float* __restrict__ basis_out,
     float* __restrict__ coef_out, float* __restrict__ sigma2_out) {
-  __shared__ float sD[kItems][kPage][kDim + 1];
+  // raw key rows (bf16 or fp32 as stored); deviations are formed on the fly as
+  // float(k) - mu, the same fp32 value for every use
+  __shared__ __align__(16) KT sK[kItems][kPage][kDim];
   __shared__ float sA[kItems][kPage][kPage + 1];
   __shared__ float sU[kItems][kPage][kPage + 1];
   __shared__ float sC[kItems][kPage][kPage];
@@ -96,25 +98,32 @@ __global__ __launch_bounds__(64) void build_kernel(
   }
   const long blk = active ? (long)page_table[(long)s * max_pages + j] : 0;
 
-  // ---- load row li of the page, track its squared norm
+  // ---- load row li of the page (16-byte loads), track its squared norm
   float energy = 0.0f;
   {
-    const KT* src = k_cache + ((blk * H_kv + h) * kPage + li) * kDim;
+    constexpr int kVec = 16 / sizeof(KT);  // elements per 16-byte load
+    const uint4* src = reinterpret_cast<const uint4*>(k_cache + ((blk * H_kv + h) * kPage + li) * kDim);
+    uint4* dst = reinterpret_cast<uint4*>(&sK[grp][li][0]);
+    uint4 w[kDim / kVec];
+#pragma unroll
+    for (int u = 0; u < kDim / kVec; ++u) w[u] = active ? src[u] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < kDim / kVec; ++u) dst[u] = w[u];
+    __syncthreads();
+#pragma unroll 8
     for (int c = 0; c < kDim; ++c) {
-      float x = active ? load_elem(src, c) : 0.0f;
-      sD[grp][li][c] = x;
+      const float x = load_elem(&sK[grp][li][0], c);
       energy = fmaf(x, x, energy);
     }
   }
   energy = group16_sum(energy) * (1.0f / kPage);
-  __syncthreads();
 
   // ---- centroid: pairwise sum over the 16 rows (exact for equal rows)
   for (int cc = 0; cc < 8; ++cc) {
     const int c = 8 * li + cc;
     float v[kPage];
 #pragma unroll
-    for (int i = 0; i < kPage; ++i) v[i] = sD[grp][i][c];
+    for (int i = 0; i < kPage; ++i) v[i] = load_elem(&sK[grp][i][0], c);
 #pragma unroll
     for (int w = 8; w > 0; w >>= 1)
 #pragma unroll
@@ -122,15 +131,32 @@ __global__ __launch_bounds__(64) void build_kernel(
     sMu[grp][c] = v[0] * (1.0f / kPage);
   }
   __syncthreads();
-  for (int c = 0; c < kDim; ++c) sD[grp][li][c] -= sMu[grp][c];
-  __syncthreads();
 
-  // ---- Gram of the deviations (same summation order for (i,j) and (j,i))
-  for (int jj = 0; jj < kPage; ++jj) {
-    float g = 0.0f;
-    for (int c = 0; c < kDim; ++c) g = fmaf(sD[grp][li][c], sD[grp][jj][c], g);
-    sA[grp][li][jj] = g;
-    sU[grp][li][jj] = (li == jj) ? 1.0f : 0.0f;
+  // ---- Gram of the deviations: entry (i, j) sums d_i[c] d_j[c] over c = 0..127
+  //      in order on both lanes, so the Gram is exactly symmetric; this lane's
+  //      deviation row is held 32 columns at a time
+  {
+    float g[kPage];
+#pragma unroll
+    for (int jj = 0; jj < kPage; ++jj) g[jj] = 0.0f;
+    for (int cb = 0; cb < kDim; cb += 32) {
+      float dl[32];
+#pragma unroll
+      for (int c = 0; c < 32; ++c) dl[c] = load_elem(&sK[grp][li][0], cb + c) - sMu[grp][cb + c];
+#pragma unroll 4
+      for (int jj = 0; jj < kPage; ++jj) {
+        float acc = g[jj];
+#pragma unroll
+        for (int c = 0; c < 32; ++c)
+          acc = fmaf(dl[c], load_elem(&sK[grp][jj][0], cb + c) - sMu[grp][cb + c], acc);
+        g[jj] = acc;
+      }
+    }
+#pragma unroll
+    for (int jj = 0; jj < kPage; ++jj) {
+      sA[grp][li][jj] = g[jj];
+      sU[grp][li][jj] = (li == jj) ? 1.0f : 0.0f;
+    }
   }
   __syncthreads();
 
@@ -216,7 +242,8 @@ __global__ __launch_bounds__(64) void build_kernel(
     for (int cc = 0; cc < 8; ++cc) {
       const int c = 8 * li + cc;
       float acc = 0.0f;
-      for (int i = 0; i < kPage; ++i) acc = fmaf(sD[grp][i][c], sU[grp][i][mode], acc);
+      for (int i = 0; i < kPage; ++i)
+        acc = fmaf(load_elem(&sK[grp][i][0], c) - sMu[grp][c], sU[grp][i][mode], acc);
       v[cc] = kept ? acc / sig : 0.0f;
     }
     // sign convention: largest |v| (first index on ties) made positive
