@@ -15,6 +15,7 @@ namespace locks {
 namespace {
 
 constexpr int kItems = 4;         // items per block
+constexpr int kRow = 20;          // LDS row stride of A and U: 16-byte aligned, conflict-free
 constexpr int kMaxSweeps = 12;
 constexpr float kZeroRel = 1e-6f;
 constexpr float kZeroAbs = 1e-10f;
@@ -28,6 +29,19 @@ __device__ __forceinline__ int partner(int t, int i) {
   p %= 15;
   if (p < 0) p += 15;
   return p;
+}
+
+__device__ __forceinline__ void ld_row(const float* p, float (&r)[kPage]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 v = reinterpret_cast<const float4*>(p)[q];
+    r[4 * q] = v.x; r[4 * q + 1] = v.y; r[4 * q + 2] = v.z; r[4 * q + 3] = v.w;
+  }
+}
+__device__ __forceinline__ void st_row(float* p, const float (&r)[kPage]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    reinterpret_cast<float4*>(p)[q] = make_float4(r[4 * q], r[4 * q + 1], r[4 * q + 2], r[4 * q + 3]);
 }
 
 __device__ __forceinline__ float group16_sum(float v) {
@@ -66,8 +80,8 @@ __global__ __launch_bounds__(64) void build_kernel(
   // raw key rows (bf16 or fp32 as stored); deviations are formed on the fly as
   // float(k) - mu, the same fp32 value for every use
   __shared__ __align__(16) KT sK[kItems][kPage][kDim];
-  __shared__ float sA[kItems][kPage][kPage + 1];
-  __shared__ float sU[kItems][kPage][kPage + 1];
+  __shared__ __align__(16) float sA[kItems][kPage][kRow];
+  __shared__ __align__(16) float sU[kItems][kPage][kRow];
   __shared__ float sC[kItems][kPage][kPage];
   __shared__ float sMu[kItems][kDim];
   __shared__ float2 sCS[kItems][kPage];
@@ -160,17 +174,26 @@ __global__ __launch_bounds__(64) void build_kernel(
   }
   __syncthreads();
 
-  // ---- cyclic Jacobi, tournament order
+  // ---- cyclic Jacobi, tournament order.  In round t lane li pairs with
+  //      p = partner(t, li); every lane reads its own row and its partner's row
+  //      of A once, applies the round's 8 column rotations to both in
+  //      registers, then the row rotation, and writes its row back.
   for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
-    float off = 0.0f, dia = 0.0f;
-    for (int jj = 0; jj < kPage; ++jj) {
-      const float a = sA[grp][li][jj];
-      if (jj == li) dia = a * a; else off = fmaf(a, a, off);
+    {
+      // off-diagonal mass summed directly (a difference of the row's total and
+      // the diagonal would be dominated by rounding near convergence)
+      float a[kPage];
+      ld_row(&sA[grp][li][0], a);
+      float off = 0.0f, d = 0.0f;
+#pragma unroll
+      for (int jj = 0; jj < kPage; ++jj) {
+        if (jj == li) d = a[jj]; else off = fmaf(a[jj], a[jj], off);
+      }
+      const float dia = group16_sum(d * d);
+      off = group16_sum(off);
+      if (__all(off <= 1e-12f * dia)) break;
     }
-    off = group16_sum(off);
-    dia = group16_sum(dia);
-    const int done = off <= 1e-12f * dia;
-    if (__all(done)) break;
+#pragma unroll
     for (int t = 0; t < 15; ++t) {
       const int p = partner(t, li);
       const int P = min(li, p), Q = max(li, p);
@@ -182,32 +205,34 @@ __global__ __launch_bounds__(64) void build_kernel(
         c = 1.0f / sqrtf(fmaf(tt, tt, 1.0f));
         sn = tt * c;
       }
-      sCS[grp][li] = make_float2(c, sn);
+      if (li == P) sCS[grp][P] = make_float2(c, sn);
       __syncthreads();
-      // columns: (A J) and (U J) on this lane's row
+      float a[kPage], b[kPage], u[kPage];
+      ld_row(&sA[grp][li][0], a);
+      ld_row(&sA[grp][p][0], b);
+      ld_row(&sU[grp][li][0], u);
+      // columns: A J and U J (pair (m, partner(t, m)) rotated by its leader's c, s)
+#pragma unroll
       for (int m = 0; m < kPage; ++m) {
         const int pm = partner(t, m);
         if (m < pm) {
           const float2 cs = sCS[grp][m];
-          const float x = sA[grp][li][m], y = sA[grp][li][pm];
-          sA[grp][li][m] = cs.x * x - cs.y * y;
-          sA[grp][li][pm] = cs.y * x + cs.x * y;
-          const float u = sU[grp][li][m], w = sU[grp][li][pm];
-          sU[grp][li][m] = cs.x * u - cs.y * w;
-          sU[grp][li][pm] = cs.y * u + cs.x * w;
+          const float ax = a[m], ay = a[pm], bx = b[m], by = b[pm], ux = u[m], uy = u[pm];
+          a[m] = cs.x * ax - cs.y * ay;
+          a[pm] = cs.y * ax + cs.x * ay;
+          b[m] = cs.x * bx - cs.y * by;
+          b[pm] = cs.y * bx + cs.x * by;
+          u[m] = cs.x * ux - cs.y * uy;
+          u[pm] = cs.y * ux + cs.x * uy;
         }
       }
-      __syncthreads();
       // rows: J^T (A J); lane P gets c*row_P - s*row_Q, lane Q gets s*row_P + c*row_Q
-      float nr[kPage];
+      const bool lead = li == P;
 #pragma unroll
-      for (int m = 0; m < kPage; ++m) {
-        const float xp = sA[grp][P][m], xq = sA[grp][Q][m];
-        nr[m] = (li == P) ? (c * xp - sn * xq) : (sn * xp + c * xq);
-      }
+      for (int m = 0; m < kPage; ++m) a[m] = lead ? (c * a[m] - sn * b[m]) : (sn * b[m] + c * a[m]);
       __syncthreads();
-#pragma unroll
-      for (int m = 0; m < kPage; ++m) sA[grp][li][m] = nr[m];
+      st_row(&sA[grp][li][0], a);
+      st_row(&sU[grp][li][0], u);
       __syncthreads();
     }
   }
