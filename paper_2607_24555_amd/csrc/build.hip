@@ -77,12 +77,16 @@ __global__ __launch_bounds__(64) void build_kernel(
     const int32_t* __restrict__ build_list, int n_items, int all_pages,
     uint8_t* __restrict__ summaries, float* __restrict__ mu_out, float* __restrict__ basis_out,
     float* __restrict__ coef_out, float* __restrict__ sigma2_out) {
-  // raw key rows (bf16 or fp32 as stored); deviations are formed on the fly as
-  // float(k) - mu, the same fp32 value for every use
-  __shared__ __align__(16) KT sK[kItems][kPage][kDim];
-  __shared__ __align__(16) float sA[kItems][kPage][kRow];
-  __shared__ __align__(16) float sU[kItems][kPage][kRow];
-  __shared__ float sC[kItems][kPage][kPage];
+  // raw key rows (bf16 or fp32 as stored; deviations are formed on the fly as
+  // float(k) - mu, the same fp32 value for every use) share LDS with the Jacobi
+  // matrices A and U, which are written once the Gram is complete
+  constexpr int kKBytes = kItems * kPage * kDim * (int)sizeof(KT);
+  constexpr int kJBytes = 2 * kItems * kPage * kRow * (int)sizeof(float);
+  __shared__ __align__(16) uint8_t sBuf[kKBytes > kJBytes ? kKBytes : kJBytes];
+  auto& sK = *reinterpret_cast<KT(*)[kItems][kPage][kDim]>(sBuf);
+  auto& sA = *reinterpret_cast<float(*)[kItems][kPage][kRow]>(sBuf);
+  auto& sU = *reinterpret_cast<float(*)[kItems][kPage][kRow]>(sBuf + kJBytes / 2);
+  __shared__ float sFlip[kItems][kMaxRank];
   __shared__ float sMu[kItems][kDim];
   __shared__ float2 sCS[kItems][kPage];
   __shared__ float sLam[kItems][kPage];
@@ -166,6 +170,7 @@ __global__ __launch_bounds__(64) void build_kernel(
         g[jj] = acc;
       }
     }
+    __syncthreads();  // every lane is done with the key rows: A and U reuse their LDS
 #pragma unroll
     for (int jj = 0; jj < kPage; ++jj) {
       sA[grp][li][jj] = g[jj];
@@ -255,7 +260,20 @@ __global__ __launch_bounds__(64) void build_kernel(
   const long out_item = all_pages ? 0 : (long)e * H_kv + h;
   uint8_t* rec = summaries + (blk * H_kv + h) * (long)rec_stride(r);
 
-  // ---- basis columns, one at a time: V[:, l] = D^T u_l / sigma_l
+  // ---- basis columns, one at a time: V[:, l] = D^T u_l / sigma_l.  This lane's
+  //      8 dimensions of the 16 key rows are re-read from global memory (the
+  //      page was just loaded, so they come from cache) and held in registers.
+  constexpr int kSliceVec = 8 * (int)sizeof(KT) / 16;  // 16-byte loads per 8-element slice
+  uint4 ks[kPage][kSliceVec];
+  {
+    const uint4* kpage = reinterpret_cast<const uint4*>(k_cache + (blk * H_kv + h) * kPage * kDim);
+#pragma unroll
+    for (int i = 0; i < kPage; ++i)
+#pragma unroll
+      for (int u = 0; u < kSliceVec; ++u)
+        ks[i][u] = active ? kpage[(i * kDim + 8 * li) / (16 / (int)sizeof(KT)) + u]
+                          : make_uint4(0, 0, 0, 0);
+  }
   float cabs = 0.0f;  // running max |C[li][:]| for the row scale
   for (int l = 0; l < r; ++l) {
     const float lam = sLam[grp][l];
@@ -264,13 +282,17 @@ __global__ __launch_bounds__(64) void build_kernel(
     const int mode = sOrd[grp][l];
     float v[8];
 #pragma unroll
-    for (int cc = 0; cc < 8; ++cc) {
-      const int c = 8 * li + cc;
-      float acc = 0.0f;
-      for (int i = 0; i < kPage; ++i)
-        acc = fmaf(load_elem(&sK[grp][i][0], c) - sMu[grp][c], sU[grp][i][mode], acc);
-      v[cc] = kept ? acc / sig : 0.0f;
+    for (int cc = 0; cc < 8; ++cc) v[cc] = 0.0f;
+    for (int i = 0; i < kPage; ++i) {
+      const float ui = sU[grp][i][mode];
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+        const float x = load_elem(reinterpret_cast<const KT*>(&ks[i][0]), cc);
+        v[cc] = fmaf(x - sMu[grp][8 * li + cc], ui, v[cc]);
+      }
     }
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) v[cc] = kept ? v[cc] / sig : 0.0f;
     // sign convention: largest |v| (first index on ties) made positive
     float best = -1.0f;
     int bidx = 0;
@@ -288,7 +310,7 @@ __global__ __launch_bounds__(64) void build_kernel(
     }
     const float flip = (bval < 0.0f) ? -1.0f : 1.0f;
     const float cval = kept ? flip * sU[grp][li][mode] * sig : 0.0f;
-    sC[grp][li][l] = cval;
+    if (li == 0) sFlip[grp][l] = flip;
     cabs = fmaxf(cabs, fabsf(cval));
     if (!active) continue;
     if (kFactors) {
@@ -307,13 +329,20 @@ __global__ __launch_bounds__(64) void build_kernel(
       if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * l) = f16_bits(vs);
     }
   }
+  __syncthreads();  // sFlip visible to the whole group
   if (!active) return;
+  // C[li][l] = flip_l * U[li][mode_l] * sigma_l (0 for a dropped mode)
+  auto coef_value = [&](int l) {
+    const float lam = sLam[grp][l];
+    const bool kept = lam > floor_ && lam > 0.0f;
+    return kept ? sFlip[grp][l] * sU[grp][li][sOrd[grp][l]] * sqrtf(lam) : 0.0f;
+  };
 
   if (kFactors) {
     float* mo = mu_out + out_item * kDim;
     for (int cc = 0; cc < 8; ++cc) mo[8 * li + cc] = sMu[grp][8 * li + cc];
     float* co = coef_out + out_item * (kPage * (long)r);
-    for (int l = 0; l < r; ++l) co[li * r + l] = sC[grp][li][l];
+    for (int l = 0; l < r; ++l) co[li * r + l] = coef_value(l);
     sigma2_out[out_item * kPage + li] = sLam[grp][li];
     return;
   }
@@ -322,7 +351,7 @@ __global__ __launch_bounds__(64) void build_kernel(
   {
     const float cs = f16_scale(cabs, 127.0f);
     for (int l = 0; l < r; ++l)
-      rec[rec_coef_off(r) + li * r + l] = (uint8_t)(quant(sC[grp][li][l], cs, 127) + 128);
+      rec[rec_coef_off(r) + li * r + l] = (uint8_t)(quant(coef_value(l), cs, 127) + 128);
     *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * (r + li)) = f16_bits(cs);
   }
   // ---- centroid: int8 with one scale
