@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="replay the step from captured HIP graphs instead of launching it")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="first run a plain fp32 copy of this many MiB four times (the "
+                         "known-size reference that scales hardware byte counters)")
     return ap.parse_args()
 
 
@@ -51,6 +54,54 @@ WORKLOADS = {
     "32k": (1, {}, "llama3.1-8b-32k: 1 seq x 32,768 tokens, 32 q / 8 kv heads, d 128, page 16, "
                    "r 8, b 2048, bf16 KV"),
 }
+
+
+# HBM traffic of the scan kernel, from two rocprofv3 counter runs of
+#   rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'locks|elementwise' -- \
+#       python bench.py --workload W --steps 4 --warmup 1 --no-dense --no-build \
+#       --no-cpu-baseline --copy-calib-mib 1024
+# and the same with WRITE_SIZE (KiB per dispatch; per-workload files under profiles/).
+# Each counter is divided by what it reads for the 1 GiB copy over 1 GiB, so the
+# result is in bytes.  Valid only for the scan sources these hashes name.
+SCAN_SOURCES = ("paper_2607_24555_amd/csrc/scan.hip", "paper_2607_24555_amd/csrc/locks_internal.h")
+SCAN_TRAFFIC = {
+    # workload: (sha256 of SCAN_SOURCES, FETCH_SIZE KiB, WRITE_SIZE KiB,
+    #            copy FETCH factor, copy WRITE factor, profile file)
+}
+
+
+def scan_sources_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in SCAN_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def scan_traffic(workload):
+    """Counted HBM bytes per scan launch, or None if not measured for the current
+    scan sources."""
+    t = SCAN_TRAFFIC.get(workload)
+    if t is None or t[0] != scan_sources_sha():
+        return None, None
+    _, fetch_kib, write_kib, ff, fw, prof = t
+    fetch, write = fetch_kib * 1024 / ff, write_kib * 1024 / fw
+    return int(fetch + write), {"fetch_bytes": int(fetch), "write_bytes": int(write),
+                                "copy_factor_fetch": ff, "copy_factor_write": fw,
+                                "source_sha": t[0], "profile": prof}
+
+
+def copy_calibration(mib, dev):
+    """A plain copy of known size (reads and writes mib MiB) for counter scaling."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(4):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def as_graphs(fn, n_copies):
@@ -133,6 +184,8 @@ def main():
     from workloads import make_workload
 
     dev = torch.device("cuda:0")
+    if args.copy_calib_mib > 0:
+        copy_calibration(args.copy_calib_mib, dev)
     wid, ov, desc = WORKLOADS[args.workload]
     t_gen = time.perf_counter()
     w = make_workload(wid, seed=args.seed, device=dev, **ov)
@@ -200,6 +253,7 @@ def main():
         dense_us, _ = timed(drun, max(4, args.steps // 4), sync)
 
     scan_gbps = alg_scan / (scan_us * 1e-6) / 1e9
+    traffic, traffic_detail = scan_traffic(args.workload)
     res = {
         "metric": METRIC,
         "value": round(step_wall_us, 2),
@@ -218,7 +272,8 @@ def main():
                    "copies_rotated": R},
         "roofline": {"bound": "hbm", "kernel": "scan_kernel (locks_score_pages)",
                      "achieved": round(scan_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(scan_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(scan_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "traffic_detail": traffic_detail,
                      "alg_bytes_per_launch": alg_scan, "unit_bytes": payload,
                      "units_per_launch": complete_heads, "avg_launch_us": round(scan_us, 2)},
         "step": {"alg_bytes": alg_step, "alg_GBps": round(alg_step / (step_wall_us * 1e-6) / 1e9, 1),

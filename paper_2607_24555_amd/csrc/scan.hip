@@ -883,6 +883,222 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
 }
 
+// ---------------------------------------------------------------------------
+// r = 8, G = 4: stage 2 with a block-diagonal B.
+//
+// A wave covers 16 pages per step, as four quads of 4 pages; every operand is
+// loaded straight from the records into the register layout it is used in.
+// For quad Q:
+//  * stage 1 (int8 MFMA, two basis sets i = 0, 1): A row m is (page 4 Q + m / 4,
+//    basis column 4 i + m % 4); the 16 B columns are the 4 heads repeated 4
+//    times.  Lane (grp, col) receives p(page 4 Q + grp, l = 4 i + j, head col % 4)
+//    in register j, so its 8 values over both sets are the basis projections of
+//    one (page, head) in natural l order.
+//  * stage 2 (f16 MFMA 16x16x32, B as hi + lo): rows are the 16 tokens, K index
+//    8 a + l is (page 4 Q + a, basis column l), columns are (a, g) = (col / 4,
+//    col % 4).  B is block diagonal: a lane contributes its 8 stage-1 values
+//    where grp == col / 4 and zeros elsewhere (its scale factor is zero), A is
+//    the coefficient row of token col of page 4 Q + grp.  Register j of lane
+//    (grp, col) is then the logit of token 4 grp + j of page 4 Q + col / 4 for
+//    head col % 4, minus the centroid logit.
+//  * page LSE: 4 values per lane, then the 4 lanes of a column.
+// The centroid MFMA (once per step) puts page 4 (m % 4) + m / 4 in row m, so
+// register Q of lane (grp, col) holds a(page 4 Q + grp, head col % 4): the
+// centroid of the lanes with grp == col / 4, which keep the result.
+// ---------------------------------------------------------------------------
+template <typename QT, int kSteps>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8g4_kernel(
+    int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
+    float* __restrict__ s_hat, SHatLayout lay, float2* __restrict__ partials) {
+  constexpr int R = 8, G = 4;
+  constexpr uint32_t kStride = rec_stride(R);
+  constexpr uint32_t kCoef = rec_coef_off(R), kMu = rec_mu_off(R), kSc = rec_scale_off(R);
+  __shared__ float2 sRun[4][64];
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int h = blockIdx.y, s = blockIdx.z;
+  const int n_c = seq_lens[s] / kPage;
+  const int pg = blockIdx.x * 4 + wave;
+  const long row0 = (long)s * H_q + (long)h * G;
+  const int32_t* pt_row = page_table + (long)s * max_pages;
+  const int ca = col >> 2, g = col & 3;
+  const bool diag = grp == ca;
+  float run_m = -INFINITY, run_s = 0.0f;
+
+  constexpr int kWavePages = 16 * kSteps;
+  if (pg * kWavePages < n_c) {
+    // record of page `page` (0..15) of the step whose blocks lanes 0..15 hold
+    auto rec = [&](int blk, int page) -> uint32_t {
+      return ((uint32_t)__shfl(blk, page, 64) * (uint32_t)H_kv + (uint32_t)h) * kStride;
+    };
+    uint4 vb[4][2];    // basis rows of quad Q, set i
+    uint2 cf[4];       // coefficient row `col` of page 4 Q + grp
+    uint2 cs[4];       // row scales of tokens 4 grp .. 4 grp + 3 of page 4 Q + ca
+    uint4 vs[4];       // basis column scales of page 4 Q + grp
+    uint32_t msw[4];   // centroid scale of page 4 Q + grp (low half)
+    uint4 mu[2];       // centroid bytes 32 grp .. 32 grp + 31 of page 4 (col % 4) + ca
+    auto issue_quad = [&](int blk, int Q) {
+      const uint32_t ra = rec(blk, 4 * Q + ca), rb = rec(blk, 4 * Q + grp);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        vb[Q][i] = *reinterpret_cast<const uint4*>(summ + ra + 64u * (4 * i + g) + 16u * grp);
+      cf[Q] = *reinterpret_cast<const uint2*>(summ + rb + kCoef + 8u * col);
+      cs[Q] = *reinterpret_cast<const uint2*>(summ + ra + kSc + 2u * (R + 4 * grp));
+      vs[Q] = *reinterpret_cast<const uint4*>(summ + rb + kSc);
+      msw[Q] = *reinterpret_cast<const uint32_t*>(summ + rb + kSc + 2u * (R + 16));
+    };
+    auto issue_mu = [&](int blk) {
+      const uint32_t rm = rec(blk, 4 * g + ca) + kMu + 32u * grp;
+      mu[0] = *reinterpret_cast<const uint4*>(summ + rm);
+      mu[1] = *reinterpret_cast<const uint4*>(summ + rm + 16u);
+    };
+    {
+      const int blk0 = lane_block(pt_row, pg * kWavePages, n_c, lane);
+      issue_mu(blk0);
+#pragma unroll
+      for (int Q = 0; Q < 4; ++Q) issue_quad(blk0, Q);
+    }
+    int blk_n1 = pg * kWavePages + 16 < n_c ? lane_block(pt_row, pg * kWavePages + 16, n_c, lane) : 0;
+    const QDigits QD = q_digits(q + (row0 + g) * kDim, grp);
+    const float inv_m = diag ? QD.inv_scale : 0.0f;  // zero off the block diagonal of B
+    float* shat_base = s_hat + lay.base(s, h) + (long)g * lay.head;
+
+#pragma unroll 1
+    for (int t = 0; t < kSteps; ++t) {
+      const int page0 = (pg * kSteps + t) * 16;
+      if (page0 >= n_c) break;
+      const bool more = t + 1 < kSteps && page0 + 16 < n_c;
+      const int blk_n2 = (t + 2 < kSteps && page0 + 32 < n_c) ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
+
+      // ---- centroid term: areg[j] = a(page 4 j + grp, head g)
+      float areg[4];
+      {
+        const uint32_t mw[8] = {mu[0].x ^ 0x80808080u, mu[0].y ^ 0x80808080u, mu[0].z ^ 0x80808080u,
+                                mu[0].w ^ 0x80808080u, mu[1].x ^ 0x80808080u, mu[1].y ^ 0x80808080u,
+                                mu[1].z ^ 0x80808080u, mu[1].w ^ 0x80808080u};
+        if (more) issue_mu(blk_n1);
+        i4v acc[3];
+#pragma unroll
+        for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
+          const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
+                         (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
+                         (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
+                         (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
+#pragma unroll
+          for (int d = 0; d < 3; ++d)
+            acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float ms = (float)as_h2(msw[j]).x;
+          const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
+          areg[j] = v * (ms * QD.inv_scale);
+        }
+      }
+
+#pragma unroll
+      for (int Q = 0; Q < 4; ++Q) {
+        __builtin_amdgcn_sched_barrier(0);
+        // ---- stage 1: vals[4 i + j] = p(page 4 Q + grp, l = 4 i + j, head g), zero off-diagonal
+        float vals[8];
+        const uint4 vq = vs[Q];
+        const uint32_t vsw[4] = {vq.x, vq.y, vq.z, vq.w};
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const uint32_t w[4] = {vb[Q][i].x, vb[Q][i].y, vb[Q][i].z, vb[Q][i].w};
+          i4v acc[3];
+#pragma unroll
+          for (int d = 0; d < 3; ++d) acc[d] = i4v{QD.bias[d], QD.bias[d], QD.bias[d], QD.bias[d]};
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
+            const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
+                           (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+#pragma unroll
+            for (int d = 0; d < 3; ++d)
+              acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int l = 4 * i + j;
+            const h2 pr = as_h2(vsw[l >> 1]);
+            const float vsc = (float)((l & 1) ? pr.y : pr.x);
+            const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
+            vals[l] = v * (vsc * inv_m);
+          }
+        }
+        const h8 A = byte8_to_h8(cf[Q].x, cf[Q].y);
+        const uint2 csq = cs[Q];
+        const float am = areg[Q];
+        if (more) issue_quad(blk_n1, Q);
+        // ---- stage 2 for the quad
+        h8 bh, bl;
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const auto hi = __builtin_amdgcn_cvt_pkrtz(vals[e], vals[e + 1]);
+          const auto lo = __builtin_amdgcn_cvt_pkrtz(vals[e] - (float)hi[0], vals[e + 1] - (float)hi[1]);
+          bh[e] = hi[0];
+          bh[e + 1] = hi[1];
+          bl[e] = lo[0];
+          bl[e + 1] = lo[1];
+        }
+        f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bh, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bl, acc, 0, 0, 0);
+        const h2 c01 = as_h2(csq.x), c23 = as_h2(csq.y);
+        float z[4] = {(float)c01.x * acc[0], (float)c01.y * acc[1], (float)c23.x * acc[2],
+                      (float)c23.y * acc[3]};
+        // z are the logits minus the centroid logit (sum over a page's tokens
+        // ~0, so sum 2^z needs no max); a max-shifted sum is taken if any lane's
+        // sum is not finite and positive.
+        float sm = __builtin_amdgcn_exp2f(z[0]) + __builtin_amdgcn_exp2f(z[1]) +
+                   __builtin_amdgcn_exp2f(z[2]) + __builtin_amdgcn_exp2f(z[3]);
+        sm = red4_sum(sm);
+        float shift = 0.0f;
+        if (__any(!(sm > 0.0f && sm < INFINITY))) {
+          shift = red4_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
+          sm = __builtin_amdgcn_exp2f(z[0] - shift) + __builtin_amdgcn_exp2f(z[1] - shift) +
+               __builtin_amdgcn_exp2f(z[2] - shift) + __builtin_amdgcn_exp2f(z[3] - shift);
+          sm = red4_sum(sm);
+        }
+        const float s2 = am + shift + __builtin_amdgcn_logf(sm);
+        const int page = page0 + 4 * Q + ca;
+        const bool live = diag && page < n_c;
+        if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
+        const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+        const bool up = s2 > run_m;
+        const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
+        run_s = live ? ns : run_s;
+        run_m = (live && up) ? s2 : run_m;
+      }
+      blk_n1 = blk_n2;
+    }
+  }
+  // ---- block partial (max, sum exp) per head over its pages, log2 domain
+  sRun[wave][lane] = make_float2(run_m, run_s);
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int gg = threadIdx.x;
+    float m = -INFINITY, l = 0.0f;
+    for (int w = 0; w < 4; ++w)
+      for (int c = gg; c < 64; c += 4) m = fmaxf(m, sRun[w][c].x);
+    if (m > -INFINITY)
+      for (int w = 0; w < 4; ++w)
+        for (int c = gg; c < 64; c += 4) {
+          const float2 v = sRun[w][c];
+          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+        }
+    partials[(row0 + gg) * gridDim.x + blockIdx.x] = make_float2(m, l);
+  }
+}
+
+constexpr int kG4Steps = 4;
+
 template <typename QT>
 hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H_kv, int max_pages,
                          const QT* q, const uint8_t* sum, const int32_t* pt, const int32_t* sl,
@@ -896,6 +1112,11 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
   if (r == 8 && G == 16) {
     hipLaunchKernelGGL((scan_r8_kernel<QT>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
                        sum, pt, sl, s_hat, lay, part);
+    return hipGetLastError();
+  }
+  if (r == 8 && G == 4) {
+    hipLaunchKernelGGL((scan_r8g4_kernel<QT, kG4Steps>), grid, dim3(256), 0, st, H_q, H_kv,
+                       max_pages, q, sum, pt, sl, s_hat, lay, part);
     return hipGetLastError();
   }
   LOCKS_SCAN_FAST(8, 4) LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(4, 4)
@@ -925,8 +1146,14 @@ static bool use_r8_kernel(const locks_cfg_t& c) {
   return c.rank == 8 && c.num_q_heads == 16 * c.num_kv_heads;
 }
 
+static bool use_r8g4_kernel(const locks_cfg_t& c) {
+  return c.rank == 8 && c.num_q_heads == 4 * c.num_kv_heads;
+}
+
 int scan_pages_per_block(const locks_cfg_t& c) {
-  return use_r8_kernel(c) ? 64 * kR8Steps : kScanPagesPerBlock;
+  if (use_r8_kernel(c)) return 64 * kR8Steps;
+  if (use_r8g4_kernel(c)) return 64 * kG4Steps;
+  return kScanPagesPerBlock;
 }
 
 hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,

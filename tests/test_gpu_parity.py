@@ -276,6 +276,7 @@ def test_build_factors_reconstruct_like_oracle(case):
     (1, [0, 5, 16, 17, 48, 200, 1000], 8, 64, "bf16"),
     (8, [0, 15, 16, 33, 160, 161, 2000], 1, 48, "bf16"),
     (4, [2048, 1, 999, 32], 15, 512, "fp32"),
+    (4, [16 * 300 + 5, 777, 16 * 64], 8, 256, "fp32"),
     (2, [4096 * 4 + 3, 64], 8, 2048, "bf16"),
     # budget above 2080 tokens: the block-level (generic) selection path
     (4, [16 * 700 + 7, 16 * 300, 5000, 16 * 257], 8, 4096, "bf16"),
