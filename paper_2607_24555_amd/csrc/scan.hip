@@ -906,6 +906,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // register Q of lane (grp, col) holds a(page 4 Q + grp, head col % 4): the
 // centroid of the lanes with grp == col / 4, which keep the result.
 // ---------------------------------------------------------------------------
+template <int N>
+struct IntTag {
+  static constexpr int value = N;
+};
+
+// Block of page min(page0 + (lane & 15), n_c - 1): always a valid page of the sequence.
+__device__ __forceinline__ int lane_block_clamped(const int32_t* __restrict__ pt_row, int page0,
+                                                  int n_c, int lane) {
+  const int pl = page0 + (lane & 15);
+  return pt_row[pl < n_c ? pl : n_c - 1];
+}
+
 template <typename QT, int kSteps>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8g4_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
@@ -916,7 +928,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   constexpr uint32_t kCoef = rec_coef_off(R), kMu = rec_mu_off(R), kSc = rec_scale_off(R);
   __shared__ float2 sRun[4][64];
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = blockIdx.y, s = blockIdx.z;
   const int n_c = seq_lens[s] / kPage;
@@ -928,155 +940,206 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   float run_m = -INFINITY, run_s = 0.0f;
 
   constexpr int kWavePages = 16 * kSteps;
-  if (pg * kWavePages < n_c) {
-    // record of page `page` (0..15) of the step whose blocks lanes 0..15 hold
-    auto rec = [&](int blk, int page) -> uint32_t {
-      return ((uint32_t)__shfl(blk, page, 64) * (uint32_t)H_kv + (uint32_t)h) * kStride;
+  const int first = pg * kWavePages;
+  if (first < n_c) {
+    const int n_steps = min(kSteps, (n_c - first + 15) / 16);
+    const QDigits QD = q_digits(q + (row0 + g) * kDim, grp);
+    const float inv_m = diag ? QD.inv_scale : 0.0f;  // zero off the block diagonal of B
+    float* shat_base = s_hat + lay.base(s, h) + (long)g * lay.head;
+
+    // record offsets of one step: ra[Q] page 4 Q + ca, rb[Q] page 4 Q + grp,
+    // rm page 4 g + ca (the centroid row of this lane)
+    struct Offs {
+      uint32_t ra[4], rb[4], rm;
+    };
+    auto offsets = [&](int blk) {
+      Offs o;
+      auto rec = [&](int page) {
+        return ((uint32_t)__shfl(blk, page, 64) * (uint32_t)H_kv + (uint32_t)h) * kStride;
+      };
+#pragma unroll
+      for (int Q = 0; Q < 4; ++Q) {
+        o.ra[Q] = rec(4 * Q + ca);
+        o.rb[Q] = rec(4 * Q + grp);
+      }
+      o.rm = rec(4 * g + ca);
+      return o;
     };
     uint4 vb[4][2];    // basis rows of quad Q, set i
     uint2 cf[4];       // coefficient row `col` of page 4 Q + grp
     uint2 cs[4];       // row scales of tokens 4 grp .. 4 grp + 3 of page 4 Q + ca
     uint4 vs[4];       // basis column scales of page 4 Q + grp
     uint32_t msw[4];   // centroid scale of page 4 Q + grp (low half)
-    uint4 mu[2];       // centroid bytes 32 grp .. 32 grp + 31 of page 4 (col % 4) + ca
-    auto issue_quad = [&](int blk, int Q) {
-      const uint32_t ra = rec(blk, 4 * Q + ca), rb = rec(blk, 4 * Q + grp);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        vb[Q][i] = *reinterpret_cast<const uint4*>(summ + ra + 64u * (4 * i + g) + 16u * grp);
-      cf[Q] = *reinterpret_cast<const uint2*>(summ + rb + kCoef + 8u * col);
-      cs[Q] = *reinterpret_cast<const uint2*>(summ + ra + kSc + 2u * (R + 4 * grp));
-      vs[Q] = *reinterpret_cast<const uint4*>(summ + rb + kSc);
-      msw[Q] = *reinterpret_cast<const uint32_t*>(summ + rb + kSc + 2u * (R + 16));
+    uint4 mu[2];       // centroid bytes 32 grp .. 32 grp + 31 of page 4 g + ca
+    // loads of one step's registers; in a run the next step's are issued right
+    // after the register's last use in the current one
+    auto ld_vb = [&](const Offs& o, int Q, int i) {
+      vb[Q][i] = *reinterpret_cast<const uint4*>(summ + o.ra[Q] + 64u * (4 * i + g) + 16u * grp);
     };
-    auto issue_mu = [&](int blk) {
-      const uint32_t rm = rec(blk, 4 * g + ca) + kMu + 32u * grp;
-      mu[0] = *reinterpret_cast<const uint4*>(summ + rm);
-      mu[1] = *reinterpret_cast<const uint4*>(summ + rm + 16u);
+    auto ld_cf = [&](const Offs& o, int Q) {
+      cf[Q] = *reinterpret_cast<const uint2*>(summ + o.rb[Q] + kCoef + 8u * col);
     };
-    {
-      const int blk0 = lane_block(pt_row, pg * kWavePages, n_c, lane);
-      issue_mu(blk0);
-#pragma unroll
-      for (int Q = 0; Q < 4; ++Q) issue_quad(blk0, Q);
-    }
-    int blk_n1 = pg * kWavePages + 16 < n_c ? lane_block(pt_row, pg * kWavePages + 16, n_c, lane) : 0;
-    const QDigits QD = q_digits(q + (row0 + g) * kDim, grp);
-    const float inv_m = diag ? QD.inv_scale : 0.0f;  // zero off the block diagonal of B
-    float* shat_base = s_hat + lay.base(s, h) + (long)g * lay.head;
+    auto ld_cs = [&](const Offs& o, int Q) {
+      cs[Q] = *reinterpret_cast<const uint2*>(summ + o.ra[Q] + kSc + 2u * (R + 4 * grp));
+    };
+    auto ld_vs = [&](const Offs& o, int Q) {
+      vs[Q] = *reinterpret_cast<const uint4*>(summ + o.rb[Q] + kSc);
+    };
+    auto ld_ms = [&](const Offs& o, int Q) {
+      msw[Q] = *reinterpret_cast<const uint32_t*>(summ + o.rb[Q] + kSc + 2u * (R + 16));
+    };
+    auto ld_mu = [&](const Offs& o) {
+      mu[0] = *reinterpret_cast<const uint4*>(summ + o.rm + kMu + 32u * grp);
+      mu[1] = *reinterpret_cast<const uint4*>(summ + o.rm + kMu + 32u * grp + 16u);
+    };
 
-#pragma unroll 1
-    for (int t = 0; t < kSteps; ++t) {
-      const int page0 = (pg * kSteps + t) * 16;
-      if (page0 >= n_c) break;
-      const bool more = t + 1 < kSteps && page0 + 16 < n_c;
-      const int blk_n2 = (t + 2 < kSteps && page0 + 32 < n_c) ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
-
-      // ---- centroid term: areg[j] = a(page 4 j + grp, head g)
-      float areg[4];
+    // kN consecutive 16-page steps from page `start`, fully unrolled so that
+    // every wait for a prefetched register counts exactly the loads issued
+    // after it
+    auto run = [&](int start, auto n_tag) {
+      constexpr int kN = decltype(n_tag)::value;
+      int blk_next = 0;  // blocks of the pages of step t + 1
       {
-        const uint32_t mw[8] = {mu[0].x ^ 0x80808080u, mu[0].y ^ 0x80808080u, mu[0].z ^ 0x80808080u,
-                                mu[0].w ^ 0x80808080u, mu[1].x ^ 0x80808080u, mu[1].y ^ 0x80808080u,
-                                mu[1].z ^ 0x80808080u, mu[1].w ^ 0x80808080u};
-        if (more) issue_mu(blk_n1);
-        i4v acc[3];
+        const int blk0 = lane_block_clamped(pt_row, start, n_c, lane);
+        if (kN > 1) blk_next = lane_block_clamped(pt_row, start + 16, n_c, lane);
+        const Offs o0 = offsets(blk0);
+        ld_mu(o0);
 #pragma unroll
-        for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
-          const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
-                         (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
-                         (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
-                         (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
-#pragma unroll
-          for (int d = 0; d < 3; ++d)
-            acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float ms = (float)as_h2(msw[j]).x;
-          const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
-          areg[j] = v * (ms * QD.inv_scale);
+        for (int Q = 0; Q < 4; ++Q) {
+          ld_vb(o0, Q, 0);
+          ld_vb(o0, Q, 1);
+          ld_vs(o0, Q);
+          ld_cf(o0, Q);
+          ld_ms(o0, Q);
+          ld_cs(o0, Q);
         }
       }
+#pragma unroll
+      for (int t = 0; t < kN; ++t) {
+        const bool pf = t + 1 < kN;
+        const int page0 = start + 16 * t;
+        Offs on;
+        int blk_after = 0;
+        if (pf) {
+          on = offsets(blk_next);
+          if (t + 2 < kN) blk_after = lane_block_clamped(pt_row, page0 + 32, n_c, lane);
+        }
 
-#pragma unroll
-      for (int Q = 0; Q < 4; ++Q) {
-        __builtin_amdgcn_sched_barrier(0);
-        // ---- stage 1: vals[4 i + j] = p(page 4 Q + grp, l = 4 i + j, head g), zero off-diagonal
-        float vals[8];
-        const uint4 vq = vs[Q];
-        const uint32_t vsw[4] = {vq.x, vq.y, vq.z, vq.w};
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const uint32_t w[4] = {vb[Q][i].x, vb[Q][i].y, vb[Q][i].z, vb[Q][i].w};
+        // ---- centroid term: areg[j] = a(page 4 j + grp, head g) / (scale of that page)
+        float areg[4];
+        {
+          const uint32_t mw[8] = {mu[0].x ^ 0x80808080u, mu[0].y ^ 0x80808080u,
+                                  mu[0].z ^ 0x80808080u, mu[0].w ^ 0x80808080u,
+                                  mu[1].x ^ 0x80808080u, mu[1].y ^ 0x80808080u,
+                                  mu[1].z ^ 0x80808080u, mu[1].w ^ 0x80808080u};
+          if (pf) ld_mu(on);
           i4v acc[3];
 #pragma unroll
-          for (int d = 0; d < 3; ++d) acc[d] = i4v{QD.bias[d], QD.bias[d], QD.bias[d], QD.bias[d]};
+          for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
-            const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
-            const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
-                           (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+            const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
+            const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
+                           (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
+                           (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
+                           (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
 #pragma unroll
             for (int d = 0; d < 3; ++d)
               acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
           }
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int l = 4 * i + j;
-            const h2 pr = as_h2(vsw[l >> 1]);
-            const float vsc = (float)((l & 1) ? pr.y : pr.x);
-            const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
-            vals[l] = v * (vsc * inv_m);
-          }
+          for (int j = 0; j < 4; ++j)
+            areg[j] = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
         }
-        const h8 A = byte8_to_h8(cf[Q].x, cf[Q].y);
-        const uint2 csq = cs[Q];
-        const float am = areg[Q];
-        if (more) issue_quad(blk_n1, Q);
-        // ---- stage 2 for the quad
-        h8 bh, bl;
+
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const auto hi = __builtin_amdgcn_cvt_pkrtz(vals[e], vals[e + 1]);
-          const auto lo = __builtin_amdgcn_cvt_pkrtz(vals[e] - (float)hi[0], vals[e + 1] - (float)hi[1]);
-          bh[e] = hi[0];
-          bh[e + 1] = hi[1];
-          bl[e] = lo[0];
-          bl[e + 1] = lo[1];
-        }
-        f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bh, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bl, acc, 0, 0, 0);
-        const h2 c01 = as_h2(csq.x), c23 = as_h2(csq.y);
-        float z[4] = {(float)c01.x * acc[0], (float)c01.y * acc[1], (float)c23.x * acc[2],
-                      (float)c23.y * acc[3]};
-        // z are the logits minus the centroid logit (sum over a page's tokens
-        // ~0, so sum 2^z needs no max); a max-shifted sum is taken if any lane's
-        // sum is not finite and positive.
-        float sm = __builtin_amdgcn_exp2f(z[0]) + __builtin_amdgcn_exp2f(z[1]) +
-                   __builtin_amdgcn_exp2f(z[2]) + __builtin_amdgcn_exp2f(z[3]);
-        sm = red4_sum(sm);
-        float shift = 0.0f;
-        if (__any(!(sm > 0.0f && sm < INFINITY))) {
-          shift = red4_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
-          sm = __builtin_amdgcn_exp2f(z[0] - shift) + __builtin_amdgcn_exp2f(z[1] - shift) +
-               __builtin_amdgcn_exp2f(z[2] - shift) + __builtin_amdgcn_exp2f(z[3] - shift);
+        for (int Q = 0; Q < 4; ++Q) {
+          __builtin_amdgcn_sched_barrier(0);
+          // ---- stage 1: vals[4 i + j] = p(page 4 Q + grp, l = 4 i + j, head g), zero off-diagonal
+          float vals[8];
+          i4v acc1[2][3];
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            const uint32_t w[4] = {vb[Q][i].x, vb[Q][i].y, vb[Q][i].z, vb[Q][i].w};
+#pragma unroll
+            for (int d = 0; d < 3; ++d) acc1[i][d] = i4v{QD.bias[d], QD.bias[d], QD.bias[d], QD.bias[d]};
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
+              const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
+                             (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+#pragma unroll
+              for (int d = 0; d < 3; ++d)
+                acc1[i][d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc1[i][d], 0, 0, 0);
+            }
+            if (pf) ld_vb(on, Q, i);
+          }
+          {
+            const uint32_t vsw[4] = {vs[Q].x, vs[Q].y, vs[Q].z, vs[Q].w};
+#pragma unroll
+            for (int l = 0; l < 8; ++l) {
+              const i4v* a3 = acc1[l >> 2];
+              const int j = l & 3;
+              const h2 pr = as_h2(vsw[l >> 1]);
+              const float vsc = (float)((l & 1) ? pr.y : pr.x);
+              const float v = fmaf((float)a3[0][j], 65536.0f, (float)(a3[1][j] * 256 + a3[2][j]));
+              vals[l] = v * (vsc * inv_m);
+            }
+            if (pf) ld_vs(on, Q);
+          }
+          const h8 A = byte8_to_h8(cf[Q].x, cf[Q].y);
+          if (pf) ld_cf(on, Q);
+          const float am = areg[Q] * ((float)as_h2(msw[Q]).x * QD.inv_scale);
+          if (pf) ld_ms(on, Q);
+          // ---- stage 2 for the quad
+          h8 bh, bl;
+#pragma unroll
+          for (int e = 0; e < 8; e += 2) {
+            const auto hi = __builtin_amdgcn_cvt_pkrtz(vals[e], vals[e + 1]);
+            const auto lo = __builtin_amdgcn_cvt_pkrtz(vals[e] - (float)hi[0], vals[e + 1] - (float)hi[1]);
+            bh[e] = hi[0];
+            bh[e + 1] = hi[1];
+            bl[e] = lo[0];
+            bl[e + 1] = lo[1];
+          }
+          f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bh, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bl, acc, 0, 0, 0);
+          const h2 c01 = as_h2(cs[Q].x), c23 = as_h2(cs[Q].y);
+          float z[4] = {(float)c01.x * acc[0], (float)c01.y * acc[1], (float)c23.x * acc[2],
+                        (float)c23.y * acc[3]};
+          if (pf) ld_cs(on, Q);
+          // z are the logits minus the centroid logit (sum over a page's tokens
+          // ~0, so sum 2^z needs no max); a max-shifted sum is taken if any
+          // lane's sum is not finite and positive.
+          float sm = __builtin_amdgcn_exp2f(z[0]) + __builtin_amdgcn_exp2f(z[1]) +
+                     __builtin_amdgcn_exp2f(z[2]) + __builtin_amdgcn_exp2f(z[3]);
           sm = red4_sum(sm);
+          float shift = 0.0f;
+          if (__any(!(sm > 0.0f && sm < INFINITY))) {
+            shift = red4_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
+            sm = __builtin_amdgcn_exp2f(z[0] - shift) + __builtin_amdgcn_exp2f(z[1] - shift) +
+                 __builtin_amdgcn_exp2f(z[2] - shift) + __builtin_amdgcn_exp2f(z[3] - shift);
+            sm = red4_sum(sm);
+          }
+          const float s2 = am + shift + __builtin_amdgcn_logf(sm);
+          const int page = page0 + 4 * Q + ca;
+          const bool live = diag && page < n_c;
+          if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
+          const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+          const bool up = s2 > run_m;
+          const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
+          run_s = live ? ns : run_s;
+          run_m = (live && up) ? s2 : run_m;
         }
-        const float s2 = am + shift + __builtin_amdgcn_logf(sm);
-        const int page = page0 + 4 * Q + ca;
-        const bool live = diag && page < n_c;
-        if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
-        const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
-        const bool up = s2 > run_m;
-        const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
-        run_s = live ? ns : run_s;
-        run_m = (live && up) ? s2 : run_m;
+        blk_next = blk_after;
       }
-      blk_n1 = blk_n2;
+    };
+    if (n_steps == kSteps) {
+      run(first, IntTag<kSteps>{});
+    } else {
+#pragma unroll 1
+      for (int t = 0; t < n_steps; ++t) run(first + 16 * t, IntTag<1>{});
     }
   }
   // ---- block partial (max, sum exp) per head over its pages, log2 domain
