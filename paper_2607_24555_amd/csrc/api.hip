@@ -35,18 +35,19 @@ int hip_status(hipError_t e) {
 struct Ws {
   float* s_hat;
   float2* part;
-  uint32_t* ckey;
-  int32_t* cidx;
-  uint32_t* thr;
+  SelectBufs sel;
   float* attn;
 };
 
 Ws carve(void* ws, const WsPlan& p) {
   char* b = static_cast<char*>(ws);
+  const SelectBufs sel{reinterpret_cast<uint32_t*>(b + p.ckey_off),
+                       reinterpret_cast<int32_t*>(b + p.cidx_off),
+                       reinterpret_cast<int32_t*>(b + p.cblk_off),
+                       reinterpret_cast<uint32_t*>(b + p.sat_off),
+                       reinterpret_cast<uint32_t*>(b + p.keys_off), p.n_chunks};
   return Ws{reinterpret_cast<float*>(b + p.s_hat_off), reinterpret_cast<float2*>(b + p.part_off),
-            reinterpret_cast<uint32_t*>(b + p.ckey_off), reinterpret_cast<int32_t*>(b + p.cidx_off),
-            reinterpret_cast<uint32_t*>(b + p.thr_off),
-            reinterpret_cast<float*>(b + p.attn_off)};
+            sel, reinterpret_cast<float*>(b + p.attn_off)};
 }
 
 int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
@@ -88,9 +89,15 @@ WsPlan plan_workspace(const locks_cfg_t& c) {
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
   p.s_hat_off = take(S * Hq * mp * sizeof(float));
   p.part_off = take(S * Hq * (size_t)scan_blocks(c) * sizeof(float2));
-  p.ckey_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(uint32_t));
-  p.cidx_off = take(S * Hkv * (size_t)p.n_chunks * K * sizeof(int32_t));
-  p.thr_off = take(S * Hkv * (size_t)p.n_chunks * sizeof(uint32_t));
+  // survivor rows: the block-level path keeps k - 2 per chunk, the fast path `width`
+  const size_t rows = (size_t)select_fast_rows(c);
+  size_t surv = (size_t)p.n_chunks * K;
+  if (rows * (size_t)select_fast_width(c) > surv) surv = rows * (size_t)select_fast_width(c);
+  p.ckey_off = take(S * Hkv * surv * sizeof(uint32_t));
+  p.cidx_off = take(S * Hkv * surv * sizeof(int32_t));
+  p.cblk_off = take(S * Hkv * surv * sizeof(int32_t));
+  p.sat_off = take(S * Hkv * rows * sizeof(uint32_t));
+  p.keys_off = take(S * Hkv * mp * sizeof(uint32_t));
   p.attn_off = take(S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float));
   p.total = off;
   return p;
@@ -105,8 +112,8 @@ static int select_impl(const locks_cfg_t* c, const void* q, const void* summarie
   const SHatLayout lay = out_all_lse ? shat_head_major(*c) : shat_head_minor(*c);
   hipError_t e = launch_scan(*c, q, summaries, page_table, seq_lens, s_hat, lay, w.part, st);
   if (e != hipSuccess) return hip_status(e);
-  const SelectBufs sb{w.ckey, w.cidx, w.thr, p.n_chunks};
-  e = launch_select(*c, seq_lens, s_hat, lay, w.part, sb, out_page_ids, out_sel_lse, st);
+  e = launch_select(*c, page_table, seq_lens, s_hat, lay, w.part, w.sel, out_page_ids,
+                    out_sel_lse, st);
   return hip_status(e);
 }
 
@@ -242,12 +249,12 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
   if (attend_select_fused(*cfg)) {
     // scan -> per-chunk selection -> attention whose blocks merge the table
     const SHatLayout lay = shat_head_minor(*cfg);
-    const SelectBufs sb{w.ckey, w.cidx, w.thr, p.n_chunks};
     rc = hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, w.s_hat, lay, w.part, st));
     if (rc) return rc;
-    rc = hip_status(launch_select_chunks(*cfg, seq_lens, w.s_hat, lay, w.part, sb, st));
+    rc = hip_status(launch_select_chunks(*cfg, page_table, seq_lens, w.s_hat, lay, w.part, w.sel,
+                                         st));
     if (rc) return rc;
-    return hip_status(launch_attend_select(*cfg, q, k_cache, v_cache, page_table, seq_lens, sb,
+    return hip_status(launch_attend_select(*cfg, q, k_cache, v_cache, page_table, seq_lens, w.sel,
                                            w.s_hat, lay, out_page_ids, out_sel_lse,
                                            pps, splits, w.attn, out, out_lse, st));
   }

@@ -178,27 +178,25 @@ __device__ __forceinline__ void load_page(PageRegs& P, const uint16_t* kp, const
 // P enters as bf16 hi + lo (two MFMAs) so the weights keep ~16 bits.
 // Chunk survivors and outputs of the selection merged into the attention kernel.
 struct SelTable {
-  const uint32_t* cand_key;
-  const int32_t* cand_idx;
-  const uint32_t* thr;
-  int n_rows;
+  SelectBufs sb;
+  int n_rows, width;
   const float* s_hat;
   SHatLayout lay;
   int32_t* out_ids;
   float* out_sel_lse;
 };
 
-template <bool kSelect, int kNK = 8>
+template <bool kSelect>
 __global__ __launch_bounds__(256) void attend_mfma_kernel(
     int H_q, int H_kv, int max_pages, int k_list, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ page_ids, int pages_per_split, int n_splits,
     float* __restrict__ partial, SelTable tb) {
-  __shared__ float sO[4][kMaxGroup][kDim];
+  __shared__ float sO[4][kDim][kMaxGroup + 1];
   __shared__ float sM[4][kMaxGroup], sL[4][kMaxGroup];
-  __shared__ int32_t s_tab[kSelect ? kFastK + 2 : 1];
-  __shared__ MergeLds<4> mergeL;
+  __shared__ int32_t s_tab[kSelect ? kFastK + 2 : 1], s_blk[kSelect ? kFastK + 2 : 1];
+  __shared__ UnionLds<4> unionL;
   const int split = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c16 = lane & 15, r4 = lane >> 4;
@@ -219,27 +217,13 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
   const int32_t* ids = page_ids ? page_ids + ((long)s * H_kv + h) * k_list : nullptr;
   if constexpr (kSelect) {
     const long unit = (long)s * H_kv + h;
-    const int K = k_list - 2 > 0 ? k_list - 2 : 0;
     const int used = n > k_list ? (n - 2) / kFastChunk + 1 : 0;
-    merge_table<kNK, 4>(k_list, n, used, tb.cand_key + unit * tb.n_rows * K,
-                       tb.cand_idx + unit * tb.n_rows * K, tb.thr + unit * tb.n_rows, s_tab,
-                       mergeL);
+    const long rb = unit * tb.n_rows * tb.width;
+    union_table<kUnionNK, 4>(k_list, n, used, tb.width, tb.sb.cand_key + rb, tb.sb.cand_idx + rb,
+                             tb.sb.cand_blk + rb, tb.sb.sat + unit * tb.n_rows,
+                             tb.sb.keys + unit * max_pages, page_table + (long)s * max_pages,
+                             s_tab, s_blk, unionL);
     ids = s_tab;
-    // this block's table entries and their estimated page LSEs (NaN without a summary)
-    const int t0 = split * pages_per_split, n_c = L / kPage;
-    const float* sb = tb.s_hat + tb.lay.base(s, h);
-    for (int e = tid; e < pages_per_split * (G + 1); e += 256) {
-      const int t = t0 + e % pages_per_split, g = e / pages_per_split;
-      if (t >= k_list) continue;
-      const int id = s_tab[t];
-      if (g == G) {
-        tb.out_ids[unit * k_list + t] = id;
-      } else {
-        const bool ok = id >= 0 && id < n_c;
-        const float v = sb[(long)(ok ? id : 0) * tb.lay.page + (long)(ok ? g : 0) * tb.lay.head];
-        tb.out_sel_lse[((long)s * H_q + h * G + g) * k_list + t] = ok ? v : __int_as_float(0x7fc00000);
-      }
-    }
   }
   auto page_at = [&](int t) -> int {
     int id = -1;
@@ -248,10 +232,17 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
   };
   const long kv_head = (long)h * kPage * kDim;
   const long kv_blk = (long)H_kv * kPage * kDim;
-  auto page_ptr = [&](int id, const uint16_t* base) {
-    const long blk = page_table[(long)s * max_pages + (id >= 0 ? id : 0)];
-    return base + blk * kv_blk + kv_head;
+  // physical block of list entry t holding page id (a valid block stands in for an
+  // empty entry); the fused step knows the blocks from the selection
+  auto blk_at = [&](int t, int id) -> long {
+    if constexpr (kSelect) {
+      const int b = t < k_list ? s_blk[t] : -1;
+      return b >= 0 ? b : s_blk[0];
+    } else {
+      return page_table[(long)s * max_pages + (id >= 0 ? id : 0)];
+    }
   };
+  auto page_ptr = [&](long blk, const uint16_t* base) { return base + blk * kv_blk + kv_head; };
 
   float m = -INFINITY, l = 0.0f;
   f4v o[8];
@@ -261,13 +252,18 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
   if (n > 0) {
     int id = page_at(t_begin);
     PageRegs cur;
-    load_page(cur, page_ptr(id, k_cache), page_ptr(id, v_cache), c16, r4);
+    {
+      const long b = blk_at(t_begin, id);
+      load_page(cur, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
+    }
     for (int t = t_begin; t < t_end; ++t) {
       // prefetch the next entry (a valid page stands in for an empty one)
       const int id_next = page_at(t + 1);
       PageRegs nxt;
-      if (t + 1 < t_end)
-        load_page(nxt, page_ptr(id_next, k_cache), page_ptr(id_next, v_cache), c16, r4);
+      if (t + 1 < t_end) {
+        const long b = blk_at(t + 1, id_next);
+        load_page(nxt, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
+      }
       if (id >= 0) {
         const int valid = min(kPage, L - id * kPage);
         f4v st = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -310,12 +306,33 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
       cur = nxt;
     }
   }
-  // combine the block's four waves; m is kept in log2 units until here
+  if constexpr (kSelect) {
+    // this block's table entries and their estimated page LSEs (NaN without a
+    // summary), written while the last page is in flight
+    const long unit = (long)s * H_kv + h;
+    const int t0 = split * pages_per_split, n_c = L / kPage;
+    const float* sb = tb.s_hat + tb.lay.base(s, h);
+    for (int e = tid; e < pages_per_split * (G + 1); e += 256) {
+      const int t = t0 + e % pages_per_split, g = e / pages_per_split;
+      if (t >= k_list) continue;
+      const int id = s_tab[t];
+      if (g == G) {
+        tb.out_ids[unit * k_list + t] = id;
+      } else {
+        const bool ok = id >= 0 && id < n_c;
+        const float v = sb[(long)(ok ? id : 0) * tb.lay.page + (long)(ok ? g : 0) * tb.lay.head];
+        tb.out_sel_lse[((long)s * H_q + h * G + g) * k_list + t] = ok ? v : __int_as_float(0x7fc00000);
+      }
+    }
+  }
+  // combine the block's four waves; m is kept in log2 units until here.  sO is
+  // [wave][d][17]: the odd row pitch keeps both the MFMA-layout writes and the
+  // d-contiguous reads free of bank conflicts
   if (r4 == 0) { sM[wave][c16] = m; sL[wave][c16] = l; }
 #pragma unroll
   for (int t8 = 0; t8 < 8; ++t8)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sO[wave][c16][32 * r4 + 8 * j + t8] = o[t8][j];
+    for (int j = 0; j < 4; ++j) sO[wave][32 * r4 + 8 * j + t8][c16] = o[t8][j];
   __syncthreads();
   for (int e = tid; e < G * (kDim + 2); e += 256) {
     const int g = e / (kDim + 2), c = e % (kDim + 2);
@@ -328,7 +345,7 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
       for (int w = 0; w < 4; ++w) {
         const float wt = sM[w][g] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(sM[w][g] - mx);
         ls += sL[w][g] * wt;
-        if (c < kDim) acc += sO[w][g][c] * wt;
+        if (c < kDim) acc += sO[w][c][g] * wt;
       }
     }
     const float v = c < kDim ? acc : (c == kDim ? (mx == -INFINITY ? mx : mx * kLn2) : ls);
@@ -344,7 +361,7 @@ __global__ __launch_bounds__(kDim) void merge_kernel(int H_q, int n_splits,
   const int hq = blockIdx.x, s = blockIdx.y, c = threadIdx.x;
   const long row = (long)s * H_q + hq;
   const float* p = partial + row * n_splits * (kDim + 2);
-  constexpr int kB = 8;
+  constexpr int kB = 32;  // splits per round trip (every split of a sparse step)
   float m = -INFINITY, l = 0.0f, o = 0.0f;
   for (int t0 = 0; t0 < n_splits; t0 += kB) {
     float mt[kB], lt[kB], ot[kB];
@@ -418,8 +435,7 @@ hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cach
 }
 
 bool attend_select_fused(const locks_cfg_t& c) {
-  return c.q_dtype == LOCKS_BF16 && c.kv_dtype == LOCKS_BF16 && select_fast_path(c) &&
-         select_fast_merge_nk(c) == 8;
+  return c.q_dtype == LOCKS_BF16 && c.kv_dtype == LOCKS_BF16 && select_fast_path(c);
 }
 
 hipError_t launch_attend_select(const locks_cfg_t& c, const void* q, const void* k_cache,
@@ -428,9 +444,8 @@ hipError_t launch_attend_select(const locks_cfg_t& c, const void* q, const void*
                                 SHatLayout lay, int32_t* out_ids, float* out_sel_lse,
                                 int pages_per_split, int n_splits, float* partial, float* out,
                                 float* out_lse, hipStream_t st) {
-  const int rows = (c.max_pages_per_seq + kFastChunk - 1) / kFastChunk;
-  const SelTable tb{sb.cand_key, sb.cand_idx, sb.thr, rows, s_hat, lay, out_ids, out_sel_lse};
-  hipLaunchKernelGGL((attend_mfma_kernel<true, 8>), dim3(n_splits, c.num_kv_heads, c.num_seqs), dim3(256),
+  const SelTable tb{sb, select_fast_rows(c), select_fast_width(c), s_hat, lay, out_ids, out_sel_lse};
+  hipLaunchKernelGGL((attend_mfma_kernel<true>), dim3(n_splits, c.num_kv_heads, c.num_seqs), dim3(256),
                      0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq, page_budget(c),
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
                      static_cast<const uint16_t*>(v_cache), page_table, seq_lens, nullptr,

@@ -81,18 +81,22 @@ inline SHatLayout shat_head_minor(const locks_cfg_t& c) {
 struct WsPlan {
   size_t s_hat_off;   // float [S][H_kv][max_pages][G]    page scores (head-minor)
   size_t part_off;    // float2 [S][H_q][scan blocks]     (max, sum exp), log2 domain
-  size_t ckey_off;    // uint32 [S][H_kv][chunks][k-2]    per-chunk survivors (keys)
-  size_t cidx_off;    // int32  [S][H_kv][chunks][k-2]    per-chunk survivors (pages)
-  size_t thr_off;     // uint32 [S][H_kv][chunks]         per-chunk cut (lower bound)
+  size_t ckey_off;    // uint32 [S][H_kv][rows][width]    per-chunk survivors (keys)
+  size_t cidx_off;    // int32  [S][H_kv][rows][width]    per-chunk survivors (pages)
+  size_t cblk_off;    // int32  [S][H_kv][rows][width]    per-chunk survivors (physical blocks)
+  size_t sat_off;     // uint32 [S][H_kv][rows]           per-chunk truncation key
+  size_t keys_off;    // uint32 [S][H_kv][max_pages]      every page's key (exact fallback)
   size_t attn_off;    // float [S][H_q][splits][d + 2]    split-K partials
   size_t total;
-  int n_chunks;       // select chunks per sequence
+  int n_chunks;       // select chunks per sequence (block-level path)
   int n_splits;       // attention splits per (seq, KV head)
 };
 
 constexpr int kScanPagesPerBlock = 256;  // 4 waves x 64 pages (generic scan kernels)
 constexpr int kSelChunk = 1024;          // pages per selection chunk (block-level path)
-constexpr int kFastChunk = 4096;         // pages per selection chunk (fast path)
+constexpr int kFastChunk = 512;          // pages per selection chunk (fast path)
+constexpr int kUnionCap = 2048;          // chunk survivors one table merge holds
+constexpr int kUnionNK = kUnionCap / 256; // ... per lane of a 4-wave block
 constexpr int kSparsePagesPerSplit = 4;   // one page per wave of a 4-wave block
 constexpr int kDensePagesPerSplit = 256;
 
@@ -119,20 +123,26 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
 struct SelectBufs {
   uint32_t* cand_key;
   int32_t* cand_idx;
-  uint32_t* thr;
+  int32_t* cand_blk;
+  uint32_t* sat;
+  uint32_t* keys;
   int n_chunks;
 };
-// Fast selection: k - 2 <= 128 and every chunk survivor fits one merge block;
-// the merge holds 8 (small) or 32 survivors per lane.
+// Fast selection: k - 2 <= kFastK and at most kUnionCap / 8 chunks of kFastChunk
+// pages.  Each chunk keeps its top select_fast_width() keys; the table is the top k - 2
+// of their union unless a chunk was truncated at or above the union's cut, in
+// which case it is recomputed exactly from every page's key.
 bool select_fast_path(const locks_cfg_t& c);
-int select_fast_merge_nk(const locks_cfg_t& c);
-// Fast path, first half: per-chunk keys and top k - 2 (survivors + cuts in sb).
-hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
-                                SHatLayout lay, const float2* partials, const SelectBufs& sb,
-                                hipStream_t st);
-hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
-                         SHatLayout lay, const float2* partials, const SelectBufs& sb,
-                         int32_t* out_page_ids, float* out_sel_lse, hipStream_t st);
+int select_fast_rows(const locks_cfg_t& c);
+int select_fast_width(const locks_cfg_t& c);
+// Fast path, first half: every page's key and each chunk's top keys (in sb).
+hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* page_table,
+                                const int32_t* seq_lens, const float* s_hat, SHatLayout lay,
+                                const float2* partials, const SelectBufs& sb, hipStream_t st);
+hipError_t launch_select(const locks_cfg_t& c, const int32_t* page_table, const int32_t* seq_lens,
+                         const float* s_hat, SHatLayout lay, const float2* partials,
+                         const SelectBufs& sb, int32_t* out_page_ids, float* out_sel_lse,
+                         hipStream_t st);
 
 hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cache,
                          const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,

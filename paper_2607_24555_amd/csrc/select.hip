@@ -338,21 +338,25 @@ __global__ __launch_bounds__(kSelThreads) void select_merge_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Fast path, used when k - 2 <= kFastK and all chunk survivors fit one 4-wave
-// block's registers.  Two kernels:
-//   chunk - one 16-wave block per 4096 pages of a (sequence, KV head): Z_g from the scan
-//           partials, the share-averaged key of every page (staged in LDS), and
-//           the chunk's top K by a histogram cut;
-//   merge - one block per (sequence, KV head): top K of all chunk survivors,
-//           sink + recent, estimated page LSEs of the table.
+// Fast path (k - 2 <= kFastK, at most kUnionCap / 8 chunks of kFastChunk pages).
+// Two kernels:
+//   chunk - one 4-wave block per kFastChunk pages of a (sequence, KV head): Z_g
+//           from the scan partials, the share-averaged key of every page
+//           (also written out in full), and the
+//           chunk's top `width` keys with their pages and physical blocks, by a
+//           histogram cut; the key at which the chunk was truncated (0 if it
+//           kept every candidate);
+//   merge - one block per (sequence, KV head): union_table over the chunk
+//           survivors, the estimated page LSEs of the table.
 // The fused decode step runs the merge inside the attention kernel instead.
 // Keys live in registers wave-major, then register-major: element u of lane l
 // in wave w has position (w * NK + u) * 64 + l, which is page order, so ties
 // resolve to lower pages.
 // ---------------------------------------------------------------------------
 
-constexpr int kChunkWaves = 16;                           // 1024-thread chunk blocks
-constexpr int kChunkNK = kFastChunk / (64 * kChunkWaves);  // keys per lane in a chunk (4)
+constexpr int kChunkThreads = 256;
+constexpr int kChunkWaves = kChunkThreads / 64;
+constexpr int kChunkNK = kFastChunk / kChunkThreads;  // keys per lane in a chunk (2)
 
 // xor-shuffle inside groups of four lanes (DPP quad permutation).
 template <int O>
@@ -365,12 +369,11 @@ __device__ __forceinline__ uint32_t page_key(float m, float sum) {
 }
 
 template <int kG>  // G when one page's G scores are contiguous (4, 8, 16), else 0
-__global__ __launch_bounds__(64 * kChunkWaves) void select_chunk_keys_kernel(
-    int H_q, int H_kv, int k, const int32_t* __restrict__ seq_lens,
-    const float* __restrict__ s_hat, SHatLayout lay, const float2* __restrict__ partials,
-    int n_parts, uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx,
-    uint32_t* __restrict__ thr, int n_rows) {
-  constexpr int kT = 64 * kChunkWaves;
+__global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
+    int H_q, int H_kv, int k, int width, int max_pages, const int32_t* __restrict__ seq_lens,
+    const int32_t* __restrict__ page_table, const float* __restrict__ s_hat, SHatLayout lay,
+    const float2* __restrict__ partials, int n_parts, SelectBufs sb, int n_rows) {
+  constexpr int kT = kChunkThreads;
   __shared__ float s_lz2[kMaxGroup];
   __shared__ __align__(16) uint32_t sk[kFastChunk];
   __shared__ CutLds<kChunkWaves> L;
@@ -383,6 +386,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void select_chunk_keys_kernel(
   const int K = k - 2;
   const int p0 = chunk * kFastChunk;
   if (K <= 0 || n <= k || p0 > n - 2) return;
+  const long unit = (long)s * H_kv + h;
   const long row0 = (long)s * H_q + (long)h * G;
   const float* base = s_hat + lay.base(s, h);
   // contiguous layout: float4 number f = kT i + tid of the chunk's span holds
@@ -398,7 +402,14 @@ __global__ __launch_bounds__(64 * kChunkWaves) void select_chunk_keys_kernel(
       v[i] = *reinterpret_cast<const float4*>(base + j * kG + 4 * (tid % LP));
     }
   }
-  if (tid < 256) {
+  // physical blocks of this thread's key positions (pages past the end reuse n - 1)
+  int32_t blk[kChunkNK];
+#pragma unroll
+  for (int u = 0; u < kChunkNK; ++u) {
+    const int j = p0 + (wave * kChunkNK + u) * 64 + lane;
+    blk[u] = page_table[(long)s * max_pages + min(j, n - 1)];
+  }
+  {
     constexpr int kPer = 16;  // partials per thread and pass (16 threads per head)
     const int g = tid >> 4, sub = tid & 15;
     const float2* pp = partials + (row0 + (g < G ? g : 0)) * n_parts;
@@ -479,75 +490,92 @@ __global__ __launch_bounds__(64 * kChunkWaves) void select_chunk_keys_kernel(
   uint32_t key[kChunkNK];
 #pragma unroll
   for (int u = 0; u < kChunkNK; ++u) key[u] = sk[(wave * kChunkNK + u) * 64 + lane];
-  const WaveCut cut = block_hist_cut<kChunkNK, kChunkWaves>(key, K, HL, L);
-  const long row = (((long)s * H_kv + h) * n_rows + chunk) * K;
+  // every page's key (0 for the sink), for an exact recut when the survivors
+  // do not suffice; the chunks that run cover pages 0 .. n - 2
+#pragma unroll
+  for (int u = 0; u < kChunkNK; ++u) {
+    const int j = p0 + (wave * kChunkNK + u) * 64 + lane;
+    if (j < n) sb.keys[unit * max_pages + j] = key[u];
+  }
+  const WaveCut cut = block_hist_cut<kChunkNK, kChunkWaves>(key, width, HL, L);
+  const long row = (unit * n_rows + chunk) * width;
   const int tot = block_emit<kChunkNK, kChunkWaves>(key, cut, L, [&](int u, int slot) {
-    cand_key[row + slot] = key[u];
-    cand_idx[row + slot] = p0 + (wave * kChunkNK + u) * 64 + lane;
+    sb.cand_key[row + slot] = key[u];
+    sb.cand_idx[row + slot] = p0 + (wave * kChunkNK + u) * 64 + lane;
+    sb.cand_blk[row + slot] = blk[u];
   });
-  for (int t = tot + tid; t < K; t += kT) { cand_key[row + t] = 0u; cand_idx[row + t] = -1; }
-  if (tid == 0) thr[((long)s * H_kv + h) * n_rows + chunk] = tot == K ? cut.T : 1u;
+  for (int t = tot + tid; t < width; t += kT) {
+    sb.cand_key[row + t] = 0u;
+    sb.cand_idx[row + t] = -1;
+    sb.cand_blk[row + t] = -1;
+  }
+  if (tid == 0) sb.sat[unit * n_rows + chunk] = cut.take_eq > width ? 0u : cut.T;
 }
 
-template <int NK>
-__global__ __launch_bounds__(256) void select_merge_fast_kernel(
-    int H_q, int H_kv, int k, int n_rows, const int32_t* __restrict__ seq_lens,
-    const float* __restrict__ s_hat, SHatLayout lay, const uint32_t* __restrict__ cand_key,
-    const int32_t* __restrict__ cand_idx, const uint32_t* __restrict__ thr,
-    int32_t* __restrict__ out_ids, float* __restrict__ out_sel_lse) {
-  __shared__ MergeLds<4> ML;
-  __shared__ int32_t s_tab[kFastK + 2];
+__global__ __launch_bounds__(kChunkThreads) void select_merge_fast_kernel(
+    int H_q, int H_kv, int k, int width, int n_rows, int max_pages,
+    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ page_table,
+    const float* __restrict__ s_hat, SHatLayout lay, SelectBufs sb, int32_t* __restrict__ out_ids,
+    float* __restrict__ out_sel_lse) {
+  __shared__ UnionLds<kChunkWaves> UL;
+  __shared__ int32_t s_tab[kFastK + 2], s_blk[kFastK + 2];
   const int h = blockIdx.x, s = blockIdx.y, tid = threadIdx.x;
   const int Ls = seq_lens[s];
   const int n = (Ls + kPage - 1) / kPage;
   const int n_c = Ls / kPage;
   const int G = H_q / H_kv;
-  const int K = k - 2 > 0 ? k - 2 : 0;
   const long row0 = (long)s * H_q + (long)h * G;
   const long unit = (long)s * H_kv + h;
   const int used = n > k ? (n - 2) / kFastChunk + 1 : 0;
-  merge_table<NK, 4>(k, n, used, cand_key + unit * n_rows * K, cand_idx + unit * n_rows * K,
-                           thr + unit * n_rows, s_tab, ML);
+  union_table<kUnionNK, kChunkWaves>(
+      k, n, used, width, sb.cand_key + unit * n_rows * width, sb.cand_idx + unit * n_rows * width,
+      sb.cand_blk + unit * n_rows * width, sb.sat + unit * n_rows, sb.keys + unit * max_pages,
+      page_table + (long)s * max_pages, s_tab, s_blk, UL);
   if (tid < k) out_ids[unit * k + tid] = s_tab[tid];
   // estimated page LSE of every table entry (NaN for a partial page or padding)
-  const float* sb = s_hat + lay.base(s, h);
-  constexpr int kPer = (kMaxGroup * (kFastK + 2) + 255) / 256;
+  const float* sbase = s_hat + lay.base(s, h);
+  constexpr int kPer = (kMaxGroup * (kFastK + 2) + kChunkThreads - 1) / kChunkThreads;
   float val[kPer];
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int e = tid + 256 * u;
+    const int e = tid + kChunkThreads * u;
     const int g = e / k, t = e - g * k;
     const int id = e < G * k ? s_tab[t] : -1;
     const bool ok = id >= 0 && id < n_c;
-    const float v = sb[(long)(ok ? id : 0) * lay.page + (long)(ok ? g : 0) * lay.head];
-    val[u] = ok ? v : __int_as_float(0x7fc00000);
+    const float x = sbase[(long)(ok ? id : 0) * lay.page + (long)(ok ? g : 0) * lay.head];
+    val[u] = ok ? x : __int_as_float(0x7fc00000);
   }
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int e = tid + 256 * u;
+    const int e = tid + kChunkThreads * u;
     if (e < G * k) out_sel_lse[row0 * k + e] = val[u];
   }
 }
 
 }  // namespace
 
-static long fast_rows(const locks_cfg_t& c) {
+int select_fast_rows(const locks_cfg_t& c) {
   return (c.max_pages_per_seq + kFastChunk - 1) / kFastChunk;
 }
 
-int select_fast_merge_nk(const locks_cfg_t& c) {
-  const long n = fast_rows(c) * (page_budget(c) - 2);
-  return n <= 64L * 4 * 8 ? 8 : 32;
+// Survivors kept per chunk: the smallest power of two >= k - 2, or fewer so
+// that all chunks' survivors fit one merge (at least 8).
+int select_fast_width(const locks_cfg_t& c) {
+  const int K = page_budget(c) - 2;
+  const long rows = select_fast_rows(c);
+  int w = 8;
+  while (w < K && 2L * w * rows <= kUnionCap) w *= 2;
+  return w;
 }
 
 bool select_fast_path(const locks_cfg_t& c) {
   const int K = page_budget(c) - 2;
-  return K <= kFastK && fast_rows(c) * K <= 64L * 4 * 32;
+  return K <= kFastK && (long)select_fast_rows(c) * select_fast_width(c) <= kUnionCap;
 }
 
-hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
-                                SHatLayout lay, const float2* partials, const SelectBufs& sb,
-                                hipStream_t st) {
+hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* page_table,
+                                const int32_t* seq_lens, const float* s_hat, SHatLayout lay,
+                                const float2* partials, const SelectBufs& sb, hipStream_t st) {
   const int k = page_budget(c);
   const int G = c.num_q_heads / c.num_kv_heads;
   const bool contiguous = lay.head == 1 && lay.page == G;
@@ -555,24 +583,25 @@ hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* seq_lens, c
   if (contiguous && G == 16) kern = select_chunk_keys_kernel<16>;
   if (contiguous && G == 8) kern = select_chunk_keys_kernel<8>;
   if (contiguous && G == 4) kern = select_chunk_keys_kernel<4>;
-  const int rows = (int)fast_rows(c);
-  hipLaunchKernelGGL(kern, dim3(rows, c.num_kv_heads, c.num_seqs), dim3(64 * kChunkWaves), 0, st,
-                     c.num_q_heads, c.num_kv_heads, k, seq_lens, s_hat, lay, partials,
-                     scan_blocks(c), sb.cand_key, sb.cand_idx, sb.thr, rows);
+  const int rows = select_fast_rows(c);
+  hipLaunchKernelGGL(kern, dim3(rows, c.num_kv_heads, c.num_seqs), dim3(kChunkThreads), 0, st,
+                     c.num_q_heads, c.num_kv_heads, k, select_fast_width(c), c.max_pages_per_seq,
+                     seq_lens, page_table, s_hat, lay, partials, scan_blocks(c), sb, rows);
   return hipGetLastError();
 }
 
-hipError_t launch_select(const locks_cfg_t& c, const int32_t* seq_lens, const float* s_hat,
-                         SHatLayout lay, const float2* partials, const SelectBufs& sb,
-                         int32_t* out_page_ids, float* out_sel_lse, hipStream_t st) {
+hipError_t launch_select(const locks_cfg_t& c, const int32_t* page_table, const int32_t* seq_lens,
+                         const float* s_hat, SHatLayout lay, const float2* partials,
+                         const SelectBufs& sb, int32_t* out_page_ids, float* out_sel_lse,
+                         hipStream_t st) {
   const int k = page_budget(c);
   if (select_fast_path(c)) {
-    hipError_t e = launch_select_chunks(c, seq_lens, s_hat, lay, partials, sb, st);
+    hipError_t e = launch_select_chunks(c, page_table, seq_lens, s_hat, lay, partials, sb, st);
     if (e != hipSuccess) return e;
-    auto* kern = select_fast_merge_nk(c) == 8 ? select_merge_fast_kernel<8> : select_merge_fast_kernel<32>;
-    hipLaunchKernelGGL(kern, dim3(c.num_kv_heads, c.num_seqs), dim3(256), 0, st, c.num_q_heads,
-                       c.num_kv_heads, k, (int)fast_rows(c), seq_lens, s_hat, lay, sb.cand_key,
-                       sb.cand_idx, sb.thr, out_page_ids, out_sel_lse);
+    hipLaunchKernelGGL(select_merge_fast_kernel, dim3(c.num_kv_heads, c.num_seqs),
+                       dim3(kChunkThreads), 0, st, c.num_q_heads, c.num_kv_heads, k,
+                       select_fast_width(c), select_fast_rows(c), c.max_pages_per_seq, seq_lens,
+                       page_table, s_hat, lay, sb, out_page_ids, out_sel_lse);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(select_chunk_kernel, dim3(sb.n_chunks, c.num_kv_heads, c.num_seqs),

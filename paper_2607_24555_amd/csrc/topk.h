@@ -297,101 +297,188 @@ __device__ __forceinline__ WaveCut block_hist_cut(const uint32_t (&key)[NK], int
   return H.cut;
 }
 
-// Survivors compacted in position order for a cheap final cut.
-constexpr int kCompactNK = 2;  // keys per lane after compaction (512 per 4-wave block)
-
+// Block-wide sum and exclusive scan of per-thread ints through double-buffered
+// per-wave slots (par alternates between consecutive calls).
 template <int NW>
-struct MergeLds {
-  CutLds<NW> L;
-  HistLds<NW> H;
-  uint32_t lo;
-  int wcnt[NW];
-  uint32_t ck[64 * NW * kCompactNK];
-  int32_t ci[64 * NW * kCompactNK];
+struct BlockLds {
+  int v[2][NW];
+  uint32_t mx[NW];
 };
 
-// Page table of one (sequence, KV head) from its chunk survivors: s_tab[0] = 0
-// (sink), s_tab[1 .. k-2] = the k - 2 best candidates ascending, s_tab[k-1] = n-1
-// (recent); with n <= k every page, then -1.  ck / ci hold `used` rows of K
-// survivors (page order inside a row, rows in page order); thr[c] is a lower
-// bound of the sequence-wide cut.  Survivors at or above the best lower bound
-// are compacted (in order) and cut there; if more than 64 * NW * kCompactNK
-// remain, the cut runs over all of them in registers.  Called by every thread
-// of an NW-wave block; requires used * K <= 64 * NW * NK; ends with a barrier.
+template <int NW>
+__device__ __forceinline__ int block_total(int v, BlockLds<NW>& B, int par) {
+  const int w = wave_sum_i(v);
+  if ((threadIdx.x & 63) == 0) B.v[par][threadIdx.x >> 6] = w;
+  __syncthreads();
+  int t = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) t += B.v[par][i];
+  return t;
+}
+
+template <int NW>
+__device__ __forceinline__ int block_excl(int v, BlockLds<NW>& B, int par) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int incl = wave_incl_scan(v);
+  if (lane == 63) B.v[par][wave] = incl;
+  __syncthreads();
+  int before = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) before += i < wave ? B.v[par][i] : 0;
+  return before + incl - v;
+}
+
+// Exact top K of keys[0 .. N) in global memory (0 = no candidate), ties to the
+// lower position; the kept positions go to out[0 .. K) in ascending order.
+// lo_hint must not exceed the K-th largest key.  Each thread owns a contiguous
+// run of keys and re-reads it in every bisection step, so this is the slow,
+// general path.  Called by every thread; ends with a barrier.
+template <int NW>
+__device__ void exact_cut_global(const uint32_t* __restrict__ keys, int N, int K,
+                                 uint32_t lo_hint, int32_t* out, BlockLds<NW>& B) {
+  constexpr int kT = 64 * NW;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int P = (N + kT - 1) / kT;
+  const int e0 = min(N, tid * P), e1 = min(N, e0 + P);
+  uint32_t kmx = 0u;
+  int nz = 0;
+  for (int e = e0; e < e1; ++e) {
+    const uint32_t v = keys[e];
+    kmx = max(kmx, v);
+    nz += v != 0u;
+  }
+  kmx = wave_max_u(kmx);
+  if (lane == 0) B.mx[wave] = kmx;
+  int par = 0;
+  const int total = block_total<NW>(nz, B, par);
+  par ^= 1;
+  uint32_t hi = 0u;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) hi = max(hi, B.mx[w]);
+  uint32_t T = 1u;
+  int take_eq = 1 << 30;
+  if (total > K) {
+    uint32_t lo = max(lo_hint, 1u);  // invariant: count(key >= lo) >= K
+    while (lo < hi) {
+      const uint32_t mid = lo + (uint32_t)((((uint64_t)hi - lo) + 1) >> 1);
+      int c = 0;
+      for (int e = e0; e < e1; ++e) c += keys[e] >= mid;
+      if (block_total<NW>(c, B, par) >= K) lo = mid; else hi = mid - 1;
+      par ^= 1;
+    }
+    T = lo;
+    int c = 0;
+    for (int e = e0; e < e1; ++e) c += keys[e] > T;
+    take_eq = K - block_total<NW>(c, B, par);
+    par ^= 1;
+  }
+  int eq = 0;
+  for (int e = e0; e < e1; ++e) {
+    const uint32_t v = keys[e];
+    eq += v != 0u && v == T;
+  }
+  const int eq_before = block_excl<NW>(eq, B, par);
+  par ^= 1;
+  int kept = 0;
+  {
+    int r = eq_before;
+    for (int e = e0; e < e1; ++e) {
+      const uint32_t v = keys[e];
+      const bool is_eq = v != 0u && v == T;
+      kept += (v != 0u && v > T) || (is_eq && r < take_eq);
+      r += is_eq;
+    }
+  }
+  int pos = block_excl<NW>(kept, B, par);
+  {
+    int r = eq_before;
+    for (int e = e0; e < e1; ++e) {
+      const uint32_t v = keys[e];
+      const bool is_eq = v != 0u && v == T;
+      if ((v != 0u && v > T) || (is_eq && r < take_eq)) out[pos++] = e;
+      r += is_eq;
+    }
+  }
+  __syncthreads();
+}
+
+template <int NW>
+struct UnionLds {
+  CutLds<NW> L;
+  HistLds<NW> H;
+  BlockLds<NW> B;
+  int fallback;
+};
+
+// Page table of one (sequence, KV head) with n pages and budget k:
+// s_tab[0] = 0 (sink), s_tab[1 .. k-2] = the k - 2 candidates of largest key in
+// ascending page order, s_tab[k-1] = n - 1 (recent); with n <= k every page,
+// then -1.  s_blk[t] is the physical block of entry t (-1 for padding).
+// Inputs: `used` rows of `width` chunk survivors (key, page, block; page order
+// inside a row, rows in page order, key 0 = empty slot); sat[c] = the key at
+// which chunk c was truncated (0 if it kept every candidate); keys = every
+// page's key for pages 0 .. n - 2 (0 for the sink).  The cut over the
+// survivors is exact unless some chunk was
+// truncated at or above it; then the whole sequence is cut again from keys.
+// Requires used * width <= 64 * NW * NK and used <= 256.  Called by every
+// thread of an NW-wave block; ends with a barrier.
 template <int NK, int NW>
-__device__ __forceinline__ void merge_table(int k, int n, int used, const uint32_t* __restrict__ ck,
-                                            const int32_t* __restrict__ ci,
-                                            const uint32_t* __restrict__ thr, int32_t* s_tab,
-                                            MergeLds<NW>& M) {
+__device__ void union_table(int k, int n, int used, int width, const uint32_t* __restrict__ ck,
+                            const int32_t* __restrict__ ci, const int32_t* __restrict__ cb,
+                            const uint32_t* __restrict__ sat, const uint32_t* __restrict__ keys,
+                            const int32_t* __restrict__ pt_row, int32_t* s_tab, int32_t* s_blk,
+                            UnionLds<NW>& U) {
+  constexpr int kT = 64 * NW;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int K = k - 2;
   if (n <= k) {
-    for (int t = tid; t < k; t += 64 * NW) s_tab[t] = t < n ? t : -1;
-  } else {
-    if (K > 0) {
-      const int N = used * K;
-      const int e0 = wave * (64 * NK) + lane;
-      uint32_t key[NK];
-      int32_t idx[NK];
-#pragma unroll
-      for (int u = 0; u < NK; ++u) {
-        const int e = min(e0 + u * 64, N - 1);
-        key[u] = ck[e];
-        idx[u] = ci[e];
-      }
-      if (wave == 0) {
-        uint32_t lo = 1u;
-        for (int c = lane; c < used; c += 64) lo = max(lo, thr[c]);
-        lo = wave_max_u(lo);
-        if (lane == 0) M.lo = lo;
-      }
-#pragma unroll
-      for (int u = 0; u < NK; ++u) pin(key[u]);
-      __syncthreads();
-      // keys below the best chunk cut cannot reach the sequence-wide top K
-      const uint32_t lo = M.lo;
-#pragma unroll
-      for (int u = 0; u < NK; ++u) key[u] = (e0 + u * 64 < N && key[u] >= lo) ? key[u] : 0u;
-      const int live = wave_count_ge(key, 1u);
-      if (lane == 0) M.wcnt[wave] = live;
-      __syncthreads();
-      int off = 0, total = 0;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        off += w < wave ? M.wcnt[w] : 0;
-        total += M.wcnt[w];
-      }
-      constexpr int kCap = 64 * NW * kCompactNK;
-      if (total <= kCap) {
-        const uint64_t lt = lanes_below();
-#pragma unroll
-        for (int u = 0; u < NK; ++u) {
-          const uint64_t m = __ballot(key[u] != 0u);
-          if (key[u]) {
-            const int slot = off + __popcll(m & lt);
-            M.ck[slot] = key[u];
-            M.ci[slot] = idx[u];
-          }
-          off += __popcll(m);
-        }
-        __syncthreads();
-        uint32_t k2[kCompactNK];
-        int e2[kCompactNK];
-#pragma unroll
-        for (int u = 0; u < kCompactNK; ++u) {
-          e2[u] = (wave * kCompactNK + u) * 64 + lane;
-          k2[u] = e2[u] < total ? M.ck[e2[u]] : 0u;
-        }
-        const WaveCut cut = block_hist_cut<kCompactNK, NW>(k2, K, M.H, M.L);
-        block_emit<kCompactNK, NW>(k2, cut, M.L, [&](int u, int slot) { s_tab[1 + slot] = M.ci[e2[u]]; });
-      } else {
-        const WaveCut cut = block_hist_cut<NK, NW>(key, K, M.H, M.L);
-        block_emit<NK, NW>(key, cut, M.L, [&](int u, int slot) { s_tab[1 + slot] = idx[u]; });
-      }
+    for (int t = tid; t < k; t += kT) {
+      s_tab[t] = t < n ? t : -1;
+      s_blk[t] = t < n ? pt_row[t] : -1;
     }
-    if (tid == 0) {
-      s_tab[0] = 0;
-      s_tab[k - 1] = n - 1;
+    __syncthreads();
+    return;
+  }
+  if (tid == 0) {
+    s_tab[0] = 0;
+    s_blk[0] = pt_row[0];
+    s_tab[k - 1] = n - 1;
+    s_blk[k - 1] = pt_row[n - 1];
+  }
+  if (K > 0) {
+    const int N = used * width;
+    uint32_t key[NK];
+    int32_t idx[NK], blk[NK];
+#pragma unroll
+    for (int u = 0; u < NK; ++u) {
+      const int e = (wave * NK + u) * 64 + lane;
+      const int ec = e < N ? e : N - 1;
+      key[u] = ck[ec];
+      idx[u] = ci[ec];
+      blk[u] = cb[ec];
+    }
+    uint32_t tr[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) tr[u] = sat[min(lane + 64 * u, used - 1)];
+#pragma unroll
+    for (int u = 0; u < NK; ++u) key[u] = (wave * NK + u) * 64 + lane < N ? key[u] : 0u;
+    const WaveCut cut = block_hist_cut<NK, NW>(key, K, U.H, U.L);
+    if (wave == 0) {
+      bool bad = false;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) bad |= lane + 64 * u < used && tr[u] != 0u && tr[u] >= cut.T;
+      const bool any = __ballot(bad) != 0ull;
+      if (lane == 0) U.fallback = any;
+    }
+    __syncthreads();
+    if (!U.fallback) {
+      block_emit<NK, NW>(key, cut, U.L, [&](int u, int slot) {
+        s_tab[1 + slot] = idx[u];
+        s_blk[1 + slot] = blk[u];
+      });
+    } else {
+      exact_cut_global<NW>(keys, n - 1, K, cut.T, s_tab + 1, U.B);  // pages 0 .. n - 2
+      for (int t = 1 + tid; t <= K; t += kT) s_blk[t] = pt_row[s_tab[t]];
     }
   }
   __syncthreads();

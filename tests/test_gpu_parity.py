@@ -282,6 +282,8 @@ def test_build_factors_reconstruct_like_oracle(case):
     (4, [16 * 700 + 7, 16 * 300, 5000, 16 * 257], 8, 4096, "bf16"),
     # more than 4096 pages per sequence: several wave-level selection chunks
     (2, [4096 * 16 * 2 + 37, 4096 * 16 + 80], 2, 256, "bf16"),
+    # 20,001 pages: each 1024-page chunk keeps fewer survivors than the table needs
+    (4, [16 * 20000 + 5], 8, 2048, "bf16"),
 ])
 def test_edge_batches(G, lens, rank, budget, kv):
     """Empty, sub-page, exact-page, tiny-budget and n <= k sequences in one batch."""
@@ -296,6 +298,35 @@ def test_edge_batches(G, lens, rank, budget, kv):
     ids2, sel2, out2, lse2 = B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws)
     torch.cuda.synchronize()
     assert torch.equal(ids, ids2) and torch.equal(out, out2)
+
+
+def test_clustered_top_pages_exact_recut():
+    """The best pages crowd into two selection chunks (far more of them than a
+    chunk keeps as survivors), so the table must come from the exact recut over
+    every page's key; it must still equal the oracle's."""
+    n = 20001
+    spec = WorkloadSpec("clustered", 1, 8, 2, [16 * (n - 1) + 3], 8, 2048, "bf16", "bf16")
+    w = build_workload(spec, 7)
+    G = 4
+    for h in range(2):
+        qhat = w.q[0, h * G:(h + 1) * G].float().mean(0)
+        qhat = qhat / qhat.norm()
+        blocks = w.page_table[0, 3000:3200].long()
+        w.k_cache[blocks, h] = (w.k_cache[blocks, h].float() + 3.0 * qhat).to(w.k_cache.dtype)
+    print("[clustered] pages 3000..3199 raised", flush=True)
+    d = Dev(w)
+    cfg = d.cfg
+    store, recs = d.oracle_summaries()
+    ids, sel, out, lse = B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws)
+    torch.cuda.synchronize()
+    for h in range(2):
+        _, _, _, ref = _oracle_unit(d, recs, 0, h)
+        inside = sum(3000 <= j < 3200 for j in ref["ids"])
+        assert inside > 64, inside  # more than any chunk's survivor row holds
+    _check_step_against_oracle("clustered", d, recs, ids, out, lse, min_same_frac=1.0)
+    ids2, sel2 = B.select(cfg, d.q, store, d.pt, d.sl, d.ws)
+    torch.cuda.synchronize()
+    assert torch.equal(ids2, ids)
 
 
 @pytest.mark.parametrize("n,budget,rank", [(5001, 1024, 4), (16389, 2048, 2)])
