@@ -30,7 +30,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--copies", type=int, default=3)
-    ap.add_argument("--workload", choices=["1m", "128k", "128k-r2", "32k"], default="1m")
+    ap.add_argument("--workload", choices=["1m", "128k", "128k-r2", "32k", "reasoning"],
+                    default="1m")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-build", action="store_true")
@@ -53,6 +54,9 @@ WORKLOADS = {
                                 "d 128, page 16, r 2, b 2048, bf16 KV"),
     "32k": (1, {}, "llama3.1-8b-32k: 1 seq x 32,768 tokens, 32 q / 8 kv heads, d 128, page 16, "
                    "r 8, b 2048, bf16 KV"),
+    "reasoning": (4, {}, "qwen3-4b-reasoning: 64 seq x U[8K,64K] tokens, 32 q / 8 kv heads, d 128, "
+                         "page 16, r 2, b 256, bf16 KV; each step appends one token per sequence "
+                         "and builds the pages that filled"),
 }
 
 
@@ -192,7 +196,8 @@ def main():
     t_gen = time.perf_counter() - t_gen
     cfg = B.config_for(w.spec, w.num_blocks, w.max_pages)
     q, pt, sl = w.q, w.page_table, w.seq_lens
-    R = max(1, args.copies)
+    growing = args.workload == "reasoning"
+    R = 1 if growing else max(1, args.copies)
     ks = [w.k_cache] + [w.k_cache.clone() for _ in range(R - 1)]
     vs = [w.v_cache] + [w.v_cache.clone() for _ in range(R - 1)]
     summ = [B.alloc_summaries(cfg, dev) for _ in range(R)]
@@ -204,10 +209,11 @@ def main():
     complete_heads = sum(L // 16 for L in w.spec.seq_lens) * cfg.num_kv_heads
     payload = B.summary_payload_bytes(cfg.rank)
     stride = B.summary_stride(cfg.rank)
-    k_sel = min(cfg.k, n_pages)
+    k_sel = min(cfg.k, max(math.ceil(L / 16) for L in w.spec.seq_lens))
     kv_page = 2 * 16 * 128 * 2
     alg_scan = complete_heads * payload
-    alg_attend = cfg.num_seqs * cfg.num_kv_heads * k_sel * kv_page
+    alg_attend = sum(min(cfg.k, math.ceil(L / 16)) for L in w.spec.seq_lens) * \
+        cfg.num_kv_heads * kv_page
     alg_step = alg_scan + alg_attend
 
     # ---- summary build (separately timed): every complete page, every copy
@@ -234,6 +240,46 @@ def main():
         B.decode_step(cfg, q, ks[i % R], vs[i % R], pt, sl, summ[i % R], ws, out_ids=ids,
                       out_sel_lse=sel, out=out, out_lse=lse)
 
+    n_built = 0
+    if growing:
+        # every step writes one new token per sequence into the paged cache (the
+        # caller's KV write), bumps seq_lens and builds the pages that just filled
+        T = args.warmup + args.steps
+        lens0 = torch.tensor(w.spec.seq_lens, dtype=torch.long)
+        gen = torch.Generator(device=dev).manual_seed(args.seed + 7)
+        new_k = torch.randn(T, cfg.num_seqs, cfg.num_kv_heads, 128, generator=gen, device=dev,
+                            dtype=torch.float32).to(ks[0].dtype)
+        new_v = torch.randn_like(new_k)
+        pos = lens0[None, :] + torch.arange(T)[:, None]            # [T][S] token index
+        if int((pos // 16).max()) >= cfg.max_pages_per_seq:
+            raise SystemExit(f"{T} appended tokens overrun the spare pages of the page table")
+        blk_at = pt.long().cpu().gather(1, (pos // 16).T).T         # [T][S] physical block
+        if int(blk_at.min()) < 0:
+            raise SystemExit(f"{T} appended tokens reach pages without a physical block")
+        rows = (pos % 16).to(dev)
+        blk_at = blk_at.to(dev)
+        lists = []
+        for t in range(T):
+            full = ((pos[t] + 1) % 16 == 0).nonzero().flatten()
+            lists.append(torch.stack([full, pos[t, full] // 16], 1).to(torch.int32).to(dev)
+                         if len(full) else None)
+        n_built = sum(0 if x is None else len(x) for x in lists[args.warmup:])
+        heads = torch.arange(cfg.num_kv_heads, device=dev)
+
+        calls = [0]  # appended tokens so far: warm-up and timed steps continue one sequence
+
+        def step(_i):
+            i = calls[0]
+            calls[0] += 1
+            b, r = blk_at[i][:, None], rows[i][:, None]
+            ks[0][b, heads[None, :], r] = new_k[i]
+            vs[0][b, heads[None, :], r] = new_v[i]
+            sl.add_(1)
+            B.decode_step(cfg, q, ks[0], vs[0], pt, sl, summ[0], ws, build_list=lists[i],
+                          out_ids=ids, out_sel_lse=sel, out=out, out_lse=lse)
+
+    if growing and args.graph:
+        raise SystemExit("--graph replays fixed launches; the reasoning workload grows every step")
     run = as_graphs(step, R) if args.graph else step
     for i in range(args.warmup):
         run(i)
@@ -280,7 +326,9 @@ def main():
                  "frac_of_peak": round(alg_step / (step_wall_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
                  "event_us": round(step_ev_us, 2), "summary_stride_bytes": stride,
                  "launch": "hip-graph replay" if args.graph else "eager",
-                 "selected_pages_per_kv_head": k_sel},
+                 "selected_pages_per_kv_head": k_sel,
+                 "pages_built_inline": n_built if growing else None,
+                 "includes_kv_append": growing},
         "dense": None if dense_us is None else {
             "us": round(dense_us, 2), "bytes": n_pages * cfg.num_kv_heads * kv_page,
             "GBps": round(n_pages * cfg.num_kv_heads * kv_page / (dense_us * 1e-6) / 1e9, 1),

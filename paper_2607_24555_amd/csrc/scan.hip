@@ -324,10 +324,11 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 //
 // Differences from the generic kernel above:
 //  * stage 1 runs on 16x16x64 int8 MFMA.  A basis nibble becomes an int8 with
-//    three ops per eight codes; each query head is written as a 22-bit fixed-point
+//    three ops per eight codes; each query head is written as a 20-bit fixed-point
 //    integer (power-of-two scale per head) split into three signed 8-bit digits,
-//    one MFMA chain per digit.  The excess-8 bias of the codes is removed exactly
-//    by starting each integer accumulator at -8 * sum(digit).  Dot products of
+//    and one int32 accumulator takes the digits most significant first, shifted
+//    by 8 bits in between (Horner's rule).  The excess-8 bias of the codes is
+//    removed exactly by adding -8 * sum(digit) at each stage.  Dot products of
 //    codes and queries are therefore exact integers.
 //  * stage-1 rows are assigned so that output register j of lane group grp holds
 //    slot 4j + grp = (page, basis column); those registers are directly the B
@@ -387,10 +388,11 @@ __device__ __forceinline__ void fast_issue(FastRegs<R>& T, const uint8_t* __rest
 __device__ __forceinline__ int sbyte(int x) { return (int)(int8_t)(x & 0xff); }
 
 // Query digits of head gcol for the int8 projection: q is scaled by a power of
-// two to a 22-bit fixed-point integer and split into three signed 8-bit digits
-// (most significant first).  Element e of MFMA half hh <-> d = 32 grp + 16 hh +
-// perm16[e], the order in which the decoders expand the packed codes.  bias[t]
-// = -8 * sum(digit t) removes the excess-8 offset of the int4 codes.
+// two to a 20-bit fixed-point integer Q (|Q| < 2^20) and split into three signed
+// 8-bit digits (most significant first).  Element e of MFMA half hh <-> d =
+// 32 grp + 16 hh + perm16[e], the order in which the decoders expand the packed
+// codes.  bias[t] = -8 * sum(digit t) removes the excess-8 offset of the int4
+// codes.
 struct QDigits {
   i4v bd[3][2];
   int bias[3];
@@ -412,8 +414,8 @@ __device__ __forceinline__ QDigits q_digits(const QT* __restrict__ qrow, int grp
   qmax = red4_max(qmax);
   int ex = 0;
   (void)frexpf(qmax, &ex);  // qmax < 2^ex
-  const float qscale = ldexpf(1.0f, 22 - ex);
-  D.inv_scale = ldexpf(1.0f, ex - 22) * c0;
+  const float qscale = ldexpf(1.0f, 20 - ex);
+  D.inv_scale = ldexpf(1.0f, ex - 20) * c0;
   float bsum[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh)
@@ -423,7 +425,9 @@ __device__ __forceinline__ QDigits q_digits(const QT* __restrict__ qrow, int grp
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb) {
         const int e = 4 * dw + bb;
-        const int Q = (qmax > 0.0f) ? (int)rintf(qf[16 * hh + kPerm16[e]] * qscale) : 0;
+        const int Q = (qmax > 0.0f)
+                          ? min(max((int)rintf(qf[16 * hh + kPerm16[e]] * qscale), -0xFFFFF), 0xFFFFF)
+                          : 0;
         const int d2 = sbyte(Q);
         const int q1 = (Q - d2) >> 8;
         const int d1 = sbyte(q1);
@@ -442,6 +446,37 @@ __device__ __forceinline__ QDigits q_digits(const QT* __restrict__ qrow, int grp
 #pragma unroll
   for (int t = 0; t < 3; ++t) D.bias[t] = -8 * (int)red4_sum(bsum[t]);
   return D;
+}
+
+// A 16-byte basis slice (32 excess-8 nibbles) as the int8 A operands of the two
+// K halves.
+__device__ __forceinline__ void nib_operands(const uint4& v, i4v (&a)[2]) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
+    a[hh] = i4v{(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu), (int)(x1 & 0x0F0F0F0Fu),
+                (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+  }
+}
+
+// Exact integer projection sum_d (n_d - 8) Q_d of excess-8 nibble codes n_d onto
+// a 20-bit query Q = 2^16 D0 + 2^8 D1 + D2, by Horner's rule over the digits in
+// one int32 accumulator: acc = 256 (256 (D0 . n') + D1 . n') + D2 . n'.  Every
+// partial value is bounded by |acc| <= 128 * 8 * 2^20 = 2^30, so nothing wraps.
+__device__ __forceinline__ i4v proj_horner(const i4v (&a)[2], const QDigits& QD) {
+  i4v acc = i4v{QD.bias[0], QD.bias[0], QD.bias[0], QD.bias[0]};
+  acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[0], QD.bd[0][0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[1], QD.bd[0][1], acc, 0, 0, 0);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = (int)(((uint32_t)acc[j] << 8) + (uint32_t)QD.bias[1]);
+  acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[0], QD.bd[1][0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[1], QD.bd[1][1], acc, 0, 0, 0);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = (int)(((uint32_t)acc[j] << 8) + (uint32_t)QD.bias[2]);
+  acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[0], QD.bd[2][0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[1], QD.bd[2][1], acc, 0, 0, 0);
+  return acc;
 }
 
 template <typename QT, int R, int NPACK>
@@ -475,7 +510,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const QDigits QD = q_digits(q + (row0 + gcol) * kDim, grp);
     const float inv_scale = QD.inv_scale;
     const i4v(&bd)[3][2] = QD.bd;
-    const int(&bias)[3] = QD.bias;
 
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -494,26 +528,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
         for (int st = 0; st < Gm::kSets; ++st) {
           if (st % 4 == 0) __builtin_amdgcn_sched_barrier(0);
-          const uint32_t w[4] = {cur.vb[st].x, cur.vb[st].y, cur.vb[st].z, cur.vb[st].w};
-          i4v acc[3];
-#pragma unroll
-          for (int d = 0; d < 3; ++d) acc[d] = i4v{bias[d], bias[d], bias[d], bias[d]};
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
-            const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
-                           (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
-#pragma unroll
-            for (int d = 0; d < 3; ++d)
-              acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bd[d][hh], acc[d], 0, 0, 0);
-          }
+          i4v a[2];
+          nib_operands(cur.vb[st], a);
+          const i4v acc = proj_horner(a, QD);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int slot = 4 * j + grp;
             const int page = st * Gm::kPPS + slot / R, l = slot % R;
             const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
-            const float v = fmaf((float)acc[0][j], 65536.0f, fmaf((float)acc[1][j], 256.0f, (float)acc[2][j]));
-            vals[4 * st + j] = v * (vs * inv_scale);
+            vals[4 * st + j] = (float)acc[j] * (vs * inv_scale);
           }
         }
         // the record registers are consumed: fetch the next 16 pages into them while
@@ -780,26 +803,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
           const int st = 2 * Q + i;
-          const uint32_t w[4] = {vb[st].x, vb[st].y, vb[st].z, vb[st].w};
-          i4v acc[3];
-#pragma unroll
-          for (int d = 0; d < 3; ++d) acc[d] = i4v{QD.bias[d], QD.bias[d], QD.bias[d], QD.bias[d]};
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
-            const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
-                           (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
-#pragma unroll
-            for (int d = 0; d < 3; ++d)
-              acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
-          }
+          i4v a[2];
+          nib_operands(vb[st], a);
+          const i4v acc = proj_horner(a, QD);
           if (more) vb[st] = load_basis<R>(summ, blk_n1, st, H_kv, h, lane);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
             const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
-            const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
-            vals[4 * i + j] = v * (vs * QD.inv_scale);
+            vals[4 * i + j] = (float)acc[j] * (vs * QD.inv_scale);
           }
         }
         // ---- stage 2 for the quad, then the page LSE in registers
@@ -1057,33 +1069,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           __builtin_amdgcn_sched_barrier(0);
           // ---- stage 1: vals[4 i + j] = p(page 4 Q + grp, l = 4 i + j, head g), zero off-diagonal
           float vals[8];
-          i4v acc1[2][3];
+          i4v acc1[2];
 #pragma unroll
           for (int i = 0; i < 2; ++i) {
-            const uint32_t w[4] = {vb[Q][i].x, vb[Q][i].y, vb[Q][i].z, vb[Q][i].w};
-#pragma unroll
-            for (int d = 0; d < 3; ++d) acc1[i][d] = i4v{QD.bias[d], QD.bias[d], QD.bias[d], QD.bias[d]};
-#pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
-              const uint32_t x0 = w[2 * hh], x1 = w[2 * hh + 1];
-              const i4v a = {(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
-                             (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
-#pragma unroll
-              for (int d = 0; d < 3; ++d)
-                acc1[i][d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc1[i][d], 0, 0, 0);
-            }
+            i4v a[2];
+            nib_operands(vb[Q][i], a);
+            acc1[i] = proj_horner(a, QD);
             if (pf) ld_vb(on, Q, i);
           }
           {
             const uint32_t vsw[4] = {vs[Q].x, vs[Q].y, vs[Q].z, vs[Q].w};
 #pragma unroll
             for (int l = 0; l < 8; ++l) {
-              const i4v* a3 = acc1[l >> 2];
               const int j = l & 3;
               const h2 pr = as_h2(vsw[l >> 1]);
               const float vsc = (float)((l & 1) ? pr.y : pr.x);
-              const float v = fmaf((float)a3[0][j], 65536.0f, (float)(a3[1][j] * 256 + a3[2][j]));
-              vals[l] = v * (vsc * inv_m);
+              vals[l] = (float)acc1[l >> 2][j] * (vsc * inv_m);
             }
             if (pf) ld_vs(on, Q);
           }

@@ -12,7 +12,7 @@ from oracle import locks_oracle as O
 from paper_2607_24555_amd import locks as B
 from tests._gpu_common import (GAP_TOL, LSE_TOL, OUT_TOL, OVERLAP_TOL, Dev, ids_of, rel_l2,
                                selection_agreement)
-from workloads import WorkloadSpec, build_workload, make_workload
+from workloads import WorkloadSpec, build_workload, config_spec, make_workload
 
 pytestmark = pytest.mark.gpu
 
@@ -327,6 +327,79 @@ def test_clustered_top_pages_exact_recut():
     ids2, sel2 = B.select(cfg, d.q, store, d.pt, d.sl, d.ws)
     torch.cuda.synchronize()
     assert torch.equal(ids2, ids)
+
+
+def test_reasoning_steps_build_filled_pages_inline():
+    """The reasoning workload's step loop (32 q / 8 kv heads, r = 2, b = 256): every
+    step writes one new token per sequence into the paged cache, bumps seq_lens
+    and lists the pages that just filled as the step's build list.  After the loop
+    the incrementally built summary store equals a fresh build of every complete
+    page bit for bit, and the last step agrees with the oracle run from scratch
+    on the final keys (GPU-built summaries: tables by the overlap rule)."""
+    spec = config_spec(4, num_seqs=4, seed=2)
+    # one sequence fills a page on the first append, one on the fifth, one sits
+    # exactly on a page boundary, one is arbitrary
+    spec.seq_lens = [16 * 600 - 1, 16 * 800 - 5, 16 * 512, spec.seq_lens[3]]
+    w = build_workload(spec, 2)
+    d = Dev(w)
+    cfg = d.cfg
+    print(f"[reasoning] lens {spec.seq_lens} r={cfg.rank} b={cfg.budget_tokens}", flush=True)
+    store = B.alloc_summaries(cfg, d.device)
+    B.build_summaries(cfg, d.k, d.pt, d.sl, store)
+    gen = torch.Generator().manual_seed(11)
+    lens = list(spec.seq_lens)
+    built = 0
+    ids = out = lse = None
+    for step in range(20):
+        pairs = []
+        for s in range(cfg.num_seqs):
+            j, r = divmod(lens[s], 16)
+            blk = int(w.page_table[s, j])
+            assert blk >= 0
+            # the new token: an earlier key of the sequence plus noise; value N(0, 1)
+            kn = (w.k_cache[int(w.page_table[s, j - 1]), :, r].float()
+                  + 0.3 * torch.randn(cfg.num_kv_heads, 128, generator=gen)).to(w.k_cache.dtype)
+            vn = torch.randn(cfg.num_kv_heads, 128, generator=gen).to(w.v_cache.dtype)
+            w.k_cache[blk, :, r] = kn
+            w.v_cache[blk, :, r] = vn
+            d.k[blk, :, r] = kn.to(d.device)
+            d.v[blk, :, r] = vn.to(d.device)
+            lens[s] += 1
+            if lens[s] % 16 == 0:
+                pairs.append((s, j))
+        d.sl.copy_(torch.tensor(lens, dtype=torch.int32))
+        bl = torch.tensor(pairs, dtype=torch.int32, device=d.device) if pairs else None
+        built += len(pairs)
+        ids, sel, out, lse = B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws,
+                                           build_list=bl)
+    torch.cuda.synchronize()
+    assert built >= 4, built
+    spec.seq_lens = lens
+    w.seq_lens = torch.tensor(lens, dtype=torch.int32)
+    fresh = B.alloc_summaries(cfg, d.device)
+    B.build_summaries(cfg, d.k, d.pt, d.sl, fresh)
+    torch.cuda.synchronize()
+    for s in range(cfg.num_seqs):
+        blocks = w.page_table[s, :lens[s] // 16].long().to(d.device)
+        assert torch.equal(store[blocks], fresh[blocks]), s
+    pairs, inter, tot = [], 0, 0
+    G = cfg.group
+    for s in range(cfg.num_seqs):
+        for h in range(cfg.num_kv_heads):
+            k, v, qg = d.unit(s, h)
+            ref = O.decode_step(qg, k, v, O.unit_summaries(k, cfg.rank), cfg.rank,
+                                cfg.budget_tokens)
+            got = ids_of(ids[s, h].tolist())
+            inter += len(set(got) & set(ref["ids"]))
+            tot += len(ref["ids"])
+            if got == ref["ids"]:
+                o = out[s, h * G:(h + 1) * G].double().cpu().numpy()
+                for g in range(G):
+                    assert rel_l2(o[g], ref["out"][g]) <= OUT_TOL
+                np.testing.assert_allclose(lse[s, h * G:(h + 1) * G].double().cpu().numpy(),
+                                           ref["lse"], atol=LSE_TOL)
+    print(f"[reasoning] {built} pages built inline; final table overlap {inter / tot:.4f}")
+    assert inter / tot >= OVERLAP_TOL
 
 
 @pytest.mark.parametrize("n,budget,rank", [(5001, 1024, 4), (16389, 2048, 2)])

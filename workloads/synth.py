@@ -81,7 +81,7 @@ def config_spec(cfg_id: int, *, rank: Optional[int] = None, seed: int = 0,
         lo, hi = 8192, 65536
         lens = torch.randint(lo, hi + 1, (n,), generator=g).tolist()
         s = WorkloadSpec("qwen3-4b-reasoning", n, 32, 8, lens, 2, 256, "bf16", "bf16",
-                         spare_pages_per_seq=4)
+                         spare_pages_per_seq=8)
     else:
         raise ValueError(f"unknown workload {cfg_id}")
     if num_seqs is not None and cfg_id != 4:
