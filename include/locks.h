@@ -54,7 +54,8 @@ enum {
   LOCKS_OK = 0,
   LOCKS_E_INVAL = -1,        /* bad configuration value or null pointer          */
   LOCKS_E_UNSUPPORTED = -2,  /* head_dim != 128, page_size != 16, G > 16,
-                                dtype unknown                                    */
+                                dtype unknown, or a summary store of 4 GiB or
+                                more (num_blocks * num_kv_heads * stride)        */
   LOCKS_E_WORKSPACE = -3,    /* ws null or smaller than locks_workspace_bytes    */
   LOCKS_E_HIP = -4           /* a HIP launch failed; see locks_last_hip_error    */
 };

@@ -23,6 +23,8 @@ int validate(const locks_cfg_t* c) {
   if (c->budget_tokens < 1 || (c->budget_tokens + kPage - 1) / kPage < 2) return LOCKS_E_INVAL;
   if (c->max_pages_per_seq < 1 || c->num_blocks < 1) return LOCKS_E_INVAL;
   if ((long)c->num_seqs * c->num_q_heads > 0x7fffffffL / kDim) return LOCKS_E_INVAL;
+  // record offsets are 32-bit: the summary store must stay below 4 GiB
+  if (summary_store_bytes(*c) > 0xffffffffull) return LOCKS_E_UNSUPPORTED;
   return LOCKS_OK;
 }
 

@@ -101,6 +101,11 @@ constexpr int kSparsePagesPerSplit = 4;   // one page per wave of a 4-wave block
 constexpr int kDensePagesPerSplit = 256;
 
 WsPlan plan_workspace(const locks_cfg_t& c);
+// Bytes of the summary store (every block's records); below 2^32 for a valid
+// configuration, so record offsets fit 32 bits.
+inline size_t summary_store_bytes(const locks_cfg_t& c) {
+  return (size_t)c.num_blocks * (size_t)c.num_kv_heads * (size_t)rec_stride(c.rank);
+}
 int page_budget(const locks_cfg_t& c);  // k = ceil(b / 16)
 int scan_pages_per_block(const locks_cfg_t& c);  // pages covered by one scan block
 inline int scan_blocks(const locks_cfg_t& c) {

@@ -338,6 +338,31 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 // ---------------------------------------------------------------------------
 
 typedef int i4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// The summary store as a raw buffer resource: 32-bit byte offsets, no 64-bit
+// address arithmetic per load, and loads past the store's end return zeros.
+constexpr int kBufWord3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t summ_rsrc(const uint8_t* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p), (short)0, (int)bytes, kBufWord3);
+}
+__device__ __forceinline__ uint4 bld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 bld8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ uint32_t bld4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+// Byte offset of the record of (physical block b, KV head h): b * (H_kv * stride)
+// + h * stride, with a 24-bit multiply (b < 2^24, the store is below 4 GiB).
+__device__ __forceinline__ uint32_t rec_off(int b, uint32_t blk_bytes, uint32_t head_off) {
+  return __umul24((uint32_t)b, blk_bytes) + head_off;
+}
 
 template <int R>
 struct FastGeom {
@@ -477,6 +502,29 @@ __device__ __forceinline__ i4v proj_horner(const i4v (&a)[2], const QDigits& QD)
   acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[0], QD.bd[2][0], acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[1], QD.bd[2][1], acc, 0, 0, 0);
   return acc;
+}
+
+// Two independent projections by the same Horner steps, interleaved so that the
+// matrix-core work of one covers the shifts of the other.
+__device__ __forceinline__ void proj_horner2(const i4v (&a0)[2], const i4v (&a1)[2],
+                                             const QDigits& QD, i4v& r0, i4v& r1) {
+  i4v x = i4v{QD.bias[0], QD.bias[0], QD.bias[0], QD.bias[0]};
+  i4v y = x;
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    x = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0[0], QD.bd[t][0], x, 0, 0, 0);
+    y = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1[0], QD.bd[t][0], y, 0, 0, 0);
+    x = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0[1], QD.bd[t][1], x, 0, 0, 0);
+    y = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1[1], QD.bd[t][1], y, 0, 0, 0);
+    if (t < 2) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] = (int)(((uint32_t)x[j] << 8) + (uint32_t)QD.bias[t + 1]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) y[j] = (int)(((uint32_t)y[j] << 8) + (uint32_t)QD.bias[t + 1]);
+    }
+  }
+  r0 = x;
+  r1 = y;
 }
 
 template <typename QT, int R, int NPACK>
@@ -634,54 +682,43 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
 }
 
-// ---------------------------------------------------------------------------
-// r = 8, G = 16: stage 2 with (page, token) rows.
-//
-// Stage 1 is the int8 projection above.  Stage 2 reconstructs the logits of
-// four pages at a time with one f16 MFMA 16x16x32 (B as hi + lo): rows m are
-// (page a = m / 4 of the quad, token 4 ps + m % 4), K index 8 kg + e is (page
-// e / 2 of the quad, basis column 4 (e % 2) + kg), so A is block diagonal and B
-// is exactly stage-1 registers vals[8 Q + e] of lane group kg.  After the four
-// passes of a quad each lane holds all 16 logits of (page 4 Q + grp, head col)
-// and takes the page LSE in registers.  The centroid MFMA reads its rows in the
-// order page 4 (row & 3) + (row >> 2), which leaves a(page 4 j + grp, head col)
-// in register j of the same lanes.  Coefficient rows are copied to LDS with
-// their bytes reordered to l = 0, 4, 1, 5, 2, 6, 3, 7, so that the two codes a
-// lane needs (l = grp, 4 + grp) are one 16-bit read.
-// ---------------------------------------------------------------------------
+// Byte offsets of what this lane loads from the records of the 16 pages whose
+// blocks lanes 0..15 hold in `blk`: its basis slice of each set and its record
+// tail chunks.  All the lane exchanges of a step are issued together.
+template <int R>
+struct StepOffs {
+  uint32_t vb[FastGeom<R>::kSets];
+  uint32_t tl[FastGeom<R>::kTailLoads];
+};
+
+template <int R>
+__device__ __forceinline__ StepOffs<R> step_offsets(int blk, uint32_t blk_bytes, uint32_t head_off,
+                                                    int lane) {
+  using Gm = FastGeom<R>;
+  const int col = lane & 15, grp = lane >> 4;
+  const int qs = 4 * (col & 3) + (col >> 2);
+  StepOffs<R> o;
+#pragma unroll
+  for (int st = 0; st < Gm::kSets; ++st) {
+    const int b = __shfl(blk, st * Gm::kPPS + qs / R, 64);
+    o.vb[st] = rec_off(b, blk_bytes, head_off) + 64u * (qs % R) + 16u * grp;
+  }
+#pragma unroll
+  for (int u = 0; u < Gm::kTailLoads; ++u) {
+    int c = lane + 64 * u;
+    c = c < 16 * Gm::kTailCh ? c : 16 * Gm::kTailCh - 1;
+    const int b = __shfl(blk, c / Gm::kTailCh, 64);
+    o.tl[u] = rec_off(b, blk_bytes, head_off) + 64u * R + (c % Gm::kTailCh) * 16;
+  }
+  return o;
+}
+
 // Physical block of page page0 + (lane & 15); lanes past the end of the
 // sequence take page0's block (a valid record that is loaded but not used).
 __device__ __forceinline__ int lane_block(const int32_t* __restrict__ pt_row, int page0, int n_c,
                                           int lane) {
   const int pl = page0 + (lane & 15);
   return pt_row[pl < n_c ? pl : page0];
-}
-
-// Basis set st of the 16 pages whose blocks lanes 0..15 hold in `blk`.
-template <int R>
-__device__ __forceinline__ uint4 load_basis(const uint8_t* __restrict__ summ, int blk, int st,
-                                            int H_kv, int h, int lane) {
-  using Gm = FastGeom<R>;
-  const int col = lane & 15, grp = lane >> 4;
-  const int qs = 4 * (col & 3) + (col >> 2);
-  const int b = __shfl(blk, st * Gm::kPPS + qs / R, 64);
-  const uint32_t off = (uint32_t)(b * H_kv + h) * (uint32_t)Gm::kStride + 64u * (qs % R) + 16u * grp;
-  return *reinterpret_cast<const uint4*>(summ + off);
-}
-
-template <int R>
-__device__ __forceinline__ void load_tail(uint4 (&tl)[FastGeom<R>::kTailLoads],
-                                          const uint8_t* __restrict__ summ, int blk, int H_kv,
-                                          int h, int lane) {
-  using Gm = FastGeom<R>;
-#pragma unroll
-  for (int u = 0; u < Gm::kTailLoads; ++u) {
-    int c = lane + 64 * u;
-    c = c < 16 * Gm::kTailCh ? c : 16 * Gm::kTailCh - 1;
-    const int b = __shfl(blk, c / Gm::kTailCh, 64);
-    const uint32_t off = (uint32_t)(b * H_kv + h) * (uint32_t)Gm::kStride + 64u * R + (c % Gm::kTailCh) * 16;
-    tl[u] = *reinterpret_cast<const uint4*>(summ + off);
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -698,15 +735,15 @@ __device__ __forceinline__ void load_tail(uint4 (&tl)[FastGeom<R>::kTailLoads],
 // in register j of the same lanes.  Coefficient rows are copied to LDS with
 // their bytes reordered to l = 0, 4, 1, 5, 2, 6, 3, 7, so that the two codes a
 // lane needs (l = grp, 4 + grp) are one 16-bit read.  Stage 1 runs per quad
-// (basis sets 2 Q, 2 Q + 1), and each consumed register set is refilled at once
-// with the next 16 pages' records.
+// (basis sets 2 Q, 2 Q + 1, their Horner steps interleaved), and each consumed
+// register set is refilled at once with the next 16 pages' records.
 // ---------------------------------------------------------------------------
 constexpr int kR8Steps = 4;  // 16-page steps per wave: a block covers 4 x 16 x kR8Steps pages
 
 template <typename QT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
-    const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
+    uint32_t summ_bytes, const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     float* __restrict__ s_hat, SHatLayout lay, float2* __restrict__ partials) {
   constexpr int R = 8;
   using Gm = FastGeom<R>;
@@ -725,13 +762,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   constexpr int kWavePages = 16 * kR8Steps;
   if (pg * kWavePages < n_c) {
+    const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
+    const uint32_t blk_bytes = (uint32_t)H_kv * (uint32_t)Gm::kStride, head_off = (uint32_t)h * Gm::kStride;
     uint4 vb[Gm::kSets];
     uint4 tl[Gm::kTailLoads];
     {
-      const int blk0 = lane_block(pt_row, pg * kWavePages, n_c, lane);
+      const StepOffs<R> o0 = step_offsets<R>(lane_block(pt_row, pg * kWavePages, n_c, lane),
+                                             blk_bytes, head_off, lane);
 #pragma unroll
-      for (int st = 0; st < Gm::kSets; ++st) vb[st] = load_basis<R>(summ, blk0, st, H_kv, h, lane);
-      load_tail<R>(tl, summ, blk0, H_kv, h, lane);
+      for (int st = 0; st < Gm::kSets; ++st) vb[st] = bld16(rs, o0.vb[st]);
+#pragma unroll
+      for (int u = 0; u < Gm::kTailLoads; ++u) tl[u] = bld16(rs, o0.tl[u]);
     }
     int blk_n1 = pg * kWavePages + 16 < n_c ? lane_block(pt_row, pg * kWavePages + 16, n_c, lane) : 0;
     const QDigits QD = q_digits(q + (row0 + col) * kDim, grp);
@@ -742,8 +783,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int t = 0; t < kR8Steps; ++t) {
       const int page0 = (pg * kR8Steps + t) * 16;
       if (page0 >= n_c) break;
-      const bool more = t + 1 < kR8Steps && page0 + 16 < n_c;
+      const bool more = __builtin_amdgcn_readfirstlane(t + 1 < kR8Steps && page0 + 16 < n_c);
       const int blk_n2 = (t + 2 < kR8Steps && page0 + 32 < n_c) ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
+      StepOffs<R> nx;
+      if (more) nx = step_offsets<R>(blk_n1, blk_bytes, head_off, lane);
       // ---- record tails to LDS; coefficient rows reordered to l = 0,4,1,5,2,6,3,7
 #pragma unroll
       for (int u = 0; u < Gm::kTailLoads; ++u) {
@@ -761,7 +804,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         }
       }
       __builtin_amdgcn_wave_barrier();
-      if (more) load_tail<R>(tl, summ, blk_n1, H_kv, h, lane);
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < Gm::kTailLoads; ++u) tl[u] = bld16(rs, nx.tl[u]);
+      }
 
       // ---- centroid term: areg[j] = a(page 4 j + grp, head col)
       float areg[4];
@@ -800,19 +846,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         // ---- stage 1 (int8 MFMA) for basis sets 2Q, 2Q+1:
         //      vals[4 i + j] = p(page 4 Q + 2 i + j / 2, l = 4 (j % 2) + grp)
         float vals[8];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const int st = 2 * Q + i;
-          i4v a[2];
-          nib_operands(vb[st], a);
-          const i4v acc = proj_horner(a, QD);
-          if (more) vb[st] = load_basis<R>(summ, blk_n1, st, H_kv, h, lane);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
-            const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
-            vals[4 * i + j] = (float)acc[j] * (vs * QD.inv_scale);
+        {
+          i4v a0[2], a1[2], acc[2];
+          nib_operands(vb[2 * Q], a0);
+          nib_operands(vb[2 * Q + 1], a1);
+          proj_horner2(a0, a1, QD, acc[0], acc[1]);
+          if (more) {
+            vb[2 * Q] = bld16(rs, nx.vb[2 * Q]);
+            vb[2 * Q + 1] = bld16(rs, nx.vb[2 * Q + 1]);
           }
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int st = 2 * Q + i;
+              const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
+              const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
+              vals[4 * i + j] = (float)acc[i][j] * (vs * QD.inv_scale);
+            }
         }
         // ---- stage 2 for the quad, then the page LSE in registers
         h8 bh, bl;
@@ -933,7 +984,7 @@ __device__ __forceinline__ int lane_block_clamped(const int32_t* __restrict__ pt
 template <typename QT, int kSteps>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8g4_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
-    const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
+    uint32_t summ_bytes, const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     float* __restrict__ s_hat, SHatLayout lay, float2* __restrict__ partials) {
   constexpr int R = 8, G = 4;
   constexpr uint32_t kStride = rec_stride(R);
@@ -964,11 +1015,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     struct Offs {
       uint32_t ra[4], rb[4], rm;
     };
+    const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
+    const uint32_t blk_bytes = (uint32_t)H_kv * kStride, head_off = (uint32_t)h * kStride;
     auto offsets = [&](int blk) {
       Offs o;
-      auto rec = [&](int page) {
-        return ((uint32_t)__shfl(blk, page, 64) * (uint32_t)H_kv + (uint32_t)h) * kStride;
-      };
+      auto rec = [&](int page) { return rec_off(__shfl(blk, page, 64), blk_bytes, head_off); };
 #pragma unroll
       for (int Q = 0; Q < 4; ++Q) {
         o.ra[Q] = rec(4 * Q + ca);
@@ -986,23 +1037,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     // loads of one step's registers; in a run the next step's are issued right
     // after the register's last use in the current one
     auto ld_vb = [&](const Offs& o, int Q, int i) {
-      vb[Q][i] = *reinterpret_cast<const uint4*>(summ + o.ra[Q] + 64u * (4 * i + g) + 16u * grp);
+      vb[Q][i] = bld16(rs, o.ra[Q] + 64u * (4 * i + g) + 16u * grp);
     };
-    auto ld_cf = [&](const Offs& o, int Q) {
-      cf[Q] = *reinterpret_cast<const uint2*>(summ + o.rb[Q] + kCoef + 8u * col);
-    };
-    auto ld_cs = [&](const Offs& o, int Q) {
-      cs[Q] = *reinterpret_cast<const uint2*>(summ + o.ra[Q] + kSc + 2u * (R + 4 * grp));
-    };
-    auto ld_vs = [&](const Offs& o, int Q) {
-      vs[Q] = *reinterpret_cast<const uint4*>(summ + o.rb[Q] + kSc);
-    };
-    auto ld_ms = [&](const Offs& o, int Q) {
-      msw[Q] = *reinterpret_cast<const uint32_t*>(summ + o.rb[Q] + kSc + 2u * (R + 16));
-    };
+    auto ld_cf = [&](const Offs& o, int Q) { cf[Q] = bld8(rs, o.rb[Q] + kCoef + 8u * col); };
+    auto ld_cs = [&](const Offs& o, int Q) { cs[Q] = bld8(rs, o.ra[Q] + kSc + 2u * (R + 4 * grp)); };
+    auto ld_vs = [&](const Offs& o, int Q) { vs[Q] = bld16(rs, o.rb[Q] + kSc); };
+    auto ld_ms = [&](const Offs& o, int Q) { msw[Q] = bld4(rs, o.rb[Q] + kSc + 2u * (R + 16)); };
     auto ld_mu = [&](const Offs& o) {
-      mu[0] = *reinterpret_cast<const uint4*>(summ + o.rm + kMu + 32u * grp);
-      mu[1] = *reinterpret_cast<const uint4*>(summ + o.rm + kMu + 32u * grp + 16u);
+      mu[0] = bld16(rs, o.rm + kMu + 32u * grp);
+      mu[1] = bld16(rs, o.rm + kMu + 32u * grp + 16u);
     };
 
     // kN consecutive 16-page steps from page `start`, fully unrolled so that
@@ -1070,12 +1113,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           // ---- stage 1: vals[4 i + j] = p(page 4 Q + grp, l = 4 i + j, head g), zero off-diagonal
           float vals[8];
           i4v acc1[2];
-#pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            i4v a[2];
-            nib_operands(vb[Q][i], a);
-            acc1[i] = proj_horner(a, QD);
-            if (pf) ld_vb(on, Q, i);
+          {
+            i4v a0[2], a1[2];
+            nib_operands(vb[Q][0], a0);
+            nib_operands(vb[Q][1], a1);
+            proj_horner2(a0, a1, QD, acc1[0], acc1[1]);
+            if (pf) {
+              ld_vb(on, Q, 0);
+              ld_vb(on, Q, 1);
+            }
           }
           {
             const uint32_t vsw[4] = {vs[Q].x, vs[Q].y, vs[Q].z, vs[Q].w};
@@ -1165,8 +1211,8 @@ constexpr int kG4Steps = 4;
 
 template <typename QT>
 hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H_kv, int max_pages,
-                         const QT* q, const uint8_t* sum, const int32_t* pt, const int32_t* sl,
-                         float* s_hat, SHatLayout lay, float2* part) {
+                         const QT* q, const uint8_t* sum, uint32_t summ_bytes, const int32_t* pt,
+                         const int32_t* sl, float* s_hat, SHatLayout lay, float2* part) {
 #define LOCKS_SCAN_FAST(RR, NP)                                                              \
   if (r == RR && G == 16 / NP) {                                                            \
     hipLaunchKernelGGL((scan_fast_kernel<QT, RR, NP>), grid, dim3(256), 0, st, H_q, H_kv,   \
@@ -1175,12 +1221,12 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
   }
   if (r == 8 && G == 16) {
     hipLaunchKernelGGL((scan_r8_kernel<QT>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
-                       sum, pt, sl, s_hat, lay, part);
+                       sum, summ_bytes, pt, sl, s_hat, lay, part);
     return hipGetLastError();
   }
   if (r == 8 && G == 4) {
     hipLaunchKernelGGL((scan_r8g4_kernel<QT, kG4Steps>), grid, dim3(256), 0, st, H_q, H_kv,
-                       max_pages, q, sum, pt, sl, s_hat, lay, part);
+                       max_pages, q, sum, summ_bytes, pt, sl, s_hat, lay, part);
     return hipGetLastError();
   }
   LOCKS_SCAN_FAST(8, 4) LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(4, 4)
@@ -1225,12 +1271,13 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
                        SHatLayout lay, float2* partials, hipStream_t st) {
   const dim3 grid(scan_blocks(c), c.num_kv_heads, c.num_seqs);
   const int G = c.num_q_heads / c.num_kv_heads;
+  const uint32_t bytes = (uint32_t)summary_store_bytes(c);
   if (c.q_dtype == LOCKS_BF16)
     return dispatch_scan(c.rank, G, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
                          static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(summaries),
-                         page_table, seq_lens, s_hat, lay, partials);
+                         bytes, page_table, seq_lens, s_hat, lay, partials);
   return dispatch_scan(c.rank, G, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                       static_cast<const float*>(q), static_cast<const uint8_t*>(summaries),
+                       static_cast<const float*>(q), static_cast<const uint8_t*>(summaries), bytes,
                        page_table, seq_lens, s_hat, lay, partials);
 }
 
