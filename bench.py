@@ -256,24 +256,25 @@ def main():
         blk_at = pt.long().cpu().gather(1, (pos // 16).T).T         # [T][S] physical block
         if int(blk_at.min()) < 0:
             raise SystemExit(f"{T} appended tokens reach pages without a physical block")
-        rows = (pos % 16).to(dev)
-        blk_at = blk_at.to(dev)
+        # flat row of (block, KV head, token slot) in the cache viewed as [rows][128]
+        hk = torch.arange(cfg.num_kv_heads)
+        flat = ((blk_at[:, :, None] * cfg.num_kv_heads + hk) * 16 + (pos % 16)[:, :, None])
+        flat = flat.reshape(T, -1).to(dev)
         lists = []
         for t in range(T):
             full = ((pos[t] + 1) % 16 == 0).nonzero().flatten()
             lists.append(torch.stack([full, pos[t, full] // 16], 1).to(torch.int32).to(dev)
                          if len(full) else None)
         n_built = sum(0 if x is None else len(x) for x in lists[args.warmup:])
-        heads = torch.arange(cfg.num_kv_heads, device=dev)
+        k_rows, v_rows = ks[0].view(-1, 128), vs[0].view(-1, 128)
 
         calls = [0]  # appended tokens so far: warm-up and timed steps continue one sequence
 
         def step(_i):
             i = calls[0]
             calls[0] += 1
-            b, r = blk_at[i][:, None], rows[i][:, None]
-            ks[0][b, heads[None, :], r] = new_k[i]
-            vs[0][b, heads[None, :], r] = new_v[i]
+            k_rows.index_copy_(0, flat[i], new_k[i].view(-1, 128))
+            v_rows.index_copy_(0, flat[i], new_v[i].view(-1, 128))
             sl.add_(1)
             B.decode_step(cfg, q, ks[0], vs[0], pt, sl, summ[0], ws, build_list=lists[i],
                           out_ids=ids, out_sel_lse=sel, out=out, out_lse=lse)

@@ -1207,6 +1207,221 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
 }
 
+// ---------------------------------------------------------------------------
+// Low rank (r in {2, 4}), G = 4: projections on the matrix cores, logits on the
+// vector ALU.
+//
+// A wave covers 16 pages per step.  Stage 1 (int8 MFMA, Horner over the query
+// digits) has rows (page, basis column) -- 16 / R pages per tile -- and the 4
+// heads repeated over the 16 columns; lanes of columns 0..3 scale their
+// projections and leave them in LDS, next to the centroid terms and the record
+// tails (coefficients and scales) of the step.  Stage 2 gives every lane one
+// (page, head) pair: z_i = a + s_i sum_l (c_il - 128) p_l for the 16 tokens in
+// fp32 (the excess-128 offset enters as one subtraction of 128 sum_l p_l), the
+// page LSE in registers, and a coalesced store of the page score.
+// ---------------------------------------------------------------------------
+constexpr int kLowSteps = 4;  // 16-page steps per wave: a block covers 256 pages
+
+template <typename QT, int R>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) void scan_low_kernel(
+    int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
+    uint32_t summ_bytes, const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
+    float* __restrict__ s_hat, SHatLayout lay, float2* __restrict__ partials) {
+  constexpr int G = 4;
+  constexpr int kPPT = 16 / R;                        // pages per stage-1 tile
+  constexpr uint32_t kStride = rec_stride(R);
+  constexpr int kTail = kStride - 64 * R;             // coefficients .. end of record
+  constexpr int kTailCh = kTail / 16;
+  constexpr int kTailLoads = (16 * kTailCh + 63) / 64;
+  constexpr int kMu = 16 * R, kSc = 16 * R + kDim;    // offsets inside the tail
+  __shared__ __align__(16) uint8_t sTail[4][16][kTail];
+  __shared__ __align__(16) float sP[4][16][G][R];
+  __shared__ float sA[4][16][G];
+  __shared__ float2 sRun[4][64];
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int h = blockIdx.y, s = blockIdx.z;
+  const int n_c = seq_lens[s] / kPage;
+  const int pg = blockIdx.x * 4 + wave;
+  const long row0 = (long)s * H_q + (long)h * G;
+  const int32_t* pt_row = page_table + (long)s * max_pages;
+  const int pp = lane >> 2, gg = lane & 3;            // stage 2: (page, head) of this lane
+  float run_m = -INFINITY, run_s = 0.0f;
+
+  constexpr int kWavePages = 16 * kLowSteps;
+  const int first = pg * kWavePages;
+  if (first < n_c) {
+    const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
+    const uint32_t blk_bytes = (uint32_t)H_kv * kStride, head_off = (uint32_t)h * kStride;
+    const QDigits QD = q_digits(q + (row0 + (col & 3)) * kDim, grp);
+    // this lane's loads of a step whose 16 pages' blocks lanes 0..15 hold in blk:
+    // basis slice of tile T (row col = (page T kPPT + col / R, column col % R)),
+    // and record-tail chunks
+    auto issue = [&](int blk, uint4 (&vb)[R], uint4 (&tl)[kTailLoads]) {
+#pragma unroll
+      for (int T = 0; T < R; ++T) {
+        const int b = __shfl(blk, T * kPPT + col / R, 64);
+        vb[T] = bld16(rs, rec_off(b, blk_bytes, head_off) + 64u * (col % R) + 16u * grp);
+      }
+#pragma unroll
+      for (int u = 0; u < kTailLoads; ++u) {
+        int c = lane + 64 * u;
+        c = c < 16 * kTailCh ? c : 16 * kTailCh - 1;
+        const int b = __shfl(blk, c / kTailCh, 64);
+        tl[u] = bld16(rs, rec_off(b, blk_bytes, head_off) + 64u * R + (c % kTailCh) * 16);
+      }
+    };
+    uint4 vb[R], tl[kTailLoads];
+    issue(lane_block_clamped(pt_row, first, n_c, lane), vb, tl);
+    const int n_steps = min(kLowSteps, (n_c - first + 15) / 16);
+    float* shat_base = s_hat + lay.base(s, h) + (long)gg * lay.head;
+
+#pragma unroll 1
+    for (int t = 0; t < n_steps; ++t) {
+      const int page0 = first + 16 * t;
+      const bool refill = __builtin_amdgcn_readfirstlane(t + 1 < n_steps);
+      const int blk_next = refill ? lane_block_clamped(pt_row, page0 + 16, n_c, lane) : 0;
+      // ---- record tails to LDS
+#pragma unroll
+      for (int u = 0; u < kTailLoads; ++u) {
+        const int c = lane + 64 * u;
+        if (c < 16 * kTailCh)
+          *reinterpret_cast<uint4*>(&sTail[wave][c / kTailCh][(c % kTailCh) * 16]) = tl[u];
+      }
+      __builtin_amdgcn_wave_barrier();
+      // ---- centroid term (one page per row; int8 codes: three digit chains)
+      {
+        const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][col][kMu + 32 * grp]);
+        const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][col][kMu + 32 * grp + 16]);
+        const uint32_t mw[8] = {m0.x ^ 0x80808080u, m0.y ^ 0x80808080u, m0.z ^ 0x80808080u,
+                                m0.w ^ 0x80808080u, m1.x ^ 0x80808080u, m1.y ^ 0x80808080u,
+                                m1.z ^ 0x80808080u, m1.w ^ 0x80808080u};
+        i4v acc[3];
+#pragma unroll
+        for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
+          const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
+                         (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
+                         (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
+                         (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
+#pragma unroll
+          for (int d = 0; d < 3; ++d)
+            acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
+        }
+        if (col < G) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int page = 4 * grp + j;
+            const float ms = lds_f16(&sTail[wave][page][kSc + 2 * (R + 16)]);
+            const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
+            sA[wave][page][col] = v * (ms * QD.inv_scale);
+          }
+        }
+      }
+      // ---- stage 1: projections of every (page, basis column) onto the 4 heads
+#pragma unroll
+      for (int T = 0; T < R; T += 2) {
+        i4v a0[2], a1[2], acc[2];
+        nib_operands(vb[T], a0);
+        nib_operands(vb[T + 1 < R ? T + 1 : T], a1);
+        proj_horner2(a0, a1, QD, acc[0], acc[1]);
+        if (col < G) {
+#pragma unroll
+          for (int i = 0; i < 2 && T + i < R; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int row = 4 * grp + j;
+              const int page = (T + i) * kPPT + row / R, l = row % R;
+              const float vs = lds_f16(&sTail[wave][page][kSc + 2 * l]);
+              sP[wave][page][col][l] = (float)acc[i][j] * (vs * QD.inv_scale);
+            }
+        }
+      }
+      if (refill) issue(blk_next, vb, tl);
+      __builtin_amdgcn_wave_barrier();
+      // ---- stage 2: the 16 logits of (page pp, head gg) and their LSE
+      {
+        float pv[R];
+        float psum = 0.0f;
+#pragma unroll
+        for (int l = 0; l < R; ++l) {
+          pv[l] = sP[wave][pp][gg][l];
+          psum += pv[l];
+        }
+        const float k128 = 128.0f * psum;
+        const float a = sA[wave][pp][gg];
+        uint32_t cw[4 * R];  // coefficient codes, row-major (16 rows x R bytes)
+#pragma unroll
+        for (int v = 0; v < R; ++v) {
+          const uint4 c4 = *reinterpret_cast<const uint4*>(&sTail[wave][pp][16 * v]);
+          cw[4 * v] = c4.x;
+          cw[4 * v + 1] = c4.y;
+          cw[4 * v + 2] = c4.z;
+          cw[4 * v + 3] = c4.w;
+        }
+        uint32_t sw[8];  // coefficient row scales (fp16 pairs)
+#pragma unroll
+        for (int v = 0; v < 8; ++v)
+          sw[v] = *reinterpret_cast<const uint32_t*>(&sTail[wave][pp][kSc + 2 * R + 4 * v]);
+        float e[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float tz = -k128;
+#pragma unroll
+          for (int l = 0; l < R; ++l) {
+            const int b = i * R + l;  // byte index of code (i, l)
+            const float c = (float)((cw[b >> 2] >> (8 * (b & 3))) & 0xffu);
+            tz = fmaf(c, pv[l], tz);
+          }
+          const h2 sc = as_h2(sw[i >> 1]);
+          e[i] = tz * (float)((i & 1) ? sc.y : sc.x);  // logit minus the centroid term
+        }
+        float sm = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(e[i]);
+        float shift = 0.0f;
+        if (!(sm > 0.0f && sm < INFINITY)) {
+          shift = e[0];
+#pragma unroll
+          for (int i = 1; i < 16; ++i) shift = fmaxf(shift, e[i]);
+          sm = 0.0f;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(e[i] - shift);
+        }
+        const float s2 = a + shift + __builtin_amdgcn_logf(sm);
+        const int page = page0 + pp;
+        const bool live = page < n_c;
+        if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
+        const float ex = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+        const bool up = s2 > run_m;
+        const float ns = up ? fmaf(run_s, ex, 1.0f) : run_s + ex;
+        run_s = live ? ns : run_s;
+        run_m = (live && up) ? s2 : run_m;
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  // ---- block partial (max, sum exp) per head over its pages, log2 domain
+  sRun[wave][lane] = make_float2(run_m, run_s);
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int g = threadIdx.x;
+    float m = -INFINITY, l = 0.0f;
+    for (int w = 0; w < 4; ++w)
+      for (int c = g; c < 64; c += G) m = fmaxf(m, sRun[w][c].x);
+    if (m > -INFINITY)
+      for (int w = 0; w < 4; ++w)
+        for (int c = g; c < 64; c += G) {
+          const float2 v = sRun[w][c];
+          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+        }
+    partials[(row0 + g) * gridDim.x + blockIdx.x] = make_float2(m, l);
+  }
+}
+
 constexpr int kG4Steps = 4;
 
 template <typename QT>
@@ -1222,6 +1437,15 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
   if (r == 8 && G == 16) {
     hipLaunchKernelGGL((scan_r8_kernel<QT>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
                        sum, summ_bytes, pt, sl, s_hat, lay, part);
+    return hipGetLastError();
+  }
+  if ((r == 2 || r == 4) && G == 4) {
+    if (r == 2)
+      hipLaunchKernelGGL((scan_low_kernel<QT, 2>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
+                         sum, summ_bytes, pt, sl, s_hat, lay, part);
+    else
+      hipLaunchKernelGGL((scan_low_kernel<QT, 4>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
+                         sum, summ_bytes, pt, sl, s_hat, lay, part);
     return hipGetLastError();
   }
   if (r == 8 && G == 4) {
