@@ -738,9 +738,9 @@ __device__ __forceinline__ int lane_block(const int32_t* __restrict__ pt_row, in
 // (basis sets 2 Q, 2 Q + 1, their Horner steps interleaved), and each consumed
 // register set is refilled at once with the next 16 pages' records.
 // ---------------------------------------------------------------------------
-constexpr int kR8Steps = 4;  // 16-page steps per wave: a block covers 4 x 16 x kR8Steps pages
-
-template <typename QT>
+// 16-page steps per wave (a block covers 4 x 16 x kSteps pages): 4 for large
+// grids, 1 when four steps would leave most compute units idle.
+template <typename QT, int kSteps>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
     uint32_t summ_bytes, const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
@@ -760,7 +760,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int32_t* pt_row = page_table + (long)s * max_pages;
   float run_m = -INFINITY, run_s = 0.0f;
 
-  constexpr int kWavePages = 16 * kR8Steps;
+  constexpr int kWavePages = 16 * kSteps;
   if (pg * kWavePages < n_c) {
     const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
     const uint32_t blk_bytes = (uint32_t)H_kv * (uint32_t)Gm::kStride, head_off = (uint32_t)h * Gm::kStride;
@@ -780,11 +780,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     float* shat_base = s_hat + lay.base(s, h) + (long)col * lay.head;
 
 #pragma unroll 1
-    for (int t = 0; t < kR8Steps; ++t) {
-      const int page0 = (pg * kR8Steps + t) * 16;
+    for (int t = 0; t < kSteps; ++t) {
+      const int page0 = (pg * kSteps + t) * 16;
       if (page0 >= n_c) break;
-      const bool more = __builtin_amdgcn_readfirstlane(t + 1 < kR8Steps && page0 + 16 < n_c);
-      const int blk_n2 = (t + 2 < kR8Steps && page0 + 32 < n_c) ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
+      const bool more = __builtin_amdgcn_readfirstlane(t + 1 < kSteps && page0 + 16 < n_c);
+      const int blk_n2 = (t + 2 < kSteps && page0 + 32 < n_c) ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
       StepOffs<R> nx;
       if (more) nx = step_offsets<R>(blk_n1, blk_bytes, head_off, lane);
       // ---- record tails to LDS; coefficient rows reordered to l = 0,4,1,5,2,6,3,7
@@ -1422,12 +1422,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   }
 }
 
-constexpr int kG4Steps = 4;
 
 template <typename QT>
-hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H_kv, int max_pages,
-                         const QT* q, const uint8_t* sum, uint32_t summ_bytes, const int32_t* pt,
-                         const int32_t* sl, float* s_hat, SHatLayout lay, float2* part) {
+hipError_t dispatch_scan(int r, int G, int steps, dim3 grid, hipStream_t st, int H_q, int H_kv,
+                         int max_pages, const QT* q, const uint8_t* sum, uint32_t summ_bytes,
+                         const int32_t* pt, const int32_t* sl, float* s_hat, SHatLayout lay,
+                         float2* part) {
 #define LOCKS_SCAN_FAST(RR, NP)                                                              \
   if (r == RR && G == 16 / NP) {                                                            \
     hipLaunchKernelGGL((scan_fast_kernel<QT, RR, NP>), grid, dim3(256), 0, st, H_q, H_kv,   \
@@ -1435,8 +1435,12 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
     return hipGetLastError();                                                               \
   }
   if (r == 8 && G == 16) {
-    hipLaunchKernelGGL((scan_r8_kernel<QT>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
-                       sum, summ_bytes, pt, sl, s_hat, lay, part);
+    if (steps == 1)
+      hipLaunchKernelGGL((scan_r8_kernel<QT, 1>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
+                         sum, summ_bytes, pt, sl, s_hat, lay, part);
+    else
+      hipLaunchKernelGGL((scan_r8_kernel<QT, 4>), grid, dim3(256), 0, st, H_q, H_kv, max_pages, q,
+                         sum, summ_bytes, pt, sl, s_hat, lay, part);
     return hipGetLastError();
   }
   if ((r == 2 || r == 4) && G == 4) {
@@ -1449,8 +1453,12 @@ hipError_t dispatch_scan(int r, int G, dim3 grid, hipStream_t st, int H_q, int H
     return hipGetLastError();
   }
   if (r == 8 && G == 4) {
-    hipLaunchKernelGGL((scan_r8g4_kernel<QT, kG4Steps>), grid, dim3(256), 0, st, H_q, H_kv,
-                       max_pages, q, sum, summ_bytes, pt, sl, s_hat, lay, part);
+    if (steps == 1)
+      hipLaunchKernelGGL((scan_r8g4_kernel<QT, 1>), grid, dim3(256), 0, st, H_q, H_kv, max_pages,
+                         q, sum, summ_bytes, pt, sl, s_hat, lay, part);
+    else
+      hipLaunchKernelGGL((scan_r8g4_kernel<QT, 4>), grid, dim3(256), 0, st, H_q, H_kv, max_pages,
+                         q, sum, summ_bytes, pt, sl, s_hat, lay, part);
     return hipGetLastError();
   }
   LOCKS_SCAN_FAST(8, 4) LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(4, 4)
@@ -1484,9 +1492,15 @@ static bool use_r8g4_kernel(const locks_cfg_t& c) {
   return c.rank == 8 && c.num_q_heads == 4 * c.num_kv_heads;
 }
 
+// 16-page steps per wave of the r = 8 kernels: 4, or 1 when a 4-step grid would
+// have fewer blocks than the GPU has compute units.
+static int r8_steps(const locks_cfg_t& c) {
+  const long blocks4 = (long)((c.max_pages_per_seq + 255) / 256) * c.num_kv_heads * c.num_seqs;
+  return blocks4 < 256 ? 1 : 4;
+}
+
 int scan_pages_per_block(const locks_cfg_t& c) {
-  if (use_r8_kernel(c)) return 64 * kR8Steps;
-  if (use_r8g4_kernel(c)) return 64 * kG4Steps;
+  if (use_r8_kernel(c) || use_r8g4_kernel(c)) return 64 * r8_steps(c);
   return kScanPagesPerBlock;
 }
 
@@ -1496,13 +1510,16 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
   const dim3 grid(scan_blocks(c), c.num_kv_heads, c.num_seqs);
   const int G = c.num_q_heads / c.num_kv_heads;
   const uint32_t bytes = (uint32_t)summary_store_bytes(c);
+  const int steps = r8_steps(c);
   if (c.q_dtype == LOCKS_BF16)
-    return dispatch_scan(c.rank, G, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                         static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(summaries),
-                         bytes, page_table, seq_lens, s_hat, lay, partials);
-  return dispatch_scan(c.rank, G, grid, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                       static_cast<const float*>(q), static_cast<const uint8_t*>(summaries), bytes,
-                       page_table, seq_lens, s_hat, lay, partials);
+    return dispatch_scan(c.rank, G, steps, grid, st, c.num_q_heads, c.num_kv_heads,
+                         c.max_pages_per_seq, static_cast<const uint16_t*>(q),
+                         static_cast<const uint8_t*>(summaries), bytes, page_table, seq_lens,
+                         s_hat, lay, partials);
+  return dispatch_scan(c.rank, G, steps, grid, st, c.num_q_heads, c.num_kv_heads,
+                       c.max_pages_per_seq, static_cast<const float*>(q),
+                       static_cast<const uint8_t*>(summaries), bytes, page_table, seq_lens, s_hat,
+                       lay, partials);
 }
 
 }  // namespace locks
