@@ -100,6 +100,21 @@ __device__ __forceinline__ float red4_sum(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Combines running (max, sum 2^(x - max)) pairs, log2 domain, over the lanes that
+// share lane % M; every lane ends with its class's total.
+template <int M>
+__device__ __forceinline__ void merge_lanes_mod(float& m, float& l) {
+#pragma unroll
+  for (int o = M; o < 64; o <<= 1) {
+    const float om = __shfl_xor(m, o, 64), ol = __shfl_xor(l, o, 64);
+    const float mm = fmaxf(m, om);
+    l = (mm > -INFINITY)
+            ? l * __builtin_amdgcn_exp2f(m - mm) + ol * __builtin_amdgcn_exp2f(om - mm)
+            : 0.0f;
+    m = mm;
+  }
+}
+
 template <int R>
 struct TileRegs {
   uint4 vb[Geom<R>::kSets];       // basis slices, MFMA A layout
@@ -928,20 +943,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       __builtin_amdgcn_wave_barrier();
     }
   }
-  // ---- block partial (max, sum exp) per head over its pages, log2 domain
-  sRun[wave][lane] = make_float2(run_m, run_s);
+  // ---- block partial (max, sum exp) per head over its pages, log2 domain: lane
+  // l holds head l % 16; the wave's lanes are merged first
+  merge_lanes_mod<16>(run_m, run_s);
+  if (lane < G) sRun[wave][lane] = make_float2(run_m, run_s);
   __syncthreads();
   if (threadIdx.x < G) {
     const int g = threadIdx.x;
     float m = -INFINITY, l = 0.0f;
-    for (int w = 0; w < 4; ++w)
-      for (int r = 0; r < 4; ++r) m = fmaxf(m, sRun[w][g + 16 * r].x);
+    for (int w = 0; w < 4; ++w) m = fmaxf(m, sRun[w][g].x);
     if (m > -INFINITY)
-      for (int w = 0; w < 4; ++w)
-        for (int r = 0; r < 4; ++r) {
-          const float2 v = sRun[w][g + 16 * r];
-          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
-        }
+      for (int w = 0; w < 4; ++w) {
+        const float2 v = sRun[w][g];
+        if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+      }
     partials[(row0 + g) * gridDim.x + blockIdx.x] = make_float2(m, l);
   }
 }
@@ -1006,8 +1021,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int first = pg * kWavePages;
   if (first < n_c) {
     const int n_steps = min(kSteps, (n_c - first + 15) / 16);
-    const QDigits QD = q_digits(q + (row0 + g) * kDim, grp);
-    const float inv_m = diag ? QD.inv_scale : 0.0f;  // zero off the block diagonal of B
+    // the query digits are formed once the first step's loads are in flight
+    QDigits QD;
+    float inv_m = 0.0f;  // scale of the stage-1 values; zero off the block diagonal of B
+    auto form_digits = [&]() {
+      QD = q_digits(q + (row0 + g) * kDim, grp);
+      inv_m = diag ? QD.inv_scale : 0.0f;
+    };
     float* shat_base = s_hat + lay.base(s, h) + (long)g * lay.head;
 
     // record offsets of one step: ra[Q] page 4 Q + ca, rb[Q] page 4 Q + grp,
@@ -1048,27 +1068,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       mu[1] = bld16(rs, o.rm + kMu + 32u * grp + 16u);
     };
 
-    // kN consecutive 16-page steps from page `start`, fully unrolled so that
-    // every wait for a prefetched register counts exactly the loads issued
-    // after it
-    auto run = [&](int start, auto n_tag) {
-      constexpr int kN = decltype(n_tag)::value;
-      int blk_next = 0;  // blocks of the pages of step t + 1
-      {
-        const int blk0 = lane_block_clamped(pt_row, start, n_c, lane);
-        if (kN > 1) blk_next = lane_block_clamped(pt_row, start + 16, n_c, lane);
-        const Offs o0 = offsets(blk0);
-        ld_mu(o0);
+    // every register of the step whose pages' blocks lanes 0..15 hold in blk
+    auto load_step = [&](int blk) {
+      const Offs o0 = offsets(blk);
+      ld_mu(o0);
 #pragma unroll
-        for (int Q = 0; Q < 4; ++Q) {
-          ld_vb(o0, Q, 0);
-          ld_vb(o0, Q, 1);
-          ld_vs(o0, Q);
-          ld_cf(o0, Q);
-          ld_ms(o0, Q);
-          ld_cs(o0, Q);
-        }
+      for (int Q = 0; Q < 4; ++Q) {
+        ld_vb(o0, Q, 0);
+        ld_vb(o0, Q, 1);
+        ld_vs(o0, Q);
+        ld_cf(o0, Q);
+        ld_ms(o0, Q);
+        ld_cs(o0, Q);
       }
+    };
+
+    // kN consecutive 16-page steps from page `start` whose first step's
+    // registers are loaded (blk_next: blocks of the second step's pages), fully
+    // unrolled so that every wait for a prefetched register counts exactly the
+    // loads issued after it
+    auto run = [&](int start, auto n_tag, int blk_next) {
+      constexpr int kN = decltype(n_tag)::value;
 #pragma unroll
       for (int t = 0; t < kN; ++t) {
         const bool pf = t + 1 < kN;
@@ -1183,26 +1203,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
     };
     if (n_steps == kSteps) {
-      run(first, IntTag<kSteps>{});
+      const int blk0 = lane_block_clamped(pt_row, first, n_c, lane);
+      const int blk1 = kSteps > 1 ? lane_block_clamped(pt_row, first + 16, n_c, lane) : 0;
+      load_step(blk0);
+      form_digits();
+      run(first, IntTag<kSteps>{}, blk1);
     } else {
+      form_digits();
 #pragma unroll 1
-      for (int t = 0; t < n_steps; ++t) run(first + 16 * t, IntTag<1>{});
+      for (int t = 0; t < n_steps; ++t) {
+        load_step(lane_block_clamped(pt_row, first + 16 * t, n_c, lane));
+        run(first + 16 * t, IntTag<1>{}, 0);
+      }
     }
   }
-  // ---- block partial (max, sum exp) per head over its pages, log2 domain
-  sRun[wave][lane] = make_float2(run_m, run_s);
+  // ---- block partial (max, sum exp) per head over its pages, log2 domain: lane
+  // l holds head l % 4; the wave's lanes are merged first
+  merge_lanes_mod<4>(run_m, run_s);
+  if (lane < G) sRun[wave][lane] = make_float2(run_m, run_s);
   __syncthreads();
   if (threadIdx.x < G) {
     const int gg = threadIdx.x;
     float m = -INFINITY, l = 0.0f;
-    for (int w = 0; w < 4; ++w)
-      for (int c = gg; c < 64; c += 4) m = fmaxf(m, sRun[w][c].x);
+    for (int w = 0; w < 4; ++w) m = fmaxf(m, sRun[w][gg].x);
     if (m > -INFINITY)
-      for (int w = 0; w < 4; ++w)
-        for (int c = gg; c < 64; c += 4) {
-          const float2 v = sRun[w][c];
-          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
-        }
+      for (int w = 0; w < 4; ++w) {
+        const float2 v = sRun[w][gg];
+        if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+      }
     partials[(row0 + gg) * gridDim.x + blockIdx.x] = make_float2(m, l);
   }
 }
@@ -1211,14 +1239,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // Low rank (r in {2, 4}), G = 4: projections on the matrix cores, logits on the
 // vector ALU.
 //
-// A wave covers 16 pages per step.  Stage 1 (int8 MFMA, Horner over the query
-// digits) has rows (page, basis column) -- 16 / R pages per tile -- and the 4
-// heads repeated over the 16 columns; lanes of columns 0..3 scale their
-// projections and leave them in LDS, next to the centroid terms and the record
-// tails (coefficients and scales) of the step.  Stage 2 gives every lane one
-// (page, head) pair: z_i = a + s_i sum_l (c_il - 128) p_l for the 16 tokens in
-// fp32 (the excess-128 offset enters as one subtraction of 128 sum_l p_l), the
-// page LSE in registers, and a coalesced store of the page score.
+// A wave covers 16 pages per step.  The step's 16 records are gathered whole by
+// 16-byte buffer loads and parked in the wave's LDS slot; the loads of the next
+// step are issued right after, so they are in flight for the whole step (the
+// scan is bound by memory latency at these record sizes, not by arithmetic).
+// Stage 1 (int8 MFMA, Horner over the query digits) has rows (page, basis
+// column) -- 16 / R pages per tile -- and the 4 heads repeated over the 16
+// columns; lanes of columns 0..3 scale their projections and leave them in LDS,
+// next to the centroid terms.  Stage 2 gives every lane one (page, head) pair:
+// z_i = a + s_i sum_l (c_il - 128) p_l for the 16 tokens in fp32 (the
+// excess-128 offset enters as one subtraction of 128 sum_l p_l), the page LSE in
+// registers, and a coalesced store of the page score.
 // ---------------------------------------------------------------------------
 constexpr int kLowSteps = 4;  // 16-page steps per wave: a block covers 256 pages
 
@@ -1230,194 +1261,263 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   constexpr int G = 4;
   constexpr int kPPT = 16 / R;                        // pages per stage-1 tile
   constexpr uint32_t kStride = rec_stride(R);
-  constexpr int kTail = kStride - 64 * R;             // coefficients .. end of record
-  constexpr int kTailCh = kTail / 16;
-  constexpr int kTailLoads = (16 * kTailCh + 63) / 64;
-  constexpr int kMu = 16 * R, kSc = 16 * R + kDim;    // offsets inside the tail
-  __shared__ __align__(16) uint8_t sTail[4][16][kTail];
+  constexpr int kCh = kStride / 16;                   // 16-byte chunks per record
+  constexpr int kLoads = (16 * kCh + 63) / 64;        // chunk loads per lane and step
+  constexpr int kCoef = rec_coef_off(R), kMu = rec_mu_off(R), kSc = rec_scale_off(R);
+  __shared__ __align__(16) uint8_t sRec[4][16][kStride];
   __shared__ __align__(16) float sP[4][16][G][R];
   __shared__ float sA[4][16][G];
   __shared__ float2 sRun[4][64];
+  __shared__ __align__(16) i4v sQ[3][2][64];  // query digit operands, shared by the waves
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = blockIdx.y, s = blockIdx.z;
   const int n_c = seq_lens[s] / kPage;
-  const int pg = blockIdx.x * 4 + wave;
   const long row0 = (long)s * H_q + (long)h * G;
+  constexpr int kWavePages = 16 * kLowSteps;
+  if (blockIdx.x * 4 * kWavePages >= n_c) {  // no complete page in this block
+    if (threadIdx.x < G)
+      partials[(row0 + threadIdx.x) * gridDim.x + blockIdx.x] = make_float2(-INFINITY, 0.0f);
+    return;
+  }
+  const int pg = blockIdx.x * 4 + wave;
+  const int first = pg * kWavePages;
+  const bool has = first < n_c;
   const int32_t* pt_row = page_table + (long)s * max_pages;
   const int pp = lane >> 2, gg = lane & 3;            // stage 2: (page, head) of this lane
   float run_m = -INFINITY, run_s = 0.0f;
 
-  constexpr int kWavePages = 16 * kLowSteps;
-  const int first = pg * kWavePages;
-  if (first < n_c) {
-    const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
-    const uint32_t blk_bytes = (uint32_t)H_kv * kStride, head_off = (uint32_t)h * kStride;
+  const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
+  const uint32_t blk_bytes = (uint32_t)H_kv * kStride, head_off = (uint32_t)h * kStride;
+  // blocks of the wave's 64 pages, page first + l in lane l (pages past the end
+  // repeat the last complete one)
+  const int blk_all = has ? pt_row[min(first + lane, n_c - 1)] : 0;
+  // chunk c = lane + 64 u of step t is chunk c % kCh of page 16 t + c / kCh; it
+  // lands at byte 16 c of the wave's LDS slot
+  auto issue = [&](int t, uint4 (&ld)[kLoads]) {
+#pragma unroll
+    for (int u = 0; u < kLoads; ++u) {
+      int c = lane + 64 * u;
+      c = c < 16 * kCh ? c : 16 * kCh - 1;
+      const int b = __shfl(blk_all, 16 * t + c / kCh, 64);
+      ld[u] = bld16(rs, rec_off(b, blk_bytes, head_off) + (c % kCh) * 16);
+    }
+  };
+  // the query digits (identical for the four waves) stay in LDS and are read at
+  // each use, leaving the registers to the loads in flight
+  int bias[3];
+  float inv_scale;
+  {
     const QDigits QD = q_digits(q + (row0 + (col & 3)) * kDim, grp);
-    // this lane's loads of a step whose 16 pages' blocks lanes 0..15 hold in blk:
-    // basis slice of tile T (row col = (page T kPPT + col / R, column col % R)),
-    // and record-tail chunks
-    auto issue = [&](int blk, uint4 (&vb)[R], uint4 (&tl)[kTailLoads]) {
+    if (wave == 0) {
 #pragma unroll
-      for (int T = 0; T < R; ++T) {
-        const int b = __shfl(blk, T * kPPT + col / R, 64);
-        vb[T] = bld16(rs, rec_off(b, blk_bytes, head_off) + 64u * (col % R) + 16u * grp);
-      }
+      for (int d = 0; d < 3; ++d)
 #pragma unroll
-      for (int u = 0; u < kTailLoads; ++u) {
-        int c = lane + 64 * u;
-        c = c < 16 * kTailCh ? c : 16 * kTailCh - 1;
-        const int b = __shfl(blk, c / kTailCh, 64);
-        tl[u] = bld16(rs, rec_off(b, blk_bytes, head_off) + 64u * R + (c % kTailCh) * 16);
-      }
-    };
-    uint4 vb[R], tl[kTailLoads];
-    issue(lane_block_clamped(pt_row, first, n_c, lane), vb, tl);
+        for (int hh = 0; hh < 2; ++hh) sQ[d][hh][lane] = QD.bd[d][hh];
+    }
+#pragma unroll
+    for (int d = 0; d < 3; ++d) bias[d] = QD.bias[d];
+    inv_scale = QD.inv_scale;
+  }
+  // the first step's records (the page-table load was in flight while the
+  // digits were formed)
+  uint4 ld[kLoads];
+  if (has) issue(0, ld);
+  __syncthreads();
+  // (the empty asm makes every use a fresh LDS read: hoisted out of the step loop
+  // the operands would take 24 registers again)
+  auto qop = [&](int d, int hh) {
+    int li = lane;
+    asm volatile("" : "+v"(li));
+    return sQ[d][hh][li];
+  };
+
+  if (has) {
     const int n_steps = min(kLowSteps, (n_c - first + 15) / 16);
     float* shat_base = s_hat + lay.base(s, h) + (long)gg * lay.head;
+    uint8_t* slot = &sRec[wave][0][0];
 
-#pragma unroll 1
-    for (int t = 0; t < n_steps; ++t) {
-      const int page0 = first + 16 * t;
-      const bool refill = __builtin_amdgcn_readfirstlane(t + 1 < n_steps);
-      const int blk_next = refill ? lane_block_clamped(pt_row, page0 + 16, n_c, lane) : 0;
-      // ---- record tails to LDS
+    // the wave's kN steps, fully unrolled so that each wait for a step's records
+    // counts exactly the memory operations issued after them (the first step's
+    // loads are in ld); the page score of a step is stored after the next step's
+    // loads are issued
+    auto run = [&](auto n_tag) {
+      constexpr int kN = decltype(n_tag)::value;
+      float st_val = 0.0f;
+      int st_page = -1;
 #pragma unroll
-      for (int u = 0; u < kTailLoads; ++u) {
-        const int c = lane + 64 * u;
-        if (c < 16 * kTailCh)
-          *reinterpret_cast<uint4*>(&sTail[wave][c / kTailCh][(c % kTailCh) * 16]) = tl[u];
-      }
-      __builtin_amdgcn_wave_barrier();
-      // ---- centroid term (one page per row; int8 codes: three digit chains)
-      {
-        const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][col][kMu + 32 * grp]);
-        const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][col][kMu + 32 * grp + 16]);
-        const uint32_t mw[8] = {m0.x ^ 0x80808080u, m0.y ^ 0x80808080u, m0.z ^ 0x80808080u,
-                                m0.w ^ 0x80808080u, m1.x ^ 0x80808080u, m1.y ^ 0x80808080u,
-                                m1.z ^ 0x80808080u, m1.w ^ 0x80808080u};
-        i4v acc[3];
+      for (int t = 0; t < kN; ++t) {
+        const int page0 = first + 16 * t;
+        // ---- this step's records to LDS, then the next step's loads
 #pragma unroll
-        for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
-          const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
-                         (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
-                         (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
-                         (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
-#pragma unroll
-          for (int d = 0; d < 3; ++d)
-            acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
+        for (int u = 0; u < kLoads; ++u) {
+          const int c = lane + 64 * u;
+          if (c < 16 * kCh) *reinterpret_cast<uint4*>(slot + 16 * c) = ld[u];
         }
-        if (col < G) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int page = 4 * grp + j;
-            const float ms = lds_f16(&sTail[wave][page][kSc + 2 * (R + 16)]);
-            const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
-            sA[wave][page][col] = v * (ms * QD.inv_scale);
+        __builtin_amdgcn_wave_barrier();
+        if (t + 1 < kN) issue(t + 1, ld);
+        if (t > 0 && st_page >= 0) shat_base[(long)st_page * lay.page] = st_val;
+        // ---- centroid term (one page per row; int8 codes: three digit chains)
+        {
+          const uint4 m0 = *reinterpret_cast<const uint4*>(&sRec[wave][col][kMu + 32 * grp]);
+          const uint4 m1 = *reinterpret_cast<const uint4*>(&sRec[wave][col][kMu + 32 * grp + 16]);
+          const uint32_t mw[8] = {m0.x ^ 0x80808080u, m0.y ^ 0x80808080u, m0.z ^ 0x80808080u,
+                                  m0.w ^ 0x80808080u, m1.x ^ 0x80808080u, m1.y ^ 0x80808080u,
+                                  m1.z ^ 0x80808080u, m1.w ^ 0x80808080u};
+          i4v acc[3];
+  #pragma unroll
+          for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
+  #pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
+            const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
+                           (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
+                           (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
+                           (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
+  #pragma unroll
+            for (int d = 0; d < 3; ++d)
+              acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, qop(d, hh), acc[d], 0, 0, 0);
           }
-        }
-      }
-      // ---- stage 1: projections of every (page, basis column) onto the 4 heads
-#pragma unroll
-      for (int T = 0; T < R; T += 2) {
-        i4v a0[2], a1[2], acc[2];
-        nib_operands(vb[T], a0);
-        nib_operands(vb[T + 1 < R ? T + 1 : T], a1);
-        proj_horner2(a0, a1, QD, acc[0], acc[1]);
-        if (col < G) {
-#pragma unroll
-          for (int i = 0; i < 2 && T + i < R; ++i)
-#pragma unroll
+          if (col < G) {
+  #pragma unroll
             for (int j = 0; j < 4; ++j) {
-              const int row = 4 * grp + j;
-              const int page = (T + i) * kPPT + row / R, l = row % R;
-              const float vs = lds_f16(&sTail[wave][page][kSc + 2 * l]);
-              sP[wave][page][col][l] = (float)acc[i][j] * (vs * QD.inv_scale);
+              const int page = 4 * grp + j;
+              const float ms = lds_f16(&sRec[wave][page][kSc + 2 * (R + 16)]);
+              const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
+              sA[wave][page][col] = v * (ms * inv_scale);
             }
-        }
-      }
-      if (refill) issue(blk_next, vb, tl);
-      __builtin_amdgcn_wave_barrier();
-      // ---- stage 2: the 16 logits of (page pp, head gg) and their LSE
-      {
-        float pv[R];
-        float psum = 0.0f;
-#pragma unroll
-        for (int l = 0; l < R; ++l) {
-          pv[l] = sP[wave][pp][gg][l];
-          psum += pv[l];
-        }
-        const float k128 = 128.0f * psum;
-        const float a = sA[wave][pp][gg];
-        uint32_t cw[4 * R];  // coefficient codes, row-major (16 rows x R bytes)
-#pragma unroll
-        for (int v = 0; v < R; ++v) {
-          const uint4 c4 = *reinterpret_cast<const uint4*>(&sTail[wave][pp][16 * v]);
-          cw[4 * v] = c4.x;
-          cw[4 * v + 1] = c4.y;
-          cw[4 * v + 2] = c4.z;
-          cw[4 * v + 3] = c4.w;
-        }
-        uint32_t sw[8];  // coefficient row scales (fp16 pairs)
-#pragma unroll
-        for (int v = 0; v < 8; ++v)
-          sw[v] = *reinterpret_cast<const uint32_t*>(&sTail[wave][pp][kSc + 2 * R + 4 * v]);
-        float e[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float tz = -k128;
-#pragma unroll
-          for (int l = 0; l < R; ++l) {
-            const int b = i * R + l;  // byte index of code (i, l)
-            const float c = (float)((cw[b >> 2] >> (8 * (b & 3))) & 0xffu);
-            tz = fmaf(c, pv[l], tz);
           }
-          const h2 sc = as_h2(sw[i >> 1]);
-          e[i] = tz * (float)((i & 1) ? sc.y : sc.x);  // logit minus the centroid term
         }
-        float sm = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(e[i]);
-        float shift = 0.0f;
-        if (!(sm > 0.0f && sm < INFINITY)) {
-          shift = e[0];
-#pragma unroll
-          for (int i = 1; i < 16; ++i) shift = fmaxf(shift, e[i]);
-          sm = 0.0f;
-#pragma unroll
-          for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(e[i] - shift);
+        // ---- stage 1: projections of every (page, basis column) onto the 4 heads
+  #pragma unroll
+        for (int T = 0; T < R; T += 2) {
+          i4v a0[2], a1[2], acc[2];
+          const int T1 = T + 1 < R ? T + 1 : T;
+          nib_operands(*reinterpret_cast<const uint4*>(
+                           &sRec[wave][T * kPPT + col / R][64 * (col % R) + 16 * grp]),
+                       a0);
+          nib_operands(*reinterpret_cast<const uint4*>(
+                           &sRec[wave][T1 * kPPT + col / R][64 * (col % R) + 16 * grp]),
+                       a1);
+          {
+            i4v x = i4v{bias[0], bias[0], bias[0], bias[0]};
+            i4v y = x;
+  #pragma unroll
+            for (int d = 0; d < 3; ++d) {
+              const i4v b0 = qop(d, 0), b1 = qop(d, 1);
+              x = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0[0], b0, x, 0, 0, 0);
+              y = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1[0], b0, y, 0, 0, 0);
+              x = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0[1], b1, x, 0, 0, 0);
+              y = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1[1], b1, y, 0, 0, 0);
+              if (d < 2) {
+  #pragma unroll
+                for (int j = 0; j < 4; ++j) x[j] = (int)(((uint32_t)x[j] << 8) + (uint32_t)bias[d + 1]);
+  #pragma unroll
+                for (int j = 0; j < 4; ++j) y[j] = (int)(((uint32_t)y[j] << 8) + (uint32_t)bias[d + 1]);
+              }
+            }
+            acc[0] = x;
+            acc[1] = y;
+          }
+          if (col < G) {
+  #pragma unroll
+            for (int i = 0; i < 2 && T + i < R; ++i)
+  #pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const int row = 4 * grp + j;
+                const int page = (T + i) * kPPT + row / R, l = row % R;
+                const float vs = lds_f16(&sRec[wave][page][kSc + 2 * l]);
+                sP[wave][page][col][l] = (float)acc[i][j] * (vs * inv_scale);
+              }
+          }
         }
-        const float s2 = a + shift + __builtin_amdgcn_logf(sm);
-        const int page = page0 + pp;
-        const bool live = page < n_c;
-        if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
-        const float ex = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
-        const bool up = s2 > run_m;
-        const float ns = up ? fmaf(run_s, ex, 1.0f) : run_s + ex;
-        run_s = live ? ns : run_s;
-        run_m = (live && up) ? s2 : run_m;
+        __builtin_amdgcn_wave_barrier();
+        // ---- stage 2: the 16 logits of (page pp, head gg) and their LSE
+        {
+          float pv[R];
+          float psum = 0.0f;
+  #pragma unroll
+          for (int l = 0; l < R; ++l) {
+            pv[l] = sP[wave][pp][gg][l];
+            psum += pv[l];
+          }
+          const float k128 = 128.0f * psum;
+          const float a = sA[wave][pp][gg];
+          uint32_t cw[4 * R];  // coefficient codes, row-major (16 rows x R bytes)
+  #pragma unroll
+          for (int v = 0; v < R; ++v) {
+            const uint4 c4 = *reinterpret_cast<const uint4*>(&sRec[wave][pp][kCoef + 16 * v]);
+            cw[4 * v] = c4.x;
+            cw[4 * v + 1] = c4.y;
+            cw[4 * v + 2] = c4.z;
+            cw[4 * v + 3] = c4.w;
+          }
+          uint32_t sw[8];  // coefficient row scales (fp16 pairs)
+  #pragma unroll
+          for (int v = 0; v < 8; ++v)
+            sw[v] = *reinterpret_cast<const uint32_t*>(&sRec[wave][pp][kSc + 2 * R + 4 * v]);
+          float e[16];
+  #pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            float tz = -k128;
+  #pragma unroll
+            for (int l = 0; l < R; ++l) {
+              const int b = i * R + l;  // byte index of code (i, l)
+              const float c = (float)((cw[b >> 2] >> (8 * (b & 3))) & 0xffu);
+              tz = fmaf(c, pv[l], tz);
+            }
+            const h2 sc = as_h2(sw[i >> 1]);
+            e[i] = tz * (float)((i & 1) ? sc.y : sc.x);  // logit minus the centroid term
+          }
+          float sm = 0.0f;
+  #pragma unroll
+          for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(e[i]);
+          float shift = 0.0f;
+          if (!(sm > 0.0f && sm < INFINITY)) {
+            shift = e[0];
+  #pragma unroll
+            for (int i = 1; i < 16; ++i) shift = fmaxf(shift, e[i]);
+            sm = 0.0f;
+  #pragma unroll
+            for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(e[i] - shift);
+          }
+          const float s2 = a + shift + __builtin_amdgcn_logf(sm);
+          const int page = page0 + pp;
+          const bool live = page < n_c;
+          // stored after the next step's loads are issued (its wait then skips the store)
+          st_val = s2 * 0.69314718055994531f;
+          st_page = live ? page : -1;
+          const float ex = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+          const bool up = s2 > run_m;
+          const float ns = up ? fmaf(run_s, ex, 1.0f) : run_s + ex;
+          run_s = live ? ns : run_s;
+          run_m = (live && up) ? s2 : run_m;
+        }
+        __builtin_amdgcn_wave_barrier();
       }
-      __builtin_amdgcn_wave_barrier();
-    }
+      if (st_page >= 0) shat_base[(long)st_page * lay.page] = st_val;
+    };
+    static_assert(kLowSteps == 4, "one unrolled run per step count");
+    if (n_steps == 4) run(IntTag<4>{});
+    else if (n_steps == 3) run(IntTag<3>{});
+    else if (n_steps == 2) run(IntTag<2>{});
+    else run(IntTag<1>{});
   }
-  // ---- block partial (max, sum exp) per head over its pages, log2 domain
-  sRun[wave][lane] = make_float2(run_m, run_s);
+  // ---- block partial (max, sum exp) per head over its pages, log2 domain: lane
+  // l holds head l % 4; the wave's lanes are merged first
+  merge_lanes_mod<4>(run_m, run_s);
+  if (lane < G) sRun[wave][lane] = make_float2(run_m, run_s);
   __syncthreads();
   if (threadIdx.x < G) {
     const int g = threadIdx.x;
     float m = -INFINITY, l = 0.0f;
-    for (int w = 0; w < 4; ++w)
-      for (int c = g; c < 64; c += G) m = fmaxf(m, sRun[w][c].x);
+    for (int w = 0; w < 4; ++w) m = fmaxf(m, sRun[w][g].x);
     if (m > -INFINITY)
-      for (int w = 0; w < 4; ++w)
-        for (int c = g; c < 64; c += G) {
-          const float2 v = sRun[w][c];
-          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
-        }
+      for (int w = 0; w < 4; ++w) {
+        const float2 v = sRun[w][g];
+        if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+      }
     partials[(row0 + g) * gridDim.x + blockIdx.x] = make_float2(m, l);
   }
 }
