@@ -736,6 +736,11 @@ __device__ __forceinline__ int lane_block(const int32_t* __restrict__ pt_row, in
   return pt_row[pl < n_c ? pl : page0];
 }
 
+template <int N>
+struct IntTag {
+  static constexpr int value = N;
+};
+
 // ---------------------------------------------------------------------------
 // r = 8, G = 16: stage 2 with (page, token) rows.
 //
@@ -779,168 +784,188 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   if (pg * kWavePages < n_c) {
     const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
     const uint32_t blk_bytes = (uint32_t)H_kv * (uint32_t)Gm::kStride, head_off = (uint32_t)h * Gm::kStride;
+    const int first = pg * kWavePages;
+    const int n_steps = min(kSteps, (n_c - first + 15) / 16);
     uint4 vb[Gm::kSets];
     uint4 tl[Gm::kTailLoads];
-    {
-      const StepOffs<R> o0 = step_offsets<R>(lane_block(pt_row, pg * kWavePages, n_c, lane),
-                                             blk_bytes, head_off, lane);
+    // the record slices of the step whose pages' blocks lanes 0..15 hold in blk
+    auto load_step = [&](int blk) {
+      const StepOffs<R> o0 = step_offsets<R>(blk, blk_bytes, head_off, lane);
 #pragma unroll
       for (int st = 0; st < Gm::kSets; ++st) vb[st] = bld16(rs, o0.vb[st]);
 #pragma unroll
       for (int u = 0; u < Gm::kTailLoads; ++u) tl[u] = bld16(rs, o0.tl[u]);
-    }
-    int blk_n1 = pg * kWavePages + 16 < n_c ? lane_block(pt_row, pg * kWavePages + 16, n_c, lane) : 0;
-    const QDigits QD = q_digits(q + (row0 + col) * kDim, grp);
+    };
+    QDigits QD;  // formed once the first step's loads are in flight
     const int a_row = col >> 2, t_row = col & 3;  // A row of this lane: (page, token)
     float* shat_base = s_hat + lay.base(s, h) + (long)col * lay.head;
 
-#pragma unroll 1
-    for (int t = 0; t < kSteps; ++t) {
-      const int page0 = (pg * kSteps + t) * 16;
-      if (page0 >= n_c) break;
-      const bool more = __builtin_amdgcn_readfirstlane(t + 1 < kSteps && page0 + 16 < n_c);
-      const int blk_n2 = (t + 2 < kSteps && page0 + 32 < n_c) ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
-      StepOffs<R> nx;
-      if (more) nx = step_offsets<R>(blk_n1, blk_bytes, head_off, lane);
-      // ---- record tails to LDS; coefficient rows reordered to l = 0,4,1,5,2,6,3,7
+    // kN consecutive steps from page `start` whose first step's slices are
+    // loaded (blk_n1: blocks of the second step's pages), fully unrolled so
+    // that every wait for a prefetched register counts exactly the loads
+    // issued after it
+    auto run = [&](int start, auto n_tag, int blk_n1) {
+      constexpr int kN = decltype(n_tag)::value;
 #pragma unroll
-      for (int u = 0; u < Gm::kTailLoads; ++u) {
-        const int c = lane + 64 * u;
-        if (c < 16 * Gm::kTailCh) {
-          const int o = c % Gm::kTailCh;
-          uint4 v = tl[u];
-          if (o < 8) {
-            v = make_uint4(__builtin_amdgcn_perm(v.y, v.x, 0x05010400u),
-                           __builtin_amdgcn_perm(v.y, v.x, 0x07030602u),
-                           __builtin_amdgcn_perm(v.w, v.z, 0x05010400u),
-                           __builtin_amdgcn_perm(v.w, v.z, 0x07030602u));
-          }
-          *reinterpret_cast<uint4*>(&sTail[wave][c / Gm::kTailCh][o * 16]) = v;
-        }
-      }
-      __builtin_amdgcn_wave_barrier();
-      if (more) {
-#pragma unroll
-        for (int u = 0; u < Gm::kTailLoads; ++u) tl[u] = bld16(rs, nx.tl[u]);
-      }
-
-      // ---- centroid term: areg[j] = a(page 4 j + grp, head col)
-      float areg[4];
-      {
-        const int cp = 4 * (col & 3) + (col >> 2);
-        const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][cp][Gm::kMu + 32 * grp]);
-        const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][cp][Gm::kMu + 32 * grp + 16]);
-        const uint32_t mw[8] = {m0.x ^ 0x80808080u, m0.y ^ 0x80808080u, m0.z ^ 0x80808080u,
-                                m0.w ^ 0x80808080u, m1.x ^ 0x80808080u, m1.y ^ 0x80808080u,
-                                m1.z ^ 0x80808080u, m1.w ^ 0x80808080u};
-        i4v acc[3];
-#pragma unroll
-        for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
-          const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
-                         (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
-                         (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
-                         (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
-#pragma unroll
-          for (int d = 0; d < 3; ++d)
-            acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float ms = lds_f16(&sTail[wave][4 * j + grp][Gm::kSc + 2 * (R + 16)]);
-          const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
-          areg[j] = v * (ms * QD.inv_scale);
-        }
-      }
-
-#pragma unroll
-      for (int Q = 0; Q < 4; ++Q) {
-        __builtin_amdgcn_sched_barrier(0);
-        // ---- stage 1 (int8 MFMA) for basis sets 2Q, 2Q+1:
-        //      vals[4 i + j] = p(page 4 Q + 2 i + j / 2, l = 4 (j % 2) + grp)
-        float vals[8];
-        {
-          i4v a0[2], a1[2], acc[2];
-          nib_operands(vb[2 * Q], a0);
-          nib_operands(vb[2 * Q + 1], a1);
-          proj_horner2(a0, a1, QD, acc[0], acc[1]);
-          if (more) {
-            vb[2 * Q] = bld16(rs, nx.vb[2 * Q]);
-            vb[2 * Q + 1] = bld16(rs, nx.vb[2 * Q + 1]);
-          }
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int st = 2 * Q + i;
-              const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
-              const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
-              vals[4 * i + j] = (float)acc[i][j] * (vs * QD.inv_scale);
+      for (int t = 0; t < kN; ++t) {
+        const int page0 = start + 16 * t;
+        const bool more = t + 1 < kN;
+        const int blk_n2 = t + 2 < kN ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
+        StepOffs<R> nx;
+        if (more) nx = step_offsets<R>(blk_n1, blk_bytes, head_off, lane);
+        // ---- record tails to LDS; coefficient rows reordered to l = 0,4,1,5,2,6,3,7
+  #pragma unroll
+        for (int u = 0; u < Gm::kTailLoads; ++u) {
+          const int c = lane + 64 * u;
+          if (c < 16 * Gm::kTailCh) {
+            const int o = c % Gm::kTailCh;
+            uint4 v = tl[u];
+            if (o < 8) {
+              v = make_uint4(__builtin_amdgcn_perm(v.y, v.x, 0x05010400u),
+                             __builtin_amdgcn_perm(v.y, v.x, 0x07030602u),
+                             __builtin_amdgcn_perm(v.w, v.z, 0x05010400u),
+                             __builtin_amdgcn_perm(v.w, v.z, 0x07030602u));
             }
+            *reinterpret_cast<uint4*>(&sTail[wave][c / Gm::kTailCh][o * 16]) = v;
+          }
         }
-        // ---- stage 2 for the quad, then the page LSE in registers
-        h8 bh, bl;
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const auto hi = __builtin_amdgcn_cvt_pkrtz(vals[e], vals[e + 1]);
-          const auto lo = __builtin_amdgcn_cvt_pkrtz(vals[e] - (float)hi[0], vals[e + 1] - (float)hi[1]);
-          bh[e] = hi[0];
-          bh[e + 1] = hi[1];
-          bl[e] = lo[0];
-          bl[e + 1] = lo[1];
+        __builtin_amdgcn_wave_barrier();
+        if (more) {
+  #pragma unroll
+          for (int u = 0; u < Gm::kTailLoads; ++u) tl[u] = bld16(rs, nx.tl[u]);
         }
-        float z[16];
-#pragma unroll
-        for (int ps = 0; ps < 4; ++ps) {
-          const uint32_t pr = *reinterpret_cast<const uint16_t*>(
-              &sTail[wave][4 * Q + a_row][(4 * ps + t_row) * R + 2 * grp]);
-          const h2 pair = as_h2(__builtin_amdgcn_perm(0x64646464u, pr, 0x05010400u)) -
-                          h2{(_Float16)1152.0f, (_Float16)1152.0f};
-          const uint32_t pw = __builtin_bit_cast(uint32_t, pair);
-          const uint4 aw = make_uint4(a_row == 0 ? pw : 0u, a_row == 1 ? pw : 0u,
-                                      a_row == 2 ? pw : 0u, a_row == 3 ? pw : 0u);
-          const h8 A = __builtin_bit_cast(h8, aw);
-          f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bh, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bl, acc, 0, 0, 0);
-          const uint2 csw = *reinterpret_cast<const uint2*>(
-              &sTail[wave][4 * Q + grp][Gm::kSc + 2 * (R + 4 * ps)]);
-          const h2 c01 = as_h2(csw.x), c23 = as_h2(csw.y);
-          z[4 * ps + 0] = (float)c01.x * acc[0];
-          z[4 * ps + 1] = (float)c01.y * acc[1];
-          z[4 * ps + 2] = (float)c23.x * acc[2];
-          z[4 * ps + 3] = (float)c23.y * acc[3];
+
+        // ---- centroid term: areg[j] = a(page 4 j + grp, head col)
+        float areg[4];
+        {
+          const int cp = 4 * (col & 3) + (col >> 2);
+          const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][cp][Gm::kMu + 32 * grp]);
+          const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][cp][Gm::kMu + 32 * grp + 16]);
+          const uint32_t mw[8] = {m0.x ^ 0x80808080u, m0.y ^ 0x80808080u, m0.z ^ 0x80808080u,
+                                  m0.w ^ 0x80808080u, m1.x ^ 0x80808080u, m1.y ^ 0x80808080u,
+                                  m1.z ^ 0x80808080u, m1.w ^ 0x80808080u};
+          i4v acc[3];
+  #pragma unroll
+          for (int d = 0; d < 3; ++d) acc[d] = i4v{0, 0, 0, 0};
+  #pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t y0 = mw[4 * hh], y1 = mw[4 * hh + 1], y2 = mw[4 * hh + 2], y3 = mw[4 * hh + 3];
+            const i4v a = {(int)__builtin_amdgcn_perm(y1, y0, 0x06040200u),
+                           (int)__builtin_amdgcn_perm(y1, y0, 0x07050301u),
+                           (int)__builtin_amdgcn_perm(y3, y2, 0x06040200u),
+                           (int)__builtin_amdgcn_perm(y3, y2, 0x07050301u)};
+  #pragma unroll
+            for (int d = 0; d < 3; ++d)
+              acc[d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, QD.bd[d][hh], acc[d], 0, 0, 0);
+          }
+  #pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float ms = lds_f16(&sTail[wave][4 * j + grp][Gm::kSc + 2 * (R + 16)]);
+            const float v = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
+            areg[j] = v * (ms * QD.inv_scale);
+          }
         }
-        // z are the logits minus the centroid logit a.  The deviations of a
-        // page's tokens sum to ~0 (the coefficient columns are orthogonal to
-        // the all-ones vector), so the largest is >= ~0 and sum 2^z is safe
-        // without a max; a max-shifted sum is taken only if it is not finite.
-        float sm = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i]);
-        float shift = 0.0f;
-        if (!(sm > 0.0f && sm < INFINITY)) {
-          shift = z[0];
-#pragma unroll
-          for (int i = 1; i < 16; ++i) shift = fmaxf(shift, z[i]);
-          sm = 0.0f;
-#pragma unroll
-          for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i] - shift);
+
+  #pragma unroll
+        for (int Q = 0; Q < 4; ++Q) {
+          __builtin_amdgcn_sched_barrier(0);
+          // ---- stage 1 (int8 MFMA) for basis sets 2Q, 2Q+1:
+          //      vals[4 i + j] = p(page 4 Q + 2 i + j / 2, l = 4 (j % 2) + grp)
+          float vals[8];
+          {
+            i4v a0[2], a1[2], acc[2];
+            nib_operands(vb[2 * Q], a0);
+            nib_operands(vb[2 * Q + 1], a1);
+            proj_horner2(a0, a1, QD, acc[0], acc[1]);
+            if (more) {
+              vb[2 * Q] = bld16(rs, nx.vb[2 * Q]);
+              vb[2 * Q + 1] = bld16(rs, nx.vb[2 * Q + 1]);
+            }
+  #pragma unroll
+            for (int i = 0; i < 2; ++i)
+  #pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const int st = 2 * Q + i;
+                const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
+                const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
+                vals[4 * i + j] = (float)acc[i][j] * (vs * QD.inv_scale);
+              }
+          }
+          // ---- stage 2 for the quad, then the page LSE in registers
+          h8 bh, bl;
+  #pragma unroll
+          for (int e = 0; e < 8; e += 2) {
+            const auto hi = __builtin_amdgcn_cvt_pkrtz(vals[e], vals[e + 1]);
+            const auto lo = __builtin_amdgcn_cvt_pkrtz(vals[e] - (float)hi[0], vals[e + 1] - (float)hi[1]);
+            bh[e] = hi[0];
+            bh[e + 1] = hi[1];
+            bl[e] = lo[0];
+            bl[e + 1] = lo[1];
+          }
+          float z[16];
+  #pragma unroll
+          for (int ps = 0; ps < 4; ++ps) {
+            const uint32_t pr = *reinterpret_cast<const uint16_t*>(
+                &sTail[wave][4 * Q + a_row][(4 * ps + t_row) * R + 2 * grp]);
+            const h2 pair = as_h2(__builtin_amdgcn_perm(0x64646464u, pr, 0x05010400u)) -
+                            h2{(_Float16)1152.0f, (_Float16)1152.0f};
+            const uint32_t pw = __builtin_bit_cast(uint32_t, pair);
+            const uint4 aw = make_uint4(a_row == 0 ? pw : 0u, a_row == 1 ? pw : 0u,
+                                        a_row == 2 ? pw : 0u, a_row == 3 ? pw : 0u);
+            const h8 A = __builtin_bit_cast(h8, aw);
+            f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bh, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bl, acc, 0, 0, 0);
+            const uint2 csw = *reinterpret_cast<const uint2*>(
+                &sTail[wave][4 * Q + grp][Gm::kSc + 2 * (R + 4 * ps)]);
+            const h2 c01 = as_h2(csw.x), c23 = as_h2(csw.y);
+            z[4 * ps + 0] = (float)c01.x * acc[0];
+            z[4 * ps + 1] = (float)c01.y * acc[1];
+            z[4 * ps + 2] = (float)c23.x * acc[2];
+            z[4 * ps + 3] = (float)c23.y * acc[3];
+          }
+          // z are the logits minus the centroid logit a.  The deviations of a
+          // page's tokens sum to ~0 (the coefficient columns are orthogonal to
+          // the all-ones vector), so the largest is >= ~0 and sum 2^z is safe
+          // without a max; a max-shifted sum is taken only if it is not finite.
+          float sm = 0.0f;
+  #pragma unroll
+          for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i]);
+          float shift = 0.0f;
+          if (!(sm > 0.0f && sm < INFINITY)) {
+            shift = z[0];
+  #pragma unroll
+            for (int i = 1; i < 16; ++i) shift = fmaxf(shift, z[i]);
+            sm = 0.0f;
+  #pragma unroll
+            for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i] - shift);
+          }
+          const float s2 = areg[Q] + shift + __builtin_amdgcn_logf(sm);
+          const int page = page0 + 4 * Q + grp;
+          const bool live = page < n_c;
+          if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
+          const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+          const bool up = s2 > run_m;
+          const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
+          run_s = live ? ns : run_s;
+          run_m = (live && up) ? s2 : run_m;
         }
-        const float s2 = areg[Q] + shift + __builtin_amdgcn_logf(sm);
-        const int page = page0 + 4 * Q + grp;
-        const bool live = page < n_c;
-        if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
-        const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
-        const bool up = s2 > run_m;
-        const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
-        run_s = live ? ns : run_s;
-        run_m = (live && up) ? s2 : run_m;
+        blk_n1 = blk_n2;
+        __builtin_amdgcn_wave_barrier();
       }
-      blk_n1 = blk_n2;
-      __builtin_amdgcn_wave_barrier();
+    };
+    if (n_steps == kSteps) {
+      load_step(lane_block(pt_row, first, n_c, lane));
+      const int blk1 = kSteps > 1 ? lane_block(pt_row, first + 16, n_c, lane) : 0;
+      QD = q_digits(q + (row0 + col) * kDim, grp);
+      run(first, IntTag<kSteps>{}, blk1);
+    } else {
+      QD = q_digits(q + (row0 + col) * kDim, grp);
+#pragma unroll 1
+      for (int t = 0; t < n_steps; ++t) {
+        load_step(lane_block(pt_row, first + 16 * t, n_c, lane));
+        run(first + 16 * t, IntTag<1>{}, 0);
+      }
     }
   }
   // ---- block partial (max, sum exp) per head over its pages, log2 domain: lane
@@ -984,10 +1009,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // register Q of lane (grp, col) holds a(page 4 Q + grp, head col % 4): the
 // centroid of the lanes with grp == col / 4, which keep the result.
 // ---------------------------------------------------------------------------
-template <int N>
-struct IntTag {
-  static constexpr int value = N;
-};
 
 // Block of page min(page0 + (lane & 15), n_c - 1): always a valid page of the sequence.
 __device__ __forceinline__ int lane_block_clamped(const int32_t* __restrict__ pt_row, int page0,
