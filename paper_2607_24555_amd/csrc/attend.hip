@@ -186,7 +186,10 @@ struct SelTable {
   float* out_sel_lse;
 };
 
-template <bool kSelect>
+// kPPW > 0: every wave owns exactly kPPW list entries and keeps up to four
+// pages in flight (fully unrolled, so each wait covers one page); kPPW == 0: any
+// count, one page in flight ahead of the one being used.
+template <bool kSelect, int kPPW>
 __global__ __launch_bounds__(256) void attend_mfma_kernel(
     int H_q, int H_kv, int max_pages, int k_list, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
@@ -249,61 +252,86 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
 #pragma unroll
   for (int t = 0; t < 8; ++t) o[t] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
 
-  if (n > 0) {
-    int id = page_at(t_begin);
-    PageRegs cur;
-    {
-      const long b = blk_at(t_begin, id);
-      load_page(cur, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
+  // one page of the list (id < 0: an empty entry, nothing to add)
+  auto use_page = [&](const PageRegs& cur, int id) {
+    if (id >= 0) {
+      const int valid = min(kPage, L - id * kPage);
+      f4v st = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(cur.k[kb]), as_bf8(qb[kb]), st, 0, 0, 0);
+      float z[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) z[j] = (4 * r4 + j < valid) ? st[j] * zs : -INFINITY;
+      const float pm = rows_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
+      const float mn = fmaxf(m, pm);
+      const float sc = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - mn);
+      float p[4], ps = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        p[j] = (z[j] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(z[j] - mn);
+        ps += p[j];
+      }
+      l = l * sc + rows_sum(ps);
+      m = mn;
+      uint32_t hi[4], lo[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        hi[j] = bf16_rne(p[j]);
+        lo[j] = bf16_rne(p[j] - __uint_as_float(hi[j] << 16));
+      }
+      const s4v bh = __builtin_bit_cast(s4v, make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16)));
+      const s4v bl = __builtin_bit_cast(s4v, make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)));
+#pragma unroll
+      for (int t8 = 0; t8 < 8; ++t8) {
+        o[t8] *= sc;
+        const uint32_t a01 = half_of(cur.v[0], t8) | (half_of(cur.v[1], t8) << 16);
+        const uint32_t a23 = half_of(cur.v[2], t8) | (half_of(cur.v[3], t8) << 16);
+        const s4v a = __builtin_bit_cast(s4v, make_uint2(a01, a23));
+        o[t8] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bh, o[t8], 0, 0, 0);
+        o[t8] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bl, o[t8], 0, 0, 0);
+      }
     }
-    for (int t = t_begin; t < t_end; ++t) {
-      // prefetch the next entry (a valid page stands in for an empty one)
-      const int id_next = page_at(t + 1);
-      PageRegs nxt;
-      if (t + 1 < t_end) {
-        const long b = blk_at(t + 1, id_next);
-        load_page(nxt, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
+  };
+  // loads list entry t into P (a valid page stands in for an empty entry)
+  auto load_entry = [&](PageRegs& P, int t) {
+    const int id = page_at(t);
+    const long b = blk_at(t, id);
+    load_page(P, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
+    return id;
+  };
+
+  if (n > 0) {
+    if constexpr (kPPW > 0) {
+      constexpr int D = kPPW < 4 ? kPPW : 4;
+      PageRegs buf[D];
+      int ids[D];
+#pragma unroll
+      for (int j = 0; j < D; ++j) ids[j] = load_entry(buf[j], t_begin + j);
+#pragma unroll
+      for (int i = 0; i < kPPW; ++i) {
+        use_page(buf[i % D], ids[i % D]);
+        if (i + D < kPPW) ids[i % D] = load_entry(buf[i % D], t_begin + i + D);
       }
-      if (id >= 0) {
-        const int valid = min(kPage, L - id * kPage);
-        f4v st = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-          st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(cur.k[kb]), as_bf8(qb[kb]), st, 0, 0, 0);
-        float z[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) z[j] = (4 * r4 + j < valid) ? st[j] * zs : -INFINITY;
-        const float pm = rows_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
-        const float mn = fmaxf(m, pm);
-        const float sc = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - mn);
-        float p[4], ps = 0.0f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          p[j] = (z[j] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(z[j] - mn);
-          ps += p[j];
-        }
-        l = l * sc + rows_sum(ps);
-        m = mn;
-        uint32_t hi[4], lo[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          hi[j] = bf16_rne(p[j]);
-          lo[j] = bf16_rne(p[j] - __uint_as_float(hi[j] << 16));
-        }
-        const s4v bh = __builtin_bit_cast(s4v, make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16)));
-        const s4v bl = __builtin_bit_cast(s4v, make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)));
-#pragma unroll
-        for (int t8 = 0; t8 < 8; ++t8) {
-          o[t8] *= sc;
-          const uint32_t a01 = half_of(cur.v[0], t8) | (half_of(cur.v[1], t8) << 16);
-          const uint32_t a23 = half_of(cur.v[2], t8) | (half_of(cur.v[3], t8) << 16);
-          const s4v a = __builtin_bit_cast(s4v, make_uint2(a01, a23));
-          o[t8] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bh, o[t8], 0, 0, 0);
-          o[t8] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bl, o[t8], 0, 0, 0);
-        }
+    } else {
+      int id = page_at(t_begin);
+      PageRegs cur;
+      {
+        const long b = blk_at(t_begin, id);
+        load_page(cur, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
       }
-      id = id_next;
-      cur = nxt;
+      for (int t = t_begin; t < t_end; ++t) {
+        // prefetch the next entry (a valid page stands in for an empty one)
+        const int id_next = page_at(t + 1);
+        PageRegs nxt;
+        if (t + 1 < t_end) {
+          const long b = blk_at(t + 1, id_next);
+          load_page(nxt, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
+        }
+        use_page(cur, id);
+        id = id_next;
+        cur = nxt;
+      }
     }
   }
   if constexpr (kSelect) {
@@ -406,6 +434,28 @@ void launch_typed(const locks_cfg_t& c, const void* q, const void* k_cache, cons
                      pages_per_split, n_splits, partial);
 }
 
+// bf16 MFMA kernel with the page count per wave fixed at compile time where the
+// list is split into 1, 2, 4 or 8 entries per wave.
+template <bool kSelect>
+void launch_mfma(const locks_cfg_t& c, dim3 grid, hipStream_t st, const uint16_t* q,
+                 const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* page_table,
+                 const int32_t* seq_lens, const int32_t* page_ids, int pages_per_split,
+                 int n_splits, float* partial, SelTable tb) {
+  const int ppw = pages_per_split % 4 == 0 ? pages_per_split / 4 : 0;
+#define LOCKS_ATTEND_MFMA(P)                                                                   \
+  hipLaunchKernelGGL((attend_mfma_kernel<kSelect, P>), grid, dim3(256), 0, st, c.num_q_heads,   \
+                     c.num_kv_heads, c.max_pages_per_seq, page_budget(c), q, k_cache, v_cache,  \
+                     page_table, seq_lens, page_ids, pages_per_split, n_splits, partial, tb)
+  switch (ppw) {
+    case 1: LOCKS_ATTEND_MFMA(1); break;
+    case 2: LOCKS_ATTEND_MFMA(2); break;
+    case 4: LOCKS_ATTEND_MFMA(4); break;
+    case 8: LOCKS_ATTEND_MFMA(8); break;
+    default: LOCKS_ATTEND_MFMA(0); break;
+  }
+#undef LOCKS_ATTEND_MFMA
+}
+
 }  // namespace
 
 hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cache,
@@ -414,12 +464,10 @@ hipError_t launch_attend(const locks_cfg_t& c, const void* q, const void* k_cach
                          float* partial, float* out, float* out_lse, hipStream_t st) {
   const bool qb = c.q_dtype == LOCKS_BF16, kb = c.kv_dtype == LOCKS_BF16;
   if (qb && kb)
-    hipLaunchKernelGGL(attend_mfma_kernel<false>, dim3(n_splits, c.num_kv_heads, c.num_seqs),
-                       dim3(256), 0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                       page_budget(c), static_cast<const uint16_t*>(q),
-                       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache),
-                       page_table, seq_lens, page_ids, pages_per_split, n_splits, partial,
-                       SelTable{});
+    launch_mfma<false>(c, dim3(n_splits, c.num_kv_heads, c.num_seqs), st,
+                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
+                       static_cast<const uint16_t*>(v_cache), page_table, seq_lens, page_ids,
+                       pages_per_split, n_splits, partial, SelTable{});
   else if (qb)
     launch_typed<uint16_t, float>(c, q, k_cache, v_cache, page_table, seq_lens, page_ids,
                                   pages_per_split, n_splits, partial, st);
@@ -445,11 +493,10 @@ hipError_t launch_attend_select(const locks_cfg_t& c, const void* q, const void*
                                 int pages_per_split, int n_splits, float* partial, float* out,
                                 float* out_lse, hipStream_t st) {
   const SelTable tb{sb, select_fast_rows(c), select_fast_width(c), s_hat, lay, out_ids, out_sel_lse};
-  hipLaunchKernelGGL((attend_mfma_kernel<true>), dim3(n_splits, c.num_kv_heads, c.num_seqs), dim3(256),
-                     0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq, page_budget(c),
-                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
-                     static_cast<const uint16_t*>(v_cache), page_table, seq_lens, nullptr,
-                     pages_per_split, n_splits, partial, tb);
+  launch_mfma<true>(c, dim3(n_splits, c.num_kv_heads, c.num_seqs), st,
+                    static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
+                    static_cast<const uint16_t*>(v_cache), page_table, seq_lens, nullptr,
+                    pages_per_split, n_splits, partial, tb);
   hipLaunchKernelGGL(merge_kernel, dim3(c.num_q_heads, c.num_seqs), dim3(kDim), 0, st,
                      c.num_q_heads, n_splits, partial, out, out_lse);
   return hipGetLastError();

@@ -423,7 +423,7 @@ struct UnionLds {
 // Requires used * width <= 64 * NW * NK and used <= 256.  Called by every
 // thread of an NW-wave block; ends with a barrier.
 template <int NK, int NW>
-__device__ void union_table(int k, int n, int used, int width, const uint32_t* __restrict__ ck,
+__device__ __forceinline__ void union_table(int k, int n, int used, int width, const uint32_t* __restrict__ ck,
                             const int32_t* __restrict__ ci, const int32_t* __restrict__ cb,
                             const uint32_t* __restrict__ sat, const uint32_t* __restrict__ keys,
                             const int32_t* __restrict__ pt_row, int32_t* s_tab, int32_t* s_blk,
