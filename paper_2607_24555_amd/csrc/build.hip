@@ -15,6 +15,8 @@ namespace locks {
 namespace {
 
 constexpr int kItems = 4;         // items per block
+
+typedef float f4 __attribute__((ext_vector_type(4)));
 constexpr int kRow = 20;          // LDS row stride of A and U: 16-byte aligned, conflict-free
 constexpr int kMaxSweeps = 12;
 constexpr float kOffRel = 1e-10f;   // Jacobi stop: off-diagonal / diagonal mass
@@ -31,6 +33,11 @@ __device__ __forceinline__ int partner(int t, int i) {
   if (p < 0) p += 15;
   return p;
 }
+
+// The block is a single wave, whose LDS operations complete in issue order: a
+// barrier inside the rotation rounds only has to keep the compiler from moving
+// LDS accesses across it.
+__device__ __forceinline__ void wave_sync() { __builtin_amdgcn_wave_barrier(); }
 
 __device__ __forceinline__ void ld_row(const float* p, float (&r)[kPage]) {
 #pragma unroll
@@ -151,32 +158,34 @@ __global__ __launch_bounds__(64) void build_kernel(
   }
   __syncthreads();
 
-  // ---- Gram of the deviations: entry (i, j) sums d_i[c] d_j[c] over c = 0..127
-  //      in order on both lanes, so the Gram is exactly symmetric; this lane's
-  //      deviation row is held 32 columns at a time
+  // ---- Gram of the deviations on the matrix cores, one item at a time: lane
+  //      (grp, li) supplies deviation row li at columns 32 grp + m as both
+  //      operands of 32 fp32 MFMAs 16x16x4, which leave G[4 grp + jj][li] in
+  //      register jj; the upper triangle is then mirrored so A is exactly
+  //      symmetric
   {
-    float g[kPage];
+    f4 acc[kItems];
 #pragma unroll
-    for (int jj = 0; jj < kPage; ++jj) g[jj] = 0.0f;
-    for (int cb = 0; cb < kDim; cb += 32) {
-      float dl[32];
-#pragma unroll
-      for (int c = 0; c < 32; ++c) dl[c] = load_elem(&sK[grp][li][0], cb + c) - sMu[grp][cb + c];
-#pragma unroll 4
-      for (int jj = 0; jj < kPage; ++jj) {
-        float acc = g[jj];
-#pragma unroll
-        for (int c = 0; c < 32; ++c)
-          acc = fmaf(dl[c], load_elem(&sK[grp][jj][0], cb + c) - sMu[grp][cb + c], acc);
-        g[jj] = acc;
+    for (int it = 0; it < kItems; ++it) {
+      acc[it] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 8
+      for (int m = 0; m < 32; ++m) {
+        const int c = 32 * grp + m;
+        const float d = load_elem(&sK[it][li][0], c) - sMu[it][c];
+        acc[it] = __builtin_amdgcn_mfma_f32_16x16x4f32(d, d, acc[it], 0, 0, 0);
       }
     }
     __syncthreads();  // every lane is done with the key rows: A and U reuse their LDS
 #pragma unroll
-    for (int jj = 0; jj < kPage; ++jj) {
-      sA[grp][li][jj] = g[jj];
-      sU[grp][li][jj] = (li == jj) ? 1.0f : 0.0f;
-    }
+    for (int it = 0; it < kItems; ++it)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) sA[it][4 * grp + jj][li] = acc[it][jj];
+#pragma unroll
+    for (int jj = 0; jj < kPage; ++jj) sU[grp][li][jj] = (li == jj) ? 1.0f : 0.0f;
+    __syncthreads();
+#pragma unroll
+    for (int jj = 0; jj < kPage; ++jj)
+      if (jj < li) sA[grp][li][jj] = sA[grp][jj][li];
   }
   __syncthreads();
 
@@ -208,13 +217,16 @@ __global__ __launch_bounds__(64) void build_kernel(
       const float app = sA[grp][P][P], aqq = sA[grp][Q][Q], apq = sA[grp][P][Q];
       float c = 1.0f, sn = 0.0f;
       if (apq != 0.0f) {
-        const float theta = (aqq - app) / (2.0f * apq);
-        const float tt = copysignf(1.0f, theta) / (fabsf(theta) + sqrtf(fmaf(theta, theta, 1.0f)));
-        c = 1.0f / sqrtf(fmaf(tt, tt, 1.0f));
+        // hardware reciprocal and square roots (about 1 ulp): the angle need
+        // not be exact, only c^2 + s^2 = 1, which holds to a few ulp
+        const float theta = (aqq - app) * __builtin_amdgcn_rcpf(2.0f * apq);
+        const float tt = copysignf(1.0f, theta) *
+                         __builtin_amdgcn_rcpf(fabsf(theta) + __builtin_amdgcn_sqrtf(fmaf(theta, theta, 1.0f)));
+        c = __builtin_amdgcn_rsqf(fmaf(tt, tt, 1.0f));
         sn = tt * c;
       }
       if (li == P) sCS[grp][P] = make_float2(c, sn);
-      __syncthreads();
+      wave_sync();
       float a[kPage], b[kPage], u[kPage];
       ld_row(&sA[grp][li][0], a);
       ld_row(&sA[grp][p][0], b);
@@ -238,10 +250,10 @@ __global__ __launch_bounds__(64) void build_kernel(
       const bool lead = li == P;
 #pragma unroll
       for (int m = 0; m < kPage; ++m) a[m] = lead ? (c * a[m] - sn * b[m]) : (sn * b[m] + c * a[m]);
-      __syncthreads();
+      wave_sync();
       st_row(&sA[grp][li][0], a);
       st_row(&sU[grp][li][0], u);
-      __syncthreads();
+      wave_sync();
     }
   }
 
