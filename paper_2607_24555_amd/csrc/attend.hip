@@ -204,6 +204,14 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c16 = lane & 15, r4 = lane >> 4;
   const int G = H_q / H_kv;
+  // the selection survivors are requested before the sequence length is known
+  UnionRegs<kUnionNK> UR;
+  if constexpr (kSelect) {
+    const long unit = (long)s * H_kv + h;
+    const long rb = unit * tb.n_rows * tb.width;
+    union_load<kUnionNK, 4>(UR, tb.n_rows, tb.width, tb.sb.cand_key + rb, tb.sb.cand_idx + rb,
+                            tb.sb.cand_blk + rb, tb.sb.sat + unit * tb.n_rows);
+  }
   const int L = seq_lens[s];
   const int n = (L + kPage - 1) / kPage;
   const float zs = kLog2e / sqrtf((float)kDim);
@@ -221,11 +229,8 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
   if constexpr (kSelect) {
     const long unit = (long)s * H_kv + h;
     const int used = n > k_list ? (n - 2) / kFastChunk + 1 : 0;
-    const long rb = unit * tb.n_rows * tb.width;
-    union_table<kUnionNK, 4>(k_list, n, used, tb.width, tb.sb.cand_key + rb, tb.sb.cand_idx + rb,
-                             tb.sb.cand_blk + rb, tb.sb.sat + unit * tb.n_rows,
-                             tb.sb.keys + unit * max_pages, page_table + (long)s * max_pages,
-                             s_tab, s_blk, unionL);
+    union_table_from<kUnionNK, 4>(UR, k_list, n, used, tb.width, tb.sb.keys + unit * max_pages,
+                                  page_table + (long)s * max_pages, s_tab, s_blk, unionL);
     ids = s_tab;
   }
   auto page_at = [&](int t) -> int {

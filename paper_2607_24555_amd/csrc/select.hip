@@ -380,15 +380,17 @@ __global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
   __shared__ HistLds<kChunkWaves> HL;
   const int chunk = blockIdx.x, h = blockIdx.y, s = blockIdx.z, tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int Ls = seq_lens[s];
-  const int n = (Ls + kPage - 1) / kPage;
+  const int Ls = seq_lens[s];  // used after the loads below are issued
   const int G = H_q / H_kv;
   const int K = k - 2;
   const int p0 = chunk * kFastChunk;
-  if (K <= 0 || n <= k || p0 > n - 2) return;
+  if (K <= 0) return;
   const long unit = (long)s * H_kv + h;
   const long row0 = (long)s * H_q + (long)h * G;
   const float* base = s_hat + lay.base(s, h);
+  // The loads below do not wait for the sequence length: positions are clamped
+  // to the page table's width, and values of positions outside 1 .. n - 2 are
+  // never used.
   // contiguous layout: float4 number f = kT i + tid of the chunk's span holds
   // heads 4 (f % LP) .. +3 of page p0 + f / LP; the LP lanes of a page are
   // adjacent.  These loads are issued before Z_g is reduced.
@@ -398,16 +400,16 @@ __global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
 #pragma unroll
     for (int i = 0; i < per; ++i) {
       const int po = (i * kT + tid) / LP;
-      const long j = min(max(p0 + po, 1), n - 2);
+      const long j = min(p0 + po, max_pages - 1);
       v[i] = *reinterpret_cast<const float4*>(base + j * kG + 4 * (tid % LP));
     }
   }
-  // physical blocks of this thread's key positions (pages past the end reuse n - 1)
+  // physical blocks of this thread's key positions
   int32_t blk[kChunkNK];
 #pragma unroll
   for (int u = 0; u < kChunkNK; ++u) {
     const int j = p0 + (wave * kChunkNK + u) * 64 + lane;
-    blk[u] = page_table[(long)s * max_pages + min(j, n - 1)];
+    blk[u] = page_table[(long)s * max_pages + min(j, max_pages - 1)];
   }
   {
     constexpr int kPer = 16;  // partials per thread and pass (16 threads per head)
@@ -443,6 +445,8 @@ __global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
     if (g < G && sub == 0) s_lz2[g] = m + __builtin_amdgcn_logf(l);
   }
   __syncthreads();
+  const int n = (Ls + kPage - 1) / kPage;
+  if (n <= k || p0 > n - 2) return;  // uniform across the block
   if constexpr (kG != 0) {
     const int q = tid % LP;
     float lzq[4];

@@ -410,6 +410,35 @@ struct UnionLds {
   int fallback;
 };
 
+// The survivor registers of the union, loaded before the sequence length is known
+// (rows x width entries of which the first used x width are valid).
+template <int NK>
+struct UnionRegs {
+  uint32_t key[NK];
+  int32_t idx[NK], blk[NK];
+  uint32_t tr[4];
+};
+
+template <int NK, int NW>
+__device__ __forceinline__ void union_load(UnionRegs<NK>& R, int rows, int width,
+                                           const uint32_t* __restrict__ ck,
+                                           const int32_t* __restrict__ ci,
+                                           const int32_t* __restrict__ cb,
+                                           const uint32_t* __restrict__ sat) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int N = rows * width;
+#pragma unroll
+  for (int u = 0; u < NK; ++u) {
+    const int e = (wave * NK + u) * 64 + lane;
+    const int ec = e < N ? e : N - 1;
+    R.key[u] = ck[ec];
+    R.idx[u] = ci[ec];
+    R.blk[u] = cb[ec];
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) R.tr[u] = sat[min(lane + 64 * u, rows - 1)];
+}
+
 // Page table of one (sequence, KV head) with n pages and budget k:
 // s_tab[0] = 0 (sink), s_tab[1 .. k-2] = the k - 2 candidates of largest key in
 // ascending page order, s_tab[k-1] = n - 1 (recent); with n <= k every page,
@@ -421,13 +450,13 @@ struct UnionLds {
 // survivors is exact unless some chunk was
 // truncated at or above it; then the whole sequence is cut again from keys.
 // Requires used * width <= 64 * NW * NK and used <= 256.  Called by every
-// thread of an NW-wave block; ends with a barrier.
+// thread of an NW-wave block, with R from union_load; ends with a barrier.
 template <int NK, int NW>
-__device__ __forceinline__ void union_table(int k, int n, int used, int width, const uint32_t* __restrict__ ck,
-                            const int32_t* __restrict__ ci, const int32_t* __restrict__ cb,
-                            const uint32_t* __restrict__ sat, const uint32_t* __restrict__ keys,
-                            const int32_t* __restrict__ pt_row, int32_t* s_tab, int32_t* s_blk,
-                            UnionLds<NW>& U) {
+__device__ __forceinline__ void union_table_from(UnionRegs<NK>& R, int k, int n, int used,
+                                                 int width, const uint32_t* __restrict__ keys,
+                                                 const int32_t* __restrict__ pt_row,
+                                                 int32_t* s_tab, int32_t* s_blk,
+                                                 UnionLds<NW>& U) {
   constexpr int kT = 64 * NW;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int K = k - 2;
@@ -447,34 +476,21 @@ __device__ __forceinline__ void union_table(int k, int n, int used, int width, c
   }
   if (K > 0) {
     const int N = used * width;
-    uint32_t key[NK];
-    int32_t idx[NK], blk[NK];
 #pragma unroll
-    for (int u = 0; u < NK; ++u) {
-      const int e = (wave * NK + u) * 64 + lane;
-      const int ec = e < N ? e : N - 1;
-      key[u] = ck[ec];
-      idx[u] = ci[ec];
-      blk[u] = cb[ec];
-    }
-    uint32_t tr[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) tr[u] = sat[min(lane + 64 * u, used - 1)];
-#pragma unroll
-    for (int u = 0; u < NK; ++u) key[u] = (wave * NK + u) * 64 + lane < N ? key[u] : 0u;
-    const WaveCut cut = block_hist_cut<NK, NW>(key, K, U.H, U.L);
+    for (int u = 0; u < NK; ++u) R.key[u] = (wave * NK + u) * 64 + lane < N ? R.key[u] : 0u;
+    const WaveCut cut = block_hist_cut<NK, NW>(R.key, K, U.H, U.L);
     if (wave == 0) {
       bool bad = false;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) bad |= lane + 64 * u < used && tr[u] != 0u && tr[u] >= cut.T;
+      for (int u = 0; u < 4; ++u) bad |= lane + 64 * u < used && R.tr[u] != 0u && R.tr[u] >= cut.T;
       const bool any = __ballot(bad) != 0ull;
       if (lane == 0) U.fallback = any;
     }
     __syncthreads();
     if (!U.fallback) {
-      block_emit<NK, NW>(key, cut, U.L, [&](int u, int slot) {
-        s_tab[1 + slot] = idx[u];
-        s_blk[1 + slot] = blk[u];
+      block_emit<NK, NW>(R.key, cut, U.L, [&](int u, int slot) {
+        s_tab[1 + slot] = R.idx[u];
+        s_blk[1 + slot] = R.blk[u];
       });
     } else {
       exact_cut_global<NW>(keys, n - 1, K, cut.T, s_tab + 1, U.B);  // pages 0 .. n - 2
@@ -482,6 +498,18 @@ __device__ __forceinline__ void union_table(int k, int n, int used, int width, c
     }
   }
   __syncthreads();
+}
+
+// union_load and union_table_from in one call.
+template <int NK, int NW>
+__device__ __forceinline__ void union_table(int k, int n, int used, int width, const uint32_t* __restrict__ ck,
+                            const int32_t* __restrict__ ci, const int32_t* __restrict__ cb,
+                            const uint32_t* __restrict__ sat, const uint32_t* __restrict__ keys,
+                            const int32_t* __restrict__ pt_row, int32_t* s_tab, int32_t* s_blk,
+                            UnionLds<NW>& U) {
+  UnionRegs<NK> R;
+  if (n > k && used > 0) union_load<NK, NW>(R, used, width, ck, ci, cb, sat);
+  union_table_from<NK, NW>(R, k, n, used, width, keys, pt_row, s_tab, s_blk, U);
 }
 
 }  // namespace locks
