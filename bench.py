@@ -71,10 +71,10 @@ SCAN_SOURCES = ("paper_2607_24555_amd/csrc/scan.hip", "paper_2607_24555_amd/csrc
 SCAN_TRAFFIC = {
     # workload: (sha256 of SCAN_SOURCES, FETCH_SIZE KiB, WRITE_SIZE KiB,
     #            copy FETCH factor, copy WRITE factor, profile file)
-    "1m": ("96d60d6dac6c4c4c", 56075.2, 9330.2, 0.500016, 1.0, "profiles/scan_1m_hbm_counters.md"),
-    "128k": ("96d60d6dac6c4c4c", 214623.7, 8603.3, 0.500016, 1.0, "profiles/scan_128k_hbm_counters.md"),
-    "128k-r2": ("96d60d6dac6c4c4c", 86662.3, 8882.0, 0.500015, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
-    "reasoning": ("96d60d6dac6c4c4c", 194299.8, 21036.9, 0.500016, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
+    "1m": ("fd1e09a254046244", 55525.3, 9937.2, 0.500015, 1.0, "profiles/scan_1m_hbm_counters.md"),
+    "128k": ("fd1e09a254046244", 215206.5, 8707.0, 0.500016, 1.0, "profiles/scan_128k_hbm_counters.md"),
+    "128k-r2": ("fd1e09a254046244", 86704.3, 8898.4, 0.500015, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
+    "reasoning": ("fd1e09a254046244", 194574.1, 21041.8, 0.500016, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
 }
 
 
