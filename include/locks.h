@@ -12,9 +12,10 @@
  *
  * Conventions shared by every call
  *  - All tensor arguments are DEVICE pointers owned by the caller; the library
- *    never allocates, frees, synchronises or throws.  Every call enqueues its
- *    kernels on `stream` (a hipStream_t; NULL = the default stream) and returns a
- *    status immediately.
+ *    never allocates device memory, frees, synchronises or throws.  Every call
+ *    enqueues its kernels on `stream` (a hipStream_t; NULL = the default stream;
+ *    locks_decode_step may fork part of its work to a side stream, see there)
+ *    and returns a status immediately.
  *  - Host-side checks (configuration, null pointers, workspace size) run before
  *    any launch; a failing check returns an error and launches nothing.
  *    Device-resident values (page-table entries, sequence lengths) are trusted:
@@ -191,7 +192,13 @@ int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cach
  * first the summaries of the n_build listed (seq, page) pairs are built (pages
  * that completed this step; n_build = 0 builds nothing, build_list may then be
  * NULL), then locks_select, then locks_sparse_attend over the selected table, all
- * on `stream`.  Outputs as in those calls. */
+ * ordered after earlier work on `stream` and before later work on it.  With bf16
+ * q and KV and a listed page that is the last complete page of its sequence, the
+ * build of those pages runs on `stream` beside the scan of the others, which the
+ * library enqueues on a side stream of its own (one per device, created on first
+ * use and kept until the process ends), forked from and joined back to `stream`
+ * by events; such calls on one device are serialised on the host.  Outputs as in
+ * those calls. */
 int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache,
                       const void* v_cache, const int32_t* page_table,
                       const int32_t* seq_lens, void* summaries,

@@ -1,6 +1,8 @@
 // Host side of the C ABI declared in include/locks.h: argument validation,
 // workspace planning and stream-ordered launches.  No allocation, no
 // synchronisation, no exceptions.
+#include <mutex>
+
 #include "locks_internal.h"
 
 namespace locks {
@@ -39,6 +41,8 @@ struct Ws {
   float2* part;
   SelectBufs sel;
   float* attn;
+  int32_t* sl_scan;
+  float2* part_x;
 };
 
 Ws carve(void* ws, const WsPlan& p) {
@@ -49,7 +53,33 @@ Ws carve(void* ws, const WsPlan& p) {
                        reinterpret_cast<uint32_t*>(b + p.sat_off),
                        reinterpret_cast<uint32_t*>(b + p.keys_off), p.n_chunks};
   return Ws{reinterpret_cast<float*>(b + p.s_hat_off), reinterpret_cast<float2*>(b + p.part_off),
-            sel, reinterpret_cast<float*>(b + p.attn_off)};
+            sel, reinterpret_cast<float*>(b + p.attn_off), reinterpret_cast<int32_t*>(b + p.slscan_off),
+            reinterpret_cast<float2*>(b + p.partx_off)};
+}
+
+// The side stream of a decode step's overlapped build (one per device, with its
+// fork and join events), created on first use and kept until the process ends.
+struct SideStream {
+  hipStream_t st = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_side_mu;  // also serialises the fork / join enqueues of one step
+SideStream g_side[kMaxDevices];
+
+hipError_t side_stream(SideStream** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  SideStream& ss = g_side[dev];
+  if (!ss.st) {
+    if ((e = hipStreamCreateWithFlags(&ss.st, hipStreamNonBlocking)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming)) != hipSuccess) return e;
+  }
+  *out = &ss;
+  return hipSuccess;
 }
 
 int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
@@ -101,6 +131,8 @@ WsPlan plan_workspace(const locks_cfg_t& c) {
   p.sat_off = take(S * Hkv * rows * sizeof(uint32_t));
   p.keys_off = take(S * Hkv * mp * sizeof(uint32_t));
   p.attn_off = take(S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float));
+  p.slscan_off = take(S * sizeof(int32_t));
+  p.partx_off = take(S * Hq * sizeof(float2));
   p.total = off;
   return p;
 }
@@ -238,11 +270,6 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (n_build > 0) {
-    rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
-                                 summaries, nullptr, nullptr, nullptr, nullptr, st));
-    if (rc) return rc;
-  }
   const WsPlan p = plan_workspace(*cfg);
   const Ws w = carve(ws, p);
   const int k = page_budget(*cfg);
@@ -251,14 +278,49 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
   if (attend_select_fused(*cfg)) {
     // scan -> per-chunk selection -> attention whose blocks merge the table
     const SHatLayout lay = shat_head_minor(*cfg);
-    rc = hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, w.s_hat, lay, w.part, st));
-    if (rc) return rc;
+    const float2* part_x = nullptr;
+    if (n_build > 0) {
+      // Listed pages that are the last complete page of their sequence (the
+      // pages that just filled) are built and scored on `stream` while a side
+      // stream, forked before them, builds the other listed pages and then scans
+      // everything but those last pages.  The builds' few blocks are dispatched
+      // first and stay resident beside the scan (the fork costs the side stream
+      // a few microseconds); `stream` joins the side stream before the selection.
+      const BuildStep bs{w.sl_scan, w.part_x, q, cfg->q_dtype == LOCKS_BF16, cfg->num_q_heads,
+                         w.s_hat, lay};
+      std::lock_guard<std::mutex> lock(g_side_mu);
+      SideStream* side = nullptr;
+      hipError_t e = side_stream(&side);
+      if (e == hipSuccess) e = hipEventRecord(side->fork, st);
+      if (e == hipSuccess) e = hipStreamWaitEvent(side->st, side->fork, 0);
+      if (e == hipSuccess)
+        e = launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false, summaries,
+                         nullptr, nullptr, nullptr, nullptr, st, kBuildLast, &bs);
+      if (e == hipSuccess)
+        e = launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false, summaries,
+                         nullptr, nullptr, nullptr, nullptr, side->st, kBuildInner, &bs);
+      if (e == hipSuccess)
+        e = launch_scan(*cfg, q, summaries, page_table, w.sl_scan, w.s_hat, lay, w.part, side->st);
+      if (e == hipSuccess) e = hipEventRecord(side->join, side->st);
+      if (e == hipSuccess) e = hipStreamWaitEvent(st, side->join, 0);
+      if ((rc = hip_status(e))) return rc;
+      part_x = w.part_x;
+    } else {
+      rc = hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, w.s_hat, lay, w.part,
+                                  st));
+      if (rc) return rc;
+    }
     rc = hip_status(launch_select_chunks(*cfg, page_table, seq_lens, w.s_hat, lay, w.part, w.sel,
-                                         st));
+                                         st, part_x, w.sl_scan));
     if (rc) return rc;
     return hip_status(launch_attend_select(*cfg, q, k_cache, v_cache, page_table, seq_lens, w.sel,
                                            w.s_hat, lay, out_page_ids, out_sel_lse,
                                            pps, splits, w.attn, out, out_lse, st));
+  }
+  if (n_build > 0) {
+    rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
+                                 summaries, nullptr, nullptr, nullptr, nullptr, st));
+    if (rc) return rc;
   }
   rc = select_impl(cfg, q, summaries, page_table, seq_lens, out_page_ids, out_sel_lse, nullptr, ws,
                    st);

@@ -78,13 +78,20 @@ __device__ __forceinline__ uint16_t f16_bits(float s) {
   return *reinterpret_cast<uint16_t*>(&h);
 }
 
-template <typename KT, bool kFactors>
+// kMode (BuildMode): kBuildAll builds every listed (or complete) page; kBuildInner
+// skips the pages that are the last complete page of their sequence, and its block 0
+// instead prepares the scan of the step (scan lengths without those pages);
+// kBuildLast builds only those pages and scores them for the step's query (Eq. 1
+// on the decoded summary), writing their page scores and one extra (max, sum)
+// partial per query head of their sequence.
+template <typename KT, bool kFactors, int kMode>
 __global__ __launch_bounds__(64) void build_kernel(
     int S, int H_kv, int max_pages, int r, const KT* __restrict__ k_cache,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ build_list, int n_items, int all_pages,
     uint8_t* __restrict__ summaries, float* __restrict__ mu_out, float* __restrict__ basis_out,
-    float* __restrict__ coef_out, float* __restrict__ sigma2_out) {
+    float* __restrict__ coef_out, float* __restrict__ sigma2_out, BuildStep bs) {
+  constexpr bool kScore = kMode == kBuildLast;
   // raw key rows (bf16 or fp32 as stored; deviations are formed on the fly as
   // float(k) - mu, the same fp32 value for every use) share LDS with the Jacobi
   // matrices A and U, which are written once the Gram is complete
@@ -99,10 +106,29 @@ __global__ __launch_bounds__(64) void build_kernel(
   __shared__ float2 sCS[kItems][kPage];
   __shared__ float sLam[kItems][kPage];
   __shared__ int sOrd[kItems][kPage];
+  // quantised basis columns (packed codes, scales) and projections of the scored pages
+  __shared__ uint32_t sVw[kScore ? kItems : 1][kScore ? kMaxRank : 1][kScore ? kPage : 1];
+  __shared__ float sVs[kScore ? kItems : 1][kScore ? kMaxRank : 1];
+  __shared__ float sP[kScore ? kItems : 1][kScore ? kMaxRank : 1];
+
+  if (kMode == kBuildInner && blockIdx.x == 0) {
+    // scan lengths: a sequence whose last complete page is listed is scanned
+    // without it (kBuildLast scores that page and writes its extra partials)
+    for (int i = threadIdx.x; i < S; i += 64) bs.sl_scan[i] = seq_lens[i];
+    __threadfence();  // the stores above complete before the ones below
+    __syncthreads();
+    for (int e = threadIdx.x; e < n_items; e += 64) {
+      const int ss = build_list[2 * e], jj = build_list[2 * e + 1];
+      if (ss < 0 || ss >= S) continue;
+      const int L = seq_lens[ss];
+      if (jj >= 0 && jj < max_pages && jj == L / kPage - 1) bs.sl_scan[ss] = L - kPage;
+    }
+    return;
+  }
 
   const int grp = threadIdx.x >> 4;
   const int li = threadIdx.x & 15;
-  const long item = (long)blockIdx.x * kItems + grp;
+  const long item = (long)(kMode == kBuildInner ? blockIdx.x - 1 : blockIdx.x) * kItems + grp;
 
   // ---- which (seq, page, KV head) this group builds
   bool active = false;
@@ -120,8 +146,16 @@ __global__ __launch_bounds__(64) void build_kernel(
       s = build_list[2 * e];
       j = build_list[2 * e + 1];
       active = s >= 0 && s < S && j >= 0 && j < max_pages && j < seq_lens[s] / kPage;
+      if (active && kMode != kBuildAll) {
+        const bool last = j == seq_lens[s] / kPage - 1;
+        active = kMode == kBuildLast ? last : !last;
+      }
     }
   }
+  if (!__any(active)) return;  // the block is one wave: nothing to build
+  // the scored builds run beside the scan and lead the step's critical path:
+  // their instructions go first on a shared SIMD
+  if (kMode == kBuildLast) __builtin_amdgcn_s_setprio(3);
   const long blk = active ? (long)page_table[(long)s * max_pages + j] : 0;
 
   // ---- load row li of the page (16-byte loads), track its squared norm
@@ -342,6 +376,10 @@ __global__ __launch_bounds__(64) void build_kernel(
       }
       *reinterpret_cast<uint32_t*>(rec + 64 * l + 4 * li) = word;
       if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * l) = f16_bits(vs);
+      if (kScore) {
+        sVw[grp][l][li] = word;
+        if (li == 0) sVs[grp][l] = vs;
+      }
     }
   }
   __syncthreads();  // sFlip visible to the whole group
@@ -363,10 +401,18 @@ __global__ __launch_bounds__(64) void build_kernel(
   }
 
   // ---- coefficient row li: int8 with its own scale
+  float chat[kScore ? kMaxRank : 1];  // decoded row (scored pages)
   {
     const float cs = f16_scale(cabs, 127.0f);
-    for (int l = 0; l < r; ++l)
-      rec[rec_coef_off(r) + li * r + l] = (uint8_t)(quant(coef_value(l), cs, 127) + 128);
+    for (int l = 0; l < r; ++l) {
+      const int code = quant(coef_value(l), cs, 127);
+      rec[rec_coef_off(r) + li * r + l] = (uint8_t)(code + 128);
+      if (kScore) {
+#pragma unroll
+        for (int u = 0; u < kMaxRank; ++u)
+          if (u == l) chat[u] = (float)code * cs;
+      }
+    }
     *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * (r + li)) = f16_bits(cs);
   }
   // ---- centroid: int8 with one scale
@@ -375,9 +421,70 @@ __global__ __launch_bounds__(64) void build_kernel(
     for (int cc = 0; cc < 8; ++cc) m = fmaxf(m, fabsf(sMu[grp][8 * li + cc]));
     m = group16_max(m);
     const float ms = f16_scale(m, 127.0f);
-    for (int cc = 0; cc < 8; ++cc)
-      rec[rec_mu_off(r) + 8 * li + cc] = (uint8_t)(quant(sMu[grp][8 * li + cc], ms, 127) + 128);
+    float mhat[8];
+    for (int cc = 0; cc < 8; ++cc) {
+      const int code = quant(sMu[grp][8 * li + cc], ms, 127);
+      rec[rec_mu_off(r) + 8 * li + cc] = (uint8_t)(code + 128);
+      mhat[cc] = (float)code * ms;
+    }
     if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * (r + kPage)) = f16_bits(ms);
+    if (kScore) {
+      // ---- page score for each query head of the group (Eq. 1 on the decoded
+      //      summary): z_i = q^T (mu + sum_l c_il v_l) / sqrt d over the 16 tokens
+      //      (token li on this lane), then their log-sum-exp
+      const int G = bs.H_q / H_kv;
+      const long qrow0 = (long)s * bs.H_q + (long)h * G;
+      // this lane's 8 query elements of head g (the next head's are requested
+      // before the current one is used)
+      auto load_q = [&](int g, float (&qv)[8]) {
+#pragma unroll
+        for (int cc = 0; cc < 8; ++cc) {
+          const long qi = (qrow0 + g) * kDim + 8 * li + cc;
+          qv[cc] = bs.q_bf16 ? bf16_bits_to_f32(static_cast<const uint16_t*>(bs.q)[qi])
+                             : static_cast<const float*>(bs.q)[qi];
+        }
+      };
+      float qn[8];
+      load_q(0, qn);
+      for (int g = 0; g < G; ++g) {
+        float qv[8];
+#pragma unroll
+        for (int cc = 0; cc < 8; ++cc) qv[cc] = qn[cc];
+        if (g + 1 < G) load_q(g + 1, qn);
+        float a = 0.0f;
+#pragma unroll
+        for (int cc = 0; cc < 8; ++cc) a = fmaf(qv[cc], mhat[cc], a);
+        a = group16_sum(a);
+        for (int l = 0; l < r; ++l) {
+          const uint32_t word = sVw[grp][l][li];
+          const float vs = sVs[grp][l];
+          float pl = 0.0f;
+#pragma unroll
+          for (int cc = 0; cc < 8; ++cc)
+            pl = fmaf(qv[cc], (float)((int)((word >> (4 * cc)) & 15u) - 8) * vs, pl);
+          pl = group16_sum(pl);
+          if (li == 0) sP[grp][l] = pl;
+        }
+        wave_sync();
+        float z = a;
+        for (int l = 0; l < r; ++l) {
+          float cl = 0.0f;
+#pragma unroll
+          for (int u = 0; u < kMaxRank; ++u)
+            if (u == l) cl = chat[u];
+          z = fmaf(cl, sP[grp][l], z);
+        }
+        z *= 0.08838834764831845f;  // 1 / sqrt(128)
+        const float mx = group16_max(z);
+        const float sm = group16_sum(expf(z - mx));
+        const float shat = mx + logf(sm);
+        if (li == 0) {
+          bs.s_hat[bs.lay.base(s, h) + (long)g * bs.lay.head + (long)j * bs.lay.page] = shat;
+          bs.part_x[qrow0 + g] = make_float2(shat * 1.4426950408889634f, 1.0f);
+        }
+        wave_sync();
+      }
+    }
   }
   // ---- zero padding up to the record stride
   {
@@ -391,39 +498,33 @@ __global__ __launch_bounds__(64) void build_kernel(
 hipError_t launch_build(const locks_cfg_t& c, const void* k_cache, const int32_t* page_table,
                         const int32_t* seq_lens, const int32_t* build_list, int32_t n_items,
                         bool all_pages, void* summaries, float* mu, float* basis, float* coef,
-                        float* sigma2, hipStream_t st) {
+                        float* sigma2, hipStream_t st, BuildMode mode, const BuildStep* step) {
   const long items = all_pages ? (long)c.num_seqs * c.max_pages_per_seq * c.num_kv_heads
                                : (long)n_items * c.num_kv_heads;
   if (items == 0) return hipSuccess;
-  const long blocks = (items + kItems - 1) / kItems;
-  if (blocks > 0x7fffffffL) return hipErrorInvalidConfiguration;
   const bool factors = mu != nullptr;
+  if (mode != kBuildAll && (all_pages || factors || step == nullptr)) return hipErrorInvalidValue;
+  const long blocks = (items + kItems - 1) / kItems + (mode == kBuildInner ? 1 : 0);
+  if (blocks > 0x7fffffffL) return hipErrorInvalidConfiguration;
   const dim3 grid((unsigned)blocks), block(64);
+  const BuildStep bs = step ? *step : BuildStep{};
+#define LOCKS_BUILD(KT, F, M)                                                                  \
+  hipLaunchKernelGGL((build_kernel<KT, F, M>), grid, block, 0, st, c.num_seqs, c.num_kv_heads,  \
+                     c.max_pages_per_seq, c.rank, static_cast<const KT*>(k_cache), page_table,  \
+                     seq_lens, build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu,    \
+                     basis, coef, sigma2, bs)
+#define LOCKS_BUILD_T(KT)                                     \
+  if (factors) LOCKS_BUILD(KT, true, kBuildAll);              \
+  else if (mode == kBuildInner) LOCKS_BUILD(KT, false, kBuildInner); \
+  else if (mode == kBuildLast) LOCKS_BUILD(KT, false, kBuildLast);   \
+  else LOCKS_BUILD(KT, false, kBuildAll)
   if (c.kv_dtype == LOCKS_BF16) {
-    auto* k = static_cast<const uint16_t*>(k_cache);
-    if (factors)
-      hipLaunchKernelGGL((build_kernel<uint16_t, true>), grid, block, 0, st, c.num_seqs,
-                         c.num_kv_heads, c.max_pages_per_seq, c.rank, k, page_table, seq_lens,
-                         build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu, basis,
-                         coef, sigma2);
-    else
-      hipLaunchKernelGGL((build_kernel<uint16_t, false>), grid, block, 0, st, c.num_seqs,
-                         c.num_kv_heads, c.max_pages_per_seq, c.rank, k, page_table, seq_lens,
-                         build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu, basis,
-                         coef, sigma2);
+    LOCKS_BUILD_T(uint16_t);
   } else {
-    auto* k = static_cast<const float*>(k_cache);
-    if (factors)
-      hipLaunchKernelGGL((build_kernel<float, true>), grid, block, 0, st, c.num_seqs,
-                         c.num_kv_heads, c.max_pages_per_seq, c.rank, k, page_table, seq_lens,
-                         build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu, basis,
-                         coef, sigma2);
-    else
-      hipLaunchKernelGGL((build_kernel<float, false>), grid, block, 0, st, c.num_seqs,
-                         c.num_kv_heads, c.max_pages_per_seq, c.rank, k, page_table, seq_lens,
-                         build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu, basis,
-                         coef, sigma2);
+    LOCKS_BUILD_T(float);
   }
+#undef LOCKS_BUILD_T
+#undef LOCKS_BUILD
   return hipGetLastError();
 }
 

@@ -87,6 +87,8 @@ struct WsPlan {
   size_t sat_off;     // uint32 [S][H_kv][rows]           per-chunk truncation key
   size_t keys_off;    // uint32 [S][H_kv][max_pages]      every page's key (exact fallback)
   size_t attn_off;    // float [S][H_q][splits][d + 2]    split-K partials
+  size_t slscan_off;  // int32 [S]                        scan lengths (overlapped builds)
+  size_t partx_off;   // float2 [S][H_q]                  extra partials (overlapped builds)
   size_t total;
   int n_chunks;       // select chunks per sequence (block-level path)
   int n_splits;       // attention splits per (seq, KV head)
@@ -116,10 +118,27 @@ inline int scan_blocks(const locks_cfg_t& c) {
 // ---------------------------------------------------------------- launchers
 // Each returns hipError_t of the launch (hipSuccess on success).
 
+// Builds of a decode step whose listed pages include the last complete page of
+// their sequence: kBuildInner builds the other listed pages and prepares the scan
+// (sl_scan = scan lengths without those last pages); kBuildLast builds the last
+// pages and scores them for q (s_hat entries, and part_x [S][H_q] in the log2
+// domain, valid for the sequences with sl_scan < seq_lens), so it may run beside
+// the scan and needs nothing from kBuildInner.
+enum BuildMode { kBuildAll = 0, kBuildInner = 1, kBuildLast = 2 };
+struct BuildStep {
+  int32_t* sl_scan;
+  float2* part_x;
+  const void* q;
+  int q_bf16;
+  int H_q;
+  float* s_hat;
+  SHatLayout lay;
+};
 hipError_t launch_build(const locks_cfg_t& c, const void* k_cache, const int32_t* page_table,
                         const int32_t* seq_lens, const int32_t* build_list, int32_t n_items,
                         bool all_pages, void* summaries, float* mu, float* basis, float* coef,
-                        float* sigma2, hipStream_t st);
+                        float* sigma2, hipStream_t st, BuildMode mode = kBuildAll,
+                        const BuildStep* step = nullptr);
 
 hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,
                        const int32_t* page_table, const int32_t* seq_lens, float* s_hat,
@@ -141,9 +160,12 @@ bool select_fast_path(const locks_cfg_t& c);
 int select_fast_rows(const locks_cfg_t& c);
 int select_fast_width(const locks_cfg_t& c);
 // Fast path, first half: every page's key and each chunk's top keys (in sb).
+// part_x (nullable): one more (max, sum) partial per query head, [S][H_q], valid
+// for the sequences with sl_scan[s] < seq_lens[s].
 hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* page_table,
                                 const int32_t* seq_lens, const float* s_hat, SHatLayout lay,
-                                const float2* partials, const SelectBufs& sb, hipStream_t st);
+                                const float2* partials, const SelectBufs& sb, hipStream_t st,
+                                const float2* part_x = nullptr, const int32_t* sl_scan = nullptr);
 hipError_t launch_select(const locks_cfg_t& c, const int32_t* page_table, const int32_t* seq_lens,
                          const float* s_hat, SHatLayout lay, const float2* partials,
                          const SelectBufs& sb, int32_t* out_page_ids, float* out_sel_lse,

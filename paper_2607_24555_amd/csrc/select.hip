@@ -372,7 +372,8 @@ template <int kG>  // G when one page's G scores are contiguous (4, 8, 16), else
 __global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
     int H_q, int H_kv, int k, int width, int max_pages, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ page_table, const float* __restrict__ s_hat, SHatLayout lay,
-    const float2* __restrict__ partials, int n_parts, SelectBufs sb, int n_rows) {
+    const float2* __restrict__ partials, int n_parts, SelectBufs sb, int n_rows,
+    const float2* __restrict__ part_x, const int32_t* __restrict__ sl_scan) {
   constexpr int kT = kChunkThreads;
   __shared__ float s_lz2[kMaxGroup];
   __shared__ __align__(16) uint32_t sk[kFastChunk];
@@ -434,6 +435,15 @@ __global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
         ll += (pv[u].y > 0.0f) ? pv[u].y * __builtin_amdgcn_exp2f(pv[u].x - mm) : 0.0f;
       m = mm;
       l = ll;
+    }
+    if (part_x && sub == 0 && g < G && sl_scan[s] < Ls) {  // the page scored by the build
+      const float2 x = part_x[row0 + g];
+      const float mm = fmaxf(m, x.x);
+      if (mm > -INFINITY) {
+        l = (m > -INFINITY ? l * __builtin_amdgcn_exp2f(m - mm) : 0.0f) +
+            (x.y > 0.0f ? x.y * __builtin_amdgcn_exp2f(x.x - mm) : 0.0f);
+        m = mm;
+      }
     }
     for (int o = 8; o > 0; o >>= 1) {
       const float om = __shfl_xor(m, o, 64), ol = __shfl_xor(l, o, 64);
@@ -579,7 +589,8 @@ bool select_fast_path(const locks_cfg_t& c) {
 
 hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* page_table,
                                 const int32_t* seq_lens, const float* s_hat, SHatLayout lay,
-                                const float2* partials, const SelectBufs& sb, hipStream_t st) {
+                                const float2* partials, const SelectBufs& sb, hipStream_t st,
+                                const float2* part_x, const int32_t* sl_scan) {
   const int k = page_budget(c);
   const int G = c.num_q_heads / c.num_kv_heads;
   const bool contiguous = lay.head == 1 && lay.page == G;
@@ -590,7 +601,8 @@ hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* page_table,
   const int rows = select_fast_rows(c);
   hipLaunchKernelGGL(kern, dim3(rows, c.num_kv_heads, c.num_seqs), dim3(kChunkThreads), 0, st,
                      c.num_q_heads, c.num_kv_heads, k, select_fast_width(c), c.max_pages_per_seq,
-                     seq_lens, page_table, s_hat, lay, partials, scan_blocks(c), sb, rows);
+                     seq_lens, page_table, s_hat, lay, partials, scan_blocks(c), sb, rows,
+                     part_x, sl_scan);
   return hipGetLastError();
 }
 
