@@ -196,9 +196,10 @@ int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cach
  * q and KV and a listed page that is the last complete page of its sequence, the
  * build of those pages runs on `stream` beside the scan of the others, which the
  * library enqueues on a side stream of its own (one per device, created on first
- * use and kept until the process ends), forked from and joined back to `stream`
- * by events; such calls on one device are serialised on the host.  Outputs as in
- * those calls. */
+ * use -- make that first call outside stream capture -- and kept until the
+ * process ends), forked from and joined back to `stream` by events, so a captured
+ * step records the fork and join too; such calls on one device are serialised on
+ * the host.  Outputs as in those calls. */
 int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache,
                       const void* v_cache, const int32_t* page_table,
                       const int32_t* seq_lens, void* summaries,

@@ -426,6 +426,69 @@ def test_identical_pages_tie_break(n, budget, rank):
     _check_step_against_oracle("ties", d, recs, ids, out, lse, min_same_frac=1.0)
 
 
+def test_decode_step_builds_last_pages_beside_the_scan():
+    """A step whose build list holds the last complete page of every sequence: those
+    pages are built and scored beside the scan of the others (side stream).  The
+    rebuilt bytes equal the store's, the outputs match the same step without a
+    build list (the scored pages differ only by rounding), and a HIP graph of the
+    step replays the eager result exactly (the first such call, which creates the
+    side stream, is eager)."""
+    d = _mk("mixed-lens")
+    cfg, dev = d.cfg, d.device
+    store = B.alloc_summaries(cfg, dev)
+    B.build_summaries(cfg, d.k, d.pt, d.sl, store)
+    torch.cuda.synchronize()
+    ref = store.clone()
+    lens = [int(x) for x in d.w.spec.seq_lens]
+    bl = torch.tensor([[s, L // 16 - 1] for s, L in enumerate(lens) if L >= 16], dtype=torch.int32,
+                      device=dev)
+    print(f"[builds] {bl.shape[0]} last pages listed, lens {lens}", flush=True)
+    ids0, sel0, out0, lse0 = B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws)
+    ids, sel = B.alloc_select_outputs(cfg, dev)
+    out, lse = B.alloc_attend_outputs(cfg, dev)
+    B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws, build_list=bl, out_ids=ids,
+                  out_sel_lse=sel, out=out, out_lse=lse)
+    torch.cuda.synchronize()
+    assert torch.equal(store, ref)
+    assert float((out - out0).abs().max()) <= 1e-4
+    assert float((lse - lse0).abs().max()) <= 1e-4
+    same = sum(len(set(a) & set(b)) for a, b in zip(ids.view(-1, ids.shape[-1]).tolist(),
+                                                     ids0.view(-1, ids0.shape[-1]).tolist()))
+    assert same >= 0.99 * ids.numel(), (same, ids.numel())
+    fin = torch.isfinite(sel0)
+    assert torch.equal(fin, torch.isfinite(sel))
+    assert float((sel[fin] - sel0[fin]).abs().max()) <= 1e-3
+    gids, gsel = B.alloc_select_outputs(cfg, dev)
+    gout, glse = B.alloc_attend_outputs(cfg, dev)
+    ws2 = B.alloc_workspace(cfg, dev)
+
+    def call():
+        B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, ws2, build_list=bl, out_ids=gids,
+                      out_sel_lse=gsel, out=gout, out_lse=glse)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (gids, gsel, gout, glse):
+            t.zero_()
+        B.decode_step(cfg, d.q, d.k, d.v, d.pt, d.sl, store, d.ws, build_list=bl)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(gids, ids), rep
+        assert torch.equal(gout, out) and torch.equal(glse, lse), rep
+        assert torch.equal(torch.nan_to_num(gsel, nan=-7.0), torch.nan_to_num(sel, nan=-7.0)), rep
+        assert torch.equal(store, ref), rep
+    print("[builds] overlapped builds: eager and 3 graph replays agree")
+
+
 @pytest.mark.parametrize("name", ["G16", "r4-G4"])
 def test_decode_step_graph_replay(name):
     """The fused step captured in a HIP graph gives the eager result on every
