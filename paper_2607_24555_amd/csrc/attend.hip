@@ -233,6 +233,29 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
                                   page_table + (long)s * max_pages, s_tab, s_blk, unionL);
     ids = s_tab;
   }
+  // this block's table entries and their estimated page LSEs (NaN without a
+  // summary): loaded now, written after the pages (pages_per_split <= 32, so at
+  // most 32 x 17 entries over the 256 threads)
+  constexpr int kSelPer = 3;
+  float sel_v[kSelPer];
+  int sel_e[kSelPer];
+  if constexpr (kSelect) {
+    const int t0 = split * pages_per_split, n_c = L / kPage;
+    const float* sb = tb.s_hat + tb.lay.base(s, h);
+#pragma unroll
+    for (int u = 0; u < kSelPer; ++u) {
+      const int e = tid + 256 * u;
+      const int t = t0 + e % pages_per_split, g = e / pages_per_split;
+      sel_e[u] = (e < pages_per_split * (G + 1) && t < k_list) ? e : -1;
+      sel_v[u] = 0.0f;
+      if (sel_e[u] >= 0 && g < G) {
+        const int id = s_tab[t];
+        const bool ok = id >= 0 && id < n_c;
+        const float v = sb[(long)(ok ? id : 0) * tb.lay.page + (long)(ok ? g : 0) * tb.lay.head];
+        sel_v[u] = ok ? v : __int_as_float(0x7fc00000);
+      }
+    }
+  }
   auto page_at = [&](int t) -> int {
     int id = -1;
     if (t < t_end) id = ids ? (t < k_list ? ids[t] : -1) : t;
@@ -340,22 +363,15 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
     }
   }
   if constexpr (kSelect) {
-    // this block's table entries and their estimated page LSEs (NaN without a
-    // summary), written while the last page is in flight
     const long unit = (long)s * H_kv + h;
-    const int t0 = split * pages_per_split, n_c = L / kPage;
-    const float* sb = tb.s_hat + tb.lay.base(s, h);
-    for (int e = tid; e < pages_per_split * (G + 1); e += 256) {
+    const int t0 = split * pages_per_split;
+#pragma unroll
+    for (int u = 0; u < kSelPer; ++u) {
+      const int e = sel_e[u];
+      if (e < 0) continue;
       const int t = t0 + e % pages_per_split, g = e / pages_per_split;
-      if (t >= k_list) continue;
-      const int id = s_tab[t];
-      if (g == G) {
-        tb.out_ids[unit * k_list + t] = id;
-      } else {
-        const bool ok = id >= 0 && id < n_c;
-        const float v = sb[(long)(ok ? id : 0) * tb.lay.page + (long)(ok ? g : 0) * tb.lay.head];
-        tb.out_sel_lse[((long)s * H_q + h * G + g) * k_list + t] = ok ? v : __int_as_float(0x7fc00000);
-      }
+      if (g == G) tb.out_ids[unit * k_list + t] = s_tab[t];
+      else tb.out_sel_lse[((long)s * H_q + h * G + g) * k_list + t] = sel_v[u];
     }
   }
   // combine the block's four waves; m is kept in log2 units until here.  sO is
