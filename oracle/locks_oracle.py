@@ -35,6 +35,12 @@ Readings of points the paper leaves open:
   in byte c//2, low nibble for even c][coefficients: 16 x r excess-128 bytes,
   row-major][centroid: 128 excess-128 bytes][float16 scales: r basis-column,
   16 coefficient-row, 1 centroid][zero padding to a multiple of 16 bytes];
+* basis precision variants (the ablation of Sec. 5 "Ablations" and the r8fp
+  control of the retention remark): an int8 basis stores each column as 128
+  excess-128 bytes with one float16 scale f16(max|v| / 127); a bf16 basis stores
+  each column as 128 little-endian bfloat16 values (round to nearest even) and
+  its column-scale slots hold 1.0.  Coefficients and centroid stay int8 and the
+  field order is unchanged;
 * sign convention: each basis column's largest-magnitude entry (first on ties)
   is made positive, the matching coefficient column flipped with it;
 * the normaliser Z_g of the share sums every page that has a summary (complete
@@ -63,14 +69,17 @@ INT8_MAX = 127
 # Summary payload accounting (Sec. 4 "Build"; App. C.1 table)
 # --------------------------------------------------------------------------
 
-def payload_bytes(r: int, d: int = HEAD_DIM, B: int = PAGE) -> int:
-    """Stored bytes per page: d*r int4 + B*r int8 + d int8 + 2-byte scales for r
-    basis columns, B coefficient rows and the centroid."""
-    return d * r // 2 + B * r + d + 2 * (r + B + 1)
+BASIS_BYTES = {"int4": 0.5, "int8": 1, "bf16": 2}   # bytes per basis element
 
 
-def record_stride(r: int) -> int:
-    p = payload_bytes(r)
+def payload_bytes(r: int, d: int = HEAD_DIM, B: int = PAGE, basis: str = "int4") -> int:
+    """Stored bytes per page: the d*r basis (int4 by default) + B*r int8 + d int8
+    + 2-byte scales for r basis columns, B coefficient rows and the centroid."""
+    return int(d * r * BASIS_BYTES[basis]) + B * r + d + 2 * (r + B + 1)
+
+
+def record_stride(r: int, basis: str = "int4") -> int:
+    p = payload_bytes(r, basis=basis)
     return (p + 15) // 16 * 16
 
 
@@ -206,20 +215,44 @@ def quantize(x: np.ndarray, qmax: int, axis) -> Tuple[np.ndarray, np.ndarray]:
     return codes.astype(np.int64), np.squeeze(s16, axis=axis)
 
 
-def encode(mu: np.ndarray, V: np.ndarray, C: np.ndarray) -> np.ndarray:
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Nearest bfloat16 (ties to even) of float32(x), as uint16 bit patterns."""
+    u = np.asarray(x, dtype=np.float64).astype(np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def bf16_value(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, dtype=np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def encode(mu: np.ndarray, V: np.ndarray, C: np.ndarray, basis: str = "int4") -> np.ndarray:
     """Quantise and pack one summary per page: mu [P][d], V [P][d][r], C [P][B][r]
-    -> uint8 records [P][record_stride(r)]."""
+    -> uint8 records [P][record_stride(r, basis)]."""
     P, d, r = V.shape
     assert d == HEAD_DIM and C.shape[1] == PAGE
-    vq, vs = quantize(V, INT4_MAX, axis=1)            # per basis column
     cq, cs = quantize(C, INT8_MAX, axis=2)            # per coefficient row (token)
     mq, ms = quantize(mu, INT8_MAX, axis=1)           # one centroid scale
-    out = np.zeros((P, record_stride(r)), dtype=np.uint8)
-    nib = (vq + 8).astype(np.uint8)                   # excess-8, [P][d][r]
-    for l in range(r):
-        col = nib[:, :, l]
-        out[:, 64 * l:64 * l + 64] = col[:, 0::2] | (col[:, 1::2] << 4)
-    off = 64 * r
+    out = np.zeros((P, record_stride(r, basis)), dtype=np.uint8)
+    cb = int(d * BASIS_BYTES[basis])                  # bytes per basis column
+    if basis == "int4":
+        vq, vs = quantize(V, INT4_MAX, axis=1)        # per basis column
+        nib = (vq + 8).astype(np.uint8)               # excess-8, [P][d][r]
+        for l in range(r):
+            col = nib[:, :, l]
+            out[:, cb * l:cb * l + cb] = col[:, 0::2] | (col[:, 1::2] << 4)
+    elif basis == "int8":
+        vq, vs = quantize(V, INT8_MAX, axis=1)
+        for l in range(r):
+            out[:, cb * l:cb * l + cb] = (vq[:, :, l] + 128).astype(np.uint8)
+    elif basis == "bf16":
+        bits = bf16_round(V)                          # [P][d][r]
+        for l in range(r):
+            out[:, cb * l:cb * l + cb] = bits[:, :, l].astype("<u2").view(np.uint8).reshape(P, cb)
+        vs = np.ones((P, r), dtype=np.float16)
+    else:
+        raise ValueError(basis)
+    off = cb * r
     out[:, off:off + PAGE * r] = (cq + 128).astype(np.uint8).reshape(P, PAGE * r)
     off += PAGE * r
     out[:, off:off + d] = (mq + 128).astype(np.uint8)
@@ -229,25 +262,36 @@ def encode(mu: np.ndarray, V: np.ndarray, C: np.ndarray) -> np.ndarray:
     return out
 
 
-def decode(records: np.ndarray, r: int) -> Dict[str, np.ndarray]:
+def decode(records: np.ndarray, r: int, basis: str = "int4") -> Dict[str, np.ndarray]:
     """Inverse of `encode`: uint8 [P][stride] -> fp64 mu [P][d], V [P][d][r], C [P][B][r]
-    (code times float16 scale), plus the raw integer codes."""
+    (code times float16 scale; bf16 basis values as stored), plus the raw codes."""
     rec = np.asarray(records, dtype=np.uint8)
     P = rec.shape[0]
     d = HEAD_DIM
+    cb = int(d * BASIS_BYTES[basis])
     vcodes = np.zeros((P, d, r), dtype=np.int64)
+    vvals = None
     for l in range(r):
-        b = rec[:, 64 * l:64 * l + 64].astype(np.int64)
-        vcodes[:, 0::2, l] = (b & 15) - 8
-        vcodes[:, 1::2, l] = (b >> 4) - 8
-    off = 64 * r
+        b = rec[:, cb * l:cb * l + cb]
+        if basis == "int4":
+            b = b.astype(np.int64)
+            vcodes[:, 0::2, l] = (b & 15) - 8
+            vcodes[:, 1::2, l] = (b >> 4) - 8
+        elif basis == "int8":
+            vcodes[:, :, l] = b.astype(np.int64) - 128
+        else:
+            if vvals is None:
+                vvals = np.zeros((P, d, r))
+            vvals[:, :, l] = bf16_value(b.copy().view("<u2"))
+    off = cb * r
     ccodes = rec[:, off:off + PAGE * r].astype(np.int64).reshape(P, PAGE, r) - 128
     off += PAGE * r
     mcodes = rec[:, off:off + d].astype(np.int64) - 128
     off += d
     sc = rec[:, off:off + 2 * (r + PAGE + 1)].copy().view("<f2").astype(np.float64)
     vs, cs, ms = sc[:, :r], sc[:, r:r + PAGE], sc[:, r + PAGE]
-    return {"mu": mcodes * ms[:, None], "V": vcodes * vs[:, None, :], "C": ccodes * cs[:, :, None],
+    V = vvals * vs[:, None, :] if basis == "bf16" else vcodes * vs[:, None, :]
+    return {"mu": mcodes * ms[:, None], "V": V, "C": ccodes * cs[:, :, None],
             "vcodes": vcodes, "ccodes": ccodes, "mcodes": mcodes,
             "vscale": vs, "cscale": cs, "mscale": ms}
 
@@ -313,23 +357,23 @@ def pages_of(keys: np.ndarray) -> Tuple[np.ndarray, int, int]:
     return keys[:n_c * PAGE].reshape(n_c, PAGE, keys.shape[1]), n_c, n
 
 
-def unit_summaries(keys: np.ndarray, r: int) -> np.ndarray:
+def unit_summaries(keys: np.ndarray, r: int, basis: str = "int4") -> np.ndarray:
     """Encoded summaries [n_c][stride] of the complete pages of one (sequence, KV head)."""
     pk, n_c, _ = pages_of(keys)
     if n_c == 0:
-        return np.zeros((0, record_stride(r)), dtype=np.uint8)
+        return np.zeros((0, record_stride(r, basis)), dtype=np.uint8)
     f = build_factors(pk, r)
-    return encode(f["mu"], f["V"], f["C"])
+    return encode(f["mu"], f["V"], f["C"], basis)
 
 
 def decode_step(q: np.ndarray, keys: np.ndarray, vals: np.ndarray, records: np.ndarray,
-                r: int, budget_tokens: int) -> Dict[str, object]:
+                r: int, budget_tokens: int, basis: str = "int4") -> Dict[str, object]:
     """Score every summarised page from its decoded record, select the shared table,
     attend over it.  records [n_c][stride] are the complete pages' summaries."""
     L = keys.shape[0]
     n_c, n = L // PAGE, (L + PAGE - 1) // PAGE
     k = (budget_tokens + PAGE - 1) // PAGE
-    dec = decode(records[:n_c], r) if n_c else None
+    dec = decode(records[:n_c], r, basis) if n_c else None
     s_hat = score(q, dec["mu"], dec["V"], dec["C"]) if n_c else np.zeros((q.shape[0], 0))
     sel = select_pages(s_hat, n, k)
     o, lse = attend(q, keys, vals, sel["ids"])

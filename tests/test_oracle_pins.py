@@ -436,3 +436,68 @@ def test_empty_and_partial_sequences():
         res = O.decode_step(q, keys, vals, rec, 8, 48)
         o, lse = O.dense_step(q, keys, vals)        # n <= k = 3 always here
         np.testing.assert_allclose(res["out"], o, atol=1e-12)
+
+
+# ---------------------------------------------------------------- basis precision variants
+# (Sec. 5 "Ablations": int8 and bf16 bases; the r8fp control of the retention remark)
+
+def test_bf16_rounding_matches_torch():
+    """The oracle's round-to-nearest-even bfloat16 against torch's conversion."""
+    rng = _rng(40)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 4, 20000),
+                        [0.0, -0.0, 1.0, -1.0, 1.00390625, 1.01171875, 3.0e38]])
+    want = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy()
+    np.testing.assert_array_equal(O.bf16_round(x).astype(np.int16), want)
+    np.testing.assert_array_equal(O.bf16_value(O.bf16_round(x)),
+                                  torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16)
+                                  .to(torch.float64).numpy())
+
+
+@pytest.mark.parametrize("basis", ["int8", "bf16"])
+def test_variant_record_roundtrip(basis):
+    """Every field decodes to its value within its rounding error (int8: s/2 of the
+    column scale; bf16: the unit roundoff 2^-8); coefficients and centroid are the same
+    int8 codes as in the int4 record, and the record holds exactly its payload."""
+    rng = _rng(41)
+    pk = _pages(rng, 12)
+    f = O.build_factors(pk, 8)
+    rec = O.encode(f["mu"], f["V"], f["C"], basis)
+    dec = O.decode(rec, 8, basis)
+    if basis == "int8":
+        s = dec["vscale"][:, None, :]
+        assert np.all(np.abs(dec["V"] - f["V"]) <= s / 2 + 1e-12)
+        assert np.all(np.abs(dec["vcodes"]) <= 127)
+        amax = np.max(np.abs(f["V"]), axis=1)
+        assert np.allclose(dec["vscale"], (amax / 127).astype(np.float16).astype(np.float64))
+    else:
+        # unit roundoff of bfloat16 (8 significant bits): |x - bf16(x)| <= 2^-8 |x|
+        assert np.all(np.abs(dec["V"] - f["V"]) <= np.abs(f["V"]) * 2.0 ** -8 * 1.0001 + 1e-30)
+        assert np.all(dec["vscale"] == 1.0)
+    ref = O.decode(O.encode(f["mu"], f["V"], f["C"]), 8)
+    np.testing.assert_array_equal(dec["ccodes"], ref["ccodes"])
+    np.testing.assert_array_equal(dec["mcodes"], ref["mcodes"])
+    used = O.payload_bytes(8, basis=basis)
+    assert np.all(rec[:, used:] == 0) and rec.shape[1] == O.record_stride(8, basis)
+    # the basis occupies d * r elements of 1 (int8) or 2 (bf16) bytes
+    assert used - O.payload_bytes(8) == D * 8 * (O.BASIS_BYTES[basis] - 0.5)
+
+
+def test_basis_precision_orders_score_error():
+    """The finer the basis, the closer the stored score is to the unquantised one (the
+    ablation's ordering): int4 > int8 > bf16 in mean |error|, and a bf16 basis with
+    an exact (unquantised) C and mu is within bf16 rounding of the fp64 score."""
+    rng = _rng(42)
+    pk = _pages(rng, 200, scale=4.0)
+    f = O.build_factors(pk, 8)
+    q = rng.standard_normal((4, D))
+    exact = O.score(q, f["mu"], f["V"], f["C"])
+    err = {}
+    for basis in ("int4", "int8", "bf16"):
+        dec = O.decode(O.encode(f["mu"], f["V"], f["C"], basis), 8, basis)
+        err[basis] = np.mean(np.abs(O.score(q, dec["mu"], dec["V"], dec["C"]) - exact))
+    assert err["int4"] > 2 * err["int8"] and err["int8"] > err["bf16"], err
+    Vb = O.bf16_value(O.bf16_round(f["V"]))
+    zb = O.score(q, f["mu"], Vb, f["C"])
+    # |dz| <= sum_l |c_l| |q . dv_l| / sqrt d <= r |C|max |q| 2^-8 / sqrt d (|dv_l| <= 2^-8 |v_l| = 2^-8)
+    bound = np.max(np.linalg.norm(q, axis=1)) * np.max(np.abs(f["C"])) * 8 * 2.0 ** -8 / math.sqrt(D)
+    assert np.max(np.abs(zb - exact)) <= bound
