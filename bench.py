@@ -30,8 +30,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--copies", type=int, default=3)
-    ap.add_argument("--workload", choices=["1m", "128k", "128k-r2", "32k", "reasoning"],
-                    default="1m")
+    ap.add_argument("--workload", choices=list(WORKLOADS), default="1m")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-build", action="store_true")
@@ -52,6 +51,10 @@ WORKLOADS = {
                     "page 16, r 8, b 2048, bf16 KV"),
     "128k-r2": (2, {"rank": 2}, "llama3.1-8b-128k: 8 seq x 131,072 tokens, 32 q / 8 kv heads, "
                                 "d 128, page 16, r 2, b 2048, bf16 KV"),
+    "128k-int8basis": (2, {"basis": 1}, "llama3.1-8b-128k: 8 seq x 131,072 tokens, 32 q / 8 kv "
+                                        "heads, d 128, page 16, r 8, int8 basis, b 2048, bf16 KV"),
+    "128k-bf16basis": (2, {"basis": 2}, "llama3.1-8b-128k: 8 seq x 131,072 tokens, 32 q / 8 kv "
+                                        "heads, d 128, page 16, r 8, bf16 basis, b 2048, bf16 KV"),
     "32k": (1, {}, "llama3.1-8b-32k: 1 seq x 32,768 tokens, 32 q / 8 kv heads, d 128, page 16, "
                    "r 8, b 2048, bf16 KV"),
     "reasoning": (4, {}, "qwen3-4b-reasoning: 64 seq x U[8K,64K] tokens, 32 q / 8 kv heads, d 128, "
@@ -156,17 +159,19 @@ def cpu_baseline(w, cfg, sample_pages):
     from threadpoolctl import threadpool_limits
 
     from oracle import locks_oracle as O
+    from paper_2607_24555_amd import locks as B
     from workloads import gather_unit
 
     k, v, q = gather_unit(w, 0, 0)
     L = min(k.shape[0], sample_pages * 16)
     k, v = k[:L], v[:L]
-    rec = O.unit_summaries(k, cfg.rank)                  # build: not part of the step
+    basis = B.BASIS_NAMES[cfg.basis]
+    rec = O.unit_summaries(k, cfg.rank, basis)           # build: not part of the step
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
         reps = 0
         while True:
-            O.decode_step(q, k, v, rec, cfg.rank, cfg.budget_tokens)
+            O.decode_step(q, k, v, rec, cfg.rank, cfg.budget_tokens, basis)
             reps += 1
             if time.perf_counter() - t0 > 10.0 or reps >= 20:
                 break
@@ -195,10 +200,13 @@ def main():
     if args.copy_calib_mib > 0:
         copy_calibration(args.copy_calib_mib, dev)
     wid, ov, desc = WORKLOADS[args.workload]
+    ov = dict(ov)
+    basis = ov.pop("basis", B.LOCKS_BASIS_INT4)
     t_gen = time.perf_counter()
     w = make_workload(wid, seed=args.seed, device=dev, **ov)
     t_gen = time.perf_counter() - t_gen
     cfg = B.config_for(w.spec, w.num_blocks, w.max_pages)
+    cfg.basis = basis
     q, pt, sl = w.q, w.page_table, w.seq_lens
     growing = args.workload == "reasoning"
     R = 1 if growing else max(1, args.copies)
@@ -211,8 +219,8 @@ def main():
     n_pages = sum(math.ceil(L / 16) for L in w.spec.seq_lens)
     page_heads = n_pages * cfg.num_kv_heads
     complete_heads = sum(L // 16 for L in w.spec.seq_lens) * cfg.num_kv_heads
-    payload = B.summary_payload_bytes(cfg.rank)
-    stride = B.summary_stride(cfg.rank)
+    payload = B.summary_payload_bytes_ex(cfg.rank, cfg.basis)
+    stride = B.summary_stride(cfg.rank, cfg.basis)
     k_sel = min(cfg.k, max(math.ceil(L / 16) for L in w.spec.seq_lens))
     kv_page = 2 * 16 * 128 * 2
     alg_scan = complete_heads * payload
@@ -320,7 +328,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": desc, "global_batch": cfg.num_seqs,
                    "seq_len": int(max(w.spec.seq_lens)), "parallelism": "single-gpu",
-                   "copies_rotated": R},
+                   "summary_basis": B.BASIS_NAMES[cfg.basis], "copies_rotated": R},
         "roofline": {"bound": "hbm", "kernel": "scan_kernel (locks_score_pages)",
                      "achieved": round(scan_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(scan_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,

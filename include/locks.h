@@ -64,6 +64,11 @@ enum {
 /* Element types of q and of the KV cache. */
 enum { LOCKS_BF16 = 0, LOCKS_FP32 = 1 };
 
+/* Precision of the stored basis V (Sec. 5 "Ablations"; the r8fp control of the
+ * retention remark): int4 (the deployed summary), int8, or bfloat16.
+ * Coefficients and centroid are int8 in all three. */
+enum { LOCKS_BASIS_INT4 = 0, LOCKS_BASIS_INT8 = 1, LOCKS_BASIS_BF16 = 2 };
+
 /* Fixed-shape configuration of one decode step (Sec. 4 "Implementation": r, B and
  * b fixed, hence fixed shapes). */
 typedef struct locks_cfg {
@@ -80,6 +85,8 @@ typedef struct locks_cfg {
   int32_t num_blocks;        /* physical blocks in the caches, >= 1             */
   int32_t kv_dtype;          /* LOCKS_BF16 or LOCKS_FP32                        */
   int32_t q_dtype;           /* LOCKS_BF16 or LOCKS_FP32                        */
+  int32_t basis;             /* LOCKS_BASIS_INT4 (0), _INT8 or _BF16; the int8
+                                and bf16 bases take r in {2, 4, 8}              */
 } locks_cfg_t;
 
 /* Stored payload of one page summary (Sec. 4 "Build"; App. C.1 table):
@@ -99,6 +106,17 @@ size_t locks_summary_payload_bytes(int32_t rank);
  *   rest              zero padding
  * Returns 0 for r outside [1, 15]. */
 size_t locks_summary_stride(int32_t rank);
+
+/* Payload and record stride for any basis precision.  The record keeps the field
+ * order above with the basis columns widened: column l at (64 << basis) * l,
+ * holding 128 excess-128 int8 codes (LOCKS_BASIS_INT8, one float16 scale per
+ * column as for int4) or 128 little-endian bfloat16 values (LOCKS_BASIS_BF16,
+ * round to nearest even; the column scales hold 1.0); the coefficients, centroid
+ * and scales follow at the same relative offsets.  Payload = (64 << basis) r +
+ * 16 r + 128 + 2 (r + 17): 818 / 1330 / 2354 bytes at r = 8.  Returns 0 for an
+ * unknown basis or r outside [1, 15]. */
+size_t locks_summary_payload_bytes_ex(int32_t rank, int32_t basis);
+size_t locks_summary_stride_ex(int32_t rank, int32_t basis);
 
 /* Bytes of workspace the select / attend / decode-step calls need for cfg
  * (0 if cfg is invalid). */

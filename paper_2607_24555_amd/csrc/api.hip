@@ -22,6 +22,9 @@ int validate(const locks_cfg_t* c) {
   if (c->num_q_heads % c->num_kv_heads) return LOCKS_E_INVAL;
   if (c->num_q_heads / c->num_kv_heads > kMaxGroup) return LOCKS_E_UNSUPPORTED;
   if (c->rank < 1 || c->rank > kMaxRank) return LOCKS_E_INVAL;
+  if (c->basis < LOCKS_BASIS_INT4 || c->basis > LOCKS_BASIS_BF16) return LOCKS_E_INVAL;
+  if (c->basis != LOCKS_BASIS_INT4 && c->rank != 2 && c->rank != 4 && c->rank != 8)
+    return LOCKS_E_UNSUPPORTED;
   if (c->budget_tokens < 1 || (c->budget_tokens + kPage - 1) / kPage < 2) return LOCKS_E_INVAL;
   if (c->max_pages_per_seq < 1 || c->num_blocks < 1) return LOCKS_E_INVAL;
   if ((long)c->num_seqs * c->num_q_heads > 0x7fffffffL / kDim) return LOCKS_E_INVAL;
@@ -165,6 +168,16 @@ size_t locks_summary_stride(int32_t rank) {
   return (rank < 1 || rank > kMaxRank) ? 0 : (size_t)rec_stride(rank);
 }
 
+size_t locks_summary_payload_bytes_ex(int32_t rank, int32_t basis) {
+  if (rank < 1 || rank > kMaxRank || basis < LOCKS_BASIS_INT4 || basis > LOCKS_BASIS_BF16) return 0;
+  return (size_t)rec_payload(rank, basis);
+}
+
+size_t locks_summary_stride_ex(int32_t rank, int32_t basis) {
+  if (rank < 1 || rank > kMaxRank || basis < LOCKS_BASIS_INT4 || basis > LOCKS_BASIS_BF16) return 0;
+  return (size_t)rec_stride(rank, basis);
+}
+
 size_t locks_workspace_bytes(const locks_cfg_t* cfg) {
   if (validate(cfg) != LOCKS_OK) return 0;
   return plan_workspace(*cfg).total;
@@ -279,7 +292,14 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
     // scan -> per-chunk selection -> attention whose blocks merge the table
     const SHatLayout lay = shat_head_minor(*cfg);
     const float2* part_x = nullptr;
-    if (n_build > 0) {
+    if (n_build > 0 && cfg->basis != LOCKS_BASIS_INT4) {
+      rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
+                                   summaries, nullptr, nullptr, nullptr, nullptr, st));
+      if (rc) return rc;
+      rc = hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, w.s_hat, lay, w.part,
+                                  st));
+      if (rc) return rc;
+    } else if (n_build > 0) {
       // Listed pages that are the last complete page of their sequence (the
       // pages that just filled) are built and scored on `stream` while a side
       // stream, forked before them, builds the other listed pages and then scans

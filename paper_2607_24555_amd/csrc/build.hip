@@ -73,6 +73,12 @@ __device__ __forceinline__ int quant(float x, float s, int qmax) {
   return (int)c;
 }
 
+// Nearest bfloat16 (ties to even) of a finite float, as its 16-bit pattern.
+__device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
 __device__ __forceinline__ uint16_t f16_bits(float s) {
   _Float16 h = (_Float16)s;
   return *reinterpret_cast<uint16_t*>(&h);
@@ -90,8 +96,8 @@ __global__ __launch_bounds__(64) void build_kernel(
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ build_list, int n_items, int all_pages,
     uint8_t* __restrict__ summaries, float* __restrict__ mu_out, float* __restrict__ basis_out,
-    float* __restrict__ coef_out, float* __restrict__ sigma2_out, BuildStep bs) {
-  constexpr bool kScore = kMode == kBuildLast;
+    float* __restrict__ coef_out, float* __restrict__ sigma2_out, BuildStep bs, int basis) {
+  constexpr bool kScore = kMode == kBuildLast;  // (int4 bases only)
   // raw key rows (bf16 or fp32 as stored; deviations are formed on the fly as
   // float(k) - mu, the same fp32 value for every use) share LDS with the Jacobi
   // matrices A and U, which are written once the Gram is complete
@@ -307,7 +313,7 @@ __global__ __launch_bounds__(64) void build_kernel(
   const float floor_ = fmaxf(kZeroRel * top, kZeroAbs * energy);
 
   const long out_item = all_pages ? 0 : (long)e * H_kv + h;
-  uint8_t* rec = summaries + (blk * H_kv + h) * (long)rec_stride(r);
+  uint8_t* rec = summaries + (blk * H_kv + h) * (long)rec_stride(r, basis);
 
   // ---- basis columns, one at a time: V[:, l] = D^T u_l / sigma_l.  This lane's
   //      8 dimensions of the 16 key rows are re-read from global memory (the
@@ -367,18 +373,35 @@ __global__ __launch_bounds__(64) void build_kernel(
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) bo[(8 * li + cc) * r + l] = flip * v[cc];
     } else {
-      const float vs = f16_scale(best, 7.0f);
-      uint32_t word = 0;
+      if (basis == 0) {  // int4, excess 8, two per byte
+        const float vs = f16_scale(best, 7.0f);
+        uint32_t word = 0;
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) {
-        const int code = quant(flip * v[cc], vs, 7);
-        word |= (uint32_t)(code + 8) << (4 * cc);
-      }
-      *reinterpret_cast<uint32_t*>(rec + 64 * l + 4 * li) = word;
-      if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * l) = f16_bits(vs);
-      if (kScore) {
-        sVw[grp][l][li] = word;
-        if (li == 0) sVs[grp][l] = vs;
+        for (int cc = 0; cc < 8; ++cc) {
+          const int code = quant(flip * v[cc], vs, 7);
+          word |= (uint32_t)(code + 8) << (4 * cc);
+        }
+        *reinterpret_cast<uint32_t*>(rec + 64 * l + 4 * li) = word;
+        if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * l) = f16_bits(vs);
+        if (kScore) {
+          sVw[grp][l][li] = word;
+          if (li == 0) sVs[grp][l] = vs;
+        }
+      } else if (basis == 1) {  // int8, excess 128
+        const float vs = f16_scale(best, 127.0f);
+        uint32_t w[2] = {0u, 0u};
+#pragma unroll
+        for (int cc = 0; cc < 8; ++cc)
+          w[cc >> 2] |= (uint32_t)(quant(flip * v[cc], vs, 127) + 128) << (8 * (cc & 3));
+        *reinterpret_cast<uint2*>(rec + 128 * l + 8 * li) = make_uint2(w[0], w[1]);
+        if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, 1) + 2 * l) = f16_bits(vs);
+      } else {  // bfloat16, round to nearest even; the column scale is 1
+        uint32_t w[4];
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2)
+          w[e2] = bf16_rne_bits(flip * v[2 * e2]) | (bf16_rne_bits(flip * v[2 * e2 + 1]) << 16);
+        *reinterpret_cast<uint4*>(rec + 256 * l + 16 * li) = make_uint4(w[0], w[1], w[2], w[3]);
+        if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, 2) + 2 * l) = f16_bits(1.0f);
       }
     }
   }
@@ -406,14 +429,14 @@ __global__ __launch_bounds__(64) void build_kernel(
     const float cs = f16_scale(cabs, 127.0f);
     for (int l = 0; l < r; ++l) {
       const int code = quant(coef_value(l), cs, 127);
-      rec[rec_coef_off(r) + li * r + l] = (uint8_t)(code + 128);
+      rec[rec_coef_off(r, basis) + li * r + l] = (uint8_t)(code + 128);
       if (kScore) {
 #pragma unroll
         for (int u = 0; u < kMaxRank; ++u)
           if (u == l) chat[u] = (float)code * cs;
       }
     }
-    *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * (r + li)) = f16_bits(cs);
+    *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, basis) + 2 * (r + li)) = f16_bits(cs);
   }
   // ---- centroid: int8 with one scale
   {
@@ -424,10 +447,10 @@ __global__ __launch_bounds__(64) void build_kernel(
     float mhat[8];
     for (int cc = 0; cc < 8; ++cc) {
       const int code = quant(sMu[grp][8 * li + cc], ms, 127);
-      rec[rec_mu_off(r) + 8 * li + cc] = (uint8_t)(code + 128);
+      rec[rec_mu_off(r, basis) + 8 * li + cc] = (uint8_t)(code + 128);
       mhat[cc] = (float)code * ms;
     }
-    if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * (r + kPage)) = f16_bits(ms);
+    if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, basis) + 2 * (r + kPage)) = f16_bits(ms);
     if (kScore) {
       // ---- page score for each query head of the group (Eq. 1 on the decoded
       //      summary): z_i = q^T (mu + sum_l c_il v_l) / sqrt d over the 16 tokens
@@ -488,8 +511,8 @@ __global__ __launch_bounds__(64) void build_kernel(
   }
   // ---- zero padding up to the record stride
   {
-    const int pad0 = rec_payload(r);
-    if (pad0 + li < rec_stride(r)) rec[pad0 + li] = 0;
+    const int pad0 = rec_payload(r, basis);
+    if (pad0 + li < rec_stride(r, basis)) rec[pad0 + li] = 0;
   }
 }
 
@@ -512,7 +535,7 @@ hipError_t launch_build(const locks_cfg_t& c, const void* k_cache, const int32_t
   hipLaunchKernelGGL((build_kernel<KT, F, M>), grid, block, 0, st, c.num_seqs, c.num_kv_heads,  \
                      c.max_pages_per_seq, c.rank, static_cast<const KT*>(k_cache), page_table,  \
                      seq_lens, build_list, n_items, (int)all_pages, (uint8_t*)summaries, mu,    \
-                     basis, coef, sigma2, bs)
+                     basis, coef, sigma2, bs, c.basis)
 #define LOCKS_BUILD_T(KT)                                     \
   if (factors) LOCKS_BUILD(KT, true, kBuildAll);              \
   else if (mode == kBuildInner) LOCKS_BUILD(KT, false, kBuildInner); \

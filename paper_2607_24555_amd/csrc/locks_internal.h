@@ -14,12 +14,15 @@ constexpr int kDim = 128;    // d
 constexpr int kMaxRank = 15; // r <= B - 1 (rank of centred page deviations)
 constexpr int kMaxGroup = 16;   // G = H_q / H_kv
 
-// Byte offsets inside one summary record for rank r (see locks_summary_stride).
-__host__ __device__ constexpr int rec_coef_off(int r) { return 64 * r; }
-__host__ __device__ constexpr int rec_mu_off(int r) { return 80 * r; }
-__host__ __device__ constexpr int rec_scale_off(int r) { return 80 * r + kDim; }
-__host__ __device__ constexpr int rec_payload(int r) { return 82 * r + 162; }
-__host__ __device__ constexpr int rec_stride(int r) { return (rec_payload(r) + 15) / 16 * 16; }
+// Byte offsets inside one summary record for rank r and basis precision b
+// (0 int4, 1 int8, 2 bf16: 64 << b bytes per basis column; see
+// locks_summary_stride_ex).
+__host__ __device__ constexpr int rec_col_bytes(int b = 0) { return 64 << b; }
+__host__ __device__ constexpr int rec_coef_off(int r, int b = 0) { return rec_col_bytes(b) * r; }
+__host__ __device__ constexpr int rec_mu_off(int r, int b = 0) { return rec_col_bytes(b) * r + 16 * r; }
+__host__ __device__ constexpr int rec_scale_off(int r, int b = 0) { return rec_mu_off(r, b) + kDim; }
+__host__ __device__ constexpr int rec_payload(int r, int b = 0) { return rec_scale_off(r, b) + 2 * (r + 17); }
+__host__ __device__ constexpr int rec_stride(int r, int b = 0) { return (rec_payload(r, b) + 15) / 16 * 16; }
 
 // ---------------------------------------------------------------- device helpers
 
@@ -106,7 +109,7 @@ WsPlan plan_workspace(const locks_cfg_t& c);
 // Bytes of the summary store (every block's records); below 2^32 for a valid
 // configuration, so record offsets fit 32 bits.
 inline size_t summary_store_bytes(const locks_cfg_t& c) {
-  return (size_t)c.num_blocks * (size_t)c.num_kv_heads * (size_t)rec_stride(c.rank);
+  return (size_t)c.num_blocks * (size_t)c.num_kv_heads * (size_t)rec_stride(c.rank, c.basis);
 }
 int page_budget(const locks_cfg_t& c);  // k = ceil(b / 16)
 int scan_pages_per_block(const locks_cfg_t& c);  // pages covered by one scan block

@@ -43,12 +43,14 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-template <int R>
+template <int R, int BB = 0>
 struct Geom {
   static constexpr int kPPS = (16 / R) > 0 ? 16 / R : 1;          // pages per stage-1 set
   static constexpr int kSets = (16 + kPPS - 1) / kPPS;
-  static constexpr int kStride = rec_stride(R);
-  static constexpr int kTail = kStride - 64 * R;                   // coef .. end of record
+  static constexpr int kColB = rec_col_bytes(BB);                  // bytes per basis column
+  static constexpr int kVW = 1 << BB;                              // 16-byte basis loads per lane and set
+  static constexpr int kStride = rec_stride(R, BB);
+  static constexpr int kTail = kStride - kColB * R;                // coef .. end of record
   static constexpr int kTailCh = kTail / 16;
   static constexpr int kTailLoads = (16 * kTailCh + 63) / 64;
   static constexpr int kMu = 16 * R;                               // offsets inside the tail
@@ -115,29 +117,44 @@ __device__ __forceinline__ void merge_lanes_mod(float& m, float& l) {
   }
 }
 
-template <int R>
+template <int R, int BB = 0>
 struct TileRegs {
-  uint4 vb[Geom<R>::kSets];       // basis slices, MFMA A layout
-  uint4 tl[Geom<R>::kTailLoads];  // record tails, 16-byte chunks
+  uint4 vb[BB == 0 ? Geom<R, BB>::kSets : 1][Geom<R, BB>::kVW];  // basis slices (int4: per tile)
+  uint4 tl[Geom<R, BB>::kTailLoads];  // record tails, 16-byte chunks
+  int blk;                            // lanes 0..15: block of page page0 + lane (-1: none)
 };
 
-// Issue the loads of one 16-page tile (no wait).
-template <int R>
-__device__ __forceinline__ void issue_tile(TileRegs<R>& T, const uint8_t* __restrict__ summaries,
+// The basis slices of stage-1 set st of a tile: lane (grp, col) takes the 32
+// elements 32 grp .. 32 grp + 31 of column l = col % R of page st kPPS + col / R
+// (16 << BB bytes).
+template <int R, int BB>
+__device__ __forceinline__ void load_set(uint4* vb, const uint8_t* __restrict__ summaries,
+                                         int my_blk, int st, int H_kv, int h, int lane) {
+  using Gm = Geom<R, BB>;
+  const int col = lane & 15, grp = lane >> 4;
+  const int pp = col / R, l = col % R;
+  const int page = st * Gm::kPPS + pp;
+  const int blk = __shfl(my_blk, page < 16 ? page : 0, 64);
+  const bool ok = col < Gm::kPPS * R && page < 16 && blk >= 0;
+#pragma unroll
+  for (int w = 0; w < Gm::kVW; ++w)
+    vb[w] = ok ? *reinterpret_cast<const uint4*>(summaries + ((long)blk * H_kv + h) * Gm::kStride +
+                                                 Gm::kColB * l + (16 << BB) * grp + 16 * w)
+               : make_uint4(0, 0, 0, 0);
+}
+
+// Issue the loads of one 16-page tile (no wait): the record tails, and for an
+// int4 basis every stage-1 slice (wider bases load theirs set by set).
+template <int R, int BB = 0>
+__device__ __forceinline__ void issue_tile(TileRegs<R, BB>& T, const uint8_t* __restrict__ summaries,
                                            const int32_t* __restrict__ pt_row, int page0, int n_c,
                                            int H_kv, int h, int lane) {
-  using Gm = Geom<R>;
-  const int col = lane & 15, grp = lane >> 4;
+  using Gm = Geom<R, BB>;
   const int my_blk = (lane < 16 && page0 + lane < n_c) ? pt_row[page0 + lane] : -1;
+  T.blk = my_blk;
+  if constexpr (BB == 0) {
 #pragma unroll
-  for (int st = 0; st < Gm::kSets; ++st) {
-    const int pp = col / R, l = col % R;
-    const int page = st * Gm::kPPS + pp;
-    const int blk = __shfl(my_blk, page < 16 ? page : 0, 64);
-    const bool ok = col < Gm::kPPS * R && page < 16 && blk >= 0;
-    T.vb[st] = ok ? *reinterpret_cast<const uint4*>(summaries + ((long)blk * H_kv + h) * Gm::kStride +
-                                                    64 * l + 16 * grp)
-                  : make_uint4(0, 0, 0, 0);
+    for (int st = 0; st < Gm::kSets; ++st) load_set<R, BB>(T.vb[st], summaries, my_blk, st, H_kv, h, lane);
   }
 #pragma unroll
   for (int u = 0; u < Gm::kTailLoads; ++u) {
@@ -146,18 +163,21 @@ __device__ __forceinline__ void issue_tile(TileRegs<R>& T, const uint8_t* __rest
     const int blk = __shfl(my_blk, page < 16 ? page : 0, 64);
     T.tl[u] = (c < 16 * Gm::kTailCh && blk >= 0)
                   ? *reinterpret_cast<const uint4*>(summaries + ((long)blk * H_kv + h) * Gm::kStride +
-                                                    64 * R + off)
+                                                    Gm::kColB * R + off)
                   : make_uint4(0, 0, 0, 0);
   }
 }
 
-template <typename QT, int R>
+// BB: basis precision (0 int4, 1 int8, 2 bf16).  Wider bases decode their slice
+// to f16 in natural element order (int8 codes exactly; bf16 values to the nearest
+// f16) and meet the natural-order query operand.
+template <typename QT, int R, int BB = 0>
 __global__ __launch_bounds__(256) void scan_mfma_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q,
     const uint8_t* __restrict__ summaries, const int32_t* __restrict__ page_table,
     const int32_t* __restrict__ seq_lens, float* __restrict__ s_hat, SHatLayout lay,
     float2* __restrict__ partials) {
-  using Gm = Geom<R>;
+  using Gm = Geom<R, BB>;
   constexpr bool kSplitQ = sizeof(QT) == 4;  // fp32 queries: f16 hi + lo
   __shared__ __align__(16) uint8_t sTail[4][16][Gm::kTail];
   __shared__ float sP[4][16][R][16];
@@ -176,8 +196,8 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
   float run_m = -INFINITY, run_s = 0.0f;  // running normaliser, log2 domain
   const int npack = 16 / G;                // pages per stage-2 pass
   if (pg * 64 < n_c) {
-  TileRegs<R> buf[2];
-  issue_tile<R>(buf[0], summaries, pt_row, pg * 64, n_c, H_kv, h, lane);
+  TileRegs<R, BB> buf[2];
+  issue_tile<R, BB>(buf[0], summaries, pt_row, pg * 64, n_c, H_kv, h, lane);
 
   // ---- B operands: column = query head, K permuted to match the decoders
   constexpr int kPerm[8] = {0, 4, 1, 5, 2, 6, 3, 7};
@@ -223,9 +243,9 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
   for (int t = 0; t < 4; ++t) {
     const int page0 = (pg * 4 + t) * 16;
     if (page0 < n_c) {
-      TileRegs<R>& cur = buf[t & 1];
+      TileRegs<R, BB>& cur = buf[t & 1];
       if (t + 1 < 4 && page0 + 16 < n_c)
-        issue_tile<R>(buf[(t + 1) & 1], summaries, pt_row, page0 + 16, n_c, H_kv, h, lane);
+        issue_tile<R, BB>(buf[(t + 1) & 1], summaries, pt_row, page0 + 16, n_c, H_kv, h, lane);
 #pragma unroll
       for (int u = 0; u < Gm::kTailLoads; ++u) {
         const int c = lane + 64 * u;
@@ -238,12 +258,35 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 #pragma unroll
       for (int st = 0; st < Gm::kSets; ++st) {
         f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-        const uint32_t w[4] = {cur.vb[st].x, cur.vb[st].y, cur.vb[st].z, cur.vb[st].w};
+        if constexpr (BB == 0) {
+          const uint32_t w[4] = {cur.vb[st][0].x, cur.vb[st][0].y, cur.vb[st][0].z, cur.vb[st][0].w};
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const h8 a = nib8_to_h8(w[ks]);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bv[ks], acc, 0, 0, 0);
-          if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bvl[ks], acc, 0, 0, 0);
+          for (int ks = 0; ks < 4; ++ks) {
+            const h8 a = nib8_to_h8(w[ks]);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bv[ks], acc, 0, 0, 0);
+            if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bvl[ks], acc, 0, 0, 0);
+          }
+        } else {
+          uint4 vw[Gm::kVW];
+          load_set<R, BB>(vw, summaries, cur.blk, st, H_kv, h, lane);
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) {
+            h8 a;
+            if constexpr (BB == 1) {
+              const uint4 v = vw[ks >> 1];
+              a = (ks & 1) ? byte8_to_h8(v.z, v.w) : byte8_to_h8(v.x, v.y);
+            } else {
+              const uint4 v = vw[ks];
+              const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                a[2 * e] = (_Float16)__uint_as_float(u[e] << 16);
+                a[2 * e + 1] = (_Float16)__uint_as_float(u[e] & 0xffff0000u);
+              }
+            }
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bm[ks], acc, 0, 0, 0);
+            if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bml[ks], acc, 0, 0, 0);
+          }
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -1545,10 +1588,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
 
 
 template <typename QT>
-hipError_t dispatch_scan(int r, int G, int steps, dim3 grid, hipStream_t st, int H_q, int H_kv,
-                         int max_pages, const QT* q, const uint8_t* sum, uint32_t summ_bytes,
-                         const int32_t* pt, const int32_t* sl, float* s_hat, SHatLayout lay,
-                         float2* part) {
+hipError_t dispatch_scan(int r, int G, int basis, int steps, dim3 grid, hipStream_t st, int H_q,
+                         int H_kv, int max_pages, const QT* q, const uint8_t* sum,
+                         uint32_t summ_bytes, const int32_t* pt, const int32_t* sl, float* s_hat,
+                         SHatLayout lay, float2* part) {
+  if (basis != LOCKS_BASIS_INT4) {  // int8 / bf16 bases: the generic kernel, r in {2, 4, 8}
+#define LOCKS_SCAN_BASIS(RR, BB)                                                            \
+    if (r == RR && basis == BB) {                                                           \
+      hipLaunchKernelGGL((scan_mfma_kernel<QT, RR, BB>), grid, dim3(256), 0, st, H_q, H_kv, \
+                         max_pages, q, sum, pt, sl, s_hat, lay, part);                      \
+      return hipGetLastError();                                                             \
+    }
+    LOCKS_SCAN_BASIS(2, 1) LOCKS_SCAN_BASIS(4, 1) LOCKS_SCAN_BASIS(8, 1)
+    LOCKS_SCAN_BASIS(2, 2) LOCKS_SCAN_BASIS(4, 2) LOCKS_SCAN_BASIS(8, 2)
+#undef LOCKS_SCAN_BASIS
+    return hipErrorInvalidValue;
+  }
 #define LOCKS_SCAN_FAST(RR, NP)                                                              \
   if (r == RR && G == 16 / NP) {                                                            \
     hipLaunchKernelGGL((scan_fast_kernel<QT, RR, NP>), grid, dim3(256), 0, st, H_q, H_kv,   \
@@ -1606,11 +1661,11 @@ hipError_t dispatch_scan(int r, int G, int steps, dim3 grid, hipStream_t st, int
 }  // namespace
 
 static bool use_r8_kernel(const locks_cfg_t& c) {
-  return c.rank == 8 && c.num_q_heads == 16 * c.num_kv_heads;
+  return c.basis == LOCKS_BASIS_INT4 && c.rank == 8 && c.num_q_heads == 16 * c.num_kv_heads;
 }
 
 static bool use_r8g4_kernel(const locks_cfg_t& c) {
-  return c.rank == 8 && c.num_q_heads == 4 * c.num_kv_heads;
+  return c.basis == LOCKS_BASIS_INT4 && c.rank == 8 && c.num_q_heads == 4 * c.num_kv_heads;
 }
 
 // 16-page steps per wave of the r = 8 kernels: 4, or 1 when a 4-step grid would
@@ -1633,11 +1688,11 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
   const uint32_t bytes = (uint32_t)summary_store_bytes(c);
   const int steps = r8_steps(c);
   if (c.q_dtype == LOCKS_BF16)
-    return dispatch_scan(c.rank, G, steps, grid, st, c.num_q_heads, c.num_kv_heads,
+    return dispatch_scan(c.rank, G, c.basis, steps, grid, st, c.num_q_heads, c.num_kv_heads,
                          c.max_pages_per_seq, static_cast<const uint16_t*>(q),
                          static_cast<const uint8_t*>(summaries), bytes, page_table, seq_lens,
                          s_hat, lay, partials);
-  return dispatch_scan(c.rank, G, steps, grid, st, c.num_q_heads, c.num_kv_heads,
+  return dispatch_scan(c.rank, G, c.basis, steps, grid, st, c.num_q_heads, c.num_kv_heads,
                        c.max_pages_per_seq, static_cast<const float*>(q),
                        static_cast<const uint8_t*>(summaries), bytes, page_table, seq_lens, s_hat,
                        lay, partials);

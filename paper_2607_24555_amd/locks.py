@@ -20,6 +20,10 @@ LIB_PATH = os.path.join(_HERE, "liblocks.so")
 
 LOCKS_BF16 = 0
 LOCKS_FP32 = 1
+LOCKS_BASIS_INT4 = 0
+LOCKS_BASIS_INT8 = 1
+LOCKS_BASIS_BF16 = 2
+BASIS_NAMES = {LOCKS_BASIS_INT4: "int4", LOCKS_BASIS_INT8: "int8", LOCKS_BASIS_BF16: "bf16"}
 PAGE = 16
 HEAD_DIM = 128
 
@@ -31,7 +35,7 @@ class LocksError(RuntimeError):
 class _Cfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "num_seqs", "num_q_heads", "num_kv_heads", "head_dim", "page_size", "rank",
-        "budget_tokens", "max_pages_per_seq", "num_blocks", "kv_dtype", "q_dtype")]
+        "budget_tokens", "max_pages_per_seq", "num_blocks", "kv_dtype", "q_dtype", "basis")]
 
 
 @dataclass
@@ -47,6 +51,7 @@ class Config:
     q_dtype: int = LOCKS_BF16
     head_dim: int = HEAD_DIM
     page_size: int = PAGE
+    basis: int = LOCKS_BASIS_INT4
 
     @property
     def group(self) -> int:
@@ -59,7 +64,7 @@ class Config:
     def c(self) -> _Cfg:
         return _Cfg(self.num_seqs, self.num_q_heads, self.num_kv_heads, self.head_dim,
                     self.page_size, self.rank, self.budget_tokens, self.max_pages_per_seq,
-                    self.num_blocks, self.kv_dtype, self.q_dtype)
+                    self.num_blocks, self.kv_dtype, self.q_dtype, self.basis)
 
 
 _lib = None
@@ -70,6 +75,8 @@ _I = ctypes.c_int32
 _SIGS = {
     "locks_summary_payload_bytes": (_SZ, [_I]),
     "locks_summary_stride": (_SZ, [_I]),
+    "locks_summary_payload_bytes_ex": (_SZ, [_I, _I]),
+    "locks_summary_stride_ex": (_SZ, [_I, _I]),
     "locks_workspace_bytes": (_SZ, [ctypes.POINTER(_Cfg)]),
     "locks_build_summaries": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _I, _P, _P]),
     "locks_build_factors": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _I, _P, _P, _P,
@@ -130,8 +137,12 @@ def summary_payload_bytes(rank: int) -> int:
     return int(lib().locks_summary_payload_bytes(rank))
 
 
-def summary_stride(rank: int) -> int:
-    return int(lib().locks_summary_stride(rank))
+def summary_stride(rank: int, basis: int = LOCKS_BASIS_INT4) -> int:
+    return int(lib().locks_summary_stride_ex(rank, basis))
+
+
+def summary_payload_bytes_ex(rank: int, basis: int) -> int:
+    return int(lib().locks_summary_payload_bytes_ex(rank, basis))
 
 
 def workspace_bytes(cfg: Config) -> int:
@@ -147,7 +158,7 @@ def alloc_workspace(cfg: Config, device="cuda") -> torch.Tensor:
 
 
 def alloc_summaries(cfg: Config, device="cuda") -> torch.Tensor:
-    return torch.zeros(cfg.num_blocks, cfg.num_kv_heads, summary_stride(cfg.rank),
+    return torch.zeros(cfg.num_blocks, cfg.num_kv_heads, summary_stride(cfg.rank, cfg.basis),
                        dtype=torch.uint8, device=device)
 
 

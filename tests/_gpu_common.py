@@ -39,7 +39,7 @@ class Dev:
                 if units is not None and (s, h) not in units:
                     continue
                 k, _, _ = gather_unit(self.w, s, h)
-                rec = O.unit_summaries(k, self.cfg.rank)
+                rec = O.unit_summaries(k, self.cfg.rank, B.BASIS_NAMES[self.cfg.basis])
                 recs[(s, h)] = rec
                 n_c = rec.shape[0]
                 if n_c:

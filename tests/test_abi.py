@@ -6,6 +6,8 @@ import re
 
 import pytest
 
+from oracle import locks_oracle as O
+
 from paper_2607_24555_amd import locks as B
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -28,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 14
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGS), "binding and header disagree"
@@ -46,6 +48,24 @@ def test_payload_and_stride(lib):
     assert [B.summary_payload_bytes(r) for r in (8, 4, 2)] == [818, 490, 326]
     assert [B.summary_stride(r) for r in (8, 4, 2)] == [832, 496, 336]
     assert B.summary_payload_bytes(0) == 0 and B.summary_stride(16) == 0
+
+
+@pytest.mark.parametrize("basis,name", [(B.LOCKS_BASIS_INT4, "int4"), (B.LOCKS_BASIS_INT8, "int8"),
+                                        (B.LOCKS_BASIS_BF16, "bf16")])
+def test_payload_and_stride_per_basis_match_the_oracle_layout(lib, basis, name):
+    for r in (1, 2, 4, 8, 15):
+        assert B.summary_payload_bytes_ex(r, basis) == O.payload_bytes(r, basis=name)
+        assert B.summary_stride(r, basis) == O.record_stride(r, name)
+    assert B.summary_stride(8, 3) == 0 and B.summary_stride(0, basis) == 0
+
+
+@pytest.mark.parametrize("bad,code", [(dict(basis=3), -1), (dict(basis=-1), -1),
+                                      (dict(basis=1, rank=3), -2), (dict(basis=2, rank=15), -2)])
+def test_bad_basis_is_rejected(lib, bad, code):
+    c = cfg(**bad).c()
+    assert lib.locks_workspace_bytes(ctypes.byref(c)) == 0
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.locks_build_summaries(ctypes.byref(c), fake, fake, fake, None, 0, fake, None) == code
 
 
 @pytest.mark.parametrize("bad,code", [
