@@ -246,6 +246,13 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
       TileRegs<R, BB>& cur = buf[t & 1];
       if (t + 1 < 4 && page0 + 16 < n_c)
         issue_tile<R, BB>(buf[(t + 1) & 1], summaries, pt_row, page0 + 16, n_c, H_kv, h, lane);
+      // wider bases: every set of this tile in flight at once, ahead of the LDS
+      // staging of its tail
+      uint4 vall[BB == 0 ? 1 : Gm::kSets][Gm::kVW];
+      if constexpr (BB != 0) {
+#pragma unroll
+        for (int st = 0; st < Gm::kSets; ++st) load_set<R, BB>(vall[st], summaries, cur.blk, st, H_kv, h, lane);
+      }
 #pragma unroll
       for (int u = 0; u < Gm::kTailLoads; ++u) {
         const int c = lane + 64 * u;
@@ -267,8 +274,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
             if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bvl[ks], acc, 0, 0, 0);
           }
         } else {
-          uint4 vw[Gm::kVW];
-          load_set<R, BB>(vw, summaries, cur.blk, st, H_kv, h, lane);
+          const uint4* vw = vall[st];
 #pragma unroll
           for (int ks = 0; ks < 4; ++ks) {
             h8 a;
