@@ -41,6 +41,17 @@ Readings of points the paper leaves open:
   each column as 128 little-endian bfloat16 values (round to nearest even) and
   its column-scale slots hold 1.0.  Coefficients and centroid stay int8 and the
   field order is unchanged;
+* KV quantisation at page finalize (Sec. 5 "KV-cache quantization under extreme
+  sparsity", the KIVI composition, and the protocol of its full grid in App. C):
+  fake quantisation, i.e. quantise then dequantise back to bfloat16 in place,
+  asymmetric min/max with 2^b levels: keys per channel over the page's 16 tokens,
+  values per token over groups of g consecutive channels (g = 32 unless stated).
+  scale s = (max - min) / (2^b - 1), code = min(rint((x - min) / s), 2^b - 1),
+  x' = bf16(code * s + min); every operation is one float32 rounding (the
+  kernel's precision, which decides the codes), the result rounded to bfloat16
+  to nearest even; a group with s = 0 is left as it is.  POST builds a page's
+  summary from the keys as written and then quantises the page; PRE quantises
+  first and builds from the quantised keys;
 * sign convention: each basis column's largest-magnitude entry (first on ties)
   is made positive, the matching coefficient column flipped with it;
 * the normaliser Z_g of the share sums every page that has a summary (complete
@@ -343,6 +354,38 @@ def select_pages(s_hat: np.ndarray, n_pages: int, k: int) -> Dict[str, object]:
     gap = float(log_mbar[order[k - 3]] - log_mbar[order[k - 2]]) if k >= 3 else math.inf
     ids = sorted(set([0, n_pages - 1] + top))
     return {"ids": ids, "log_mbar": log_mbar, "gap": gap}
+
+
+# --------------------------------------------------------------------------
+# KIVI fake quantisation of a finalised page (Sec. 5 "KV-cache quantization
+# under extreme sparsity"; App. C full-grid protocol)
+# --------------------------------------------------------------------------
+
+def kivi_fake_quant(x: np.ndarray, bits: int, axis) -> np.ndarray:
+    """Asymmetric b-bit min/max quantise-dequantise of every slice of the float32
+    array x along `axis` (one scale and zero point per slice), float32 throughout;
+    returns the float32 values before the final bfloat16 rounding."""
+    x = np.asarray(x, dtype=np.float32)
+    levels = np.float32(2 ** bits - 1)
+    mn = np.min(x, axis=axis, keepdims=True)
+    mx = np.max(x, axis=axis, keepdims=True)
+    s = (mx - mn) / levels                                  # float32 / float32
+    live = s > 0
+    safe = np.where(live, s, np.float32(1.0))
+    code = np.minimum(np.rint((x - mn) / safe), levels)     # ties to even
+    y = code * safe + mn                                    # two float32 roundings
+    return np.where(live, y, x).astype(np.float32)
+
+
+def kivi_page(keys: np.ndarray, vals: np.ndarray, bits: int, v_group: int = 32):
+    """One finalised page [B][d] of keys and of values, bfloat16 in and out (as
+    float64 arrays of bfloat16 values): keys per channel over the page's tokens,
+    values per token over groups of v_group channels."""
+    kq = kivi_fake_quant(keys, bits, axis=0)
+    B, d = vals.shape
+    vq = kivi_fake_quant(np.asarray(vals).reshape(B, d // v_group, v_group), bits,
+                         axis=2).reshape(B, d)
+    return bf16_value(bf16_round(kq)), bf16_value(bf16_round(vq))
 
 
 # --------------------------------------------------------------------------

@@ -501,3 +501,62 @@ def test_basis_precision_orders_score_error():
     # |dz| <= sum_l |c_l| |q . dv_l| / sqrt d <= r |C|max |q| 2^-8 / sqrt d (|dv_l| <= 2^-8 |v_l| = 2^-8)
     bound = np.max(np.linalg.norm(q, axis=1)) * np.max(np.abs(f["C"])) * 8 * 2.0 ** -8 / math.sqrt(D)
     assert np.max(np.abs(zb - exact)) <= bound
+
+
+# --------------------------------------------------------------------------
+# KIVI fake quantisation at page finalize (Sec. 5 "KV-cache quantization under
+# extreme sparsity"; App. C full-grid protocol)
+# --------------------------------------------------------------------------
+
+def test_kivi_worked_examples_by_hand():
+    """Asymmetric 2-bit min/max on hand-computed slices: min 0, max 15 gives scale
+    5 and reconstruction 5 * rint(x / 5) (ties to even at 2.5 and 7.5); an offset
+    slice keeps its zero point; a negative slice works from its minimum."""
+    x = np.array([0, 1, 2, 2.5, 3, 7, 7.5, 8, 12, 13, 15], dtype=np.float32)
+    want = np.array([0, 0, 0, 0, 5, 5, 10, 10, 10, 15, 15], dtype=np.float32)
+    np.testing.assert_array_equal(O.kivi_fake_quant(x, 2, axis=0), want)
+    np.testing.assert_array_equal(O.kivi_fake_quant(x + 100, 2, axis=0), want + 100)
+    # from the minimum -15: (x + 15) / 5 = 3, 2.8, 2.6, 2.5, 2.4, 1.6, 1.5, 1.4, 0.6,
+    # 0.4, 0 rounds to 3, 3, 3, 2, 2, 2, 2, 1, 1, 0, 0 (2.5 and 1.5 to even)
+    np.testing.assert_array_equal(O.kivi_fake_quant(-x, 2, axis=0), np.array(
+        [0, 0, 0, -5, -5, -5, -5, -10, -10, -15, -15], dtype=np.float32))
+    # 4 bits on 0..15: every integer is a level, nothing moves
+    t = np.arange(16, dtype=np.float32)
+    np.testing.assert_array_equal(O.kivi_fake_quant(t, 4, axis=0), t)
+    # 2^b - 1 levels above the minimum, not 2^b: 3 bits on 0..14 step 2 is exact
+    np.testing.assert_array_equal(O.kivi_fake_quant(2 * t[:8], 3, axis=0), 2 * t[:8])
+
+
+def test_kivi_page_axes_keys_per_channel_values_per_token_group():
+    """Keys that are constant along tokens (different per channel) and values that
+    are constant inside each 32-channel group of a token pass unchanged; the
+    transposed arrangement does not."""
+    rng = np.random.default_rng(5)
+    chan = O.bf16_value(O.bf16_round(rng.normal(size=128) * 3))
+    keys = np.tile(chan, (16, 1))
+    tok = O.bf16_value(O.bf16_round(rng.normal(size=(16, 4)) * 3))
+    vals = np.repeat(tok, 32, axis=1)
+    kq, vq = O.kivi_page(keys, vals, 2, 32)
+    np.testing.assert_array_equal(kq, keys)
+    np.testing.assert_array_equal(vq, vals)
+    kq2, vq2 = O.kivi_page(vals[:, :128], keys, 2, 32)
+    assert np.any(kq2 != vals) and np.any(vq2 != keys)
+
+
+@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("g", [16, 32, 128])
+def test_kivi_levels_extremes_and_error_bound(bits, g):
+    """Per slice: at most 2^b distinct values, minimum and maximum reproduced
+    exactly (bf16 inputs), and every value within half a step plus half a bf16
+    unit of the result."""
+    rng = np.random.default_rng(bits * 1000 + g)
+    keys = O.bf16_value(O.bf16_round(rng.normal(size=(16, 128)) * 2 + rng.normal(size=128)))
+    vals = O.bf16_value(O.bf16_round(rng.normal(size=(16, 128))))
+    kq, vq = O.kivi_page(keys, vals, bits, g)
+    for orig, out in ((keys.T, kq.T), (vals.reshape(-1, g), vq.reshape(-1, g))):
+        for a, b in zip(orig, out):
+            assert len(np.unique(b)) <= 2 ** bits
+            assert b.min() == a.min() and b.max() == a.max()
+            step = (a.max() - a.min()) / (2 ** bits - 1)
+            tol = step / 2 * (1 + 1e-5) + np.abs(b) * 2.0 ** -8
+            assert np.all(np.abs(b - a) <= tol)
