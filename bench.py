@@ -37,6 +37,13 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="replay the step from captured HIP graphs instead of launching it")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--kivi", type=int, default=0, metavar="BITS",
+                    help="KIVI fake quantisation of finalised pages at BITS bits (values in "
+                         "groups of 32 channels): every complete page before timing, and in the "
+                         "reasoning loop the pages that fill, inside the step")
+    ap.add_argument("--kivi-stage", choices=("post", "pre"), default="post")
+    ap.add_argument("--no-kivi-pass", action="store_true",
+                    help="skip the separately timed KIVI pass over every complete page")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="first run a plain fp32 copy of this many MiB four times (the "
                          "known-size reference that scales hardware byte counters)")
@@ -236,6 +243,17 @@ def main():
     if not args.no_build:
         _, build_us = timed(lambda i: B.build_summaries(cfg, ks[i % R], pt, sl, summ[i % R]),
                             R, sync)
+    kivi = None
+    if args.kivi:
+        stage = B.LOCKS_KIVI_PRE if args.kivi_stage == "pre" else B.LOCKS_KIVI_POST
+        kivi = B.Kivi(args.kivi, 32, stage)
+        # pages finalised before the timed steps: quantised, summaries from the keys
+        # as written (POST) or rebuilt from the quantised keys (PRE)
+        for i in range(R):
+            B.kivi_quantize(cfg, kivi, ks[i], vs[i], pt, sl)
+            if stage == B.LOCKS_KIVI_PRE:
+                B.build_summaries(cfg, ks[i], pt, sl, summ[i])
+        sync()
 
     # ---- scan alone (dominant kernel): roofline on its algorithmic bytes
     all_lse = torch.empty(cfg.num_seqs, cfg.num_q_heads, cfg.max_pages_per_seq, device=dev)
@@ -289,7 +307,7 @@ def main():
             v_rows.index_copy_(0, flat[i], new_v[i].view(-1, 128))
             sl.add_(1)
             B.decode_step(cfg, q, ks[0], vs[0], pt, sl, summ[0], ws, build_list=lists[i],
-                          out_ids=ids, out_sel_lse=sel, out=out, out_lse=lse)
+                          out_ids=ids, out_sel_lse=sel, out=out, out_lse=lse, kivi=kivi)
 
     if growing and args.graph:
         raise SystemExit("--graph replays fixed launches; the reasoning workload grows every step")
@@ -311,6 +329,16 @@ def main():
             drun(i)
         dense_us, _ = timed(drun, max(4, args.steps // 4), sync)
 
+    # ---- KIVI fake quantisation of every complete page (separately timed, last:
+    # it rewrites the caches in place)
+    kivi_us = None
+    if not args.no_kivi_pass:
+        kp = B.Kivi(args.kivi or 4, 32, B.LOCKS_KIVI_POST)
+        B.kivi_quantize(cfg, kp, ks[0], vs[0], pt, sl)
+        _, kivi_us = timed(lambda i: B.kivi_quantize(cfg, kp, ks[i % R], vs[i % R], pt, sl),
+                           max(R, 4), sync)
+    kivi_bytes = complete_heads * 16 * 128 * 2 * 2 * 2   # K and V, read and written
+
     scan_gbps = alg_scan / (scan_us * 1e-6) / 1e9
     traffic, traffic_detail = scan_traffic(args.workload)
     res = {
@@ -328,7 +356,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": desc, "global_batch": cfg.num_seqs,
                    "seq_len": int(max(w.spec.seq_lens)), "parallelism": "single-gpu",
-                   "summary_basis": B.BASIS_NAMES[cfg.basis], "copies_rotated": R},
+                   "summary_basis": B.BASIS_NAMES[cfg.basis], "copies_rotated": R,
+                   "kivi": None if kivi is None else {"bits": kivi.bits, "v_group": kivi.v_group,
+                                                      "stage": args.kivi_stage}},
         "roofline": {"bound": "hbm", "kernel": "scan_kernel (locks_score_pages)",
                      "achieved": round(scan_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(scan_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
@@ -349,6 +379,10 @@ def main():
         "build": None if build_us is None else {
             "us": round(build_us, 1), "pages": complete_heads,
             "read_GBps": round(complete_heads * 16 * 128 * 2 / (build_us * 1e-6) / 1e9, 1)},
+        "kivi_pass": None if kivi_us is None else {
+            "us": round(kivi_us, 1), "pages": complete_heads, "bits": args.kivi or 4,
+            "v_group": 32, "bytes": kivi_bytes,
+            "GBps": round(kivi_bytes / (kivi_us * 1e-6) / 1e9, 1)},
         "gen_s": round(t_gen, 1),
     }
     if not args.no_cpu_baseline:

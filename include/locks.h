@@ -225,6 +225,53 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
                       int32_t* out_page_ids, float* out_sel_lse, float* out,
                       float* out_lse, void* ws, size_t ws_bytes, void* stream);
 
+/* KV-cache quantisation of finalised pages (Sec. 5 "KV-cache quantization under
+ * extreme sparsity"; App. C, protocol of the full KIVI grid): KIVI's asymmetric
+ * min/max quantiser applied as fake quantisation -- quantise, then dequantise back
+ * to bfloat16 in place -- to complete pages only (the partial last page stays as
+ * written).  Keys share one scale and zero point per channel over the page's 16
+ * tokens; values one per token and group of v_group consecutive channels.  Each
+ * slice x with min m and max M: s = (M - m) / (2^bits - 1) and
+ *   x' = bf16(min(rint((x - m) / s), 2^bits - 1) * s + m),
+ * every operation one IEEE float32 rounding (rint and the final bfloat16 rounding
+ * to nearest even); a slice with s = 0 keeps its values.
+ * The stage orders the quantiser against the summary build in the fused step:
+ * POST builds a page's summary from the keys as written and then quantises the
+ * page, so selection sees unquantised keys and attention quantised KV; PRE
+ * quantises first and builds the summary from the quantised keys. */
+enum { LOCKS_KIVI_POST = 0, LOCKS_KIVI_PRE = 1 };
+typedef struct locks_kivi {
+  int32_t bits;     /* b in [1, 8], 2^b levels (the paper's grid: 4 and 2)     */
+  int32_t v_group;  /* channels per value scale: 8, 16, 32, 64 or 128          */
+  int32_t stage;    /* LOCKS_KIVI_POST or LOCKS_KIVI_PRE                       */
+} locks_kivi_t;
+
+/* Fake-quantise, in place, the K and V of complete pages: every complete page of
+ * every sequence (page_list NULL, n_pages 0) or the n_pages listed (seq, logical
+ * page) int32 pairs in device memory (pairs that name no complete page are
+ * skipped; a page may be listed once per call -- duplicates race).  All KV heads of
+ * a page are quantised; kivi->stage is not used here.  Quantising a page twice is
+ * not the identity in general, so each page should be finalised once.
+ * Returns LOCKS_E_UNSUPPORTED unless kv_dtype is LOCKS_BF16, LOCKS_E_INVAL for a
+ * null kivi / cache / page_table / seq_lens, bits or v_group out of range,
+ * n_pages < 0, or n_pages > 0 with a null page_list. */
+int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* k_cache,
+                        void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
+                        const int32_t* page_list, int32_t n_pages, void* stream);
+
+/* locks_decode_step on a KIVI-quantised cache: the n_build listed pages (the
+ * pages that were finalised this step) are fake-quantised as locks_kivi_quantize
+ * does, before their summary build (kivi->stage == LOCKS_KIVI_PRE) or after it
+ * (LOCKS_KIVI_POST), and in both cases before the attention reads them; the rest
+ * of the step is locks_decode_step's.  kivi == NULL is locks_decode_step itself.
+ * The caches must be bf16 when kivi is given (else LOCKS_E_UNSUPPORTED). */
+int locks_decode_step_kivi(const locks_cfg_t* cfg, const locks_kivi_t* kivi, const void* q,
+                           void* k_cache, void* v_cache, const int32_t* page_table,
+                           const int32_t* seq_lens, void* summaries,
+                           const int32_t* build_list, int32_t n_build,
+                           int32_t* out_page_ids, float* out_sel_lse, float* out,
+                           float* out_lse, void* ws, size_t ws_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* locks_strerror(int status);
 

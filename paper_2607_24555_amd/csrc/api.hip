@@ -270,19 +270,51 @@ int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cach
                                   out_lse, static_cast<hipStream_t>(stream)));
 }
 
-int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache,
-                      const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
-                      void* summaries, const int32_t* build_list, int32_t n_build,
-                      int32_t* out_page_ids, float* out_sel_lse, float* out, float* out_lse,
-                      void* ws, size_t ws_bytes, void* stream) {
+int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* k_cache,
+                        void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
+                        const int32_t* page_list, int32_t n_pages, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (cfg->kv_dtype != LOCKS_BF16) return LOCKS_E_UNSUPPORTED;
+  if (!kivi || !kivi_valid(*kivi) || !k_cache || !v_cache || !page_table || !seq_lens ||
+      n_pages < 0 || (n_pages > 0 && !page_list))
+    return LOCKS_E_INVAL;
+  if (cfg->num_seqs == 0) return LOCKS_OK;
+  return hip_status(launch_kivi(*cfg, *kivi, k_cache, v_cache, page_table, seq_lens, page_list,
+                                n_pages, page_list == nullptr, static_cast<hipStream_t>(stream)));
+}
+
+static int decode_step_impl(const locks_cfg_t* cfg, const locks_kivi_t* kivi, const void* q,
+                            const void* k_cache, const void* v_cache, const int32_t* page_table,
+                            const int32_t* seq_lens, void* summaries, const int32_t* build_list,
+                            int32_t n_build, int32_t* out_page_ids, float* out_sel_lse,
+                            float* out, float* out_lse, void* ws, size_t ws_bytes, void* stream) {
   int rc = validate(cfg);
   if (rc) return rc;
   if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !summaries || !out_page_ids ||
       !out_sel_lse || !out || n_build < 0 || (n_build > 0 && !build_list))
     return LOCKS_E_INVAL;
+  if (kivi && cfg->kv_dtype != LOCKS_BF16) return LOCKS_E_UNSUPPORTED;
+  if (kivi && !kivi_valid(*kivi)) return LOCKS_E_INVAL;
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  // KIVI finalisation of the listed pages: PRE before anything reads them, POST
+  // once their builds are enqueued (and, with the forked scan, once it is joined).
+  if (!kivi || n_build == 0) kivi = nullptr;
+  void* kq = const_cast<void*>(k_cache);
+  void* vq = const_cast<void*>(v_cache);
+  if (kivi && kivi->stage == LOCKS_KIVI_PRE) {
+    rc = hip_status(launch_kivi(*cfg, *kivi, kq, vq, page_table, seq_lens, build_list, n_build,
+                                false, st));
+    if (rc) return rc;
+  }
+  const bool post = kivi && kivi->stage == LOCKS_KIVI_POST;
+  auto post_kivi = [&]() -> int {
+    if (!post) return LOCKS_OK;
+    return hip_status(launch_kivi(*cfg, *kivi, kq, vq, page_table, seq_lens, build_list, n_build,
+                                  false, st));
+  };
   const WsPlan p = plan_workspace(*cfg);
   const Ws w = carve(ws, p);
   const int k = page_budget(*cfg);
@@ -296,6 +328,7 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
       rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
                                    summaries, nullptr, nullptr, nullptr, nullptr, st));
       if (rc) return rc;
+      if ((rc = post_kivi())) return rc;
       rc = hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, w.s_hat, lay, w.part,
                                   st));
       if (rc) return rc;
@@ -324,6 +357,7 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
       if (e == hipSuccess) e = hipEventRecord(side->join, side->st);
       if (e == hipSuccess) e = hipStreamWaitEvent(st, side->join, 0);
       if ((rc = hip_status(e))) return rc;
+      if ((rc = post_kivi())) return rc;
       part_x = w.part_x;
     } else {
       rc = hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, w.s_hat, lay, w.part,
@@ -341,12 +375,33 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
     rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
                                  summaries, nullptr, nullptr, nullptr, nullptr, st));
     if (rc) return rc;
+    if ((rc = post_kivi())) return rc;
   }
   rc = select_impl(cfg, q, summaries, page_table, seq_lens, out_page_ids, out_sel_lse, nullptr, ws,
                    st);
   if (rc) return rc;
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, out_page_ids,
                                   pps, splits, w.attn, out, out_lse, st));
+}
+
+int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                      const void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
+                      void* summaries, const int32_t* build_list, int32_t n_build,
+                      int32_t* out_page_ids, float* out_sel_lse, float* out, float* out_lse,
+                      void* ws, size_t ws_bytes, void* stream) {
+  return decode_step_impl(cfg, nullptr, q, k_cache, v_cache, page_table, seq_lens, summaries,
+                          build_list, n_build, out_page_ids, out_sel_lse, out, out_lse, ws,
+                          ws_bytes, stream);
+}
+
+int locks_decode_step_kivi(const locks_cfg_t* cfg, const locks_kivi_t* kivi, const void* q,
+                           void* k_cache, void* v_cache, const int32_t* page_table,
+                           const int32_t* seq_lens, void* summaries, const int32_t* build_list,
+                           int32_t n_build, int32_t* out_page_ids, float* out_sel_lse, float* out,
+                           float* out_lse, void* ws, size_t ws_bytes, void* stream) {
+  return decode_step_impl(cfg, kivi, q, k_cache, v_cache, page_table, seq_lens, summaries,
+                          build_list, n_build, out_page_ids, out_sel_lse, out, out_lse, ws,
+                          ws_bytes, stream);
 }
 
 const char* locks_strerror(int status) {

@@ -67,6 +67,15 @@ class Config:
                     self.num_blocks, self.kv_dtype, self.q_dtype, self.basis)
 
 
+LOCKS_KIVI_POST = 0
+LOCKS_KIVI_PRE = 1
+
+
+class Kivi(ctypes.Structure):
+    """KIVI fake quantisation of finalised pages: bits, value channel group, stage."""
+    _fields_ = [("bits", ctypes.c_int32), ("v_group", ctypes.c_int32), ("stage", ctypes.c_int32)]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _SZ = ctypes.c_size_t
@@ -90,6 +99,11 @@ _SIGS = {
                                           _SZ, _P]),
     "locks_decode_step": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P, _I,
                                          _P, _P, _P, _P, _P, _SZ, _P]),
+    "locks_kivi_quantize": (ctypes.c_int, [ctypes.POINTER(_Cfg), ctypes.POINTER(Kivi), _P, _P, _P,
+                                           _P, _P, _I, _P]),
+    "locks_decode_step_kivi": (ctypes.c_int, [ctypes.POINTER(_Cfg), ctypes.POINTER(Kivi), _P, _P,
+                                              _P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _P, _SZ,
+                                              _P]),
     "locks_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "locks_last_hip_error": (ctypes.c_int, []),
 }
@@ -245,18 +259,36 @@ def dense_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, ws, out
 
 def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summaries, ws,
                 build_list: Optional[torch.Tensor] = None, out_ids=None, out_sel_lse=None,
-                out=None, out_lse=None, stream=None):
+                out=None, out_lse=None, stream=None, kivi: Optional[Kivi] = None):
+    """The fused step; with `kivi` the listed pages are KIVI fake-quantised in place
+    (before or after their build, per kivi.stage) -- locks_decode_step_kivi."""
     if out_ids is None:
         out_ids, out_sel_lse = alloc_select_outputs(cfg, q.device)
     if out is None:
         out, out_lse = alloc_attend_outputs(cfg, q.device)
     n = 0 if build_list is None else int(build_list.shape[0])
     c = cfg.c()
-    _check(lib().locks_decode_step(ctypes.byref(c), _ptr(q), _ptr(k_cache), _ptr(v_cache),
-                                   _ptr(page_table), _ptr(seq_lens), _ptr(summaries),
-                                   _ptr(build_list), n, _ptr(out_ids), _ptr(out_sel_lse),
-                                   _ptr(out), _ptr(out_lse), _ptr(ws), ws.numel(), _stream(stream)))
+    args = (_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table), _ptr(seq_lens),
+            _ptr(summaries), _ptr(build_list), n, _ptr(out_ids), _ptr(out_sel_lse), _ptr(out),
+            _ptr(out_lse), _ptr(ws), ws.numel(), _stream(stream))
+    if kivi is None:
+        _check(lib().locks_decode_step(ctypes.byref(c), *args))
+    else:
+        _check(lib().locks_decode_step_kivi(ctypes.byref(c), ctypes.byref(kivi), *args))
     return out_ids, out_sel_lse, out, out_lse
+
+
+def kivi_quantize(cfg: Config, kivi: Kivi, k_cache, v_cache, page_table, seq_lens,
+                  page_list: Optional[torch.Tensor] = None, stream=None):
+    """KIVI fake quantisation, in place, of every complete page (page_list None) or of
+    the listed (seq, page) pairs [n][2] int32 -- locks_kivi_quantize."""
+    n = 0 if page_list is None else int(page_list.shape[0])
+    if page_list is not None and n == 0:
+        return                      # an empty list names no page (NULL would mean all)
+    c = cfg.c()
+    _check(lib().locks_kivi_quantize(ctypes.byref(c), ctypes.byref(kivi), _ptr(k_cache),
+                                     _ptr(v_cache), _ptr(page_table), _ptr(seq_lens),
+                                     _ptr(page_list), n, _stream(stream)))
 
 
 def config_for(spec, num_blocks: int, max_pages: int) -> Config:

@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 16
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGS), "binding and header disagree"
@@ -124,3 +124,51 @@ def test_workspace_grows_with_shape(lib):
     small = cfg().c()
     big = cfg(max_pages_per_seq=4096).c()
     assert lib.locks_workspace_bytes(ctypes.byref(big)) > lib.locks_workspace_bytes(ctypes.byref(small))
+
+
+@pytest.mark.parametrize("kv,code", [
+    (dict(bits=0), -1), (dict(bits=9), -1), (dict(v_group=24), -1), (dict(v_group=256), -1),
+    (dict(v_group=4), -1), (dict(stage=2), -1), (dict(stage=-1), -1),
+])
+def test_kivi_bad_arguments_are_rejected_before_launch(lib, kv, code):
+    c = cfg().c()
+    k = B.Kivi(4, 32, B.LOCKS_KIVI_POST)
+    for name, val in kv.items():
+        setattr(k, name, val)
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.locks_kivi_quantize(ctypes.byref(c), ctypes.byref(k), fake, fake, fake, fake, None, 0,
+                                   None) == code
+    need = lib.locks_workspace_bytes(ctypes.byref(c))
+    assert lib.locks_decode_step_kivi(ctypes.byref(c), ctypes.byref(k), fake, fake, fake, fake, fake,
+                                      fake, fake, 1, fake, fake, fake, None, fake, need, None) == code
+
+
+def test_kivi_null_pointers_dtype_and_empty_batch(lib):
+    c = cfg().c()
+    k = B.Kivi(2, 32, B.LOCKS_KIVI_PRE)
+    fake = ctypes.c_void_p(0x1000)
+    q = lib.locks_kivi_quantize
+    assert q(ctypes.byref(c), None, fake, fake, fake, fake, None, 0, None) == -1
+    assert q(ctypes.byref(c), ctypes.byref(k), None, fake, fake, fake, None, 0, None) == -1
+    assert q(ctypes.byref(c), ctypes.byref(k), fake, fake, fake, None, None, 0, None) == -1
+    assert q(ctypes.byref(c), ctypes.byref(k), fake, fake, fake, fake, None, 3, None) == -1
+    assert q(ctypes.byref(c), ctypes.byref(k), fake, fake, fake, fake, fake, -1, None) == -1
+    # fake quantisation rounds to bfloat16: an fp32 cache is not supported
+    c32 = cfg(kv_dtype=B.LOCKS_FP32, q_dtype=B.LOCKS_FP32).c()
+    assert q(ctypes.byref(c32), ctypes.byref(k), fake, fake, fake, fake, None, 0, None) == -2
+    need32 = lib.locks_workspace_bytes(ctypes.byref(c32))
+    assert lib.locks_decode_step_kivi(ctypes.byref(c32), ctypes.byref(k), fake, fake, fake, fake,
+                                      fake, fake, fake, 1, fake, fake, fake, None, fake, need32,
+                                      None) == -2
+    # no sequences: nothing launched
+    c0 = cfg(num_seqs=0).c()
+    assert q(ctypes.byref(c0), ctypes.byref(k), fake, fake, fake, fake, None, 0, None) == 0
+    need0 = lib.locks_workspace_bytes(ctypes.byref(c0))
+    ws = ctypes.c_void_p(0x10000)
+    assert lib.locks_decode_step_kivi(ctypes.byref(c0), ctypes.byref(k), fake, fake, fake, fake,
+                                      fake, fake, None, 0, fake, fake, fake, None, ws, need0,
+                                      None) == 0
+    # a null kivi is the plain step (its own argument checks apply)
+    need = lib.locks_workspace_bytes(ctypes.byref(c))
+    assert lib.locks_decode_step_kivi(ctypes.byref(c), None, None, fake, fake, fake, fake, fake,
+                                      None, 0, fake, fake, fake, None, fake, need, None) == -1
