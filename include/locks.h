@@ -262,9 +262,11 @@ int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* 
 /* locks_decode_step on a KIVI-quantised cache: the n_build listed pages (the
  * pages that were finalised this step) are fake-quantised as locks_kivi_quantize
  * does, before their summary build (kivi->stage == LOCKS_KIVI_PRE) or after it
- * (LOCKS_KIVI_POST), and in both cases before the attention reads them; the rest
- * of the step is locks_decode_step's.  kivi == NULL is locks_decode_step itself.
- * The caches must be bf16 when kivi is given (else LOCKS_E_UNSUPPORTED). */
+ * (LOCKS_KIVI_POST), and in both cases before the attention reads them; each
+ * page is quantised on the stream that builds it, so when the step builds the
+ * last pages beside the scan their quantisation runs beside the scan too.  The
+ * rest of the step is locks_decode_step's.  kivi == NULL is locks_decode_step
+ * itself.  The caches must be bf16 when kivi is given (else LOCKS_E_UNSUPPORTED). */
 int locks_decode_step_kivi(const locks_cfg_t* cfg, const locks_kivi_t* kivi, const void* q,
                            void* k_cache, void* v_cache, const int32_t* page_table,
                            const int32_t* seq_lens, void* summaries,

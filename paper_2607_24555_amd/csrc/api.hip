@@ -299,22 +299,20 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_kivi_t* kivi, co
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  // KIVI finalisation of the listed pages: PRE before anything reads them, POST
-  // once their builds are enqueued (and, with the forked scan, once it is joined).
+  // KIVI finalisation of the listed pages, always on the stream that builds them:
+  // PRE right before their build, POST right after it; either way before the
+  // attention reads them.
   if (!kivi || n_build == 0) kivi = nullptr;
   void* kq = const_cast<void*>(k_cache);
   void* vq = const_cast<void*>(v_cache);
-  if (kivi && kivi->stage == LOCKS_KIVI_PRE) {
-    rc = hip_status(launch_kivi(*cfg, *kivi, kq, vq, page_table, seq_lens, build_list, n_build,
-                                false, st));
-    if (rc) return rc;
-  }
-  const bool post = kivi && kivi->stage == LOCKS_KIVI_POST;
-  auto post_kivi = [&]() -> int {
-    if (!post) return LOCKS_OK;
-    return hip_status(launch_kivi(*cfg, *kivi, kq, vq, page_table, seq_lens, build_list, n_build,
-                                  false, st));
+  auto kivi_at = [&](int stage, hipStream_t on, KiviPages which) -> hipError_t {
+    if (!kivi || kivi->stage != stage) return hipSuccess;
+    return launch_kivi(*cfg, *kivi, kq, vq, page_table, seq_lens, build_list, n_build, false, on,
+                       which);
   };
+  const bool forked = attend_select_fused(*cfg) && n_build > 0 && cfg->basis == LOCKS_BASIS_INT4;
+  if (!forked && (rc = hip_status(kivi_at(LOCKS_KIVI_PRE, st, kKiviAny)))) return rc;
+  auto post_kivi = [&]() -> int { return hip_status(kivi_at(LOCKS_KIVI_POST, st, kKiviAny)); };
   const WsPlan p = plan_workspace(*cfg);
   const Ws w = carve(ws, p);
   const int k = page_budget(*cfg);
@@ -346,18 +344,21 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_kivi_t* kivi, co
       hipError_t e = side_stream(&side);
       if (e == hipSuccess) e = hipEventRecord(side->fork, st);
       if (e == hipSuccess) e = hipStreamWaitEvent(side->st, side->fork, 0);
+      if (e == hipSuccess) e = kivi_at(LOCKS_KIVI_PRE, st, kKiviLast);
       if (e == hipSuccess)
         e = launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false, summaries,
                          nullptr, nullptr, nullptr, nullptr, st, kBuildLast, &bs);
+      if (e == hipSuccess) e = kivi_at(LOCKS_KIVI_POST, st, kKiviLast);
+      if (e == hipSuccess) e = kivi_at(LOCKS_KIVI_PRE, side->st, kKiviInner);
       if (e == hipSuccess)
         e = launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false, summaries,
                          nullptr, nullptr, nullptr, nullptr, side->st, kBuildInner, &bs);
+      if (e == hipSuccess) e = kivi_at(LOCKS_KIVI_POST, side->st, kKiviInner);
       if (e == hipSuccess)
         e = launch_scan(*cfg, q, summaries, page_table, w.sl_scan, w.s_hat, lay, w.part, side->st);
       if (e == hipSuccess) e = hipEventRecord(side->join, side->st);
       if (e == hipSuccess) e = hipStreamWaitEvent(st, side->join, 0);
       if ((rc = hip_status(e))) return rc;
-      if ((rc = post_kivi())) return rc;
       part_x = w.part_x;
     } else {
       rc = hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, w.s_hat, lay, w.part,

@@ -42,7 +42,7 @@ __global__ __launch_bounds__(64 * kKiviWaves) void kivi_kernel(
     uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ page_list, long n_units, int all_pages, int num_seqs,
-    int num_kv_heads, int max_pages, float levels) {
+    int num_kv_heads, int max_pages, float levels, int which) {
   const long unit = (long)blockIdx.x * kKiviWaves + (threadIdx.x >> 6);
   if (unit >= n_units) return;
   const int lane = threadIdx.x & 63;
@@ -57,7 +57,9 @@ __global__ __launch_bounds__(64 * kKiviWaves) void kivi_kernel(
     j = page_list[2 * item + 1];
     if (s < 0 || s >= num_seqs || j >= max_pages) return;
   }
-  if (j < 0 || j >= seq_lens[s] / kPage) return;  // only complete pages are finalised
+  const int n_complete = seq_lens[s] / kPage;
+  if (j < 0 || j >= n_complete) return;  // only complete pages are finalised
+  if (which != kKiviAny && (j == n_complete - 1) != (which == kKiviLast)) return;
   const long blk = page_table[(long)s * max_pages + j];
   const size_t base = ((size_t)blk * num_kv_heads + h) * (kPage * kDim);
   const int cg = lane & 15, tg = lane >> 4;
@@ -161,7 +163,7 @@ bool kivi_valid(const locks_kivi_t& kv) {
 hipError_t launch_kivi(const locks_cfg_t& c, const locks_kivi_t& kv, void* k_cache,
                        void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
                        const int32_t* page_list, int32_t n_items, bool all_pages,
-                       hipStream_t st) {
+                       hipStream_t st, KiviPages which) {
   const long items = all_pages ? (long)c.num_seqs * c.max_pages_per_seq : (long)n_items;
   const long units = items * c.num_kv_heads;
   if (units <= 0) return hipSuccess;
@@ -173,7 +175,7 @@ hipError_t launch_kivi(const locks_cfg_t& c, const locks_kivi_t& kv, void* k_cac
 #define LOCKS_KIVI_LAUNCH(GL)                                                              \
   hipLaunchKernelGGL(kivi_kernel<GL>, grid, block, 0, st, kc, vc, page_table, seq_lens,    \
                      page_list, units, all, c.num_seqs, c.num_kv_heads, c.max_pages_per_seq, \
-                     levels)
+                     levels, (int)which)
   switch (kv.v_group) {
     case 8: LOCKS_KIVI_LAUNCH(1); break;
     case 16: LOCKS_KIVI_LAUNCH(2); break;

@@ -190,11 +190,14 @@ hipError_t launch_attend_select(const locks_cfg_t& c, const void* q, const void*
                                 float* out_lse, hipStream_t st);
 
 // KIVI fake quantisation of the listed (seq, page) pairs' K and V, or of every
-// complete page when all_pages (bf16 caches).
+// complete page when all_pages (bf16 caches).  `which` narrows the pages to the
+// last complete page of each sequence (kKiviLast) or to the others (kKiviInner),
+// the split of a decode step's builds.
+enum KiviPages { kKiviAny = 0, kKiviLast = 1, kKiviInner = 2 };
 bool kivi_valid(const locks_kivi_t& kv);
 hipError_t launch_kivi(const locks_cfg_t& c, const locks_kivi_t& kv, void* k_cache,
                        void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
                        const int32_t* page_list, int32_t n_items, bool all_pages,
-                       hipStream_t st);
+                       hipStream_t st, KiviPages which = kKiviAny);
 
 }  // namespace locks

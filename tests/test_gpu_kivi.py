@@ -152,8 +152,8 @@ def _finalised_state(d, w, listed, kv, stage):
 
 
 @pytest.mark.parametrize("stage", [B.LOCKS_KIVI_POST, B.LOCKS_KIVI_PRE])
-@pytest.mark.parametrize("bits", [4, 2])
-def test_decode_step_on_quantised_cache(stage, bits):
+@pytest.mark.parametrize("bits,inner", [(4, False), (2, False), (4, True)])
+def test_decode_step_on_quantised_cache(stage, bits, inner):
     """The fused step with the pages that filled this step in its build list: the
     listed pages are quantised before (PRE) or after (POST) their build, the caches
     afterwards equal the oracle's quantised caches bit for bit, and tables and
@@ -165,6 +165,8 @@ def test_decode_step_on_quantised_cache(stage, bits):
     d = Dev(w)
     cfg = d.cfg
     listed = [(s, int(w.seq_lens[s]) // PAGE - 1) for s in range(spec.num_seqs)]
+    if inner:   # pages other than the last complete one (built on the forked stream)
+        listed += [(0, 7), (2, int(w.seq_lens[2]) // PAGE - 2), (3, 40)]
     kv = B.Kivi(bits, 32, stage)
     name = "POST" if stage == B.LOCKS_KIVI_POST else "PRE"
     print(f"[kivi step] {name} bits {bits} listed {listed}", flush=True)

@@ -10,8 +10,8 @@ import torch
 
 from oracle import locks_oracle as O
 from paper_2607_24555_amd import locks as B
-from tests._gpu_common import (GAP_TOL, LSE_TOL, OUT_TOL, OVERLAP_TOL, Dev, ids_of, rel_l2,
-                               selection_agreement)
+from tests._gpu_common import (GAP_TOL, LSE_TOL, OUT_TOL, OVERLAP_TOL, Dev, ids_of, parse_codes,
+                               rel_l2, selection_agreement)
 from workloads import WorkloadSpec, build_workload, config_spec, make_workload
 
 pytestmark = pytest.mark.gpu
@@ -192,19 +192,6 @@ def test_decode_step_with_gpu_built_summaries(case):
     assert inter / max(tot, 1) >= OVERLAP_TOL
 
 
-def _parse_codes(rec, r):
-    """Integer codes of records laid out as include/locks.h documents (test-local)."""
-    rec = rec.astype(np.int64)
-    v = np.empty((rec.shape[0], 128, r), np.int64)
-    for l in range(r):
-        b = rec[:, 64 * l:64 * l + 64]
-        v[:, 0::2, l] = (b & 15) - 8
-        v[:, 1::2, l] = (b >> 4) - 8
-    c = rec[:, 64 * r:80 * r] - 128
-    m = rec[:, 80 * r:80 * r + 128] - 128
-    return {"vcodes": v, "ccodes": c, "mcodes": m}
-
-
 def test_build_codes_match_oracle(case):
     """GPU-built records against oracle-built records: every code within +-1 and at
     least 99.9% identical on pages with a clear spectral gap at r."""
@@ -226,8 +213,8 @@ def test_build_codes_match_oracle(case):
             lam = f["sigma2"]
             gapped = (lam[:, r - 1] - lam[:, r]) > 1e-3 * lam[:, r - 1]
             blocks = d.w.page_table[s, :n_c].long().to(d.device)
-            got = _parse_codes(store[blocks, h].cpu().numpy(), r)
-            want = _parse_codes(rec, r)
+            got = parse_codes(store[blocks, h].cpu().numpy(), r)
+            want = parse_codes(rec, r)
             for key in ("vcodes", "ccodes", "mcodes"):
                 a, b = got[key][gapped], want[key][gapped]
                 assert np.max(np.abs(a - b)) <= 1, (key, s, h)
