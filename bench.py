@@ -42,6 +42,9 @@ def parse():
                          "groups of 32 channels): every complete page before timing, and in the "
                          "reasoning loop the pages that fill, inside the step")
     ap.add_argument("--kivi-stage", choices=("post", "pre"), default="post")
+    ap.add_argument("--torch-kv-write", action="store_true",
+                    help="reasoning loop: write the new token's K and V with torch copies "
+                         "before the step instead of inside it")
     ap.add_argument("--no-kivi-pass", action="store_true",
                     help="skip the separately timed KIVI pass over every complete page")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
@@ -304,11 +307,16 @@ def main():
         def step(_i):
             i = calls[0]
             calls[0] += 1
-            k_rows.index_copy_(0, flat[i], new_k[i].view(-1, 128))
-            v_rows.index_copy_(0, flat[i], new_v[i].view(-1, 128))
             sl.add_(1)
-            B.decode_step(cfg, q, ks[0], vs[0], pt, sl, summ[0], ws, build_list=lists[i],
-                          out_ids=ids, out_sel_lse=sel, out=out, out_lse=lse, kivi=kivi)
+            if args.torch_kv_write:
+                k_rows.index_copy_(0, flat[i], new_k[i].view(-1, 128))
+                v_rows.index_copy_(0, flat[i], new_v[i].view(-1, 128))
+                B.decode_step(cfg, q, ks[0], vs[0], pt, sl, summ[0], ws, build_list=lists[i],
+                              out_ids=ids, out_sel_lse=sel, out=out, out_lse=lse, kivi=kivi)
+            else:   # the step writes the new token's K and V itself, beside the scan
+                B.decode_step(cfg, q, ks[0], vs[0], pt, sl, summ[0], ws, build_list=lists[i],
+                              out_ids=ids, out_sel_lse=sel, out=out, out_lse=lse, kivi=kivi,
+                              k_new=new_k[i], v_new=new_v[i])
 
     if growing and args.graph:
         raise SystemExit("--graph replays fixed launches; the reasoning workload grows every step")
@@ -372,7 +380,10 @@ def main():
                  "launch": "hip-graph replay" if args.graph else "eager",
                  "selected_pages_per_kv_head": k_sel,
                  "pages_built_inline": n_built if growing else None,
-                 "includes_kv_append": growing},
+                 "includes_kv_append": growing,
+                 "kv_append": (None if not growing else
+                               "torch index_copy before the step" if args.torch_kv_write else
+                               "inside the step (locks_decode_step_ex)")},
         "dense": None if dense_us is None else {
             "us": round(dense_us, 2), "bytes": n_pages * cfg.num_kv_heads * kv_page,
             "GBps": round(n_pages * cfg.num_kv_heads * kv_page / (dense_us * 1e-6) / 1e9, 1),

@@ -259,20 +259,41 @@ int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* 
                         void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
                         const int32_t* page_list, int32_t n_pages, void* stream);
 
-/* locks_decode_step on a KIVI-quantised cache: the n_build listed pages (the
- * pages that were finalised this step) are fake-quantised as locks_kivi_quantize
- * does, before their summary build (kivi->stage == LOCKS_KIVI_PRE) or after it
- * (LOCKS_KIVI_POST), and in both cases before the attention reads them; each
- * page is quantised on the stream that builds it, so when the step builds the
- * last pages beside the scan their quantisation runs beside the scan too.  The
- * rest of the step is locks_decode_step's.  kivi == NULL is locks_decode_step
- * itself.  The caches must be bf16 when kivi is given (else LOCKS_E_UNSUPPORTED). */
-int locks_decode_step_kivi(const locks_cfg_t* cfg, const locks_kivi_t* kivi, const void* q,
-                           void* k_cache, void* v_cache, const int32_t* page_table,
-                           const int32_t* seq_lens, void* summaries,
-                           const int32_t* build_list, int32_t n_build,
-                           int32_t* out_page_ids, float* out_sel_lse, float* out,
-                           float* out_lse, void* ws, size_t ws_bytes, void* stream);
+/* The caller's KV write of a decode step (App. E: the new token's KV write is
+ * scheduled beside the selection): for every sequence s with seq_lens[s] >= 1,
+ * the key and value rows k_new[s][h], v_new[s][h] ([num_seqs][num_kv_heads][128],
+ * kv_dtype) are copied into the slot of token seq_lens[s] - 1, i.e. logical page
+ * (seq_lens[s] - 1) / 16 (its block must be in page_table), row (seq_lens[s] - 1)
+ * % 16, of every KV head.  seq_lens already counts the new token; nothing else is
+ * written.  Returns LOCKS_E_INVAL for a null argument. */
+int locks_append_kv(const locks_cfg_t* cfg, const void* k_new, const void* v_new,
+                    void* k_cache, void* v_cache, const int32_t* page_table,
+                    const int32_t* seq_lens, void* stream);
+
+/* Options of locks_decode_step_ex; all fields NULL is locks_decode_step. */
+typedef struct locks_step_opts {
+  const locks_kivi_t* kivi;  /* NULL, or KIVI fake quantisation of the listed pages */
+  const void* k_new;         /* NULL, or this step's new key and value rows, as     */
+  const void* v_new;         /* locks_append_kv takes them (both or neither)        */
+} locks_step_opts_t;
+
+/* locks_decode_step with the new token's KV write and KV-cache quantisation folded
+ * in.  With k_new / v_new the step first writes each sequence's newest token as
+ * locks_append_kv does (seq_lens already counting it); when the step builds the
+ * last complete pages beside the scan, this write runs beside the scan too, on
+ * `stream` before those builds.  With kivi the n_build listed pages (the pages
+ * finalised this step) are fake-quantised as locks_kivi_quantize does, before
+ * their summary build (kivi->stage == LOCKS_KIVI_PRE) or after it
+ * (LOCKS_KIVI_POST), each on the stream that builds it, and before the attention
+ * reads them (kivi requires bf16 caches, else LOCKS_E_UNSUPPORTED).  The rest of
+ * the step is locks_decode_step's; opts == NULL is locks_decode_step itself.
+ * Returns LOCKS_E_INVAL when exactly one of k_new, v_new is given. */
+int locks_decode_step_ex(const locks_cfg_t* cfg, const locks_step_opts_t* opts, const void* q,
+                         void* k_cache, void* v_cache, const int32_t* page_table,
+                         const int32_t* seq_lens, void* summaries,
+                         const int32_t* build_list, int32_t n_build,
+                         int32_t* out_page_ids, float* out_sel_lse, float* out,
+                         float* out_lse, void* ws, size_t ws_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* locks_strerror(int status);

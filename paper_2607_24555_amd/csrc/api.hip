@@ -284,7 +284,18 @@ int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* 
                                 n_pages, page_list == nullptr, static_cast<hipStream_t>(stream)));
 }
 
-static int decode_step_impl(const locks_cfg_t* cfg, const locks_kivi_t* kivi, const void* q,
+int locks_append_kv(const locks_cfg_t* cfg, const void* k_new, const void* v_new, void* k_cache,
+                    void* v_cache, const int32_t* page_table, const int32_t* seq_lens,
+                    void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!k_new || !v_new || !k_cache || !v_cache || !page_table || !seq_lens) return LOCKS_E_INVAL;
+  if (cfg->num_seqs == 0) return LOCKS_OK;
+  return hip_status(launch_append(*cfg, k_new, v_new, k_cache, v_cache, page_table, seq_lens,
+                                  static_cast<hipStream_t>(stream)));
+}
+
+static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opts, const void* q,
                             const void* k_cache, const void* v_cache, const int32_t* page_table,
                             const int32_t* seq_lens, void* summaries, const int32_t* build_list,
                             int32_t n_build, int32_t* out_page_ids, float* out_sel_lse,
@@ -294,6 +305,10 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_kivi_t* kivi, co
   if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !summaries || !out_page_ids ||
       !out_sel_lse || !out || n_build < 0 || (n_build > 0 && !build_list))
     return LOCKS_E_INVAL;
+  const locks_kivi_t* kivi = opts ? opts->kivi : nullptr;
+  const void* k_new = opts ? opts->k_new : nullptr;
+  const void* v_new = opts ? opts->v_new : nullptr;
+  if ((k_new == nullptr) != (v_new == nullptr)) return LOCKS_E_INVAL;
   if (kivi && cfg->kv_dtype != LOCKS_BF16) return LOCKS_E_UNSUPPORTED;
   if (kivi && !kivi_valid(*kivi)) return LOCKS_E_INVAL;
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
@@ -310,7 +325,13 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_kivi_t* kivi, co
     return launch_kivi(*cfg, *kivi, kq, vq, page_table, seq_lens, build_list, n_build, false, on,
                        which);
   };
+  // the new token's KV write: beside the scan when the step forks it, else first
+  auto append = [&]() -> hipError_t {
+    if (!k_new) return hipSuccess;
+    return launch_append(*cfg, k_new, v_new, kq, vq, page_table, seq_lens, st);
+  };
   const bool forked = attend_select_fused(*cfg) && n_build > 0 && cfg->basis == LOCKS_BASIS_INT4;
+  if (!forked && (rc = hip_status(append()))) return rc;
   if (!forked && (rc = hip_status(kivi_at(LOCKS_KIVI_PRE, st, kKiviAny)))) return rc;
   auto post_kivi = [&]() -> int { return hip_status(kivi_at(LOCKS_KIVI_POST, st, kKiviAny)); };
   const WsPlan p = plan_workspace(*cfg);
@@ -344,6 +365,7 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_kivi_t* kivi, co
       hipError_t e = side_stream(&side);
       if (e == hipSuccess) e = hipEventRecord(side->fork, st);
       if (e == hipSuccess) e = hipStreamWaitEvent(side->st, side->fork, 0);
+      if (e == hipSuccess) e = append();
       if (e == hipSuccess) e = kivi_at(LOCKS_KIVI_PRE, st, kKiviLast);
       if (e == hipSuccess)
         e = launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false, summaries,
@@ -395,12 +417,12 @@ int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache
                           ws_bytes, stream);
 }
 
-int locks_decode_step_kivi(const locks_cfg_t* cfg, const locks_kivi_t* kivi, const void* q,
-                           void* k_cache, void* v_cache, const int32_t* page_table,
-                           const int32_t* seq_lens, void* summaries, const int32_t* build_list,
-                           int32_t n_build, int32_t* out_page_ids, float* out_sel_lse, float* out,
-                           float* out_lse, void* ws, size_t ws_bytes, void* stream) {
-  return decode_step_impl(cfg, kivi, q, k_cache, v_cache, page_table, seq_lens, summaries,
+int locks_decode_step_ex(const locks_cfg_t* cfg, const locks_step_opts_t* opts, const void* q,
+                         void* k_cache, void* v_cache, const int32_t* page_table,
+                         const int32_t* seq_lens, void* summaries, const int32_t* build_list,
+                         int32_t n_build, int32_t* out_page_ids, float* out_sel_lse, float* out,
+                         float* out_lse, void* ws, size_t ws_bytes, void* stream) {
+  return decode_step_impl(cfg, opts, q, k_cache, v_cache, page_table, seq_lens, summaries,
                           build_list, n_build, out_page_ids, out_sel_lse, out, out_lse, ws,
                           ws_bytes, stream);
 }

@@ -200,4 +200,10 @@ hipError_t launch_kivi(const locks_cfg_t& c, const locks_kivi_t& kv, void* k_cac
                        const int32_t* page_list, int32_t n_items, bool all_pages,
                        hipStream_t st, KiviPages which = kKiviAny);
 
+// The newest token of every sequence (token seq_lens[s] - 1, skipped for an empty
+// sequence) copied from k_new / v_new [S][H_kv][128] into the paged caches.
+hipError_t launch_append(const locks_cfg_t& c, const void* k_new, const void* v_new,
+                         void* k_cache, void* v_cache, const int32_t* page_table,
+                         const int32_t* seq_lens, hipStream_t st);
+
 }  // namespace locks

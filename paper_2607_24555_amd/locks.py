@@ -76,6 +76,12 @@ class Kivi(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32), ("v_group", ctypes.c_int32), ("stage", ctypes.c_int32)]
 
 
+class StepOpts(ctypes.Structure):
+    """Options of locks_decode_step_ex: KIVI, and the step's new KV rows."""
+    _fields_ = [("kivi", ctypes.POINTER(Kivi)), ("k_new", ctypes.c_void_p),
+                ("v_new", ctypes.c_void_p)]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _SZ = ctypes.c_size_t
@@ -101,9 +107,10 @@ _SIGS = {
                                          _P, _P, _P, _P, _P, _SZ, _P]),
     "locks_kivi_quantize": (ctypes.c_int, [ctypes.POINTER(_Cfg), ctypes.POINTER(Kivi), _P, _P, _P,
                                            _P, _P, _I, _P]),
-    "locks_decode_step_kivi": (ctypes.c_int, [ctypes.POINTER(_Cfg), ctypes.POINTER(Kivi), _P, _P,
-                                              _P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _P, _SZ,
-                                              _P]),
+    "locks_decode_step_ex": (ctypes.c_int, [ctypes.POINTER(_Cfg), ctypes.POINTER(StepOpts), _P,
+                                            _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _P, _SZ,
+                                            _P]),
+    "locks_append_kv": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P]),
     "locks_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "locks_last_hip_error": (ctypes.c_int, []),
 }
@@ -259,9 +266,12 @@ def dense_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, ws, out
 
 def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summaries, ws,
                 build_list: Optional[torch.Tensor] = None, out_ids=None, out_sel_lse=None,
-                out=None, out_lse=None, stream=None, kivi: Optional[Kivi] = None):
-    """The fused step; with `kivi` the listed pages are KIVI fake-quantised in place
-    (before or after their build, per kivi.stage) -- locks_decode_step_kivi."""
+                out=None, out_lse=None, stream=None, kivi: Optional[Kivi] = None,
+                k_new=None, v_new=None):
+    """The fused step.  With `kivi` the listed pages are KIVI fake-quantised in place
+    (before or after their build, per kivi.stage); with k_new / v_new [S][H_kv][128]
+    the step first writes each sequence's newest token (seq_lens counting it) --
+    locks_decode_step_ex."""
     if out_ids is None:
         out_ids, out_sel_lse = alloc_select_outputs(cfg, q.device)
     if out is None:
@@ -271,11 +281,21 @@ def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summarie
     args = (_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table), _ptr(seq_lens),
             _ptr(summaries), _ptr(build_list), n, _ptr(out_ids), _ptr(out_sel_lse), _ptr(out),
             _ptr(out_lse), _ptr(ws), ws.numel(), _stream(stream))
-    if kivi is None:
+    if kivi is None and k_new is None and v_new is None:
         _check(lib().locks_decode_step(ctypes.byref(c), *args))
     else:
-        _check(lib().locks_decode_step_kivi(ctypes.byref(c), ctypes.byref(kivi), *args))
+        opts = StepOpts(ctypes.pointer(kivi) if kivi is not None else None, _ptr(k_new),
+                        _ptr(v_new))
+        _check(lib().locks_decode_step_ex(ctypes.byref(c), ctypes.byref(opts), *args))
     return out_ids, out_sel_lse, out, out_lse
+
+
+def append_kv(cfg: Config, k_new, v_new, k_cache, v_cache, page_table, seq_lens, stream=None):
+    """Write each sequence's newest token (token seq_lens[s] - 1) from k_new / v_new
+    [S][H_kv][128] into the paged caches -- locks_append_kv."""
+    c = cfg.c()
+    _check(lib().locks_append_kv(ctypes.byref(c), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
+                                 _ptr(v_cache), _ptr(page_table), _ptr(seq_lens), _stream(stream)))
 
 
 def kivi_quantize(cfg: Config, kivi: Kivi, k_cache, v_cache, page_table, seq_lens,

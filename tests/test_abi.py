@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 17
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGS), "binding and header disagree"
@@ -139,8 +139,9 @@ def test_kivi_bad_arguments_are_rejected_before_launch(lib, kv, code):
     assert lib.locks_kivi_quantize(ctypes.byref(c), ctypes.byref(k), fake, fake, fake, fake, None, 0,
                                    None) == code
     need = lib.locks_workspace_bytes(ctypes.byref(c))
-    assert lib.locks_decode_step_kivi(ctypes.byref(c), ctypes.byref(k), fake, fake, fake, fake, fake,
-                                      fake, fake, 1, fake, fake, fake, None, fake, need, None) == code
+    o = B.StepOpts(ctypes.pointer(k), None, None)
+    assert lib.locks_decode_step_ex(ctypes.byref(c), ctypes.byref(o), fake, fake, fake, fake, fake,
+                                    fake, fake, 1, fake, fake, fake, None, fake, need, None) == code
 
 
 def test_kivi_null_pointers_dtype_and_empty_batch(lib):
@@ -157,18 +158,36 @@ def test_kivi_null_pointers_dtype_and_empty_batch(lib):
     c32 = cfg(kv_dtype=B.LOCKS_FP32, q_dtype=B.LOCKS_FP32).c()
     assert q(ctypes.byref(c32), ctypes.byref(k), fake, fake, fake, fake, None, 0, None) == -2
     need32 = lib.locks_workspace_bytes(ctypes.byref(c32))
-    assert lib.locks_decode_step_kivi(ctypes.byref(c32), ctypes.byref(k), fake, fake, fake, fake,
-                                      fake, fake, fake, 1, fake, fake, fake, None, fake, need32,
-                                      None) == -2
+    o = B.StepOpts(ctypes.pointer(k), None, None)
+    assert lib.locks_decode_step_ex(ctypes.byref(c32), ctypes.byref(o), fake, fake, fake, fake,
+                                    fake, fake, fake, 1, fake, fake, fake, None, fake, need32,
+                                    None) == -2
     # no sequences: nothing launched
     c0 = cfg(num_seqs=0).c()
     assert q(ctypes.byref(c0), ctypes.byref(k), fake, fake, fake, fake, None, 0, None) == 0
     need0 = lib.locks_workspace_bytes(ctypes.byref(c0))
     ws = ctypes.c_void_p(0x10000)
-    assert lib.locks_decode_step_kivi(ctypes.byref(c0), ctypes.byref(k), fake, fake, fake, fake,
-                                      fake, fake, None, 0, fake, fake, fake, None, ws, need0,
-                                      None) == 0
-    # a null kivi is the plain step (its own argument checks apply)
+    assert lib.locks_decode_step_ex(ctypes.byref(c0), ctypes.byref(o), fake, fake, fake, fake,
+                                    fake, fake, None, 0, fake, fake, fake, None, ws, need0,
+                                    None) == 0
+    # null options are the plain step (its own argument checks apply)
     need = lib.locks_workspace_bytes(ctypes.byref(c))
-    assert lib.locks_decode_step_kivi(ctypes.byref(c), None, None, fake, fake, fake, fake, fake,
-                                      None, 0, fake, fake, fake, None, fake, need, None) == -1
+    assert lib.locks_decode_step_ex(ctypes.byref(c), None, None, fake, fake, fake, fake, fake,
+                                    None, 0, fake, fake, fake, None, fake, need, None) == -1
+
+
+def test_append_and_step_options_are_checked(lib):
+    c = cfg().c()
+    fake = ctypes.c_void_p(0x1000)
+    ap = lib.locks_append_kv
+    assert ap(ctypes.byref(c), None, fake, fake, fake, fake, fake, None) == -1
+    assert ap(ctypes.byref(c), fake, None, fake, fake, fake, fake, None) == -1
+    assert ap(ctypes.byref(c), fake, fake, fake, fake, fake, None, None) == -1
+    assert ap(ctypes.byref(cfg(head_dim=64).c()), fake, fake, fake, fake, fake, fake, None) == -2
+    assert ap(ctypes.byref(cfg(num_seqs=0).c()), fake, fake, fake, fake, fake, fake, None) == 0
+    need = lib.locks_workspace_bytes(ctypes.byref(c))
+    for kn, vn in ((fake, None), (None, fake)):   # both new rows or neither
+        o = B.StepOpts(None, kn, vn)
+        assert lib.locks_decode_step_ex(ctypes.byref(c), ctypes.byref(o), fake, fake, fake, fake,
+                                        fake, fake, None, 0, fake, fake, fake, None, fake, need,
+                                        None) == -1
