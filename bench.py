@@ -84,11 +84,11 @@ SCAN_SOURCES = ("paper_2607_24555_amd/csrc/scan.hip", "paper_2607_24555_amd/csrc
 SCAN_TRAFFIC = {
     # workload: (sha256 of SCAN_SOURCES, FETCH_SIZE KiB, WRITE_SIZE KiB,
     #            copy FETCH factor, copy WRITE factor, profile file)
-    "1m": ("5b0ee560ea8f75ea", 55422.7, 9549.1, 0.500016, 1.0, "profiles/scan_1m_hbm_counters.md"),
-    "128k": ("5b0ee560ea8f75ea", 215220.5, 8728.5, 0.500016, 1.0, "profiles/scan_128k_hbm_counters.md"),
-    "128k-r2": ("5b0ee560ea8f75ea", 86731.6, 8915.8, 0.500015, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
-    "reasoning": ("5b0ee560ea8f75ea", 194574.8, 21060.2, 0.500015, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
-    "32k": ("5b0ee560ea8f75ea", 6774.2, 288.0, 0.500015, 1.0, "profiles/scan_32k_hbm_counters.md"),
+    "1m": ("8d99963bb7b2aee9", 55463.8, 9504.1, 0.500016, 1.0, "profiles/scan_1m_hbm_counters.md"),
+    "128k": ("8d99963bb7b2aee9", 215079.6, 8705.9, 0.500016, 1.0, "profiles/scan_128k_hbm_counters.md"),
+    "128k-r2": ("8d99963bb7b2aee9", 86690.5, 8914.9, 0.500016, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
+    "reasoning": ("8d99963bb7b2aee9", 194571.9, 21038.6, 0.500016, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
+    "32k": ("8d99963bb7b2aee9", 6774.2, 288.0, 0.500015, 1.0, "profiles/scan_32k_hbm_counters.md"),
 }
 
 
