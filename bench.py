@@ -84,11 +84,11 @@ SCAN_SOURCES = ("paper_2607_24555_amd/csrc/scan.hip", "paper_2607_24555_amd/csrc
 SCAN_TRAFFIC = {
     # workload: (sha256 of SCAN_SOURCES, FETCH_SIZE KiB, WRITE_SIZE KiB,
     #            copy FETCH factor, copy WRITE factor, profile file)
-    "1m": ("8d99963bb7b2aee9", 55463.8, 9504.1, 0.500016, 1.0, "profiles/scan_1m_hbm_counters.md"),
-    "128k": ("8d99963bb7b2aee9", 215079.6, 8705.9, 0.500016, 1.0, "profiles/scan_128k_hbm_counters.md"),
-    "128k-r2": ("8d99963bb7b2aee9", 86690.5, 8914.9, 0.500016, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
-    "reasoning": ("8d99963bb7b2aee9", 194571.9, 21038.6, 0.500016, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
-    "32k": ("8d99963bb7b2aee9", 6774.2, 288.0, 0.500015, 1.0, "profiles/scan_32k_hbm_counters.md"),
+    "1m": ("d263b7a576261335", 55610.2, 9468.7, 0.500015, 1.0, "profiles/scan_1m_hbm_counters.md"),
+    "128k": ("d263b7a576261335", 215102.7, 8729.0, 0.500015, 1.0, "profiles/scan_128k_hbm_counters.md"),
+    "128k-r2": ("d263b7a576261335", 86759.6, 8934.0, 0.500016, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
+    "reasoning": ("d263b7a576261335", 194688.8, 22087.2, 0.500016, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
+    "32k": ("d263b7a576261335", 6774.7, 288.0, 0.500015, 1.0, "profiles/scan_32k_hbm_counters.md"),
 }
 
 
