@@ -322,6 +322,77 @@ def test_select_matches_brute_force(G):
         assert _coverage_lib(q, keys, sel["ids"]).mean() == pytest.approx(best, abs=1e-12)
         if sel["gap"] > 1e-9:
             assert sel["ids"] == best_set
+        # the share-average key of each page is the group-mean coverage of that page
+        # alone (scipy softmax over every token), and the ranking gap is the log ratio
+        # of the weakest kept candidate to the strongest candidate left out of the
+        # brute-force optimum
+        share = np.array([_coverage_lib(q, keys, [j]).mean() for j in range(n)])
+        np.testing.assert_allclose(sel["log_mbar"], np.log(share), atol=1e-12, rtol=0)
+        if k >= 3:
+            kept = [j for j in best_set if 0 < j < n - 1]
+            left = [j for j in range(1, n - 1) if j not in best_set]
+            want_gap = math.log(min(share[kept])) - math.log(max(share[left]))
+            assert sel["gap"] == pytest.approx(want_gap, abs=1e-12)
+        else:
+            assert sel["gap"] == math.inf
+
+
+def test_select_gap_and_share_keys_by_hand():
+    """Values worked out by hand from the share-average combine (Sec. 4 "Score") and
+    the gap reading (log mbar of the (k-2)-th minus the (k-1)-th best candidate,
+    natural log).  An off-by-one in the cut index, a dropped -log G, a log base
+    other than e or a normaliser over the candidates only fails one of these."""
+    # G = 1, six complete pages with masses 1, 4, 2, 8, 3, 5 (Z = 23); k = 4 keeps
+    # two candidates of pages 1..4: page 3 (8/23) and page 1 (4/23); the next is
+    # page 4 (3/23), so the gap is ln(4/3).
+    s = np.log(np.array([[1.0, 4.0, 2.0, 8.0, 3.0, 5.0]]))
+    sel = O.select_pages(s, 6, 4)
+    assert sel["ids"] == [0, 1, 3, 5]
+    np.testing.assert_allclose(sel["log_mbar"], np.log(np.array([1, 4, 2, 8, 3, 5]) / 23.0),
+                               atol=1e-14, rtol=0)
+    assert sel["gap"] == pytest.approx(math.log(4.0 / 3.0), abs=1e-14)
+    # k = 5 keeps three (8, 4, 3 of 23); the next candidate holds 2/23: gap ln(3/2)
+    sel = O.select_pages(s, 6, 5)
+    assert sel["ids"] == [0, 1, 3, 4, 5]
+    assert sel["gap"] == pytest.approx(math.log(1.5), abs=1e-14)
+    # G = 2 with unequal normalisers.  Head 0 masses 1, 1, 1, 1, 1, 1 (Z = 6), head 1
+    # masses 1, 1/6, 1/3, 1/2, 2, 1/12 (Z = 49/12).
+    # Shares: head 0 all 1/6; head 1 (12/49)(1, 1/6, 1/3, 1/2, 2, 1/12)
+    #       = 12/49, 2/49, 4/49, 6/49, 24/49, 1/49.
+    # mbar = (1/2)(1/6 + head-1 share):
+    #   page 0: (49 + 72) / 588 = 121/588      page 1: (49 + 12) / 588 = 61/588
+    #   page 2: (49 + 24) / 588 = 73/588       page 3: (49 + 36) / 588 = 85/588
+    #   page 4: (49 + 144) / 588 = 193/588     page 5: (49 + 6) / 588 = 55/588
+    # (they sum to 1).  Candidates 1..4 ranked: 4, 3, 2, 1.  k = 4 keeps pages 4
+    # and 3; gap = ln(85/73).
+    h1 = np.array([1.0, 1 / 6, 1 / 3, 1 / 2, 2.0, 1 / 12])
+    s2 = np.log(np.stack([np.ones(6), h1]))
+    want = np.log(np.array([121, 61, 73, 85, 193, 55]) / 588.0)
+    sel = O.select_pages(s2, 6, 4)
+    np.testing.assert_allclose(sel["log_mbar"], want, atol=1e-14, rtol=0)
+    assert sel["ids"] == [0, 3, 4, 5]
+    assert sel["gap"] == pytest.approx(math.log(85 / 73), abs=1e-14)
+    # adding a constant to one head's scores changes neither shares nor table
+    sel_shift = O.select_pages(s2 + np.array([[3.0], [-7.0]]), 6, 4)
+    np.testing.assert_allclose(sel_shift["log_mbar"], want, atol=1e-13, rtol=0)
+    # G = 4, seven pages with a partial recent page (n = 7, six summarised): heads
+    # 0..3 are heads 0 and 1 above, twice, with page 6 carrying no score, so
+    # mbar of the summarised pages is as above and the candidates are pages 1..5;
+    # k = 3 keeps page 4 (193/588) against page 3 (85/588): gap ln(193/85).
+    s4 = np.concatenate([s2, s2])
+    sel = O.select_pages(s4, 7, 3)
+    np.testing.assert_allclose(sel["log_mbar"], want, atol=1e-14, rtol=0)
+    assert sel["ids"] == [0, 4, 6]
+    assert sel["gap"] == pytest.approx(math.log(193 / 85), abs=1e-14)
+    # an exact tie at the cut: pages 1 and 2 share one key; k = 3 keeps page 1
+    # (lower index) and the gap is 0
+    st = np.log(np.array([[5.0, 2.0, 2.0, 1.0]]))
+    sel = O.select_pages(st, 4, 3)
+    assert sel["ids"] == [0, 1, 3] and sel["gap"] == 0.0
+    # no cut: k = 2 keeps sink and recent only; n <= k keeps everything
+    assert O.select_pages(s, 6, 2)["gap"] == math.inf
+    assert O.select_pages(s, 6, 2)["ids"] == [0, 5]
+    assert O.select_pages(s, 6, 6)["gap"] == math.inf
 
 
 def test_select_g1_is_plain_ranking_and_small_n():
