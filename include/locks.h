@@ -213,11 +213,11 @@ int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cach
  * ordered after earlier work on `stream` and before later work on it.  With bf16
  * q and KV and a listed page that is the last complete page of its sequence, the
  * build of those pages runs on `stream` beside the scan of the others, which the
- * library enqueues on a side stream of its own (one per device, created on first
- * use -- make that first call outside stream capture -- and kept until the
- * process ends), forked from and joined back to `stream` by events, so a captured
- * step records the fork and join too; such calls on one device are serialised on
- * the host.  Outputs as in those calls. */
+ * library enqueues on a side stream of its own (one per device, created by
+ * locks_init or else on first use -- a call that creates it cannot be captured --
+ * and kept until the process ends), forked from and joined back to `stream` by
+ * events, so a captured step records the fork and join too; such calls on one
+ * device are serialised on the host.  Outputs as in those calls. */
 int locks_decode_step(const locks_cfg_t* cfg, const void* q, const void* k_cache,
                       const void* v_cache, const int32_t* page_table,
                       const int32_t* seq_lens, void* summaries,
@@ -294,6 +294,14 @@ int locks_decode_step_ex(const locks_cfg_t* cfg, const locks_step_opts_t* opts, 
                          const int32_t* build_list, int32_t n_build,
                          int32_t* out_page_ids, float* out_sel_lse, float* out,
                          float* out_lse, void* ws, size_t ws_bytes, void* stream);
+
+/* Set-up for the current device (App. E: the step replays from a captured graph):
+ * creates the device's side stream and its two events that locks_decode_step
+ * forks to, so that no later call creates them -- in particular none under stream
+ * capture.  Call it once per device, with that device current, before the first
+ * step that may be captured; calling it again is a no-op.  Returns LOCKS_E_HIP
+ * if the stream or an event cannot be created. */
+int locks_init(void);
 
 /* Static description of a status code. */
 const char* locks_strerror(int status);

@@ -70,16 +70,22 @@ constexpr int kMaxDevices = 64;
 std::mutex g_side_mu;  // also serialises the fork / join enqueues of one step
 SideStream g_side[kMaxDevices];
 
-hipError_t side_stream(SideStream** out) {
+// The current device's side stream, created here unless `create` is false (then
+// *out is null when it does not exist yet).  Callers hold g_side_mu.
+hipError_t side_stream(SideStream** out, bool create = true) {
+  *out = nullptr;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
   SideStream& ss = g_side[dev];
-  if (!ss.st) {
-    if ((e = hipStreamCreateWithFlags(&ss.st, hipStreamNonBlocking)) != hipSuccess) return e;
-    if ((e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess) return e;
-    if ((e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming)) != hipSuccess) return e;
+  if (!ss.st || !ss.fork || !ss.join) {
+    if (!create) return hipSuccess;
+    if (!ss.st && (e = hipStreamCreateWithFlags(&ss.st, hipStreamNonBlocking)) != hipSuccess) return e;
+    if (!ss.fork && (e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess)
+      return e;
+    if (!ss.join && (e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming)) != hipSuccess)
+      return e;
   }
   *out = &ss;
   return hipSuccess;
@@ -425,6 +431,12 @@ int locks_decode_step_ex(const locks_cfg_t* cfg, const locks_step_opts_t* opts, 
   return decode_step_impl(cfg, opts, q, k_cache, v_cache, page_table, seq_lens, summaries,
                           build_list, n_build, out_page_ids, out_sel_lse, out, out_lse, ws,
                           ws_bytes, stream);
+}
+
+int locks_init(void) {
+  std::lock_guard<std::mutex> lock(g_side_mu);
+  SideStream* side = nullptr;
+  return hip_status(side_stream(&side));
 }
 
 const char* locks_strerror(int status) {

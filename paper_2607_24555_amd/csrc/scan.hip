@@ -399,7 +399,8 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Fast path for r in {2, 4, 8} and G in {4, 16} (G = 16 / NPACK).
+// Fast path for r in {2, 4, 8} and G in {4, 16} (G = 16 / NPACK); dispatched for
+// r in {2, 4} at G = 16 only (r = 8, and G = 4, have the kernels further below).
 //
 // Differences from the generic kernel above:
 //  * stage 1 runs on 16x16x64 int8 MFMA.  A basis nibble becomes an int8 with
@@ -1658,8 +1659,8 @@ hipError_t dispatch_scan(int r, int G, int basis, int steps, dim3 grid, hipStrea
                          q, sum, summ_bytes, pt, sl, s_hat, lay, part);
     return hipGetLastError();
   }
-  LOCKS_SCAN_FAST(8, 4) LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(4, 4)
-  LOCKS_SCAN_FAST(2, 1) LOCKS_SCAN_FAST(2, 4)
+  // r = 2 and 4 at G = 16 (G = 4 took the low-rank kernel above)
+  LOCKS_SCAN_FAST(4, 1) LOCKS_SCAN_FAST(2, 1)
 #undef LOCKS_SCAN_FAST
 #define LOCKS_SCAN_MFMA_CASE(RR)                                                             \
   case RR:                                                                                  \

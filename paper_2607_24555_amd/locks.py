@@ -59,7 +59,7 @@ class Config:
 
     @property
     def k(self) -> int:
-        return (self.budget_tokens + PAGE - 1) // PAGE
+        return (self.budget_tokens + self.page_size - 1) // self.page_size
 
     def c(self) -> _Cfg:
         return _Cfg(self.num_seqs, self.num_q_heads, self.num_kv_heads, self.head_dim,
@@ -111,6 +111,7 @@ _SIGS = {
                                             _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _P, _SZ,
                                             _P]),
     "locks_append_kv": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P]),
+    "locks_init": (ctypes.c_int, []),
     "locks_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "locks_last_hip_error": (ctypes.c_int, []),
 }
@@ -142,6 +143,71 @@ def _ptr(t: Optional[torch.Tensor]):
     return ctypes.c_void_p(t.data_ptr())
 
 
+_TORCH_OF = {LOCKS_BF16: torch.bfloat16, LOCKS_FP32: torch.float32}
+
+
+def _need(name: str, t: Optional[torch.Tensor], shape, dtype, optional: bool = False):
+    """Checks a tensor argument against the layout include/locks.h documents for
+    cfg before anything reaches the library: the kernels trust shapes and dtypes,
+    so a mismatch would read or write outside the allocation."""
+    if t is None:
+        if optional:
+            return
+        raise LocksError(f"{name} is required")
+    if t.dtype != dtype:
+        raise LocksError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise LocksError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _same_device(*ts):
+    devs = {t.device for t in ts if t is not None}
+    if len(devs) > 1:
+        raise LocksError(f"tensors on several devices: {sorted(map(str, devs))}")
+
+
+def _check_q(cfg: "Config", q):
+    _need("q", q, (cfg.num_seqs, cfg.num_q_heads, cfg.head_dim), _TORCH_OF[cfg.q_dtype])
+
+
+def _check_tables(cfg: "Config", page_table, seq_lens):
+    _need("page_table", page_table, (cfg.num_seqs, cfg.max_pages_per_seq), torch.int32)
+    _need("seq_lens", seq_lens, (cfg.num_seqs,), torch.int32)
+
+
+def _check_cache(cfg: "Config", name: str, cache):
+    _need(name, cache, (cfg.num_blocks, cfg.num_kv_heads, cfg.page_size, cfg.head_dim),
+          _TORCH_OF[cfg.kv_dtype])
+
+
+def _check_summaries(cfg: "Config", summaries):
+    _need("summaries", summaries,
+          (cfg.num_blocks, cfg.num_kv_heads, summary_stride(cfg.rank, cfg.basis)), torch.uint8)
+
+
+def _check_list(name: str, lst):
+    if lst is not None and (lst.dtype != torch.int32 or lst.dim() != 2 or lst.shape[1] != 2):
+        raise LocksError(f"{name}: expected int32 [n][2] (sequence, page) pairs, got "
+                         f"{lst.dtype} {tuple(lst.shape)}")
+
+
+def _check_ws(ws):
+    if ws is None or ws.dtype != torch.uint8 or ws.dim() != 1:
+        raise LocksError("ws: expected a 1-D uint8 workspace (alloc_workspace)")
+
+
+def _check_select_out(cfg: "Config", out_ids, out_sel_lse, out_all_lse=None):
+    _need("out_ids", out_ids, (cfg.num_seqs, cfg.num_kv_heads, cfg.k), torch.int32)
+    _need("out_sel_lse", out_sel_lse, (cfg.num_seqs, cfg.num_q_heads, cfg.k), torch.float32)
+    _need("out_all_lse", out_all_lse, (cfg.num_seqs, cfg.num_q_heads, cfg.max_pages_per_seq),
+          torch.float32, optional=True)
+
+
+def _check_attend_out(cfg: "Config", out, out_lse):
+    _need("out", out, (cfg.num_seqs, cfg.num_q_heads, cfg.head_dim), torch.float32)
+    _need("out_lse", out_lse, (cfg.num_seqs, cfg.num_q_heads), torch.float32, optional=True)
+
+
 def _stream(stream) -> Optional[ctypes.c_void_p]:
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
@@ -152,6 +218,11 @@ def _check(rc: int):
         L = lib()
         msg = L.locks_strerror(rc).decode()
         raise LocksError(f"liblocks status {rc}: {msg} (hip error {L.locks_last_hip_error()})")
+
+
+def init():
+    """locks_init: create the current device's side stream before any capture."""
+    _check(lib().locks_init())
 
 
 def summary_payload_bytes(rank: int) -> int:
@@ -185,6 +256,11 @@ def alloc_summaries(cfg: Config, device="cuda") -> torch.Tensor:
 
 def build_summaries(cfg: Config, k_cache, page_table, seq_lens, summaries,
                     build_list: Optional[torch.Tensor] = None, stream=None):
+    _check_cache(cfg, "k_cache", k_cache)
+    _check_tables(cfg, page_table, seq_lens)
+    _check_summaries(cfg, summaries)
+    _check_list("build_list", build_list)
+    _same_device(k_cache, page_table, seq_lens, summaries, build_list)
     c = cfg.c()
     n = 0 if build_list is None else int(build_list.shape[0])
     _check(lib().locks_build_summaries(ctypes.byref(c), _ptr(k_cache), _ptr(page_table),
@@ -194,12 +270,18 @@ def build_summaries(cfg: Config, k_cache, page_table, seq_lens, summaries,
 
 def build_factors(cfg: Config, k_cache, page_table, seq_lens, build_list: torch.Tensor,
                   stream=None):
+    _check_cache(cfg, "k_cache", k_cache)
+    _check_tables(cfg, page_table, seq_lens)
+    _check_list("build_list", build_list)
+    if build_list is None:
+        raise LocksError("build_factors needs a build list")
+    _same_device(k_cache, page_table, seq_lens, build_list)
     n = int(build_list.shape[0])
     dev = k_cache.device
     mu = torch.zeros(n, cfg.num_kv_heads, HEAD_DIM, device=dev)
     basis = torch.zeros(n, cfg.num_kv_heads, HEAD_DIM, cfg.rank, device=dev)
-    coef = torch.zeros(n, cfg.num_kv_heads, PAGE, cfg.rank, device=dev)
-    sigma2 = torch.zeros(n, cfg.num_kv_heads, PAGE, device=dev)
+    coef = torch.zeros(n, cfg.num_kv_heads, cfg.page_size, cfg.rank, device=dev)
+    sigma2 = torch.zeros(n, cfg.num_kv_heads, cfg.page_size, device=dev)
     c = cfg.c()
     _check(lib().locks_build_factors(ctypes.byref(c), _ptr(k_cache), _ptr(page_table),
                                      _ptr(seq_lens), _ptr(build_list), n, _ptr(mu), _ptr(basis),
@@ -217,6 +299,12 @@ def select(cfg: Config, q, summaries, page_table, seq_lens, ws, out_ids=None, ou
            out_all_lse=None, stream=None):
     if out_ids is None:
         out_ids, out_sel_lse = alloc_select_outputs(cfg, q.device)
+    _check_q(cfg, q)
+    _check_summaries(cfg, summaries)
+    _check_tables(cfg, page_table, seq_lens)
+    _check_ws(ws)
+    _check_select_out(cfg, out_ids, out_sel_lse, out_all_lse)
+    _same_device(q, summaries, page_table, seq_lens, ws, out_ids, out_sel_lse, out_all_lse)
     c = cfg.c()
     _check(lib().locks_select(ctypes.byref(c), _ptr(q), _ptr(summaries), _ptr(page_table),
                               _ptr(seq_lens), _ptr(out_ids), _ptr(out_sel_lse), _ptr(out_all_lse),
@@ -229,6 +317,13 @@ def score_pages(cfg: Config, q, summaries, page_table, seq_lens, ws, out_all_lse
     if out_all_lse is None:
         out_all_lse = torch.empty(cfg.num_seqs, cfg.num_q_heads, cfg.max_pages_per_seq,
                                   dtype=torch.float32, device=q.device)
+    _check_q(cfg, q)
+    _check_summaries(cfg, summaries)
+    _check_tables(cfg, page_table, seq_lens)
+    _check_ws(ws)
+    _need("out_all_lse", out_all_lse, (cfg.num_seqs, cfg.num_q_heads, cfg.max_pages_per_seq),
+          torch.float32)
+    _same_device(q, summaries, page_table, seq_lens, ws, out_all_lse)
     c = cfg.c()
     _check(lib().locks_score_pages(ctypes.byref(c), _ptr(q), _ptr(summaries), _ptr(page_table),
                                    _ptr(seq_lens), _ptr(out_all_lse), _ptr(ws), ws.numel(),
@@ -246,6 +341,14 @@ def sparse_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, page_i
                   out=None, out_lse=None, stream=None):
     if out is None:
         out, out_lse = alloc_attend_outputs(cfg, q.device)
+    _check_q(cfg, q)
+    _check_cache(cfg, "k_cache", k_cache)
+    _check_cache(cfg, "v_cache", v_cache)
+    _check_tables(cfg, page_table, seq_lens)
+    _need("page_ids", page_ids, (cfg.num_seqs, cfg.num_kv_heads, cfg.k), torch.int32)
+    _check_ws(ws)
+    _check_attend_out(cfg, out, out_lse)
+    _same_device(q, k_cache, v_cache, page_table, seq_lens, page_ids, ws, out, out_lse)
     c = cfg.c()
     _check(lib().locks_sparse_attend(ctypes.byref(c), _ptr(q), _ptr(k_cache), _ptr(v_cache),
                                      _ptr(page_table), _ptr(seq_lens), _ptr(page_ids), _ptr(out),
@@ -257,6 +360,13 @@ def dense_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, ws, out
                  out_lse=None, stream=None):
     if out is None:
         out, out_lse = alloc_attend_outputs(cfg, q.device)
+    _check_q(cfg, q)
+    _check_cache(cfg, "k_cache", k_cache)
+    _check_cache(cfg, "v_cache", v_cache)
+    _check_tables(cfg, page_table, seq_lens)
+    _check_ws(ws)
+    _check_attend_out(cfg, out, out_lse)
+    _same_device(q, k_cache, v_cache, page_table, seq_lens, ws, out, out_lse)
     c = cfg.c()
     _check(lib().locks_dense_attend(ctypes.byref(c), _ptr(q), _ptr(k_cache), _ptr(v_cache),
                                     _ptr(page_table), _ptr(seq_lens), _ptr(out), _ptr(out_lse),
@@ -276,6 +386,20 @@ def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summarie
         out_ids, out_sel_lse = alloc_select_outputs(cfg, q.device)
     if out is None:
         out, out_lse = alloc_attend_outputs(cfg, q.device)
+    _check_q(cfg, q)
+    _check_cache(cfg, "k_cache", k_cache)
+    _check_cache(cfg, "v_cache", v_cache)
+    _check_tables(cfg, page_table, seq_lens)
+    _check_summaries(cfg, summaries)
+    _check_list("build_list", build_list)
+    _check_ws(ws)
+    _check_select_out(cfg, out_ids, out_sel_lse)
+    _check_attend_out(cfg, out, out_lse)
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        _need(name, t, (cfg.num_seqs, cfg.num_kv_heads, cfg.head_dim), _TORCH_OF[cfg.kv_dtype],
+              optional=True)
+    _same_device(q, k_cache, v_cache, page_table, seq_lens, summaries, build_list, ws, out_ids,
+                 out_sel_lse, out, out_lse, k_new, v_new)
     n = 0 if build_list is None else int(build_list.shape[0])
     c = cfg.c()
     args = (_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table), _ptr(seq_lens),
@@ -293,6 +417,12 @@ def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summarie
 def append_kv(cfg: Config, k_new, v_new, k_cache, v_cache, page_table, seq_lens, stream=None):
     """Write each sequence's newest token (token seq_lens[s] - 1) from k_new / v_new
     [S][H_kv][128] into the paged caches -- locks_append_kv."""
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        _need(name, t, (cfg.num_seqs, cfg.num_kv_heads, cfg.head_dim), _TORCH_OF[cfg.kv_dtype])
+    _check_cache(cfg, "k_cache", k_cache)
+    _check_cache(cfg, "v_cache", v_cache)
+    _check_tables(cfg, page_table, seq_lens)
+    _same_device(k_new, v_new, k_cache, v_cache, page_table, seq_lens)
     c = cfg.c()
     _check(lib().locks_append_kv(ctypes.byref(c), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
                                  _ptr(v_cache), _ptr(page_table), _ptr(seq_lens), _stream(stream)))
@@ -305,6 +435,11 @@ def kivi_quantize(cfg: Config, kivi: Kivi, k_cache, v_cache, page_table, seq_len
     n = 0 if page_list is None else int(page_list.shape[0])
     if page_list is not None and n == 0:
         return                      # an empty list names no page (NULL would mean all)
+    _check_cache(cfg, "k_cache", k_cache)
+    _check_cache(cfg, "v_cache", v_cache)
+    _check_tables(cfg, page_table, seq_lens)
+    _check_list("page_list", page_list)
+    _same_device(k_cache, v_cache, page_table, seq_lens, page_list)
     c = cfg.c()
     _check(lib().locks_kivi_quantize(ctypes.byref(c), ctypes.byref(kivi), _ptr(k_cache),
                                      _ptr(v_cache), _ptr(page_table), _ptr(seq_lens),
