@@ -295,10 +295,38 @@ int locks_decode_step_ex(const locks_cfg_t* cfg, const locks_step_opts_t* opts, 
                          int32_t* out_page_ids, float* out_sel_lse, float* out,
                          float* out_lse, void* ws, size_t ws_bytes, void* stream);
 
+/* Workspace bytes that locks_decode_step_static holds per device: 64 MiB, enough
+ * for every configuration whose locks_workspace_bytes is at most that (the 1M-token
+ * single-sequence step needs about 13 MiB, 8 x 128K about 16 MiB, 64 sequences of
+ * up to 64K tokens about 57 MiB). */
+#define LOCKS_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* locks_decode_step without a caller workspace, for callers that cannot allocate
+ * device memory at all: code under stream capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  The step's scratch lives in a static device array of
+ * LOCKS_STATIC_SCRATCH_BYTES inside the library (one per device, held until the
+ * process ends); the call itself allocates nothing -- no device memory, and no
+ * stream or event either: when the overlapped build of the last pages (see
+ * locks_decode_step) would need the device's side stream and locks_init has not
+ * created it, the listed pages are built before the scan on `stream` instead
+ * (the same step; those pages' scores come out of the scan rather than the build,
+ * equal up to float rounding).  Every call on a device shares that device's array
+ * and leaves its contents behind; no call needs it cleared, but calls that overlap
+ * on one device (two streams, two threads, two graphs in flight) race on it and
+ * must be ordered by the caller.  Arguments, outputs and errors as in
+ * locks_decode_step, plus LOCKS_E_WORKSPACE when locks_workspace_bytes(cfg)
+ * exceeds LOCKS_STATIC_SCRATCH_BYTES (nothing is launched). */
+int locks_decode_step_static(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                             const void* v_cache, const int32_t* page_table,
+                             const int32_t* seq_lens, void* summaries,
+                             const int32_t* build_list, int32_t n_build, int32_t* out_page_ids,
+                             float* out_sel_lse, float* out, float* out_lse, void* stream);
+
 /* Set-up for the current device (App. E: the step replays from a captured graph):
  * creates the device's side stream and its two events that locks_decode_step
  * forks to, so that no later call creates them -- in particular none under stream
- * capture.  Call it once per device, with that device current, before the first
+ * capture -- and looks up the device address of locks_decode_step_static's
+ * scratch array.  Call it once per device, with that device current, before the first
  * step that may be captured; calling it again is a no-op.  Returns LOCKS_E_HIP
  * if the stream or an event cannot be created. */
 int locks_init(void);

@@ -91,6 +91,33 @@ hipError_t side_stream(SideStream** out, bool create = true) {
   return hipSuccess;
 }
 
+// Workspace of locks_decode_step_static: one array per device (each GPU the library
+// runs on holds it until the process ends).  Host code never uses the array's name
+// as an address: the device address comes from hipGetSymbolAddress, once per
+// device with that device current, and is kept in g_scratch.
+constexpr size_t kStaticScratchBytes = LOCKS_STATIC_SCRATCH_BYTES;
+__device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];
+
+// The current device's address of `scratch`, resolved on first use.
+hipError_t scratch_ptr(void** out) {
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return hipSuccess;
+}
+
 int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
   const WsPlan p = plan_workspace(*c);
   if (!ws || ws_bytes < p.total) return LOCKS_E_WORKSPACE;
@@ -301,11 +328,15 @@ int locks_append_kv(const locks_cfg_t* cfg, const void* k_new, const void* v_new
                                   static_cast<hipStream_t>(stream)));
 }
 
+// create_side: the overlapped build may create the device's side stream; without
+// it (the allocation-free entry point) a missing side stream means the listed pages
+// are built before the scan on `stream`.
 static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opts, const void* q,
                             const void* k_cache, const void* v_cache, const int32_t* page_table,
                             const int32_t* seq_lens, void* summaries, const int32_t* build_list,
                             int32_t n_build, int32_t* out_page_ids, float* out_sel_lse,
-                            float* out, float* out_lse, void* ws, size_t ws_bytes, void* stream) {
+                            float* out, float* out_lse, void* ws, size_t ws_bytes, void* stream,
+                            bool create_side = true) {
   int rc = validate(cfg);
   if (rc) return rc;
   if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !summaries || !out_page_ids ||
@@ -336,7 +367,15 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opt
     if (!k_new) return hipSuccess;
     return launch_append(*cfg, k_new, v_new, kq, vq, page_table, seq_lens, st);
   };
-  const bool forked = attend_select_fused(*cfg) && n_build > 0 && cfg->basis == LOCKS_BASIS_INT4;
+  // The pages that just filled are built beside the scan on a side stream (bf16 q
+  // and KV, int4 basis); the lock also serialises the fork / join enqueues.
+  std::unique_lock<std::mutex> side_lock;
+  SideStream* side = nullptr;
+  if (attend_select_fused(*cfg) && n_build > 0 && cfg->basis == LOCKS_BASIS_INT4) {
+    side_lock = std::unique_lock<std::mutex>(g_side_mu);
+    if ((rc = hip_status(side_stream(&side, create_side)))) return rc;
+  }
+  const bool forked = side != nullptr;
   if (!forked && (rc = hip_status(append()))) return rc;
   if (!forked && (rc = hip_status(kivi_at(LOCKS_KIVI_PRE, st, kKiviAny)))) return rc;
   auto post_kivi = [&]() -> int { return hip_status(kivi_at(LOCKS_KIVI_POST, st, kKiviAny)); };
@@ -349,7 +388,7 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opt
     // scan -> per-chunk selection -> attention whose blocks merge the table
     const SHatLayout lay = shat_head_minor(*cfg);
     const float2* part_x = nullptr;
-    if (n_build > 0 && cfg->basis != LOCKS_BASIS_INT4) {
+    if (n_build > 0 && !forked) {
       rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
                                    summaries, nullptr, nullptr, nullptr, nullptr, st));
       if (rc) return rc;
@@ -366,10 +405,7 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opt
       // a few microseconds); `stream` joins the side stream before the selection.
       const BuildStep bs{w.sl_scan, w.part_x, q, cfg->q_dtype == LOCKS_BF16, cfg->num_q_heads,
                          w.s_hat, lay};
-      std::lock_guard<std::mutex> lock(g_side_mu);
-      SideStream* side = nullptr;
-      hipError_t e = side_stream(&side);
-      if (e == hipSuccess) e = hipEventRecord(side->fork, st);
+      hipError_t e = hipEventRecord(side->fork, st);
       if (e == hipSuccess) e = hipStreamWaitEvent(side->st, side->fork, 0);
       if (e == hipSuccess) e = append();
       if (e == hipSuccess) e = kivi_at(LOCKS_KIVI_PRE, st, kKiviLast);
@@ -433,7 +469,25 @@ int locks_decode_step_ex(const locks_cfg_t* cfg, const locks_step_opts_t* opts, 
                           ws_bytes, stream);
 }
 
+int locks_decode_step_static(const locks_cfg_t* cfg, const void* q, const void* k_cache,
+                             const void* v_cache, const int32_t* page_table,
+                             const int32_t* seq_lens, void* summaries,
+                             const int32_t* build_list, int32_t n_build, int32_t* out_page_ids,
+                             float* out_sel_lse, float* out, float* out_lse, void* stream) {
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (plan_workspace(*cfg).total > kStaticScratchBytes) return LOCKS_E_WORKSPACE;
+  void* ws = nullptr;
+  if ((rc = hip_status(scratch_ptr(&ws)))) return rc;
+  return decode_step_impl(cfg, nullptr, q, k_cache, v_cache, page_table, seq_lens, summaries,
+                          build_list, n_build, out_page_ids, out_sel_lse, out, out_lse, ws,
+                          kStaticScratchBytes, stream, /*create_side=*/false);
+}
+
 int locks_init(void) {
+  void* ws = nullptr;
+  int rc = hip_status(scratch_ptr(&ws));
+  if (rc) return rc;
   std::lock_guard<std::mutex> lock(g_side_mu);
   SideStream* side = nullptr;
   return hip_status(side_stream(&side));

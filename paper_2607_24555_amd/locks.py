@@ -112,6 +112,8 @@ _SIGS = {
                                             _P]),
     "locks_append_kv": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P]),
     "locks_init": (ctypes.c_int, []),
+    "locks_decode_step_static": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P,
+                                                _I, _P, _P, _P, _P, _P]),
     "locks_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "locks_last_hip_error": (ctypes.c_int, []),
 }
@@ -411,6 +413,37 @@ def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summarie
         opts = StepOpts(ctypes.pointer(kivi) if kivi is not None else None, _ptr(k_new),
                         _ptr(v_new))
         _check(lib().locks_decode_step_ex(ctypes.byref(c), ctypes.byref(opts), *args))
+    return out_ids, out_sel_lse, out, out_lse
+
+
+STATIC_SCRATCH_BYTES = 64 << 20
+
+
+def decode_step_static(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summaries,
+                       build_list: Optional[torch.Tensor] = None, out_ids=None, out_sel_lse=None,
+                       out=None, out_lse=None, stream=None):
+    """locks_decode_step_static: the fused step on the library's static device scratch
+    (no workspace argument; the call allocates nothing)."""
+    if out_ids is None:
+        out_ids, out_sel_lse = alloc_select_outputs(cfg, q.device)
+    if out is None:
+        out, out_lse = alloc_attend_outputs(cfg, q.device)
+    _check_q(cfg, q)
+    _check_cache(cfg, "k_cache", k_cache)
+    _check_cache(cfg, "v_cache", v_cache)
+    _check_tables(cfg, page_table, seq_lens)
+    _check_summaries(cfg, summaries)
+    _check_list("build_list", build_list)
+    _check_select_out(cfg, out_ids, out_sel_lse)
+    _check_attend_out(cfg, out, out_lse)
+    _same_device(q, k_cache, v_cache, page_table, seq_lens, summaries, build_list, out_ids,
+                 out_sel_lse, out, out_lse)
+    n = 0 if build_list is None else int(build_list.shape[0])
+    c = cfg.c()
+    _check(lib().locks_decode_step_static(
+        ctypes.byref(c), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table), _ptr(seq_lens),
+        _ptr(summaries), _ptr(build_list), n, _ptr(out_ids), _ptr(out_sel_lse), _ptr(out),
+        _ptr(out_lse), _stream(stream)))
     return out_ids, out_sel_lse, out, out_lse
 
 
