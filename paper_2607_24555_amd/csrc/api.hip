@@ -136,8 +136,19 @@ int sparse_pages_per_split(const locks_cfg_t& c) {
   return pps;
 }
 
+// Dense baseline: pages per split block, 256 (64 per wave), halved while the grid
+// would hold fewer than 512 blocks -- two per compute unit -- so that short
+// contexts and small batches still fill the chip.
+int dense_pages_per_split(const locks_cfg_t& c) {
+  const long units = (long)c.num_seqs * c.num_kv_heads;
+  int pps = kDensePagesPerSplit;
+  while (pps > 4 && units * ((c.max_pages_per_seq + pps - 1) / pps) < 512) pps /= 2;
+  return pps;
+}
+
 int dense_splits(const locks_cfg_t& c) {
-  return (c.max_pages_per_seq + kDensePagesPerSplit - 1) / kDensePagesPerSplit;
+  const int pps = dense_pages_per_split(c);
+  return (c.max_pages_per_seq + pps - 1) / pps;
 }
 
 }  // namespace
@@ -299,7 +310,7 @@ int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cach
   if (cfg->num_seqs == 0) return LOCKS_OK;
   const WsPlan p = plan_workspace(*cfg);
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, nullptr,
-                                  kDensePagesPerSplit, dense_splits(*cfg), carve(ws, p).attn, out,
+                                  dense_pages_per_split(*cfg), dense_splits(*cfg), carve(ws, p).attn, out,
                                   out_lse, static_cast<hipStream_t>(stream)));
 }
 

@@ -316,6 +316,14 @@ def select(cfg: Config, q, summaries, page_table, seq_lens, ws, out_ids=None, ou
 
 def score_pages(cfg: Config, q, summaries, page_table, seq_lens, ws, out_all_lse=None,
                 stream=None):
+    call = prepare_score_pages(cfg, q, summaries, page_table, seq_lens, ws, out_all_lse)
+    call(stream)
+    return call.outputs
+
+
+def prepare_score_pages(cfg: Config, q, summaries, page_table, seq_lens, ws,
+                        out_all_lse=None) -> "PreparedCall":
+    """score_pages' checks and marshalling, done once (see PreparedCall)."""
     if out_all_lse is None:
         out_all_lse = torch.empty(cfg.num_seqs, cfg.num_q_heads, cfg.max_pages_per_seq,
                                   dtype=torch.float32, device=q.device)
@@ -326,11 +334,9 @@ def score_pages(cfg: Config, q, summaries, page_table, seq_lens, ws, out_all_lse
     _need("out_all_lse", out_all_lse, (cfg.num_seqs, cfg.num_q_heads, cfg.max_pages_per_seq),
           torch.float32)
     _same_device(q, summaries, page_table, seq_lens, ws, out_all_lse)
-    c = cfg.c()
-    _check(lib().locks_score_pages(ctypes.byref(c), _ptr(q), _ptr(summaries), _ptr(page_table),
-                                   _ptr(seq_lens), _ptr(out_all_lse), _ptr(ws), ws.numel(),
-                                   _stream(stream)))
-    return out_all_lse
+    return PreparedCall(lib().locks_score_pages, cfg.c(),
+                        (_ptr(q), _ptr(summaries), _ptr(page_table), _ptr(seq_lens),
+                         _ptr(out_all_lse), _ptr(ws), ws.numel()), None, out_all_lse)
 
 
 def alloc_attend_outputs(cfg: Config, device="cuda"):
@@ -360,6 +366,14 @@ def sparse_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, page_i
 
 def dense_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, ws, out=None,
                  out_lse=None, stream=None):
+    call = prepare_dense_attend(cfg, q, k_cache, v_cache, page_table, seq_lens, ws, out, out_lse)
+    call(stream)
+    return call.outputs
+
+
+def prepare_dense_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, ws, out=None,
+                         out_lse=None) -> "PreparedCall":
+    """dense_attend's checks and marshalling, done once (see PreparedCall)."""
     if out is None:
         out, out_lse = alloc_attend_outputs(cfg, q.device)
     _check_q(cfg, q)
@@ -369,11 +383,9 @@ def dense_attend(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, ws, out
     _check_ws(ws)
     _check_attend_out(cfg, out, out_lse)
     _same_device(q, k_cache, v_cache, page_table, seq_lens, ws, out, out_lse)
-    c = cfg.c()
-    _check(lib().locks_dense_attend(ctypes.byref(c), _ptr(q), _ptr(k_cache), _ptr(v_cache),
-                                    _ptr(page_table), _ptr(seq_lens), _ptr(out), _ptr(out_lse),
-                                    _ptr(ws), ws.numel(), _stream(stream)))
-    return out, out_lse
+    return PreparedCall(lib().locks_dense_attend, cfg.c(),
+                        (_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table), _ptr(seq_lens),
+                         _ptr(out), _ptr(out_lse), _ptr(ws), ws.numel()), None, (out, out_lse))
 
 
 def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summaries, ws,
@@ -384,6 +396,36 @@ def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summarie
     (before or after their build, per kivi.stage); with k_new / v_new [S][H_kv][128]
     the step first writes each sequence's newest token (seq_lens counting it) --
     locks_decode_step_ex."""
+    step = prepare_decode_step(cfg, q, k_cache, v_cache, page_table, seq_lens, summaries, ws,
+                               build_list, out_ids, out_sel_lse, out, out_lse, kivi, k_new, v_new)
+    step(stream)
+    return step.outputs
+
+
+class PreparedCall:
+    """One library call with its arguments checked and marshalled once: every call
+    of the object enqueues the same call on the given or current stream.  For
+    fixed-shape loops over fixed buffers (the deployment pattern of Sec. 4
+    "Implementation"), where per-call argument checks would cost host time."""
+
+    def __init__(self, fn, cfg_struct, args, opts, outputs):
+        self._fn, self._c, self._args, self._opts = fn, cfg_struct, args, opts
+        self.outputs = outputs
+
+    def __call__(self, stream=None):
+        if self._opts is None:
+            _check(self._fn(ctypes.byref(self._c), *self._args, _stream(stream)))
+        else:
+            _check(self._fn(ctypes.byref(self._c), ctypes.byref(self._opts), *self._args,
+                            _stream(stream)))
+
+
+def prepare_decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summaries, ws,
+                        build_list: Optional[torch.Tensor] = None, out_ids=None,
+                        out_sel_lse=None, out=None, out_lse=None, kivi: Optional[Kivi] = None,
+                        k_new=None, v_new=None) -> PreparedCall:
+    """decode_step's checks and marshalling, done once; returns the PreparedCall.
+    The tensors must stay alive (and keep their storage) while it is used."""
     if out_ids is None:
         out_ids, out_sel_lse = alloc_select_outputs(cfg, q.device)
     if out is None:
@@ -406,14 +448,12 @@ def decode_step(cfg: Config, q, k_cache, v_cache, page_table, seq_lens, summarie
     c = cfg.c()
     args = (_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table), _ptr(seq_lens),
             _ptr(summaries), _ptr(build_list), n, _ptr(out_ids), _ptr(out_sel_lse), _ptr(out),
-            _ptr(out_lse), _ptr(ws), ws.numel(), _stream(stream))
+            _ptr(out_lse), _ptr(ws), ws.numel())
+    outputs = (out_ids, out_sel_lse, out, out_lse)
     if kivi is None and k_new is None and v_new is None:
-        _check(lib().locks_decode_step(ctypes.byref(c), *args))
-    else:
-        opts = StepOpts(ctypes.pointer(kivi) if kivi is not None else None, _ptr(k_new),
-                        _ptr(v_new))
-        _check(lib().locks_decode_step_ex(ctypes.byref(c), ctypes.byref(opts), *args))
-    return out_ids, out_sel_lse, out, out_lse
+        return PreparedCall(lib().locks_decode_step, c, args, None, outputs)
+    opts = StepOpts(ctypes.pointer(kivi) if kivi is not None else None, _ptr(k_new), _ptr(v_new))
+    return PreparedCall(lib().locks_decode_step_ex, c, args, opts, outputs)
 
 
 STATIC_SCRATCH_BYTES = 64 << 20

@@ -65,7 +65,8 @@ class WorkloadSpec:
 def config_spec(cfg_id: int, *, rank: Optional[int] = None, seed: int = 0,
                 num_seqs: Optional[int] = None, seq_len: Optional[int] = None,
                 num_kv_heads: Optional[int] = None, num_q_heads: Optional[int] = None,
-                budget_tokens: Optional[int] = None) -> WorkloadSpec:
+                budget_tokens: Optional[int] = None,
+                spare_pages: Optional[int] = None) -> WorkloadSpec:
     """The five decode-step workloads; keyword overrides shrink them for tests."""
     if cfg_id == 0:
         s = WorkloadSpec("tiny-1h-4k", 1, 1, 1, [4096], 8, 256, "fp32", "fp32")
@@ -97,6 +98,8 @@ def config_spec(cfg_id: int, *, rank: Optional[int] = None, seed: int = 0,
         s.rank = rank
     if budget_tokens is not None:
         s.budget_tokens = budget_tokens
+    if spare_pages is not None:
+        s.spare_pages_per_seq = spare_pages
     return s
 
 
