@@ -30,11 +30,13 @@ Readings of points the paper leaves open:
   coefficient rows and the centroid |code| <= 127; scale = f16(max|x| / qmax)
   (clamped to the largest finite float16), code = clamp(rint(x / scale)) with
   ties to even, scale 0 => codes 0;
+* pages hold B = 16 tokens unless stated; B = 32 and 64 are the page sizes of
+  App. D.3 "Page size", where the budget buys k = ceil(b / B) pages;
 * byte layout (one record per (physical block, KV head)):
   [basis: r columns x 64 bytes, column l holds d=128 excess-8 nibbles, element c
-  in byte c//2, low nibble for even c][coefficients: 16 x r excess-128 bytes,
+  in byte c//2, low nibble for even c][coefficients: B x r excess-128 bytes,
   row-major][centroid: 128 excess-128 bytes][float16 scales: r basis-column,
-  16 coefficient-row, 1 centroid][zero padding to a multiple of 16 bytes];
+  B coefficient-row, 1 centroid][zero padding to a multiple of 16 bytes];
 * basis precision variants (the ablation of Sec. 5 "Ablations" and the r8fp
   control of the retention remark): an int8 basis stores each column as 128
   excess-128 bytes with one float16 scale f16(max|v| / 127); a bf16 basis stores
@@ -86,11 +88,17 @@ BASIS_BYTES = {"int4": 0.5, "int8": 1, "bf16": 2}   # bytes per basis element
 def payload_bytes(r: int, d: int = HEAD_DIM, B: int = PAGE, basis: str = "int4") -> int:
     """Stored bytes per page: the d*r basis (int4 by default) + B*r int8 + d int8
     + 2-byte scales for r basis columns, B coefficient rows and the centroid."""
-    return int(d * r * BASIS_BYTES[basis]) + B * r + d + 2 * (r + B + 1)
+    return logical_payload_bytes(r, d, B, basis) + 2 * (r + B + 1)
 
 
-def record_stride(r: int, basis: str = "int4") -> int:
-    p = payload_bytes(r, basis=basis)
+def logical_payload_bytes(r: int, d: int = HEAD_DIM, B: int = PAGE, basis: str = "int4") -> int:
+    """The summary's entries without their scales: d*r basis entries (int4 by
+    default) plus B*r + d int8 bytes (Sec. 4 "Build"; App. D.3 "Page size")."""
+    return int(d * r * BASIS_BYTES[basis]) + B * r + d
+
+
+def record_stride(r: int, basis: str = "int4", B: int = PAGE) -> int:
+    p = payload_bytes(r, B=B, basis=basis)
     return (p + 15) // 16 * 16
 
 
@@ -117,24 +125,25 @@ def logits(q: np.ndarray, keys: np.ndarray) -> np.ndarray:
     return (q @ keys.T) / math.sqrt(keys.shape[1])
 
 
-def exact_page_lse(q: np.ndarray, keys: np.ndarray, n_pages: Optional[int] = None) -> np.ndarray:
-    """s_j(q) = log sum_{i in P_j} exp(q^T k_i / sqrt d) for pages of 16 tokens.
+def exact_page_lse(q: np.ndarray, keys: np.ndarray, n_pages: Optional[int] = None,
+                   B: int = PAGE) -> np.ndarray:
+    """s_j(q) = log sum_{i in P_j} exp(q^T k_i / sqrt d) for pages of B tokens.
 
     q [G][d], keys [L][d]; returns [G][n] over the pages that hold tokens
     (a partial last page uses its valid tokens only)."""
     L = keys.shape[0]
-    n = (L + PAGE - 1) // PAGE if n_pages is None else n_pages
+    n = (L + B - 1) // B if n_pages is None else n_pages
     z = logits(q, keys)
     out = np.empty((q.shape[0], n))
     for j in range(n):
-        out[:, j] = _lse(z[:, j * PAGE:min(L, (j + 1) * PAGE)], axis=1)
+        out[:, j] = _lse(z[:, j * B:min(L, (j + 1) * B)], axis=1)
     return out
 
 
 def attend(q: np.ndarray, keys: np.ndarray, vals: np.ndarray,
-           pages: Optional[List[int]] = None) -> Tuple[np.ndarray, np.ndarray]:
-    """Softmax attention of each query over the tokens of the given pages
-    (all tokens when pages is None), renormalised over that set.
+           pages: Optional[List[int]] = None, B: int = PAGE) -> Tuple[np.ndarray, np.ndarray]:
+    """Softmax attention of each query over the tokens of the given pages of B
+    tokens (all tokens when pages is None), renormalised over that set.
 
     Returns (o [G][d], lse [G]) with lse the log of the softmax denominator."""
     L = keys.shape[0]
@@ -142,7 +151,7 @@ def attend(q: np.ndarray, keys: np.ndarray, vals: np.ndarray,
     if pages is None:
         idx = np.arange(L)
     else:
-        idx = np.concatenate([np.arange(j * PAGE, min(L, (j + 1) * PAGE)) for j in pages]
+        idx = np.concatenate([np.arange(j * B, min(L, (j + 1) * B)) for j in pages]
                              ) if len(pages) else np.zeros(0, dtype=np.int64)
     if idx.size == 0:
         return np.zeros((G, vals.shape[1] if vals.ndim == 2 else HEAD_DIM)), np.full(G, -np.inf)
@@ -152,9 +161,9 @@ def attend(q: np.ndarray, keys: np.ndarray, vals: np.ndarray,
     return p @ vals[idx], lse
 
 
-def coverage(q: np.ndarray, keys: np.ndarray, pages: List[int]) -> np.ndarray:
+def coverage(q: np.ndarray, keys: np.ndarray, pages: List[int], B: int = PAGE) -> np.ndarray:
     """gamma_S(q): share of the full softmax mass that falls in pages S, per query."""
-    s = exact_page_lse(q, keys)
+    s = exact_page_lse(q, keys, B=B)
     tot = _lse(s, axis=1)
     sel = _lse(s[:, pages], axis=1) if len(pages) else np.full(q.shape[0], -np.inf)
     return np.exp(sel - tot)
@@ -241,10 +250,11 @@ def encode(mu: np.ndarray, V: np.ndarray, C: np.ndarray, basis: str = "int4") ->
     """Quantise and pack one summary per page: mu [P][d], V [P][d][r], C [P][B][r]
     -> uint8 records [P][record_stride(r, basis)]."""
     P, d, r = V.shape
-    assert d == HEAD_DIM and C.shape[1] == PAGE
+    B = C.shape[1]                                    # tokens per page
+    assert d == HEAD_DIM
     cq, cs = quantize(C, INT8_MAX, axis=2)            # per coefficient row (token)
     mq, ms = quantize(mu, INT8_MAX, axis=1)           # one centroid scale
-    out = np.zeros((P, record_stride(r, basis)), dtype=np.uint8)
+    out = np.zeros((P, record_stride(r, basis, B)), dtype=np.uint8)
     cb = int(d * BASIS_BYTES[basis])                  # bytes per basis column
     if basis == "int4":
         vq, vs = quantize(V, INT4_MAX, axis=1)        # per basis column
@@ -264,17 +274,18 @@ def encode(mu: np.ndarray, V: np.ndarray, C: np.ndarray, basis: str = "int4") ->
     else:
         raise ValueError(basis)
     off = cb * r
-    out[:, off:off + PAGE * r] = (cq + 128).astype(np.uint8).reshape(P, PAGE * r)
-    off += PAGE * r
+    out[:, off:off + B * r] = (cq + 128).astype(np.uint8).reshape(P, B * r)
+    off += B * r
     out[:, off:off + d] = (mq + 128).astype(np.uint8)
     off += d
-    scales = np.concatenate([vs.reshape(P, r), cs.reshape(P, PAGE), ms.reshape(P, 1)], axis=1)
-    out[:, off:off + 2 * (r + PAGE + 1)] = scales.astype("<f2").view(np.uint8).reshape(P, -1)
+    scales = np.concatenate([vs.reshape(P, r), cs.reshape(P, B), ms.reshape(P, 1)], axis=1)
+    out[:, off:off + 2 * (r + B + 1)] = scales.astype("<f2").view(np.uint8).reshape(P, -1)
     return out
 
 
-def decode(records: np.ndarray, r: int, basis: str = "int4") -> Dict[str, np.ndarray]:
-    """Inverse of `encode`: uint8 [P][stride] -> fp64 mu [P][d], V [P][d][r], C [P][B][r]
+def decode(records: np.ndarray, r: int, basis: str = "int4", B: int = PAGE) -> Dict[str, np.ndarray]:
+    """Inverse of `encode` for pages of B tokens: uint8 [P][stride] -> fp64 mu [P][d],
+    V [P][d][r], C [P][B][r]
     (code times float16 scale; bf16 basis values as stored), plus the raw codes."""
     rec = np.asarray(records, dtype=np.uint8)
     P = rec.shape[0]
@@ -295,12 +306,12 @@ def decode(records: np.ndarray, r: int, basis: str = "int4") -> Dict[str, np.nda
                 vvals = np.zeros((P, d, r))
             vvals[:, :, l] = bf16_value(b.copy().view("<u2"))
     off = cb * r
-    ccodes = rec[:, off:off + PAGE * r].astype(np.int64).reshape(P, PAGE, r) - 128
-    off += PAGE * r
+    ccodes = rec[:, off:off + B * r].astype(np.int64).reshape(P, B, r) - 128
+    off += B * r
     mcodes = rec[:, off:off + d].astype(np.int64) - 128
     off += d
-    sc = rec[:, off:off + 2 * (r + PAGE + 1)].copy().view("<f2").astype(np.float64)
-    vs, cs, ms = sc[:, :r], sc[:, r:r + PAGE], sc[:, r + PAGE]
+    sc = rec[:, off:off + 2 * (r + B + 1)].copy().view("<f2").astype(np.float64)
+    vs, cs, ms = sc[:, :r], sc[:, r:r + B], sc[:, r + B]
     V = vvals * vs[:, None, :] if basis == "bf16" else vcodes * vs[:, None, :]
     return {"mu": mcodes * ms[:, None], "V": V, "C": ccodes * cs[:, :, None],
             "vcodes": vcodes, "ccodes": ccodes, "mcodes": mcodes,
@@ -392,34 +403,36 @@ def kivi_page(keys: np.ndarray, vals: np.ndarray, bits: int, v_group: int = 32):
 # One decode step for one (sequence, KV head)
 # --------------------------------------------------------------------------
 
-def pages_of(keys: np.ndarray) -> Tuple[np.ndarray, int, int]:
+def pages_of(keys: np.ndarray, B: int = PAGE) -> Tuple[np.ndarray, int, int]:
     """Split [L][d] keys into complete pages [n_c][B][d]; returns (pages, n_c, n)."""
     L = keys.shape[0]
-    n_c = L // PAGE
-    n = (L + PAGE - 1) // PAGE
-    return keys[:n_c * PAGE].reshape(n_c, PAGE, keys.shape[1]), n_c, n
+    n_c = L // B
+    n = (L + B - 1) // B
+    return keys[:n_c * B].reshape(n_c, B, keys.shape[1]), n_c, n
 
 
-def unit_summaries(keys: np.ndarray, r: int, basis: str = "int4") -> np.ndarray:
-    """Encoded summaries [n_c][stride] of the complete pages of one (sequence, KV head)."""
-    pk, n_c, _ = pages_of(keys)
+def unit_summaries(keys: np.ndarray, r: int, basis: str = "int4", B: int = PAGE) -> np.ndarray:
+    """Encoded summaries [n_c][stride] of the complete B-token pages of one
+    (sequence, KV head)."""
+    pk, n_c, _ = pages_of(keys, B)
     if n_c == 0:
-        return np.zeros((0, record_stride(r, basis)), dtype=np.uint8)
+        return np.zeros((0, record_stride(r, basis, B)), dtype=np.uint8)
     f = build_factors(pk, r)
     return encode(f["mu"], f["V"], f["C"], basis)
 
 
 def decode_step(q: np.ndarray, keys: np.ndarray, vals: np.ndarray, records: np.ndarray,
-                r: int, budget_tokens: int, basis: str = "int4") -> Dict[str, object]:
+                r: int, budget_tokens: int, basis: str = "int4", B: int = PAGE) -> Dict[str, object]:
     """Score every summarised page from its decoded record, select the shared table,
-    attend over it.  records [n_c][stride] are the complete pages' summaries."""
+    attend over it.  records [n_c][stride] are the complete pages' summaries; pages
+    hold B tokens and the page budget is k = ceil(b / B) (App. D.3 "Page size")."""
     L = keys.shape[0]
-    n_c, n = L // PAGE, (L + PAGE - 1) // PAGE
-    k = (budget_tokens + PAGE - 1) // PAGE
-    dec = decode(records[:n_c], r, basis) if n_c else None
+    n_c, n = L // B, (L + B - 1) // B
+    k = (budget_tokens + B - 1) // B
+    dec = decode(records[:n_c], r, basis, B) if n_c else None
     s_hat = score(q, dec["mu"], dec["V"], dec["C"]) if n_c else np.zeros((q.shape[0], 0))
     sel = select_pages(s_hat, n, k)
-    o, lse = attend(q, keys, vals, sel["ids"])
+    o, lse = attend(q, keys, vals, sel["ids"], B)
     sel_lse = np.full((q.shape[0], k), np.nan)
     for t, j in enumerate(sel["ids"]):
         if j < n_c:

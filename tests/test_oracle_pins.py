@@ -292,41 +292,42 @@ def test_record_byte_layout_by_hand():
 
 # ---------------------------------------------------------------- combine + select
 
-def _coverage_lib(q, keys, pages):
-    """gamma_S(q) from scipy's softmax over every token."""
+def _coverage_lib(q, keys, pages, Bp=16):
+    """gamma_S(q) from scipy's softmax over every token (pages of Bp tokens)."""
     z = q @ keys.T / math.sqrt(D)
     p = scipy.special.softmax(z, axis=1)
-    idx = np.concatenate([np.arange(16 * j, min(keys.shape[0], 16 * j + 16)) for j in pages])
+    idx = np.concatenate([np.arange(Bp * j, min(keys.shape[0], Bp * j + Bp)) for j in pages])
     return p[:, idx].sum(1)
 
 
-@pytest.mark.parametrize("G", [1, 2, 4])
-def test_select_matches_brute_force(G):
+@pytest.mark.parametrize("G,Bp", [(1, 16), (2, 16), (4, 16), (2, 32), (4, 64)])
+def test_select_matches_brute_force(G, Bp):
     """Cor. 'Group-shared selection': with exact shares, sink + recent + top-(k-2) by mbar
-    maximises the group-mean coverage over all k-sets containing sink and recent."""
+    maximises the group-mean coverage over all k-sets containing sink and recent
+    (pages of 16, 32 or 64 tokens)."""
     for seed in range(12):
         rng = _rng(100 + seed)
         n = int(rng.integers(4, 10))
         k = int(rng.integers(2, n))
-        keys = rng.standard_normal((16 * n, D)) * rng.uniform(0.5, 3.0, size=(16 * n, 1))
-        keys[:16] *= rng.uniform(0.2, 3.0)      # sink mass varies across heads
+        keys = rng.standard_normal((Bp * n, D)) * rng.uniform(0.5, 3.0, size=(Bp * n, 1))
+        keys[:Bp] *= rng.uniform(0.2, 3.0)      # sink mass varies across heads
         q = rng.standard_normal((G, D)) * rng.uniform(0.5, 2.5, size=(G, 1))
-        s = O.exact_page_lse(q, keys)
+        s = O.exact_page_lse(q, keys, B=Bp)
         sel = O.select_pages(s, n, k)
         best, best_set = -1.0, None
         for rest in itertools.combinations(range(1, n - 1), k - 2):
             S = sorted((0, n - 1) + rest)
-            val = _coverage_lib(q, keys, S).mean()
+            val = _coverage_lib(q, keys, S, Bp).mean()
             if val > best + 1e-12:
                 best, best_set = val, S
-        assert _coverage_lib(q, keys, sel["ids"]).mean() == pytest.approx(best, abs=1e-12)
+        assert _coverage_lib(q, keys, sel["ids"], Bp).mean() == pytest.approx(best, abs=1e-12)
         if sel["gap"] > 1e-9:
             assert sel["ids"] == best_set
         # the share-average key of each page is the group-mean coverage of that page
         # alone (scipy softmax over every token), and the ranking gap is the log ratio
         # of the weakest kept candidate to the strongest candidate left out of the
         # brute-force optimum
-        share = np.array([_coverage_lib(q, keys, [j]).mean() for j in range(n)])
+        share = np.array([_coverage_lib(q, keys, [j], Bp).mean() for j in range(n)])
         np.testing.assert_allclose(sel["log_mbar"], np.log(share), atol=1e-12, rtol=0)
         if k >= 3:
             kept = [j for j in best_set if 0 < j < n - 1]
@@ -631,3 +632,121 @@ def test_kivi_levels_extremes_and_error_bound(bits, g):
             step = (a.max() - a.min()) / (2 ** bits - 1)
             tol = step / 2 * (1 + 1e-5) + np.abs(b) * 2.0 ** -8
             assert np.all(np.abs(b - a) <= tol)
+
+
+# ---------------------------------------------------------------- page size (App. D.3)
+
+def test_page_size_payload_fractions_match_paper():
+    """App. D.3: at r = 8 the logical summary falls from 9.4% of the page's KV bytes at
+    B = 16 to 5.5% and 3.5% at B = 32 and 64; the budget buys k = ceil(b / B) pages,
+    two of them free at b = 256, B = 64."""
+    g = _gold("page_size.json")
+    r = g["rank"]
+    for B_s, pct in g["logical_payload_percent"].items():
+        Bp = int(B_s)
+        logical = O.logical_payload_bytes(r, B=Bp)
+        assert logical == D * r // 2 + Bp * r + D
+        assert round(100 * logical / O.kv_bytes_per_page(2, B=Bp), 1) == pct
+        # the stored record adds r + B + 1 float16 scales
+        assert O.payload_bytes(r, B=Bp) == logical + 2 * (r + Bp + 1)
+        assert O.record_stride(r, B=Bp) % 16 == 0
+    # b = 256 at B = 64: k = 4 pages, sink and recent take two, two are chosen
+    rng = _rng(61)
+    keys = rng.standard_normal((64 * 20 + 5, D))
+    vals = rng.standard_normal((64 * 20 + 5, D))
+    q = rng.standard_normal((2, D))
+    rec = O.unit_summaries(keys, 8, B=64)
+    st = O.decode_step(q, keys, vals, rec, 8, 256, B=64)
+    assert len(st["ids"]) == 4 and st["ids"][0] == 0 and st["ids"][-1] == 20
+    assert len(st["ids"]) - 2 == g["free_pages_at_b256_B64"]
+
+
+def _pages_B(rng, n, Bp, rank=8, scale=3.0):
+    out = np.empty((n, Bp, D))
+    for p in range(n):
+        U = np.linalg.qr(rng.standard_normal((D, rank)))[0]
+        c = rng.standard_normal((Bp, rank)) * scale * (0.7 ** np.arange(rank))
+        out[p] = rng.standard_normal(D) + c @ U.T + 0.05 * rng.standard_normal((Bp, D))
+    return out
+
+
+@pytest.mark.parametrize("Bp", [32, 64])
+def test_page_size_build_matches_svd(Bp):
+    """Cor. 'per-page basis is residual-optimal' on B x B Grams: energies and residuals
+    equal the truncated SVD of the centred page; exact reconstruction at full rank."""
+    rng = _rng(62 + Bp)
+    pk = _pages_B(rng, 6, Bp, rank=12)
+    for r in (2, 8, 15):
+        f = O.build_factors(pk, r)
+        for p in range(pk.shape[0]):
+            Dm = pk[p] - pk[p].mean(0)
+            sv = scipy.linalg.svd(Dm, compute_uv=False, lapack_driver="gesvd")
+            np.testing.assert_allclose(np.sqrt(f["sigma2"][p, :Bp - 1]), sv[:Bp - 1], rtol=1e-8,
+                                       atol=1e-8)
+            V, C = f["V"][p], f["C"][p]
+            np.testing.assert_allclose(V.T @ V, np.eye(r), atol=1e-10)
+            np.testing.assert_allclose(C, Dm @ V, atol=1e-9)
+            resid = np.sum((Dm - C @ V.T) ** 2)
+            assert resid == pytest.approx(np.sum(sv[r:] ** 2), rel=1e-8, abs=1e-9)
+    full = O.build_factors(pk, Bp - 1)
+    rec = full["mu"][:, None, :] + np.einsum("pil,pcl->pic", full["C"], full["V"])
+    np.testing.assert_allclose(rec, pk, atol=1e-9)
+    # full rank: the reconstructed page score is the exact page log-mass of B tokens,
+    # itself the log-sum-exp of its 16-token halves (scipy)
+    q = rng.standard_normal((3, D)) * 1.5
+    got = O.score(q, full["mu"], full["V"], full["C"])
+    want = O.exact_page_lse(q, pk.reshape(-1, D), B=Bp)
+    np.testing.assert_allclose(got, want, atol=1e-10)
+    halves = O.exact_page_lse(q, pk.reshape(-1, D), B=16).reshape(3, -1, Bp // 16)
+    np.testing.assert_allclose(want, scipy.special.logsumexp(halves, axis=2), atol=1e-12)
+
+
+@pytest.mark.parametrize("Bp", [32, 64])
+def test_page_size_record_layout_and_roundtrip(Bp):
+    """The record of a B-token page: [basis r x 64 B][coefficients B x r][centroid
+    128][float16 scales: r basis, B coefficient rows, 1 centroid][padding];
+    decoding restores every entry within half a quantisation step."""
+    rng = _rng(70 + Bp)
+    r = 4
+    pk = _pages_B(rng, 5, Bp)
+    f = O.build_factors(pk, r)
+    rec = O.encode(f["mu"], f["V"], f["C"])
+    assert rec.shape[1] == O.record_stride(r, B=Bp)
+    dec = O.decode(rec, r, B=Bp)
+    assert np.all(np.abs(dec["V"] - f["V"]) <= dec["vscale"][:, None, :] / 2 + 1e-12)
+    assert np.all(np.abs(dec["C"] - f["C"]) <= dec["cscale"][:, :, None] / 2 + 1e-12)
+    assert np.all(np.abs(dec["mu"] - f["mu"]) <= dec["mscale"][:, None] / 2 + 1e-12)
+    # the same bytes read by hand
+    p = 2
+    coef = rec[p, 64 * r:64 * r + Bp * r].astype(np.int64) - 128
+    np.testing.assert_array_equal(coef.reshape(Bp, r), dec["ccodes"][p])
+    mu = rec[p, 64 * r + Bp * r:64 * r + Bp * r + 128].astype(np.int64) - 128
+    np.testing.assert_array_equal(mu, dec["mcodes"][p])
+    sc = rec[p, 64 * r + Bp * r + 128:64 * r + Bp * r + 128 + 2 * (r + Bp + 1)].view("<f2")
+    np.testing.assert_array_equal(sc[r:r + Bp].astype(np.float64), dec["cscale"][p])
+    assert np.all(rec[:, O.payload_bytes(r, B=Bp):] == 0)
+
+
+@pytest.mark.parametrize("Bp", [32, 64])
+def test_page_size_attention_and_dense(Bp):
+    """A B-token page is B consecutive tokens: attention over page j at page size B
+    equals attention over its 16-token pages; a budget covering every page is dense
+    attention."""
+    rng = _rng(80 + Bp)
+    L = Bp * 9 + 7
+    keys = rng.standard_normal((L, D))
+    vals = rng.standard_normal((L, D))
+    q = rng.standard_normal((4, D))
+    sub = Bp // 16
+    for pages in ([0], [3, 9], [1, 2, 5, 9]):
+        o1, l1 = O.attend(q, keys, vals, pages, B=Bp)
+        small = [sub * j + i for j in pages for i in range(sub) if 16 * (sub * j + i) < L]
+        o2, l2 = O.attend(q, keys, vals, small, B=16)
+        np.testing.assert_allclose(o1, o2, atol=1e-12)
+        np.testing.assert_allclose(l1, l2, atol=1e-12)
+    rec = O.unit_summaries(keys, 8, B=Bp)
+    st = O.decode_step(q, keys, vals, rec, 8, Bp * 10, B=Bp)
+    o_d, l_d = O.dense_step(q, keys, vals)
+    assert st["ids"] == list(range(10))
+    np.testing.assert_allclose(st["out"], o_d, atol=1e-12)
+    np.testing.assert_allclose(st["lse"], l_d, atol=1e-12)
