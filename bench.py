@@ -379,8 +379,8 @@ def run_block(name, args, dev, with_oracle, rest):
 
     n_pages = sum(math.ceil(L / 16) for L in w.spec.seq_lens)
     complete_heads = sum(L // 16 for L in w.spec.seq_lens) * cfg.num_kv_heads
-    payload = B.summary_payload_bytes_ex(cfg.rank, cfg.basis)
-    stride = B.summary_stride(cfg.rank, cfg.basis)
+    payload = B.summary_payload_bytes_ex(cfg.rank, cfg.basis, cfg.page_size)
+    stride = B.summary_stride(cfg.rank, cfg.basis, cfg.page_size)
     k_sel = min(cfg.k, max(math.ceil(L / 16) for L in w.spec.seq_lens))
     kv_page = 2 * 16 * 128 * 2
     alg_scan = complete_heads * payload

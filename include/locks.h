@@ -2,9 +2,10 @@
  * locks.h -- C ABI of the Locks per-step sparse decode attention for AMD
  * Instinct MI355X (gfx950).
  *
- * The method (arXiv 2607.24555): every 16-token KV page keeps a resident rank-r
- * spectral summary of its keys (Sec. 4 "Build"); every decode step rebuilds each
- * page's 16 logits from its summary and takes their log-sum-exp (Sec. 4 "Score",
+ * The method (arXiv 2607.24555): every KV page of B tokens (B = 16; 32 and 64 are
+ * the page sizes of App. D.3) keeps a resident rank-r spectral summary of its keys
+ * (Sec. 4 "Build"); every decode step rebuilds each page's B logits from its
+ * summary and takes their log-sum-exp (Sec. 4 "Score",
  * Eq. (1)), averages the normalised page shares over the GQA group, keeps the
  * sink page, the most recent page and the top (k-2) other pages (Sec. 4, Cor.
  * "Group-shared selection"), and runs exact attention over those pages only
@@ -19,20 +20,21 @@
  *  - Host-side checks (configuration, null pointers, workspace size) run before
  *    any launch; a failing check returns an error and launches nothing.
  *    Device-resident values (page-table entries, sequence lengths) are trusted:
- *    page_table[s][j] must be a valid block for every j < ceil(seq_lens[s]/16),
- *    and seq_lens[s] <= 16 * max_pages_per_seq.  Entries past a sequence's last
- *    page are never read.
+ *    page_table[s][j] must be a valid block for every j < ceil(seq_lens[s]/B),
+ *    and seq_lens[s] <= B * max_pages_per_seq (B = page_size).  Entries past a
+ *    sequence's last page are never read.
  *  - Layouts (row-major, innermost last):
  *      q           [num_seqs][num_q_heads][128]          (q_dtype)
- *      k/v cache   [num_blocks][num_kv_heads][16][128]   (kv_dtype)
+ *      k/v cache   [num_blocks][num_kv_heads][B][128]    (kv_dtype, B = page_size)
  *      page_table  int32 [num_seqs][max_pages_per_seq]   logical page -> block
  *      seq_lens    int32 [num_seqs]                      tokens per sequence
- *      summaries   uint8 [num_blocks][num_kv_heads][locks_summary_stride(rank)]
+ *      summaries   uint8 [num_blocks][num_kv_heads][stride]
+ *                  stride = locks_summary_stride_page(rank, basis, page_size)
  *    Query head h belongs to KV head h / (num_q_heads / num_kv_heads).
  *  - Page ids returned and accepted by this API are LOGICAL page indices within
- *    their sequence.  Page j holds tokens [16j, 16j+16); page 0 is the sink and
- *    page ceil(L/16)-1 is the most recent page.  A page has a summary only once
- *    it is complete (16 tokens).
+ *    their sequence.  Page j holds tokens [Bj, Bj+B); page 0 is the sink and
+ *    page ceil(L/B)-1 is the most recent page.  A page has a summary only once
+ *    it is complete (B tokens).
  *  - The workspace `ws` (caller-allocated, >= locks_workspace_bytes(cfg) bytes,
  *    256-byte aligned) holds per-call scratch; its content need not be
  *    initialised and is meaningless after the call.  No call clears memory, so a
@@ -54,9 +56,10 @@ extern "C" {
 enum {
   LOCKS_OK = 0,
   LOCKS_E_INVAL = -1,        /* bad configuration value or null pointer          */
-  LOCKS_E_UNSUPPORTED = -2,  /* head_dim != 128, page_size != 16, G > 16,
-                                dtype unknown, or a summary store of 4 GiB or
-                                more (num_blocks * num_kv_heads * stride)        */
+  LOCKS_E_UNSUPPORTED = -2,  /* head_dim != 128, page_size not 16, 32 or 64, an
+                                int8 / bf16 basis or KIVI with page_size != 16,
+                                G > 16, dtype unknown, or a summary store of
+                                4 GiB or more (num_blocks * num_kv_heads * stride) */
   LOCKS_E_WORKSPACE = -3,    /* ws null or smaller than locks_workspace_bytes    */
   LOCKS_E_HIP = -4           /* a HIP launch failed; see locks_last_hip_error    */
 };
@@ -76,9 +79,9 @@ typedef struct locks_cfg {
   int32_t num_q_heads;       /* H_q, a multiple of H_kv; G = H_q / H_kv <= 16   */
   int32_t num_kv_heads;      /* H_kv >= 1                                       */
   int32_t head_dim;          /* d, must be 128                                  */
-  int32_t page_size;         /* B, must be 16                                   */
+  int32_t page_size;         /* B: 16, or 32 / 64 (App. D.3 "Page size")        */
   int32_t rank;              /* r in [1, 15]                                    */
-  int32_t budget_tokens;     /* b; the page budget k = ceil(b / 16) must be >= 2
+  int32_t budget_tokens;     /* b; the page budget k = ceil(b / B) must be >= 2
                                 (sink and most recent page take two slots,
                                 Sec. 2 and App. C.1 "Budget counting")          */
   int32_t max_pages_per_seq; /* row stride of page_table, >= 1                  */
@@ -118,12 +121,20 @@ size_t locks_summary_stride(int32_t rank);
 size_t locks_summary_payload_bytes_ex(int32_t rank, int32_t basis);
 size_t locks_summary_stride_ex(int32_t rank, int32_t basis);
 
+/* Payload and record stride for pages of page_size = B tokens (16, 32 or 64;
+ * App. D.3 "Page size"): the coefficient block holds B rows and the scales
+ * r + B + 1 entries, so for the int4 basis payload = 64 r + B r + 128 + 2 (r + B + 1)
+ * (978 and 1298 bytes at r = 8 for B = 32 and 64), the fields in the order above.
+ * Returns 0 for an unknown basis or page size or r outside [1, 15]. */
+size_t locks_summary_payload_bytes_page(int32_t rank, int32_t basis, int32_t page_size);
+size_t locks_summary_stride_page(int32_t rank, int32_t basis, int32_t page_size);
+
 /* Bytes of workspace the select / attend / decode-step calls need for cfg
  * (0 if cfg is invalid). */
 size_t locks_workspace_bytes(const locks_cfg_t* cfg);
 
 /* Build the summaries of complete pages (Sec. 4 "Build"): per (page, KV head)
- * centre the 16 keys, eigendecompose the 16 x 16 Gram of the deviations, keep the
+ * centre the B keys, eigendecompose the B x B Gram of the deviations, keep the
  * r leading nonzero modes (a mode counts as zero when its eigenvalue is at most
  * max(1e-6 * leading eigenvalue, 1e-10 * mean squared key norm)), form the
  * orthonormal basis V = D^T U_r S_r^{-1} and coefficients C = U_r S_r, make each
@@ -145,8 +156,8 @@ int locks_build_summaries(const locks_cfg_t* cfg, const void* k_cache,
  * n_build listed (seq, page) pairs (build_list required) and each KV head, write
  *   mu     float [n_build][H_kv][128]
  *   basis  float [n_build][H_kv][128][r]   (sign convention as above)
- *   coef   float [n_build][H_kv][16][r]
- *   sigma2 float [n_build][H_kv][16]       all Gram eigenvalues, descending, >= 0
+ *   coef   float [n_build][H_kv][B][r]
+ *   sigma2 float [n_build][H_kv][B]        all Gram eigenvalues, descending, >= 0
  * Dropped modes have zero basis and coefficient columns.  Listed pairs that are
  * not complete pages leave their rows untouched. */
 int locks_build_factors(const locks_cfg_t* cfg, const void* k_cache,
@@ -187,7 +198,7 @@ int locks_select(const locks_cfg_t* cfg, const void* q, const void* summaries,
  * pages, softmax renormalised over that set (Sec. 2; App. E "sparse decode"):
  *   o_g = sum_{i in S} softmax_S(q_g^T k_i / sqrt(128)) v_i.
  * The partial last page contributes its valid tokens only; -1 entries of
- * page_ids are skipped; ids must be < ceil(seq_lens[s]/16).
+ * page_ids are skipped; ids must be < ceil(seq_lens[s]/B).
  *   page_ids  int32 [S][H_kv][k] (k from cfg->budget_tokens)
  *   out       float [S][H_q][128]
  *   out_lse   nullable float [S][H_q], log of the softmax denominator
@@ -252,7 +263,8 @@ typedef struct locks_kivi {
  * skipped; a page may be listed once per call -- duplicates race).  All KV heads of
  * a page are quantised; kivi->stage is not used here.  Quantising a page twice is
  * not the identity in general, so each page should be finalised once.
- * Returns LOCKS_E_UNSUPPORTED unless kv_dtype is LOCKS_BF16, LOCKS_E_INVAL for a
+ * Returns LOCKS_E_UNSUPPORTED unless kv_dtype is LOCKS_BF16 and page_size is 16,
+ * LOCKS_E_INVAL for a
  * null kivi / cache / page_table / seq_lens, bits or v_group out of range,
  * n_pages < 0, or n_pages > 0 with a null page_list. */
 int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* k_cache,
@@ -263,8 +275,8 @@ int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* 
  * scheduled beside the selection): for every sequence s with seq_lens[s] >= 1,
  * the key and value rows k_new[s][h], v_new[s][h] ([num_seqs][num_kv_heads][128],
  * kv_dtype) are copied into the slot of token seq_lens[s] - 1, i.e. logical page
- * (seq_lens[s] - 1) / 16 (its block must be in page_table), row (seq_lens[s] - 1)
- * % 16, of every KV head.  seq_lens already counts the new token; nothing else is
+ * (seq_lens[s] - 1) / B (its block must be in page_table), row (seq_lens[s] - 1)
+ * % B, of every KV head.  seq_lens already counts the new token; nothing else is
  * written.  Returns LOCKS_E_INVAL for a null argument. */
 int locks_append_kv(const locks_cfg_t* cfg, const void* k_new, const void* v_new,
                     void* k_cache, void* v_cache, const int32_t* page_table,
@@ -285,7 +297,8 @@ typedef struct locks_step_opts {
  * finalised this step) are fake-quantised as locks_kivi_quantize does, before
  * their summary build (kivi->stage == LOCKS_KIVI_PRE) or after it
  * (LOCKS_KIVI_POST), each on the stream that builds it, and before the attention
- * reads them (kivi requires bf16 caches, else LOCKS_E_UNSUPPORTED).  The rest of
+ * reads them (kivi requires bf16 caches and 16-token pages, else
+ * LOCKS_E_UNSUPPORTED).  The rest of
  * the step is locks_decode_step's; opts == NULL is locks_decode_step itself.
  * Returns LOCKS_E_INVAL when exactly one of k_new, v_new is given. */
 int locks_decode_step_ex(const locks_cfg_t* cfg, const locks_step_opts_t* opts, const void* q,

@@ -14,7 +14,8 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 int validate(const locks_cfg_t* c) {
   if (!c) return LOCKS_E_INVAL;
-  if (c->head_dim != kDim || c->page_size != kPage) return LOCKS_E_UNSUPPORTED;
+  if (c->head_dim != kDim) return LOCKS_E_UNSUPPORTED;
+  if (c->page_size != 16 && c->page_size != 32 && c->page_size != 64) return LOCKS_E_UNSUPPORTED;
   if ((c->kv_dtype != LOCKS_BF16 && c->kv_dtype != LOCKS_FP32) ||
       (c->q_dtype != LOCKS_BF16 && c->q_dtype != LOCKS_FP32))
     return LOCKS_E_UNSUPPORTED;
@@ -25,7 +26,9 @@ int validate(const locks_cfg_t* c) {
   if (c->basis < LOCKS_BASIS_INT4 || c->basis > LOCKS_BASIS_BF16) return LOCKS_E_INVAL;
   if (c->basis != LOCKS_BASIS_INT4 && c->rank != 2 && c->rank != 4 && c->rank != 8)
     return LOCKS_E_UNSUPPORTED;
-  if (c->budget_tokens < 1 || (c->budget_tokens + kPage - 1) / kPage < 2) return LOCKS_E_INVAL;
+  if (c->basis != LOCKS_BASIS_INT4 && c->page_size != kPage) return LOCKS_E_UNSUPPORTED;
+  if (c->budget_tokens < 1 || (c->budget_tokens + c->page_size - 1) / c->page_size < 2)
+    return LOCKS_E_INVAL;
   if (c->max_pages_per_seq < 1 || c->num_blocks < 1) return LOCKS_E_INVAL;
   if ((long)c->num_seqs * c->num_q_heads > 0x7fffffffL / kDim) return LOCKS_E_INVAL;
   // record offsets are 32-bit: the summary store must stay below 4 GiB
@@ -128,12 +131,18 @@ int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
 // Table entries per attention block: 4 (one page per wave), doubled while the
 // grid would exceed ~512 blocks, so large batches stream several pages per
 // wave instead of paying per-block latency many times over.
+// (Counted in 16-token units: a table entry of B tokens is B / 16 of them.)
 int sparse_pages_per_split(const locks_cfg_t& c) {
   const long units = (long)c.num_seqs * c.num_kv_heads;
-  const int k = page_budget(c);
+  const int k = page_budget(c) << sub_page_log2(c);
   int pps = kSparsePagesPerSplit;
   while (pps < 32 && units * ((k + pps - 1) / pps) > 512) pps *= 2;
   return pps;
+}
+
+int sparse_splits(const locks_cfg_t& c) {
+  const int pps = sparse_pages_per_split(c);
+  return ((page_budget(c) << sub_page_log2(c)) + pps - 1) / pps;
 }
 
 // Dense baseline: pages per split block, 256 (64 per wave), halved while the grid
@@ -141,19 +150,34 @@ int sparse_pages_per_split(const locks_cfg_t& c) {
 // contexts and small batches still fill the chip.
 int dense_pages_per_split(const locks_cfg_t& c) {
   const long units = (long)c.num_seqs * c.num_kv_heads;
+  const long span = (long)c.max_pages_per_seq << sub_page_log2(c);
   int pps = kDensePagesPerSplit;
-  while (pps > 4 && units * ((c.max_pages_per_seq + pps - 1) / pps) < 512) pps /= 2;
+  while (pps > 4 && units * ((span + pps - 1) / pps) < 512) pps /= 2;
   return pps;
 }
 
 int dense_splits(const locks_cfg_t& c) {
   const int pps = dense_pages_per_split(c);
-  return (c.max_pages_per_seq + pps - 1) / pps;
+  return (int)((((long)c.max_pages_per_seq << sub_page_log2(c)) + pps - 1) / pps);
+}
+
+// The build for the configuration's page size: the Jacobi kernel for 16-token
+// pages (which also serves a step's overlapped build), the tridiagonal one for 32
+// and 64.
+hipError_t build_pages(const locks_cfg_t& c, const void* k_cache, const int32_t* page_table,
+                       const int32_t* seq_lens, const int32_t* build_list, int32_t n_items,
+                       bool all_pages, void* summaries, float* mu, float* basis, float* coef,
+                       float* sigma2, hipStream_t st) {
+  if (c.page_size != kPage)
+    return launch_build_page(c, k_cache, page_table, seq_lens, build_list, n_items, all_pages,
+                             summaries, mu, basis, coef, sigma2, st);
+  return launch_build(c, k_cache, page_table, seq_lens, build_list, n_items, all_pages, summaries,
+                      mu, basis, coef, sigma2, st);
 }
 
 }  // namespace
 
-int page_budget(const locks_cfg_t& c) { return (c.budget_tokens + kPage - 1) / kPage; }
+int page_budget(const locks_cfg_t& c) { return (c.budget_tokens + c.page_size - 1) / c.page_size; }
 
 WsPlan plan_workspace(const locks_cfg_t& c) {
   WsPlan p{};
@@ -162,8 +186,8 @@ WsPlan plan_workspace(const locks_cfg_t& c) {
   const int k = page_budget(c);
   const size_t K = k > 2 ? (size_t)(k - 2) : 1;
   p.n_chunks = (int)((mp + kSelChunk - 1) / kSelChunk);
-  const int sparse_splits = (k + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
-  p.n_splits = sparse_splits > dense_splits(c) ? sparse_splits : dense_splits(c);
+  const int sp = ((k << sub_page_log2(c)) + kSparsePagesPerSplit - 1) / kSparsePagesPerSplit;
+  p.n_splits = sp > dense_splits(c) ? sp : dense_splits(c);
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
   p.s_hat_off = take(S * Hq * mp * sizeof(float));
@@ -222,6 +246,18 @@ size_t locks_summary_stride_ex(int32_t rank, int32_t basis) {
   return (size_t)rec_stride(rank, basis);
 }
 
+size_t locks_summary_payload_bytes_page(int32_t rank, int32_t basis, int32_t page_size) {
+  if (rank < 1 || rank > kMaxRank || basis < LOCKS_BASIS_INT4 || basis > LOCKS_BASIS_BF16) return 0;
+  if (page_size != 16 && page_size != 32 && page_size != 64) return 0;
+  return (size_t)rec_payload(rank, basis, page_size);
+}
+
+size_t locks_summary_stride_page(int32_t rank, int32_t basis, int32_t page_size) {
+  if (rank < 1 || rank > kMaxRank || basis < LOCKS_BASIS_INT4 || basis > LOCKS_BASIS_BF16) return 0;
+  if (page_size != 16 && page_size != 32 && page_size != 64) return 0;
+  return (size_t)rec_stride(rank, basis, page_size);
+}
+
 size_t locks_workspace_bytes(const locks_cfg_t* cfg) {
   if (validate(cfg) != LOCKS_OK) return 0;
   return plan_workspace(*cfg).total;
@@ -236,9 +272,9 @@ int locks_build_summaries(const locks_cfg_t* cfg, const void* k_cache, const int
   if (build_list == nullptr && n_build > 0) return LOCKS_E_INVAL;
   if (cfg->num_seqs == 0) return LOCKS_OK;
   const bool all = build_list == nullptr;
-  return hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, all,
-                                 summaries, nullptr, nullptr, nullptr, nullptr,
-                                 static_cast<hipStream_t>(stream)));
+  return hip_status(build_pages(*cfg, k_cache, page_table, seq_lens, build_list, n_build, all,
+                                summaries, nullptr, nullptr, nullptr, nullptr,
+                                static_cast<hipStream_t>(stream)));
 }
 
 int locks_build_factors(const locks_cfg_t* cfg, const void* k_cache, const int32_t* page_table,
@@ -250,8 +286,8 @@ int locks_build_factors(const locks_cfg_t* cfg, const void* k_cache, const int32
       !coef || !sigma2)
     return LOCKS_E_INVAL;
   if (cfg->num_seqs == 0 || n_build == 0) return LOCKS_OK;
-  return hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
-                                 nullptr, mu, basis, coef, sigma2, static_cast<hipStream_t>(stream)));
+  return hip_status(build_pages(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
+                                nullptr, mu, basis, coef, sigma2, static_cast<hipStream_t>(stream)));
 }
 
 int locks_select(const locks_cfg_t* cfg, const void* q, const void* summaries,
@@ -292,9 +328,8 @@ int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cac
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
   const WsPlan p = plan_workspace(*cfg);
-  const int k = page_budget(*cfg);
   const int pps = sparse_pages_per_split(*cfg);
-  const int splits = (k + pps - 1) / pps;
+  const int splits = sparse_splits(*cfg);
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, page_ids,
                                   pps, splits, carve(ws, p).attn, out, out_lse,
                                   static_cast<hipStream_t>(stream)));
@@ -319,7 +354,7 @@ int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* 
                         const int32_t* page_list, int32_t n_pages, void* stream) {
   int rc = validate(cfg);
   if (rc) return rc;
-  if (cfg->kv_dtype != LOCKS_BF16) return LOCKS_E_UNSUPPORTED;
+  if (cfg->kv_dtype != LOCKS_BF16 || cfg->page_size != kPage) return LOCKS_E_UNSUPPORTED;
   if (!kivi || !kivi_valid(*kivi) || !k_cache || !v_cache || !page_table || !seq_lens ||
       n_pages < 0 || (n_pages > 0 && !page_list))
     return LOCKS_E_INVAL;
@@ -357,7 +392,7 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opt
   const void* k_new = opts ? opts->k_new : nullptr;
   const void* v_new = opts ? opts->v_new : nullptr;
   if ((k_new == nullptr) != (v_new == nullptr)) return LOCKS_E_INVAL;
-  if (kivi && cfg->kv_dtype != LOCKS_BF16) return LOCKS_E_UNSUPPORTED;
+  if (kivi && (cfg->kv_dtype != LOCKS_BF16 || cfg->page_size != kPage)) return LOCKS_E_UNSUPPORTED;
   if (kivi && !kivi_valid(*kivi)) return LOCKS_E_INVAL;
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
@@ -382,7 +417,8 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opt
   // and KV, int4 basis); the lock also serialises the fork / join enqueues.
   std::unique_lock<std::mutex> side_lock;
   SideStream* side = nullptr;
-  if (attend_select_fused(*cfg) && n_build > 0 && cfg->basis == LOCKS_BASIS_INT4) {
+  if (attend_select_fused(*cfg) && n_build > 0 && cfg->basis == LOCKS_BASIS_INT4 &&
+      cfg->page_size == kPage) {
     side_lock = std::unique_lock<std::mutex>(g_side_mu);
     if ((rc = hip_status(side_stream(&side, create_side)))) return rc;
   }
@@ -392,15 +428,14 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opt
   auto post_kivi = [&]() -> int { return hip_status(kivi_at(LOCKS_KIVI_POST, st, kKiviAny)); };
   const WsPlan p = plan_workspace(*cfg);
   const Ws w = carve(ws, p);
-  const int k = page_budget(*cfg);
   const int pps = sparse_pages_per_split(*cfg);
-  const int splits = (k + pps - 1) / pps;
+  const int splits = sparse_splits(*cfg);
   if (attend_select_fused(*cfg)) {
     // scan -> per-chunk selection -> attention whose blocks merge the table
     const SHatLayout lay = shat_head_minor(*cfg);
     const float2* part_x = nullptr;
     if (n_build > 0 && !forked) {
-      rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
+      rc = hip_status(build_pages(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
                                    summaries, nullptr, nullptr, nullptr, nullptr, st));
       if (rc) return rc;
       if ((rc = post_kivi())) return rc;
@@ -448,7 +483,7 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opt
                                            pps, splits, w.attn, out, out_lse, st));
   }
   if (n_build > 0) {
-    rc = hip_status(launch_build(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
+    rc = hip_status(build_pages(*cfg, k_cache, page_table, seq_lens, build_list, n_build, false,
                                  summaries, nullptr, nullptr, nullptr, nullptr, st));
     if (rc) return rc;
     if ((rc = post_kivi())) return rc;

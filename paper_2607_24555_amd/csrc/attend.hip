@@ -29,10 +29,12 @@ constexpr int kAttnBlock = 256;
 template <typename T>
 __device__ __forceinline__ float ld(const T* p, size_t i) { return load_elem(p, i); }
 
+// Work is counted in 16-token sub-pages: unit t of the list is sub-page t % nsub
+// of list entry t / nsub (nsub = B / 16 for pages of B tokens).
 template <typename QT, typename KT>
 __global__ __launch_bounds__(kAttnBlock) void attend_kernel(
-    int H_q, int H_kv, int max_pages, int k_list, const QT* __restrict__ q,
-    const KT* __restrict__ k_cache, const KT* __restrict__ v_cache,
+    int H_q, int H_kv, int max_pages, int k_list, int pgsz, int lg_sub,
+    const QT* __restrict__ q, const KT* __restrict__ k_cache, const KT* __restrict__ v_cache,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ page_ids, int pages_per_split, int n_splits,
     float* __restrict__ partial) {
@@ -47,7 +49,7 @@ __global__ __launch_bounds__(kAttnBlock) void attend_kernel(
   const int tid = threadIdx.x;
   const int G = H_q / H_kv;
   const int L = seq_lens[s];
-  const int n = (L + kPage - 1) / kPage;
+  const int n = (L + pgsz - 1) / pgsz;
   const float zscale = 1.0f / sqrtf((float)kDim);
 
   for (int e = tid; e < G * kDim; e += kAttnBlock) {
@@ -59,16 +61,19 @@ __global__ __launch_bounds__(kAttnBlock) void attend_kernel(
 
   const int t0 = split * pages_per_split;
   for (int t = t0; t < t0 + pages_per_split; ++t) {
+    const int entry = t >> lg_sub, sub = t & ((1 << lg_sub) - 1);
     int id;
     if (page_ids) {
-      id = t < k_list ? page_ids[((long)s * H_kv + h) * k_list + t] : -1;
+      id = entry < k_list ? page_ids[((long)s * H_kv + h) * k_list + entry] : -1;
     } else {
-      id = t;
+      id = entry;
     }
     if (id < 0 || id >= n) continue;  // uniform across the block
+    const int tok0 = id * pgsz + sub * kPage;
+    if (tok0 >= L) continue;
     const long blk = page_table[(long)s * max_pages + id];
-    const int valid = min(kPage, L - id * kPage);
-    const long base = ((blk * H_kv + h) * kPage) * kDim;
+    const int valid = min(kPage, L - tok0);
+    const long base = ((blk * H_kv + h) * pgsz + sub * kPage) * kDim;
     for (int e = tid; e < kPage * kDim; e += kAttnBlock) {
       sK[e / kDim][e % kDim] = ld(k_cache, base + e);
       sV[e / kDim][e % kDim] = ld(v_cache, base + e);
@@ -191,7 +196,8 @@ struct SelTable {
 // count, one page in flight ahead of the one being used.
 template <bool kSelect, int kPPW>
 __global__ __launch_bounds__(256) void attend_mfma_kernel(
-    int H_q, int H_kv, int max_pages, int k_list, const uint16_t* __restrict__ q,
+    int H_q, int H_kv, int max_pages, int k_list, int pgsz, int lg_sub,
+    const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ page_ids, int pages_per_split, int n_splits,
@@ -213,8 +219,9 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
                             tb.sb.cand_blk + rb, tb.sb.sat + unit * tb.n_rows);
   }
   const int L = seq_lens[s];
-  const int n = (L + kPage - 1) / kPage;
+  const int n = (L + pgsz - 1) / pgsz;
   const float zs = kLog2e / sqrtf((float)kDim);
+  const int sub_mask = (1 << lg_sub) - 1;
 
   uint4 qb[4];
   {
@@ -234,19 +241,20 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
     ids = s_tab;
   }
   // this block's table entries and their estimated page LSEs (NaN without a
-  // summary): loaded now, written after the pages (pages_per_split <= 32, so at
-  // most 32 x 17 entries over the 256 threads)
+  // summary): loaded now, written after the pages (at most 32 entries per block,
+  // so at most 32 x 17 values over the 256 threads)
   constexpr int kSelPer = 3;
+  const int epb = pages_per_split >> lg_sub;  // table entries per block
   float sel_v[kSelPer];
   int sel_e[kSelPer];
   if constexpr (kSelect) {
-    const int t0 = split * pages_per_split, n_c = L / kPage;
+    const int t0 = split * epb, n_c = L / pgsz;
     const float* sb = tb.s_hat + tb.lay.base(s, h);
 #pragma unroll
     for (int u = 0; u < kSelPer; ++u) {
       const int e = tid + 256 * u;
-      const int t = t0 + e % pages_per_split, g = e / pages_per_split;
-      sel_e[u] = (e < pages_per_split * (G + 1) && t < k_list) ? e : -1;
+      const int t = t0 + e % epb, g = e / epb;
+      sel_e[u] = (e < epb * (G + 1) && t < k_list) ? e : -1;
       sel_v[u] = 0.0f;
       if (sel_e[u] >= 0 && g < G) {
         const int id = s_tab[t];
@@ -256,34 +264,41 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
       }
     }
   }
+  // unit t: sub-page t & sub_mask of list entry t >> lg_sub; returns the unit's
+  // first token (-1: nothing to attend)
   auto page_at = [&](int t) -> int {
     int id = -1;
-    if (t < t_end) id = ids ? (t < k_list ? ids[t] : -1) : t;
-    return (id >= 0 && id < n) ? id : -1;
+    const int entry = t >> lg_sub;
+    if (t < t_end) id = ids ? (entry < k_list ? ids[entry] : -1) : entry;
+    const int tok0 = (id >= 0 && id < n) ? id * pgsz + (t & sub_mask) * kPage : -1;
+    return tok0 < L ? tok0 : -1;
   };
-  const long kv_head = (long)h * kPage * kDim;
-  const long kv_blk = (long)H_kv * kPage * kDim;
-  // physical block of list entry t holding page id (a valid block stands in for an
-  // empty entry); the fused step knows the blocks from the selection
-  auto blk_at = [&](int t, int id) -> long {
+  const long kv_head = (long)h * pgsz * kDim;
+  const long kv_blk = (long)H_kv * pgsz * kDim;
+  // physical block of unit t starting at token tok0 (a valid block stands in for an
+  // empty unit); the fused step knows the blocks from the selection
+  auto blk_at = [&](int t, int tok0) -> long {
     if constexpr (kSelect) {
-      const int b = t < k_list ? s_blk[t] : -1;
+      const int entry = t >> lg_sub;
+      const int b = entry < k_list ? s_blk[entry] : -1;
       return b >= 0 ? b : s_blk[0];
     } else {
-      return page_table[(long)s * max_pages + (id >= 0 ? id : 0)];
+      return page_table[(long)s * max_pages + (tok0 >= 0 ? tok0 / pgsz : 0)];
     }
   };
-  auto page_ptr = [&](long blk, const uint16_t* base) { return base + blk * kv_blk + kv_head; };
+  auto page_ptr = [&](long blk, int t, const uint16_t* base) {
+    return base + blk * kv_blk + kv_head + (long)(t & sub_mask) * kPage * kDim;
+  };
 
   float m = -INFINITY, l = 0.0f;
   f4v o[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t) o[t] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
 
-  // one page of the list (id < 0: an empty entry, nothing to add)
-  auto use_page = [&](const PageRegs& cur, int id) {
-    if (id >= 0) {
-      const int valid = min(kPage, L - id * kPage);
+  // one 16-token unit of the list (tok0 < 0: an empty unit, nothing to add)
+  auto use_page = [&](const PageRegs& cur, int tok0) {
+    if (tok0 >= 0) {
+      const int valid = min(kPage, L - tok0);
       f4v st = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
@@ -321,12 +336,12 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
       }
     }
   };
-  // loads list entry t into P (a valid page stands in for an empty entry)
+  // loads unit t into P (a valid page stands in for an empty unit)
   auto load_entry = [&](PageRegs& P, int t) {
-    const int id = page_at(t);
-    const long b = blk_at(t, id);
-    load_page(P, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
-    return id;
+    const int tok0 = page_at(t);
+    const long b = blk_at(t, tok0);
+    load_page(P, page_ptr(b, t, k_cache), page_ptr(b, t, v_cache), c16, r4);
+    return tok0;
   };
 
   if (n > 0) {
@@ -346,15 +361,15 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
       PageRegs cur;
       {
         const long b = blk_at(t_begin, id);
-        load_page(cur, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
+        load_page(cur, page_ptr(b, t_begin, k_cache), page_ptr(b, t_begin, v_cache), c16, r4);
       }
       for (int t = t_begin; t < t_end; ++t) {
-        // prefetch the next entry (a valid page stands in for an empty one)
+        // prefetch the next unit (a valid page stands in for an empty one)
         const int id_next = page_at(t + 1);
         PageRegs nxt;
         if (t + 1 < t_end) {
           const long b = blk_at(t + 1, id_next);
-          load_page(nxt, page_ptr(b, k_cache), page_ptr(b, v_cache), c16, r4);
+          load_page(nxt, page_ptr(b, t + 1, k_cache), page_ptr(b, t + 1, v_cache), c16, r4);
         }
         use_page(cur, id);
         id = id_next;
@@ -364,12 +379,12 @@ __global__ __launch_bounds__(256) void attend_mfma_kernel(
   }
   if constexpr (kSelect) {
     const long unit = (long)s * H_kv + h;
-    const int t0 = split * pages_per_split;
+    const int t0 = split * epb;
 #pragma unroll
     for (int u = 0; u < kSelPer; ++u) {
       const int e = sel_e[u];
       if (e < 0) continue;
-      const int t = t0 + e % pages_per_split, g = e / pages_per_split;
+      const int t = t0 + e % epb, g = e / epb;
       if (g == G) tb.out_ids[unit * k_list + t] = s_tab[t];
       else tb.out_sel_lse[((long)s * H_q + h * G + g) * k_list + t] = sel_v[u];
     }
@@ -450,7 +465,8 @@ void launch_typed(const locks_cfg_t& c, const void* q, const void* k_cache, cons
                   int pages_per_split, int n_splits, float* partial, hipStream_t st) {
   hipLaunchKernelGGL((attend_kernel<QT, KT>), dim3(n_splits, c.num_kv_heads, c.num_seqs),
                      dim3(kAttnBlock), 0, st, c.num_q_heads, c.num_kv_heads, c.max_pages_per_seq,
-                     page_budget(c), static_cast<const QT*>(q), static_cast<const KT*>(k_cache),
+                     page_budget(c), c.page_size, sub_page_log2(c), static_cast<const QT*>(q),
+                     static_cast<const KT*>(k_cache),
                      static_cast<const KT*>(v_cache), page_table, seq_lens, page_ids,
                      pages_per_split, n_splits, partial);
 }
@@ -465,8 +481,9 @@ void launch_mfma(const locks_cfg_t& c, dim3 grid, hipStream_t st, const uint16_t
   const int ppw = pages_per_split % 4 == 0 ? pages_per_split / 4 : 0;
 #define LOCKS_ATTEND_MFMA(P)                                                                   \
   hipLaunchKernelGGL((attend_mfma_kernel<kSelect, P>), grid, dim3(256), 0, st, c.num_q_heads,   \
-                     c.num_kv_heads, c.max_pages_per_seq, page_budget(c), q, k_cache, v_cache,  \
-                     page_table, seq_lens, page_ids, pages_per_split, n_splits, partial, tb)
+                     c.num_kv_heads, c.max_pages_per_seq, page_budget(c), c.page_size,          \
+                     sub_page_log2(c), q, k_cache, v_cache, page_table, seq_lens, page_ids,     \
+                     pages_per_split, n_splits, partial, tb)
   switch (ppw) {
     case 1: LOCKS_ATTEND_MFMA(1); break;
     case 2: LOCKS_ATTEND_MFMA(2); break;

@@ -14,15 +14,23 @@ constexpr int kDim = 128;    // d
 constexpr int kMaxRank = 15; // r <= B - 1 (rank of centred page deviations)
 constexpr int kMaxGroup = 16;   // G = H_q / H_kv
 
-// Byte offsets inside one summary record for rank r and basis precision b
-// (0 int4, 1 int8, 2 bf16: 64 << b bytes per basis column; see
-// locks_summary_stride_ex).
+// Byte offsets inside one summary record for rank r, basis precision b (0 int4,
+// 1 int8, 2 bf16: 64 << b bytes per basis column; see locks_summary_stride_ex) and
+// pages of P tokens (16, 32 or 64; P coefficient rows and P + r + 1 scales).
 __host__ __device__ constexpr int rec_col_bytes(int b = 0) { return 64 << b; }
 __host__ __device__ constexpr int rec_coef_off(int r, int b = 0) { return rec_col_bytes(b) * r; }
-__host__ __device__ constexpr int rec_mu_off(int r, int b = 0) { return rec_col_bytes(b) * r + 16 * r; }
-__host__ __device__ constexpr int rec_scale_off(int r, int b = 0) { return rec_mu_off(r, b) + kDim; }
-__host__ __device__ constexpr int rec_payload(int r, int b = 0) { return rec_scale_off(r, b) + 2 * (r + 17); }
-__host__ __device__ constexpr int rec_stride(int r, int b = 0) { return (rec_payload(r, b) + 15) / 16 * 16; }
+__host__ __device__ constexpr int rec_mu_off(int r, int b = 0, int P = kPage) {
+  return rec_col_bytes(b) * r + P * r;
+}
+__host__ __device__ constexpr int rec_scale_off(int r, int b = 0, int P = kPage) {
+  return rec_mu_off(r, b, P) + kDim;
+}
+__host__ __device__ constexpr int rec_payload(int r, int b = 0, int P = kPage) {
+  return rec_scale_off(r, b, P) + 2 * (r + P + 1);
+}
+__host__ __device__ constexpr int rec_stride(int r, int b = 0, int P = kPage) {
+  return (rec_payload(r, b, P) + 15) / 16 * 16;
+}
 
 // ---------------------------------------------------------------- device helpers
 
@@ -109,9 +117,14 @@ WsPlan plan_workspace(const locks_cfg_t& c);
 // Bytes of the summary store (every block's records); below 2^32 for a valid
 // configuration, so record offsets fit 32 bits.
 inline size_t summary_store_bytes(const locks_cfg_t& c) {
-  return (size_t)c.num_blocks * (size_t)c.num_kv_heads * (size_t)rec_stride(c.rank, c.basis);
+  return (size_t)c.num_blocks * (size_t)c.num_kv_heads *
+         (size_t)rec_stride(c.rank, c.basis, c.page_size);
 }
-int page_budget(const locks_cfg_t& c);  // k = ceil(b / 16)
+int page_budget(const locks_cfg_t& c);  // k = ceil(b / B)
+// Attention works on 16-token units: a page of B tokens is B / 16 of them.
+inline int sub_page_log2(const locks_cfg_t& c) {
+  return c.page_size == 64 ? 2 : (c.page_size == 32 ? 1 : 0);
+}
 int scan_pages_per_block(const locks_cfg_t& c);  // pages covered by one scan block
 inline int scan_blocks(const locks_cfg_t& c) {
   const int ppb = scan_pages_per_block(c);
@@ -142,6 +155,13 @@ hipError_t launch_build(const locks_cfg_t& c, const void* k_cache, const int32_t
                         bool all_pages, void* summaries, float* mu, float* basis, float* coef,
                         float* sigma2, hipStream_t st, BuildMode mode = kBuildAll,
                         const BuildStep* step = nullptr);
+
+// The same build for pages of B = 16, 32 or 64 tokens (tridiagonal eigensolver);
+// every listed or complete page, or the unquantised factors when mu != nullptr.
+hipError_t launch_build_page(const locks_cfg_t& c, const void* k_cache, const int32_t* page_table,
+                             const int32_t* seq_lens, const int32_t* build_list, int32_t n_items,
+                             bool all_pages, void* summaries, float* mu, float* basis,
+                             float* coef, float* sigma2, hipStream_t st);
 
 hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summaries,
                        const int32_t* page_table, const int32_t* seq_lens, float* s_hat,

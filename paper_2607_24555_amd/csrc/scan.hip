@@ -1609,6 +1609,280 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
 }
 
 
+// ---------------------------------------------------------------------------
+// Pages of B = 32 or 64 tokens (App. D.3 "Page size"), int4 basis.  The generic
+// kernel's two stages with tiles of 8 pages: stage 1 (f16 MFMA, rows (page, basis
+// column), columns the query heads) and the centroid projection are unchanged,
+// the record tail holds B coefficient rows, and stage 2 runs one page at a time on
+// fp32 MFMA 16x16x4 with the B tokens as rows (B / 16 row tiles) and the heads as
+// columns; each lane then holds 4 B / 16 logits of one head and the page LSE
+// takes its max and sum over them and the three other lanes of the head.
+// ---------------------------------------------------------------------------
+template <int R, int B>
+struct PageGeom {
+  static constexpr int kTP = 8;                                   // pages per tile
+  static constexpr int kPPS = (16 / R) > 0 ? 16 / R : 1;          // pages per stage-1 set
+  static constexpr int kSets = (kTP + kPPS - 1) / kPPS;
+  static constexpr int kStride = rec_stride(R, 0, B);
+  static constexpr int kTail = kStride - 64 * R;                  // coef .. end of record
+  static constexpr int kTailCh = kTail / 16;
+  static constexpr int kTailLoads = (kTP * kTailCh + 63) / 64;
+  static constexpr int kMu = B * R;                               // offsets inside the tail
+  static constexpr int kSc = B * R + kDim;
+  static constexpr int kTiles = 64 / kTP;                         // tiles per wave (64 pages)
+};
+
+template <int R, int B>
+struct PageRegs {
+  uint4 vb[PageGeom<R, B>::kSets];
+  uint4 tl[PageGeom<R, B>::kTailLoads];
+  int blk;  // lanes 0 .. kTP - 1: block of page page0 + lane (-1: none)
+};
+
+template <int R, int B>
+__device__ __forceinline__ void issue_page_tile(PageRegs<R, B>& T, const uint8_t* __restrict__ summ,
+                                                const int32_t* __restrict__ pt_row, int page0,
+                                                int n_c, int H_kv, int h, int lane) {
+  using Gm = PageGeom<R, B>;
+  const int col = lane & 15, grp = lane >> 4;
+  const int my_blk = (lane < Gm::kTP && page0 + lane < n_c) ? pt_row[page0 + lane] : -1;
+  T.blk = my_blk;
+  const int pp = col / R, l = col % R;
+#pragma unroll
+  for (int st = 0; st < Gm::kSets; ++st) {
+    const int page = st * Gm::kPPS + pp;
+    const int blk = __shfl(my_blk, page < Gm::kTP ? page : 0, 64);
+    const bool ok = col < Gm::kPPS * R && page < Gm::kTP && blk >= 0;
+    T.vb[st] = ok ? *reinterpret_cast<const uint4*>(summ + ((long)blk * H_kv + h) * Gm::kStride +
+                                                    64 * l + 16 * grp)
+                  : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < Gm::kTailLoads; ++u) {
+    const int c = lane + 64 * u;
+    const int page = c / Gm::kTailCh, off = (c % Gm::kTailCh) * 16;
+    const int blk = __shfl(my_blk, page < Gm::kTP ? page : 0, 64);
+    T.tl[u] = (c < Gm::kTP * Gm::kTailCh && blk >= 0)
+                  ? *reinterpret_cast<const uint4*>(summ + ((long)blk * H_kv + h) * Gm::kStride +
+                                                    64 * R + off)
+                  : make_uint4(0, 0, 0, 0);
+  }
+}
+
+template <typename QT, int R, int B>
+__global__ __launch_bounds__(256) void scan_page_kernel(
+    int H_q, int H_kv, int max_pages, const QT* __restrict__ q,
+    const uint8_t* __restrict__ summaries, const int32_t* __restrict__ page_table,
+    const int32_t* __restrict__ seq_lens, float* __restrict__ s_hat, SHatLayout lay,
+    float2* __restrict__ partials) {
+  using Gm = PageGeom<R, B>;
+  constexpr bool kSplitQ = sizeof(QT) == 4;  // fp32 queries: f16 hi + lo
+  constexpr int kKS = (R + 3) / 4;           // stage-2 k-steps
+  constexpr int kRT = B / 16;                // stage-2 row tiles
+  __shared__ __align__(16) uint8_t sTail[4][Gm::kTP][Gm::kTail];
+  __shared__ float sP[4][Gm::kTP][R][16];
+  __shared__ float sA[4][Gm::kTP][16];
+  __shared__ float2 sRun[4][16];
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int h = blockIdx.y, s = blockIdx.z;
+  const int G = H_q / H_kv;
+  const int n_c = seq_lens[s] / B;
+  const int pg = scan_chunk() * 4 + wave;  // 64-page group of this wave
+  const long row0 = (long)s * H_q + (long)h * G;
+  const int32_t* pt_row = page_table + (long)s * max_pages;
+  float run_m = -INFINITY, run_s = 0.0f;  // running normaliser of head col, log2 domain
+  if (pg * 64 < n_c) {
+    PageRegs<R, B> buf[2];
+    issue_page_tile<R, B>(buf[0], summaries, pt_row, pg * 64, n_c, H_kv, h, lane);
+
+    // ---- B operands: column = query head, K permuted to match the decoders
+    constexpr int kPerm[8] = {0, 4, 1, 5, 2, 6, 3, 7};
+    float qv[4][8], qm[4][8];
+    float qmax = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        const int cv = 32 * grp + 8 * ks + kPerm[jj], cm = 32 * grp + 8 * ks + jj;
+        const float a = col < G ? load_q(q, (row0 + col) * kDim + cv) : 0.0f;
+        const float b = col < G ? load_q(q, (row0 + col) * kDim + cm) : 0.0f;
+        qv[ks][jj] = a;
+        qm[ks][jj] = b;
+        qmax = fmaxf(qmax, fabsf(a));
+      }
+    qmax = warp_max(qmax);
+    // power-of-two range scale so that every query element fits f16 exactly
+    float qs = 1.0f;
+    while (qmax * qs > 16384.0f) qs *= 0.5f;
+    const float inv_qs = 1.0f / qs;
+    h8 bv[4], bm[4], bvl[4], bml[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        const float a = qv[ks][jj] * qs, b = qm[ks][jj] * qs;
+        const _Float16 ah = (_Float16)a, bh = (_Float16)b;
+        bv[ks][jj] = ah;
+        bm[ks][jj] = bh;
+        bvl[ks][jj] = (_Float16)(a - (float)ah);
+        bml[ks][jj] = (_Float16)(b - (float)bh);
+      }
+
+    constexpr float kLn2 = 0.69314718055994531f;
+    const float c0 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
+
+    for (int t = 0; t < Gm::kTiles; ++t) {
+      const int page0 = pg * 64 + t * Gm::kTP;
+      if (page0 >= n_c) break;
+      PageRegs<R, B>& cur = buf[t & 1];
+      if (t + 1 < Gm::kTiles && page0 + Gm::kTP < n_c)
+        issue_page_tile<R, B>(buf[(t + 1) & 1], summaries, pt_row, page0 + Gm::kTP, n_c, H_kv, h,
+                              lane);
+#pragma unroll
+      for (int u = 0; u < Gm::kTailLoads; ++u) {
+        const int c = lane + 64 * u;
+        if (c < Gm::kTP * Gm::kTailCh)
+          *reinterpret_cast<uint4*>(&sTail[wave][c / Gm::kTailCh][(c % Gm::kTailCh) * 16]) =
+              cur.tl[u];
+      }
+      __builtin_amdgcn_wave_barrier();
+
+      // ---- stage 1: p = V^T q (scaled by the basis column scales)
+#pragma unroll
+      for (int st = 0; st < Gm::kSets; ++st) {
+        f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        const uint32_t w[4] = {cur.vb[st].x, cur.vb[st].y, cur.vb[st].z, cur.vb[st].w};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const h8 a = nib8_to_h8(w[ks]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bv[ks], acc, 0, 0, 0);
+          if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bvl[ks], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int m = 4 * grp + jj;
+          const int pp = m / R, l = m % R;
+          const int page = st * Gm::kPPS + pp;
+          if (m < Gm::kPPS * R && page < Gm::kTP && col < G)
+            sP[wave][page][l][col] = acc[jj] * inv_qs * lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
+        }
+      }
+      // ---- centroid term a = mu^T q, one page per row
+      {
+        const int cp = col < Gm::kTP ? col : 0;
+        const uint4 m0 = *reinterpret_cast<const uint4*>(&sTail[wave][cp][Gm::kMu + 32 * grp]);
+        const uint4 m1 = *reinterpret_cast<const uint4*>(&sTail[wave][cp][Gm::kMu + 32 * grp + 16]);
+        const uint32_t w[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+        f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const h8 a = byte8_to_h8(w[2 * ks], w[2 * ks + 1]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bm[ks], acc, 0, 0, 0);
+          if (kSplitQ) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bml[ks], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int page = 4 * grp + jj;
+          if (page < Gm::kTP && col < G)
+            sA[wave][page][col] =
+                acc[jj] * inv_qs * c0 * lds_f16(&sTail[wave][page][Gm::kSc + 2 * (R + B)]);
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+
+      // ---- stage 2, one page at a time: z[token][head] over B / 16 row tiles
+      for (int p = 0; p < Gm::kTP; ++p) {
+        if (page0 + p >= n_c) break;
+        float z[kRT][4];
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) {
+          f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int kstep = 0; kstep < kKS; ++kstep) {
+            const int l = 4 * kstep + grp;
+            const int tok = 16 * rt + col;
+            const float a = l < R ? (float)((int)sTail[wave][p][tok * R + l] - 128) : 0.0f;
+            const float b = (l < R && col < G) ? sP[wave][p][l < R ? l : 0][col] : 0.0f;
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+          }
+          const uint2 csw = *reinterpret_cast<const uint2*>(
+              &sTail[wave][p][Gm::kSc + 2 * (R + 16 * rt + 4 * grp)]);
+          const h2 cs01 = as_h2(csw.x), cs23 = as_h2(csw.y);
+          const float av = sA[wave][p][col];
+          z[rt][0] = fmaf((float)cs01.x * c0, acc[0], av);
+          z[rt][1] = fmaf((float)cs01.y * c0, acc[1], av);
+          z[rt][2] = fmaf((float)cs23.x * c0, acc[2], av);
+          z[rt][3] = fmaf((float)cs23.y * c0, acc[3], av);
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt)
+          mx = fmaxf(mx, fmaxf(fmaxf(z[rt][0], z[rt][1]), fmaxf(z[rt][2], z[rt][3])));
+        mx = red4_max(mx);
+        float sm = 0.0f;
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) sm += __builtin_amdgcn_exp2f(z[rt][jj] - mx);
+        sm = red4_sum(sm);
+        const float s2 = mx + __builtin_amdgcn_logf(sm);  // log2-domain page score
+        if (col < G) {
+          if (grp == 0)
+            s_hat[lay.base(s, h) + col * lay.head + (long)(page0 + p) * lay.page] = s2 * kLn2;
+          const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+          if (s2 > run_m) { run_s = fmaf(run_s, e, 1.0f); run_m = s2; }
+          else run_s += e;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  // ---- block partial (max, sum exp) per head over its pages (log2 domain)
+  if (lane < 16) sRun[wave][lane] = make_float2(run_m, run_s);
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int g = threadIdx.x;
+    float m = -INFINITY, l = 0.0f;
+    for (int w = 0; w < 4; ++w) m = fmaxf(m, sRun[w][g].x);
+    if (m > -INFINITY)
+      for (int w = 0; w < 4; ++w) {
+        const float2 v = sRun[w][g];
+        if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+      }
+    partials[(row0 + g) * gridDim.x + blockIdx.x] = make_float2(m, l);
+  }
+}
+
+
+template <typename QT>
+hipError_t dispatch_scan_page(int r, int B, dim3 grid, hipStream_t st, int H_q, int H_kv,
+                              int max_pages, const QT* q, const uint8_t* sum, const int32_t* pt,
+                              const int32_t* sl, float* s_hat, SHatLayout lay, float2* part) {
+#define LOCKS_SCAN_PAGE_CASE(RR)                                                              \
+  case RR:                                                                                   \
+    if (B == 32)                                                                             \
+      hipLaunchKernelGGL((scan_page_kernel<QT, RR, 32>), grid, dim3(256), 0, st, H_q, H_kv,  \
+                         max_pages, q, sum, pt, sl, s_hat, lay, part);                       \
+    else                                                                                     \
+      hipLaunchKernelGGL((scan_page_kernel<QT, RR, 64>), grid, dim3(256), 0, st, H_q, H_kv,  \
+                         max_pages, q, sum, pt, sl, s_hat, lay, part);                       \
+    break;
+  if (B != 32 && B != 64) return hipErrorInvalidValue;
+  switch (r) {
+    LOCKS_SCAN_PAGE_CASE(1) LOCKS_SCAN_PAGE_CASE(2) LOCKS_SCAN_PAGE_CASE(3)
+    LOCKS_SCAN_PAGE_CASE(4) LOCKS_SCAN_PAGE_CASE(5) LOCKS_SCAN_PAGE_CASE(6)
+    LOCKS_SCAN_PAGE_CASE(7) LOCKS_SCAN_PAGE_CASE(8) LOCKS_SCAN_PAGE_CASE(9)
+    LOCKS_SCAN_PAGE_CASE(10) LOCKS_SCAN_PAGE_CASE(11) LOCKS_SCAN_PAGE_CASE(12)
+    LOCKS_SCAN_PAGE_CASE(13) LOCKS_SCAN_PAGE_CASE(14) LOCKS_SCAN_PAGE_CASE(15)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef LOCKS_SCAN_PAGE_CASE
+  return hipGetLastError();
+}
+
 template <typename QT>
 hipError_t dispatch_scan(int r, int G, int basis, int steps, dim3 grid, hipStream_t st, int H_q,
                          int H_kv, int max_pages, const QT* q, const uint8_t* sum,
@@ -1683,11 +1957,13 @@ hipError_t dispatch_scan(int r, int G, int basis, int steps, dim3 grid, hipStrea
 }  // namespace
 
 static bool use_r8_kernel(const locks_cfg_t& c) {
-  return c.basis == LOCKS_BASIS_INT4 && c.rank == 8 && c.num_q_heads == 16 * c.num_kv_heads;
+  return c.page_size == kPage && c.basis == LOCKS_BASIS_INT4 && c.rank == 8 &&
+         c.num_q_heads == 16 * c.num_kv_heads;
 }
 
 static bool use_r8g4_kernel(const locks_cfg_t& c) {
-  return c.basis == LOCKS_BASIS_INT4 && c.rank == 8 && c.num_q_heads == 4 * c.num_kv_heads;
+  return c.page_size == kPage && c.basis == LOCKS_BASIS_INT4 && c.rank == 8 &&
+         c.num_q_heads == 4 * c.num_kv_heads;
 }
 
 // 16-page steps per wave of the r = 8 kernels: 4, or 1 when a 4-step grid would
@@ -1709,6 +1985,17 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
   const int G = c.num_q_heads / c.num_kv_heads;
   const uint32_t bytes = (uint32_t)summary_store_bytes(c);
   const int steps = r8_steps(c);
+  if (c.page_size != kPage) {
+    if (c.q_dtype == LOCKS_BF16)
+      return dispatch_scan_page(c.rank, c.page_size, grid, st, c.num_q_heads, c.num_kv_heads,
+                                c.max_pages_per_seq, static_cast<const uint16_t*>(q),
+                                static_cast<const uint8_t*>(summaries), page_table, seq_lens,
+                                s_hat, lay, partials);
+    return dispatch_scan_page(c.rank, c.page_size, grid, st, c.num_q_heads, c.num_kv_heads,
+                              c.max_pages_per_seq, static_cast<const float*>(q),
+                              static_cast<const uint8_t*>(summaries), page_table, seq_lens, s_hat,
+                              lay, partials);
+  }
   if (c.q_dtype == LOCKS_BF16)
     return dispatch_scan(c.rank, G, c.basis, steps, grid, st, c.num_q_heads, c.num_kv_heads,
                          c.max_pages_per_seq, static_cast<const uint16_t*>(q),

@@ -133,7 +133,7 @@ __device__ __forceinline__ int select_top(const uint32_t (&key)[NK], int K, bool
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_chunk_kernel(
-    int H_q, int H_kv, int k, int n_chunks, const int32_t* __restrict__ seq_lens,
+    int H_q, int H_kv, int k, int n_chunks, int pgsz, const int32_t* __restrict__ seq_lens,
     const float* __restrict__ s_hat, SHatLayout lay, const float2* __restrict__ partials,
     int n_parts, uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx) {
   __shared__ Red red;
@@ -141,7 +141,7 @@ __global__ __launch_bounds__(kSelThreads) void select_chunk_kernel(
   const int chunk = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
   const int tid = threadIdx.x;
   const int L = seq_lens[s];
-  const int n = (L + kPage - 1) / kPage;
+  const int n = (L + pgsz - 1) / pgsz;
   const int G = H_q / H_kv;
   const int K = k - 2;
   const int p0 = chunk * kSelChunk;
@@ -301,7 +301,7 @@ __device__ void merge_select(int N, int K, const uint32_t* __restrict__ gk,
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_merge_kernel(
-    int H_q, int H_kv, int k, int n_chunks, const int32_t* __restrict__ seq_lens,
+    int H_q, int H_kv, int k, int n_chunks, int pgsz, const int32_t* __restrict__ seq_lens,
     const float* __restrict__ s_hat, SHatLayout lay, const uint32_t* __restrict__ cand_key,
     const int32_t* __restrict__ cand_idx, int32_t* __restrict__ out_ids,
     float* __restrict__ out_sel_lse) {
@@ -309,8 +309,8 @@ __global__ __launch_bounds__(kSelThreads) void select_merge_kernel(
   const int h = blockIdx.x, s = blockIdx.y;
   const int tid = threadIdx.x;
   const int L = seq_lens[s];
-  const int n = (L + kPage - 1) / kPage;
-  const int n_c = L / kPage;
+  const int n = (L + pgsz - 1) / pgsz;
+  const int n_c = L / pgsz;
   const int G = H_q / H_kv;
   const int K = k - 2;
   const long row0 = (long)s * H_q + (long)h * G;
@@ -370,10 +370,11 @@ __device__ __forceinline__ uint32_t page_key(float m, float sum) {
 
 template <int kG>  // G when one page's G scores are contiguous (4, 8, 16), else 0
 __global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
-    int H_q, int H_kv, int k, int width, int max_pages, const int32_t* __restrict__ seq_lens,
-    const int32_t* __restrict__ page_table, const float* __restrict__ s_hat, SHatLayout lay,
-    const float2* __restrict__ partials, int n_parts, SelectBufs sb, int n_rows,
-    const float2* __restrict__ part_x, const int32_t* __restrict__ sl_scan) {
+    int H_q, int H_kv, int k, int width, int max_pages, int pgsz,
+    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ page_table,
+    const float* __restrict__ s_hat, SHatLayout lay, const float2* __restrict__ partials,
+    int n_parts, SelectBufs sb, int n_rows, const float2* __restrict__ part_x,
+    const int32_t* __restrict__ sl_scan) {
   constexpr int kT = kChunkThreads;
   __shared__ float s_lz2[kMaxGroup];
   __shared__ __align__(16) uint32_t sk[kFastChunk];
@@ -455,7 +456,7 @@ __global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
     if (g < G && sub == 0) s_lz2[g] = m + __builtin_amdgcn_logf(l);
   }
   __syncthreads();
-  const int n = (Ls + kPage - 1) / kPage;
+  const int n = (Ls + pgsz - 1) / pgsz;
   if (n <= k || p0 > n - 2) return;  // uniform across the block
   if constexpr (kG != 0) {
     const int q = tid % LP;
@@ -527,7 +528,7 @@ __global__ __launch_bounds__(kChunkThreads) void select_chunk_keys_kernel(
 }
 
 __global__ __launch_bounds__(kChunkThreads) void select_merge_fast_kernel(
-    int H_q, int H_kv, int k, int width, int n_rows, int max_pages,
+    int H_q, int H_kv, int k, int width, int n_rows, int max_pages, int pgsz,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ page_table,
     const float* __restrict__ s_hat, SHatLayout lay, SelectBufs sb, int32_t* __restrict__ out_ids,
     float* __restrict__ out_sel_lse) {
@@ -535,8 +536,8 @@ __global__ __launch_bounds__(kChunkThreads) void select_merge_fast_kernel(
   __shared__ int32_t s_tab[kFastK + 2], s_blk[kFastK + 2];
   const int h = blockIdx.x, s = blockIdx.y, tid = threadIdx.x;
   const int Ls = seq_lens[s];
-  const int n = (Ls + kPage - 1) / kPage;
-  const int n_c = Ls / kPage;
+  const int n = (Ls + pgsz - 1) / pgsz;
+  const int n_c = Ls / pgsz;
   const int G = H_q / H_kv;
   const long row0 = (long)s * H_q + (long)h * G;
   const long unit = (long)s * H_kv + h;
@@ -601,8 +602,8 @@ hipError_t launch_select_chunks(const locks_cfg_t& c, const int32_t* page_table,
   const int rows = select_fast_rows(c);
   hipLaunchKernelGGL(kern, dim3(rows, c.num_kv_heads, c.num_seqs), dim3(kChunkThreads), 0, st,
                      c.num_q_heads, c.num_kv_heads, k, select_fast_width(c), c.max_pages_per_seq,
-                     seq_lens, page_table, s_hat, lay, partials, scan_blocks(c), sb, rows,
-                     part_x, sl_scan);
+                     c.page_size, seq_lens, page_table, s_hat, lay, partials, scan_blocks(c), sb,
+                     rows, part_x, sl_scan);
   return hipGetLastError();
 }
 
@@ -616,16 +617,17 @@ hipError_t launch_select(const locks_cfg_t& c, const int32_t* page_table, const 
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(select_merge_fast_kernel, dim3(c.num_kv_heads, c.num_seqs),
                        dim3(kChunkThreads), 0, st, c.num_q_heads, c.num_kv_heads, k,
-                       select_fast_width(c), select_fast_rows(c), c.max_pages_per_seq, seq_lens,
-                       page_table, s_hat, lay, sb, out_page_ids, out_sel_lse);
+                       select_fast_width(c), select_fast_rows(c), c.max_pages_per_seq, c.page_size,
+                       seq_lens, page_table, s_hat, lay, sb, out_page_ids, out_sel_lse);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(select_chunk_kernel, dim3(sb.n_chunks, c.num_kv_heads, c.num_seqs),
                      dim3(kSelThreads), 0, st, c.num_q_heads, c.num_kv_heads, k, sb.n_chunks,
-                     seq_lens, s_hat, lay, partials, scan_blocks(c), sb.cand_key, sb.cand_idx);
+                     c.page_size, seq_lens, s_hat, lay, partials, scan_blocks(c), sb.cand_key,
+                     sb.cand_idx);
   hipLaunchKernelGGL(select_merge_kernel, dim3(c.num_kv_heads, c.num_seqs), dim3(kSelThreads), 0,
-                     st, c.num_q_heads, c.num_kv_heads, k, sb.n_chunks, seq_lens, s_hat, lay,
-                     sb.cand_key, sb.cand_idx, out_page_ids, out_sel_lse);
+                     st, c.num_q_heads, c.num_kv_heads, k, sb.n_chunks, c.page_size, seq_lens,
+                     s_hat, lay, sb.cand_key, sb.cand_idx, out_page_ids, out_sel_lse);
   return hipGetLastError();
 }
 

@@ -92,6 +92,8 @@ _SIGS = {
     "locks_summary_stride": (_SZ, [_I]),
     "locks_summary_payload_bytes_ex": (_SZ, [_I, _I]),
     "locks_summary_stride_ex": (_SZ, [_I, _I]),
+    "locks_summary_payload_bytes_page": (_SZ, [_I, _I, _I]),
+    "locks_summary_stride_page": (_SZ, [_I, _I, _I]),
     "locks_workspace_bytes": (_SZ, [ctypes.POINTER(_Cfg)]),
     "locks_build_summaries": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _I, _P, _P]),
     "locks_build_factors": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _I, _P, _P, _P,
@@ -184,7 +186,8 @@ def _check_cache(cfg: "Config", name: str, cache):
 
 def _check_summaries(cfg: "Config", summaries):
     _need("summaries", summaries,
-          (cfg.num_blocks, cfg.num_kv_heads, summary_stride(cfg.rank, cfg.basis)), torch.uint8)
+          (cfg.num_blocks, cfg.num_kv_heads, summary_stride(cfg.rank, cfg.basis, cfg.page_size)),
+          torch.uint8)
 
 
 def _check_list(name: str, lst):
@@ -231,12 +234,12 @@ def summary_payload_bytes(rank: int) -> int:
     return int(lib().locks_summary_payload_bytes(rank))
 
 
-def summary_stride(rank: int, basis: int = LOCKS_BASIS_INT4) -> int:
-    return int(lib().locks_summary_stride_ex(rank, basis))
+def summary_stride(rank: int, basis: int = LOCKS_BASIS_INT4, page_size: int = PAGE) -> int:
+    return int(lib().locks_summary_stride_page(rank, basis, page_size))
 
 
-def summary_payload_bytes_ex(rank: int, basis: int) -> int:
-    return int(lib().locks_summary_payload_bytes_ex(rank, basis))
+def summary_payload_bytes_ex(rank: int, basis: int, page_size: int = PAGE) -> int:
+    return int(lib().locks_summary_payload_bytes_page(rank, basis, page_size))
 
 
 def workspace_bytes(cfg: Config) -> int:
@@ -252,8 +255,9 @@ def alloc_workspace(cfg: Config, device="cuda") -> torch.Tensor:
 
 
 def alloc_summaries(cfg: Config, device="cuda") -> torch.Tensor:
-    return torch.zeros(cfg.num_blocks, cfg.num_kv_heads, summary_stride(cfg.rank, cfg.basis),
-                       dtype=torch.uint8, device=device)
+    return torch.zeros(cfg.num_blocks, cfg.num_kv_heads,
+                       summary_stride(cfg.rank, cfg.basis, cfg.page_size), dtype=torch.uint8,
+                       device=device)
 
 
 def build_summaries(cfg: Config, k_cache, page_table, seq_lens, summaries,
@@ -523,8 +527,9 @@ def config_for(spec, num_blocks: int, max_pages: int) -> Config:
     """Config of a workloads.WorkloadSpec laid out with num_blocks / max_pages."""
     dt = {"bf16": LOCKS_BF16, "fp32": LOCKS_FP32}
     return Config(spec.num_seqs, spec.num_q_heads, spec.num_kv_heads, spec.rank,
-                  spec.budget_tokens, max_pages, num_blocks, dt[spec.kv_dtype], dt[spec.q_dtype])
+                  spec.budget_tokens, max_pages, num_blocks, dt[spec.kv_dtype], dt[spec.q_dtype],
+                  page_size=getattr(spec, "page_size", PAGE))
 
 
-def page_count(seq_len: int) -> int:
-    return math.ceil(seq_len / PAGE)
+def page_count(seq_len: int, page_size: int = PAGE) -> int:
+    return math.ceil(seq_len / page_size)

@@ -39,7 +39,8 @@ class Dev:
                 if units is not None and (s, h) not in units:
                     continue
                 k, _, _ = gather_unit(self.w, s, h)
-                rec = O.unit_summaries(k, self.cfg.rank, B.BASIS_NAMES[self.cfg.basis])
+                rec = O.unit_summaries(k, self.cfg.rank, B.BASIS_NAMES[self.cfg.basis],
+                                       self.cfg.page_size)
                 recs[(s, h)] = rec
                 n_c = rec.shape[0]
                 if n_c:
@@ -93,15 +94,15 @@ def near_tie_overlap(results):
     return common / total if total else 1.0
 
 
-def check_attention_on_table(qg, k, v, got, o, l):
+def check_attention_on_table(qg, k, v, got, o, l, page_size=PAGE):
     """GPU output o [G][d] and LSE l [G] of one (sequence, KV head) against the
-    oracle's attention over the GPU's own table (Sec. 2): rel-L2 <= OUT_TOL per
-    head, LSE within LSE_TOL; an empty table gives 0 and -inf.  Returns the worst
-    rel-L2."""
+    oracle's attention over the GPU's own table of pages of page_size tokens
+    (Sec. 2): rel-L2 <= OUT_TOL per head, LSE within LSE_TOL; an empty table gives
+    0 and -inf.  Returns the worst rel-L2."""
     if not got:
         assert np.all(o == 0) and np.all(np.isneginf(l)), (o, l)
         return 0.0
-    o_ref, l_ref = O.attend(qg, k, v, got)
+    o_ref, l_ref = O.attend(qg, k, v, got, page_size)
     worst = max(rel_l2(o[g], o_ref[g]) for g in range(qg.shape[0]))
     assert worst <= OUT_TOL, worst
     np.testing.assert_allclose(l, l_ref, atol=LSE_TOL)

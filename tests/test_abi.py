@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 21
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGS), "binding and header disagree"
@@ -42,6 +42,14 @@ def cfg(**kw):
     for k, v in kw.items():
         setattr(c, k, v)
     return c
+
+
+def test_payload_and_stride_per_page_size_match_the_oracle(lib):
+    for Bp in (16, 32, 64):
+        for r in (1, 2, 4, 8, 15):
+            assert B.summary_payload_bytes_ex(r, 0, Bp) == O.payload_bytes(r, B=Bp)
+            assert B.summary_stride(r, 0, Bp) == O.record_stride(r, "int4", Bp)
+    assert B.summary_stride(8, 0, 48) == 0 and B.summary_payload_bytes_ex(8, 0, 8) == 0
 
 
 def test_payload_and_stride(lib):
@@ -69,7 +77,9 @@ def test_bad_basis_is_rejected(lib, bad, code):
 
 
 @pytest.mark.parametrize("bad,code", [
-    (dict(head_dim=64), -2), (dict(page_size=32), -2), (dict(kv_dtype=7), -2),
+    (dict(head_dim=64), -2), (dict(page_size=8), -2), (dict(page_size=48), -2),
+    (dict(page_size=128), -2), (dict(page_size=32, basis=1), -2),
+    (dict(page_size=64, budget_tokens=64), -1), (dict(kv_dtype=7), -2),
     (dict(rank=0), -1), (dict(rank=16), -1), (dict(num_q_heads=7), -1),
     (dict(budget_tokens=16), -1), (dict(budget_tokens=0), -1), (dict(max_pages_per_seq=0), -1),
     (dict(num_blocks=0), -1), (dict(num_kv_heads=0), -1), (dict(num_seqs=-1), -1),

@@ -22,9 +22,12 @@ per-page low-rank key structure, Sec. 3 / App. B, not a copy of its traces):
 * values are N(0, 1);
 * bf16 workloads round keys, values and queries to bf16 (round-to-nearest-even).
 
-Physical layout: k_cache / v_cache are [num_blocks][H_kv][16][128]; logical page
-j of sequence s lives in block page_table[s][j]; blocks are a seeded random
-permutation, so consecutive logical pages are scattered in memory.
+Physical layout: k_cache / v_cache are [num_blocks][H_kv][B][128] for pages of
+B = page_size tokens (16 unless stated); logical page j of sequence s lives in
+block page_table[s][j]; blocks are a seeded random permutation, so consecutive
+logical pages are scattered in memory.  The tokens do not depend on the page size
+(the per-page subspace above is drawn per 16 tokens), so workloads of different
+page sizes hold the same keys and values.
 """
 from __future__ import annotations
 
@@ -60,13 +63,16 @@ class WorkloadSpec:
     kv_dtype: str  # "bf16" | "fp32"
     q_dtype: str
     spare_pages_per_seq: int = 0  # free blocks reserved for appended tokens
+    page_size: int = PAGE         # tokens per KV page (16, 32 or 64); the key recipe
+                                  # below is the same for every page size
 
 
 def config_spec(cfg_id: int, *, rank: Optional[int] = None, seed: int = 0,
                 num_seqs: Optional[int] = None, seq_len: Optional[int] = None,
                 num_kv_heads: Optional[int] = None, num_q_heads: Optional[int] = None,
                 budget_tokens: Optional[int] = None,
-                spare_pages: Optional[int] = None) -> WorkloadSpec:
+                spare_pages: Optional[int] = None,
+                page_size: Optional[int] = None) -> WorkloadSpec:
     """The five decode-step workloads; keyword overrides shrink them for tests."""
     if cfg_id == 0:
         s = WorkloadSpec("tiny-1h-4k", 1, 1, 1, [4096], 8, 256, "fp32", "fp32")
@@ -100,6 +106,8 @@ def config_spec(cfg_id: int, *, rank: Optional[int] = None, seed: int = 0,
         s.budget_tokens = budget_tokens
     if spare_pages is not None:
         s.spare_pages_per_seq = spare_pages
+    if page_size is not None:
+        s.page_size = page_size
     return s
 
 
@@ -107,7 +115,7 @@ def config_spec(cfg_id: int, *, rank: Optional[int] = None, seed: int = 0,
 class Workload:
     spec: WorkloadSpec
     q: torch.Tensor            # [S][H_q][128]
-    k_cache: torch.Tensor      # [num_blocks][H_kv][16][128]
+    k_cache: torch.Tensor      # [num_blocks][H_kv][page_size][128]
     v_cache: torch.Tensor
     page_table: torch.Tensor   # int32 [S][max_pages]
     seq_lens: torch.Tensor     # int32 [S]
@@ -207,10 +215,11 @@ def build_workload(spec: WorkloadSpec, seed: int = 0, device="cpu") -> Workload:
     if Hq % Hkv:
         raise ValueError("query heads must be a multiple of KV heads")
     G = Hq // Hkv
+    P = spec.page_size
     kvt, qt = _torch_dtype(spec.kv_dtype), _torch_dtype(spec.q_dtype)
     g0 = _gen(seed, 3, device="cpu")
     outliers = torch.randperm(HEAD_DIM, generator=g0)[:N_OUTLIERS].to(dev)
-    n_pages = [(L + PAGE - 1) // PAGE for L in spec.seq_lens]
+    n_pages = [(L + P - 1) // P for L in spec.seq_lens]
     max_pages = max(1, max(n + spec.spare_pages_per_seq for n in n_pages))
     total = sum(n + spec.spare_pages_per_seq for n in n_pages)
     total = max(total, 1)
@@ -221,8 +230,8 @@ def build_workload(spec: WorkloadSpec, seed: int = 0, device="cpu") -> Workload:
         m = n_pages[s] + spec.spare_pages_per_seq
         page_table[s, :m] = perm[off:off + m]
         off += m
-    k_cache = torch.zeros(total, Hkv, PAGE, HEAD_DIM, dtype=kvt, device=dev)
-    v_cache = torch.zeros(total, Hkv, PAGE, HEAD_DIM, dtype=kvt, device=dev)
+    k_cache = torch.zeros(total, Hkv, P, HEAD_DIM, dtype=kvt, device=dev)
+    v_cache = torch.zeros(total, Hkv, P, HEAD_DIM, dtype=kvt, device=dev)
     q = torch.empty(S, Hq, HEAD_DIM, dtype=torch.float32, device=dev)
     carriers: Dict[tuple, List[int]] = {}
     pt_dev = page_table.to(dev).long()
@@ -236,14 +245,14 @@ def build_workload(spec: WorkloadSpec, seed: int = 0, device="cpu") -> Workload:
             car: List[int] = []
             if L > 0:
                 keys, vals, car = unit_tokens(spec, seed, s, h, mean, qg, dev)
-                n = (L + PAGE - 1) // PAGE
-                kp = torch.zeros(n * PAGE, HEAD_DIM, device=dev)
-                vp = torch.zeros(n * PAGE, HEAD_DIM, device=dev)
+                n = (L + P - 1) // P
+                kp = torch.zeros(n * P, HEAD_DIM, device=dev)
+                vp = torch.zeros(n * P, HEAD_DIM, device=dev)
                 kp[:L] = keys
                 vp[:L] = vals
                 blocks = pt_dev[s, :n]
-                k_cache[blocks, h] = _round(kp.view(n, PAGE, HEAD_DIM), kvt)
-                v_cache[blocks, h] = _round(vp.view(n, PAGE, HEAD_DIM), kvt)
+                k_cache[blocks, h] = _round(kp.view(n, P, HEAD_DIM), kvt)
+                v_cache[blocks, h] = _round(vp.view(n, P, HEAD_DIM), kvt)
             q[s, h * G:(h + 1) * G] = qg
             carriers[(s, h)] = car
     return Workload(spec, _round(q, qt), k_cache, v_cache, page_table.to(dev),
@@ -253,11 +262,12 @@ def build_workload(spec: WorkloadSpec, seed: int = 0, device="cpu") -> Workload:
 def gather_unit(w: Workload, seq: int, kvh: int):
     """Host fp64 copies of one (sequence, KV head): keys [L][d], values [L][d], q [G][d]."""
     L = int(w.spec.seq_lens[seq])
-    n = (L + PAGE - 1) // PAGE
+    P = w.spec.page_size
+    n = (L + P - 1) // P
     G = w.spec.num_q_heads // w.spec.num_kv_heads
     blocks = w.page_table[seq, :n].long().cpu()
     k = w.k_cache.index_select(0, blocks.to(w.k_cache.device))[:, kvh].double().cpu()
     v = w.v_cache.index_select(0, blocks.to(w.v_cache.device))[:, kvh].double().cpu()
     q = w.q[seq, kvh * G:(kvh + 1) * G].double().cpu()
-    return (k.reshape(n * PAGE, HEAD_DIM)[:L].numpy(), v.reshape(n * PAGE, HEAD_DIM)[:L].numpy(),
+    return (k.reshape(n * P, HEAD_DIM)[:L].numpy(), v.reshape(n * P, HEAD_DIM)[:L].numpy(),
             q.numpy())
