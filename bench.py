@@ -89,6 +89,15 @@ WORKLOADS = {
                                         "heads, d 128, page 16, r 8, bf16 basis, b 2048, bf16 KV"),
     "32k": (1, {}, "llama3.1-8b-32k: 1 seq x 32,768 tokens, 32 q / 8 kv heads, d 128, page 16, "
                    "r 8, b 2048, bf16 KV"),
+    # page sizes of App. D.3: the same keys and values in pages of 32 and 64 tokens
+    "1m-B32": (3, {"page_size": 32}, "glm4-9b-1m: 1 seq x 1,048,576 tokens, 32 q / 2 kv heads, "
+                                     "d 128, page 32, r 8, b 2048, bf16 KV"),
+    "1m-B64": (3, {"page_size": 64}, "glm4-9b-1m: 1 seq x 1,048,576 tokens, 32 q / 2 kv heads, "
+                                     "d 128, page 64, r 8, b 2048, bf16 KV"),
+    "128k-B32": (2, {"page_size": 32}, "llama3.1-8b-128k: 8 seq x 131,072 tokens, 32 q / 8 kv "
+                                       "heads, d 128, page 32, r 8, b 2048, bf16 KV"),
+    "128k-B64": (2, {"page_size": 64}, "llama3.1-8b-128k: 8 seq x 131,072 tokens, 32 q / 8 kv "
+                                       "heads, d 128, page 64, r 8, b 2048, bf16 KV"),
     "reasoning": (4, {}, "qwen3-4b-reasoning: 64 seq x U[8K,64K] tokens, 32 q / 8 kv heads, d 128, "
                          "page 16, r 2, b 256, bf16 KV; each step appends one token per sequence "
                          "and builds the pages that filled"),
@@ -268,7 +277,7 @@ def oracle_unit(w, cfg, s, h):
     from workloads import gather_unit
     k, v, q = gather_unit(w, s, h)
     basis = B.BASIS_NAMES[cfg.basis]
-    rec = O.unit_summaries(k, cfg.rank, basis)
+    rec = O.unit_summaries(k, cfg.rank, basis, cfg.page_size)
     return k, v, q, rec
 
 
@@ -284,7 +293,8 @@ def cpu_step(k, v, q, rec, cfg, min_s=10.0, max_reps=20):
         t0 = time.perf_counter()
         reps = 0
         while True:
-            ref = O.decode_step(q, k, v, rec, cfg.rank, cfg.budget_tokens, basis)
+            ref = O.decode_step(q, k, v, rec, cfg.rank, cfg.budget_tokens, basis,
+                                cfg.page_size)
             reps += 1
             if time.perf_counter() - t0 > min_s or reps >= max_reps:
                 break
@@ -301,7 +311,8 @@ def parity_gate(ref, k, v, q, cfg, ids, sel, out, lse, s, h):
     from oracle import locks_oracle as O
     G = cfg.group
     L = k.shape[0]
-    n_c, n = L // 16, -(-L // 16)
+    P = cfg.page_size
+    n_c, n = L // P, -(-L // P)
     got = [int(x) for x in ids[s, h].tolist() if int(x) >= 0]
     hs = slice(h * G, (h + 1) * G)
     gsel = sel[s, hs].double().cpu().numpy()
@@ -333,7 +344,7 @@ def parity_gate(ref, k, v, q, cfg, ids, sel, out, lse, s, h):
     det["max_sel_lse_err"] = err
     if err > LSE_TOL:
         problems.append("page LSE error")
-    o_ref, l_ref = O.attend(q, k, v, got)
+    o_ref, l_ref = O.attend(q, k, v, got, P)
     rel = max(float(np.linalg.norm(o[g] - o_ref[g]) / max(np.linalg.norm(o_ref[g]), 1e-30))
               for g in range(G))
     det["max_rel_l2"] = rel
@@ -377,14 +388,15 @@ def run_block(name, args, dev, with_oracle, rest):
     ws = B.alloc_workspace(cfg, dev)
     sync = torch.cuda.synchronize
 
-    n_pages = sum(math.ceil(L / 16) for L in w.spec.seq_lens)
-    complete_heads = sum(L // 16 for L in w.spec.seq_lens) * cfg.num_kv_heads
+    P = cfg.page_size
+    n_pages = sum(math.ceil(L / P) for L in w.spec.seq_lens)
+    complete_heads = sum(L // P for L in w.spec.seq_lens) * cfg.num_kv_heads
     payload = B.summary_payload_bytes_ex(cfg.rank, cfg.basis, cfg.page_size)
     stride = B.summary_stride(cfg.rank, cfg.basis, cfg.page_size)
-    k_sel = min(cfg.k, max(math.ceil(L / 16) for L in w.spec.seq_lens))
-    kv_page = 2 * 16 * 128 * 2
+    k_sel = min(cfg.k, max(math.ceil(L / P) for L in w.spec.seq_lens))
+    kv_page = 2 * P * 128 * 2
     alg_scan = complete_heads * payload
-    alg_attend = sum(min(cfg.k, math.ceil(L / 16)) for L in w.spec.seq_lens) * \
+    alg_attend = sum(min(cfg.k, math.ceil(L / P)) for L in w.spec.seq_lens) * \
         cfg.num_kv_heads * kv_page
     alg_step = alg_scan + alg_attend
 
@@ -415,7 +427,7 @@ def run_block(name, args, dev, with_oracle, rest):
     if with_oracle and not growing and not args.kivi:
         t_or = time.perf_counter()
         k0, v0, q0, rec0 = oracle_unit(w, cfg, *gate_unit)
-        n_c0 = k0.shape[0] // 16
+        n_c0 = k0.shape[0] // P
         blocks = pt[gate_unit[0], :n_c0].long()
         summ[0][blocks, gate_unit[1]] = torch.from_numpy(rec0).to(dev)
         sync()
@@ -545,25 +557,25 @@ def run_block(name, args, dev, with_oracle, rest):
 
     # ---- build against both ceilings
     if build_us is not None:
-        fl = build_flops(16, 128, cfg.rank) * complete_heads
-        rd = complete_heads * 16 * 128 * 2
+        fl = build_flops(P, 128, cfg.rank) * complete_heads
+        rd = complete_heads * P * 128 * 2
         wr = complete_heads * payload
         block["build"] = {
             "us": round(build_us, 1), "pages": complete_heads,
             "read_GBps": round(rd / (build_us * 1e-6) / 1e9, 1),
             "hbm_frac": round((rd + wr) / (build_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-            "flops_per_page_head": build_flops(16, 128, cfg.rank),
+            "flops_per_page_head": build_flops(P, 128, cfg.rank),
             "TFLOPs": round(fl / (build_us * 1e-6) / 1e12, 2),
             "valu_frac": round(fl / (build_us * 1e-6) / 1e12 / FP32_VALU_PEAK_TFLOPS, 4)}
 
     # ---- KIVI fake quantisation of every complete page (separately timed, last:
     # it rewrites the caches in place)
-    if rest.get("kivi_pass"):
+    if rest.get("kivi_pass") and P == 16:
         kp = B.Kivi(args.kivi or 4, 32, B.LOCKS_KIVI_POST)
         B.kivi_quantize(cfg, kp, ks[0], vs[0], pt, sl)
         _, kivi_us = timed(lambda i: B.kivi_quantize(cfg, kp, ks[i % R], vs[i % R], pt, sl),
                            max(R, 4), sync)
-        kivi_bytes = complete_heads * 16 * 128 * 2 * 2 * 2   # K and V, read and written
+        kivi_bytes = complete_heads * P * 128 * 2 * 2 * 2   # K and V, read and written
         block["kivi_pass"] = {"us": round(kivi_us, 1), "pages": complete_heads,
                               "bits": args.kivi or 4, "v_group": 32, "bytes": kivi_bytes,
                               "GBps": round(kivi_bytes / (kivi_us * 1e-6) / 1e9, 1)}
@@ -582,7 +594,7 @@ def run_block(name, args, dev, with_oracle, rest):
             rest["fail"] = True
         if rest.get("cpu_baseline"):
             units = cfg.num_seqs * cfg.num_kv_heads
-            unit_pages = -(-k0.shape[0] // 16)
+            unit_pages = -(-k0.shape[0] // P)
             page_heads = n_pages * cfg.num_kv_heads
             scale = page_heads / unit_pages
             rest["cpu_baseline"] = {
