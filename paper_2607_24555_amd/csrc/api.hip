@@ -161,9 +161,9 @@ int dense_splits(const locks_cfg_t& c) {
   return (int)((((long)c.max_pages_per_seq << sub_page_log2(c)) + pps - 1) / pps);
 }
 
-// The build for the configuration's page size: the Jacobi kernel for 16-token
-// pages (which also serves a step's overlapped build), the tridiagonal one for 32
-// and 64.
+// The build for the configuration's page size: the register-resident kernel of
+// build.hip for 16-token pages (which also serves a step's overlapped build), the
+// LDS-resident one of build_page.hip for 32 and 64.
 hipError_t build_pages(const locks_cfg_t& c, const void* k_cache, const int32_t* page_table,
                        const int32_t* seq_lens, const int32_t* build_list, int32_t n_items,
                        bool all_pages, void* summaries, float* mu, float* basis, float* coef,

@@ -3,13 +3,12 @@
 // modes, form V = D^T U_r S_r^{-1} and C = U_r S_r, quantise and pack.
 //
 // Mapping: one 64-lane wave per block, four (page, KV head) items per wave, 16
-// lanes per item with lane i owning row i of the page.  The symmetric 16 x 16
-// eigenproblem is solved by cyclic Jacobi in round-robin (tournament) order: each
-// of the 15 rounds of a sweep rotates 8 disjoint index pairs at once, so the 16
-// lanes of an item update their own rows in parallel.  Everything is fp32; the
-// Gram is formed with the same summation order for (i, j) and (j, i), so it is
-// exactly symmetric.
+// lanes per item with lane i owning row i of the page.  The Gram is formed on the
+// matrix cores with the same summation order for (i, j) and (j, i), so it is
+// exactly symmetric; its eigenpairs come from the register-resident tridiagonal
+// solver of tridiag16.h (one 16-lane DPP row per item).  Everything is fp32.
 #include "locks_internal.h"
+#include "tridiag16.h"
 
 namespace locks {
 namespace {
@@ -18,21 +17,8 @@ constexpr int kItems = 4;         // items per block
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 constexpr int kRow = 20;          // LDS row stride of A and U: 16-byte aligned, conflict-free
-constexpr int kMaxSweeps = 12;
-constexpr float kOffRel = 1e-10f;   // Jacobi stop: off-diagonal / diagonal mass
 constexpr float kZeroRel = 1e-6f;
 constexpr float kZeroAbs = 1e-10f;
-
-// Tournament pairing of 16 indices (circle method): index 15 meets t in round t,
-// the others meet (2t - i) mod 15.  Over the 15 rounds every pair meets once.
-__device__ __forceinline__ int partner(int t, int i) {
-  if (i == 15) return t;
-  if (i == t) return 15;
-  int p = 2 * t - i;
-  p %= 15;
-  if (p < 0) p += 15;
-  return p;
-}
 
 // The block is a single wave, whose LDS operations complete in issue order: a
 // barrier inside the rotation rounds only has to keep the compiler from moving
@@ -46,19 +32,32 @@ __device__ __forceinline__ void ld_row(const float* p, float (&r)[kPage]) {
     r[4 * q] = v.x; r[4 * q + 1] = v.y; r[4 * q + 2] = v.z; r[4 * q + 3] = v.w;
   }
 }
-__device__ __forceinline__ void st_row(float* p, const float (&r)[kPage]) {
-#pragma unroll
-  for (int q = 0; q < 4; ++q)
-    reinterpret_cast<float4*>(p)[q] = make_float4(r[4 * q], r[4 * q + 1], r[4 * q + 2], r[4 * q + 3]);
+
+// sum / max over the 16 lanes of an item (one DPP row)
+__device__ __forceinline__ float group16_sum(float v) { return tri16::row_sum(v); }
+__device__ __forceinline__ float group16_max(float v) {
+  v = fmaxf(v, tri16::dpp<0xB1>(v));
+  v = fmaxf(v, tri16::dpp<0x4E>(v));
+  v = fmaxf(v, tri16::dpp<0x141>(v));
+  return fmaxf(v, tri16::dpp<0x140>(v));
 }
 
-__device__ __forceinline__ float group16_sum(float v) {
-  for (int o = 8; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+// Elements of a 16-byte chunk of bf16 or fp32 keys as floats.
+template <typename KT>
+__device__ __forceinline__ void chunk_to_f(const uint4& w, float* out);
+template <>
+__device__ __forceinline__ void chunk_to_f<uint16_t>(const uint4& w, float* out) {
+  const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    out[2 * e] = __uint_as_float(u[e] << 16);
+    out[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+  }
 }
-__device__ __forceinline__ float group16_max(float v) {
-  for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+template <>
+__device__ __forceinline__ void chunk_to_f<float>(const uint4& w, float* out) {
+  out[0] = __uint_as_float(w.x); out[1] = __uint_as_float(w.y);
+  out[2] = __uint_as_float(w.z); out[3] = __uint_as_float(w.w);
 }
 
 __device__ __forceinline__ float f16_scale(float amax, float qmax) {
@@ -99,8 +98,8 @@ __global__ __launch_bounds__(64) void build_kernel(
     float* __restrict__ coef_out, float* __restrict__ sigma2_out, BuildStep bs, int basis) {
   constexpr bool kScore = kMode == kBuildLast;  // (int4 bases only)
   // raw key rows (bf16 or fp32 as stored; deviations are formed on the fly as
-  // float(k) - mu, the same fp32 value for every use) share LDS with the Jacobi
-  // matrices A and U, which are written once the Gram is complete
+  // float(k) - mu, the same fp32 value for every use) share LDS with the Gram A
+  // and the eigenvectors U, which are written once the Gram is complete
   constexpr int kKBytes = kItems * kPage * kDim * (int)sizeof(KT);
   constexpr int kJBytes = 2 * kItems * kPage * kRow * (int)sizeof(float);
   __shared__ __align__(16) uint8_t sBuf[kKBytes > kJBytes ? kKBytes : kJBytes];
@@ -109,7 +108,6 @@ __global__ __launch_bounds__(64) void build_kernel(
   auto& sU = *reinterpret_cast<float(*)[kItems][kPage][kRow]>(sBuf + kJBytes / 2);
   __shared__ float sFlip[kItems][kMaxRank];
   __shared__ float sMu[kItems][kDim];
-  __shared__ float2 sCS[kItems][kPage];
   __shared__ float sLam[kItems][kPage];
   __shared__ int sOrd[kItems][kPage];
   // quantised basis columns (packed codes, scales) and projections of the scored pages
@@ -175,26 +173,36 @@ __global__ __launch_bounds__(64) void build_kernel(
     for (int u = 0; u < kDim / kVec; ++u) w[u] = active ? src[u] : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int u = 0; u < kDim / kVec; ++u) dst[u] = w[u];
-    __syncthreads();
-#pragma unroll 8
-    for (int c = 0; c < kDim; ++c) {
-      const float x = load_elem(&sK[grp][li][0], c);
-      energy = fmaf(x, x, energy);
+#pragma unroll
+    for (int u = 0; u < kDim / kVec; ++u) {
+      float x[kVec];
+      chunk_to_f<KT>(w[u], x);
+#pragma unroll
+      for (int c = 0; c < kVec; ++c) energy = fmaf(x[c], x[c], energy);
     }
+    __syncthreads();
   }
   energy = group16_sum(energy) * (1.0f / kPage);
 
-  // ---- centroid: pairwise sum over the 16 rows (exact for equal rows)
-  for (int cc = 0; cc < 8; ++cc) {
-    const int c = 8 * li + cc;
-    float v[kPage];
+  // ---- centroid of the lane's 8 columns: pairwise sum over the 16 rows (exact
+  //      for equal rows)
+  {
+    float v[kPage][8];
 #pragma unroll
-    for (int i = 0; i < kPage; ++i) v[i] = load_elem(&sK[grp][i][0], c);
+    for (int i = 0; i < kPage; ++i) {
+      const uint4* row = reinterpret_cast<const uint4*>(&sK[grp][i][8 * li]);
+#pragma unroll
+      for (int u = 0; u < 8 / (16 / (int)sizeof(KT)); ++u)
+        chunk_to_f<KT>(row[u], &v[i][u * (16 / (int)sizeof(KT))]);
+    }
 #pragma unroll
     for (int w = 8; w > 0; w >>= 1)
 #pragma unroll
-      for (int i = 0; i < w; ++i) v[i] = v[i] + v[i + w];
-    sMu[grp][c] = v[0] * (1.0f / kPage);
+      for (int i = 0; i < w; ++i)
+#pragma unroll
+        for (int cc = 0; cc < 8; ++cc) v[i][cc] = v[i][cc] + v[i + w][cc];
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) sMu[grp][8 * li + cc] = v[0][cc] * (1.0f / kPage);
   }
   __syncthreads();
 
@@ -208,11 +216,17 @@ __global__ __launch_bounds__(64) void build_kernel(
 #pragma unroll
     for (int it = 0; it < kItems; ++it) {
       acc[it] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 8
-      for (int m = 0; m < 32; ++m) {
-        const int c = 32 * grp + m;
-        const float d = load_elem(&sK[it][li][0], c) - sMu[it][c];
-        acc[it] = __builtin_amdgcn_mfma_f32_16x16x4f32(d, d, acc[it], 0, 0, 0);
+      constexpr int kVec = 16 / (int)sizeof(KT);
+#pragma unroll
+      for (int ch = 0; ch < 32 / kVec; ++ch) {
+        const int c0 = 32 * grp + kVec * ch;
+        float x[kVec];
+        chunk_to_f<KT>(*reinterpret_cast<const uint4*>(&sK[it][li][c0]), x);
+#pragma unroll
+        for (int m = 0; m < kVec; ++m) {
+          const float d = x[m] - sMu[it][c0 + m];
+          acc[it] = __builtin_amdgcn_mfma_f32_16x16x4f32(d, d, acc[it], 0, 0, 0);
+        }
       }
     }
     __syncthreads();  // every lane is done with the key rows: A and U reuse their LDS
@@ -220,8 +234,6 @@ __global__ __launch_bounds__(64) void build_kernel(
     for (int it = 0; it < kItems; ++it)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) sA[it][4 * grp + jj][li] = acc[it][jj];
-#pragma unroll
-    for (int jj = 0; jj < kPage; ++jj) sU[grp][li][jj] = (li == jj) ? 1.0f : 0.0f;
     __syncthreads();
 #pragma unroll
     for (int jj = 0; jj < kPage; ++jj)
@@ -229,84 +241,19 @@ __global__ __launch_bounds__(64) void build_kernel(
   }
   __syncthreads();
 
-  // ---- cyclic Jacobi, tournament order.  In round t lane li pairs with
-  //      p = partner(t, li); every lane reads its own row and its partner's row
-  //      of A once, applies the round's 8 column rotations to both in
-  //      registers, then the row rotation, and writes its row back.
-  for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
-    {
-      // off-diagonal mass summed directly (a difference of the row's total and
-      // the diagonal would be dominated by rounding near convergence)
-      float a[kPage];
-      ld_row(&sA[grp][li][0], a);
-      float off = 0.0f, d = 0.0f;
-#pragma unroll
-      for (int jj = 0; jj < kPage; ++jj) {
-        if (jj == li) d = a[jj]; else off = fmaf(a[jj], a[jj], off);
-      }
-      const float dia = group16_sum(d * d);
-      off = group16_sum(off);
-      // converged when the off-diagonal entries are ~1e-5 of the diagonal: fp32
-      // rotations cannot reduce them reliably further
-      if (__all(off <= kOffRel * dia)) break;
-    }
-#pragma unroll
-    for (int t = 0; t < 15; ++t) {
-      const int p = partner(t, li);
-      const int P = min(li, p), Q = max(li, p);
-      const float app = sA[grp][P][P], aqq = sA[grp][Q][Q], apq = sA[grp][P][Q];
-      float c = 1.0f, sn = 0.0f;
-      if (apq != 0.0f) {
-        // hardware reciprocal and square roots (about 1 ulp): the angle need
-        // not be exact, only c^2 + s^2 = 1, which holds to a few ulp
-        const float theta = (aqq - app) * __builtin_amdgcn_rcpf(2.0f * apq);
-        const float tt = copysignf(1.0f, theta) *
-                         __builtin_amdgcn_rcpf(fabsf(theta) + __builtin_amdgcn_sqrtf(fmaf(theta, theta, 1.0f)));
-        c = __builtin_amdgcn_rsqf(fmaf(tt, tt, 1.0f));
-        sn = tt * c;
-      }
-      if (li == P) sCS[grp][P] = make_float2(c, sn);
-      wave_sync();
-      float a[kPage], b[kPage], u[kPage];
-      ld_row(&sA[grp][li][0], a);
-      ld_row(&sA[grp][p][0], b);
-      ld_row(&sU[grp][li][0], u);
-      // columns: A J and U J (pair (m, partner(t, m)) rotated by its leader's c, s)
-#pragma unroll
-      for (int m = 0; m < kPage; ++m) {
-        const int pm = partner(t, m);
-        if (m < pm) {
-          const float2 cs = sCS[grp][m];
-          const float ax = a[m], ay = a[pm], bx = b[m], by = b[pm], ux = u[m], uy = u[pm];
-          a[m] = cs.x * ax - cs.y * ay;
-          a[pm] = cs.y * ax + cs.x * ay;
-          b[m] = cs.x * bx - cs.y * by;
-          b[pm] = cs.y * bx + cs.x * by;
-          u[m] = cs.x * ux - cs.y * uy;
-          u[pm] = cs.y * ux + cs.x * uy;
-        }
-      }
-      // rows: J^T (A J); lane P gets c*row_P - s*row_Q, lane Q gets s*row_P + c*row_Q
-      const bool lead = li == P;
-#pragma unroll
-      for (int m = 0; m < kPage; ++m) a[m] = lead ? (c * a[m] - sn * b[m]) : (sn * b[m] + c * a[m]);
-      wave_sync();
-      st_row(&sA[grp][li][0], a);
-      st_row(&sU[grp][li][0], u);
-      wave_sync();
-    }
-  }
-
-  // ---- eigenvalues descending (ties by index), zero-mode floor
+  // ---- eigenpairs of the Gram: Householder tridiagonalisation, multisection
+  //      and inverse iteration in registers; the solver's LDS scratch is A's
   {
-    const float lam = sA[grp][li][li];
-    int rank = 0;
-    for (int m = 0; m < kPage; ++m) {
-      const float o = sA[grp][m][m];
-      rank += (o > lam) || (o == lam && m < li);
-    }
-    sOrd[grp][rank] = li;
-    sLam[grp][rank] = fmaxf(lam, 0.0f);
+    float a[kPage];
+    ld_row(&sA[grp][li][0], a);
+    __syncthreads();
+    float lam, u[kMaxRank];
+    tri16::eig16<kFactors, kMaxRank>(a, li, r, lam, u, &sA[grp][0][0]);
+    sLam[grp][li] = fmaxf(lam, 0.0f);
+    sOrd[grp][li] = li;
+#pragma unroll
+    for (int l = 0; l < kMaxRank; ++l)
+      if (l < r) sU[grp][li][l] = u[l];
   }
   __syncthreads();
   const float top = sLam[grp][0];

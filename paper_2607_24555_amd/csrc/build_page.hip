@@ -35,18 +35,50 @@ struct PG {
   static constexpr int kVec = B + 1;          // LDS stride (floats) of a lane's vector
 };
 
-// Sum / max over the B lanes of an item (lane groups of B consecutive lanes).
+template <int C>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), C, 0xF, 0xF, false));
+}
+// Sum / max over the B lanes of an item (lane groups of B consecutive lanes):
+// within a 16-lane row by DPP (quad xor 1, quad xor 2, half-row mirror, row
+// mirror), across rows by lane swaps.
 template <int B>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int o = B / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  if (B >= 32) v += __shfl_xor(v, 16, 64);
+  if (B >= 64) v += __shfl_xor(v, 32, 64);
   return v;
 }
 template <int B>
 __device__ __forceinline__ float group_max(float v) {
-#pragma unroll
-  for (int o = B / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  v = fmaxf(v, dpp_f<0xB1>(v));
+  v = fmaxf(v, dpp_f<0x4E>(v));
+  v = fmaxf(v, dpp_f<0x141>(v));
+  v = fmaxf(v, dpp_f<0x140>(v));
+  if (B >= 32) v = fmaxf(v, __shfl_xor(v, 16, 64));
+  if (B >= 64) v = fmaxf(v, __shfl_xor(v, 32, 64));
   return v;
+}
+
+// Elements of a 16-byte chunk of bf16 or fp32 keys as floats.
+template <typename KT>
+__device__ __forceinline__ void chunk_to_f(const uint4& w, float* out);
+template <>
+__device__ __forceinline__ void chunk_to_f<uint16_t>(const uint4& w, float* out) {
+  const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    out[2 * e] = __uint_as_float(u[e] << 16);
+    out[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+  }
+}
+template <>
+__device__ __forceinline__ void chunk_to_f<float>(const uint4& w, float* out) {
+  out[0] = __uint_as_float(w.x); out[1] = __uint_as_float(w.y);
+  out[2] = __uint_as_float(w.z); out[3] = __uint_as_float(w.w);
 }
 
 __device__ __forceinline__ float f16_scale(float amax, float qmax) {
@@ -142,28 +174,34 @@ __global__ __launch_bounds__(64) void build_page_kernel(
     uint4* dst = reinterpret_cast<uint4*>(&sK[it][i][0]);
 #pragma unroll
     for (int u = 0; u < kDim / kV; ++u) dst[u] = w[u];
-    __syncthreads();
-#pragma unroll 8
-    for (int c = 0; c < kDim; ++c) {
-      const float x = key_at(&sK[it][i][0], c);
-      energy = fmaf(x, x, energy);
+#pragma unroll
+    for (int u = 0; u < kDim / kV; ++u) {
+      float x[kV];
+      chunk_to_f<KT>(w[u], x);
+#pragma unroll
+      for (int e2 = 0; e2 < kV; ++e2) energy = fmaf(x[e2], x[e2], energy);
     }
+    __syncthreads();
   }
   energy = group_sum<B>(energy) * (1.0f / B);
 
   // ---- centroid of the lane's kCols columns: pairwise sum over the B rows
   //      (exact when the rows are equal)
+  {
+    constexpr int kC = P::kCols;
+    float v[B][kC];
 #pragma unroll
-  for (int cc = 0; cc < P::kCols; ++cc) {
-    const int c = P::kCols * i + cc;
-    float v[B];
+    for (int t = 0; t < B; ++t)
 #pragma unroll
-    for (int t = 0; t < B; ++t) v[t] = key_at(&sK[it][t][0], c);
+      for (int cc = 0; cc < kC; ++cc) v[t][cc] = key_at(&sK[it][t][0], kC * i + cc);
 #pragma unroll
     for (int w = B / 2; w > 0; w >>= 1)
 #pragma unroll
-      for (int t = 0; t < w; ++t) v[t] = v[t] + v[t + w];
-    sMu[it][c] = v[0] * (1.0f / B);
+      for (int t = 0; t < w; ++t)
+#pragma unroll
+        for (int cc = 0; cc < kC; ++cc) v[t][cc] = v[t][cc] + v[t + w][cc];
+#pragma unroll
+    for (int cc = 0; cc < kC; ++cc) sMu[it][kC * i + cc] = v[0][cc] * (1.0f / B);
   }
   __syncthreads();
 
@@ -184,12 +222,20 @@ __global__ __launch_bounds__(64) void build_page_kernel(
 #pragma unroll
         for (int U = T; U < kT; ++U) {
           f4 a = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 8
-          for (int m = 0; m < 32; ++m) {
-            const int c = 32 * q4 + m;
-            const float x = key_at(&sK[t][16 * T + l16][0], c) - sMu[t][c];
-            const float y = key_at(&sK[t][16 * U + l16][0], c) - sMu[t][c];
-            a = __builtin_amdgcn_mfma_f32_16x16x4f32(x, y, a, 0, 0, 0);
+          constexpr int kV = 16 / sizeof(KT);
+#pragma unroll
+          for (int ch = 0; ch < 32 / kV; ++ch) {
+            const int c0 = 32 * q4 + kV * ch;
+            const uint4 wx = *reinterpret_cast<const uint4*>(&sK[t][16 * T + l16][c0]);
+            const uint4 wy = *reinterpret_cast<const uint4*>(&sK[t][16 * U + l16][c0]);
+            float xs[kV], ys[kV];
+            chunk_to_f<KT>(wx, xs);
+            chunk_to_f<KT>(wy, ys);
+#pragma unroll
+            for (int e2 = 0; e2 < kV; ++e2) {
+              const float m2 = sMu[t][c0 + e2];
+              a = __builtin_amdgcn_mfma_f32_16x16x4f32(xs[e2] - m2, ys[e2] - m2, a, 0, 0, 0);
+            }
           }
           acc[t][tile++] = a;
         }
@@ -593,7 +639,6 @@ hipError_t launch_build_page(const locks_cfg_t& c, const void* k_cache, const in
                      (uint8_t*)summaries, mu, basis, coef, sigma2, c.basis)
 #define LOCKS_BUILD_PAGE_B(KT)                                                                 \
   switch (c.page_size) {                                                                       \
-    case 16: if (factors) LOCKS_BUILD_PAGE(KT, 16, true); else LOCKS_BUILD_PAGE(KT, 16, false); break; \
     case 32: if (factors) LOCKS_BUILD_PAGE(KT, 32, true); else LOCKS_BUILD_PAGE(KT, 32, false); break; \
     case 64: if (factors) LOCKS_BUILD_PAGE(KT, 64, true); else LOCKS_BUILD_PAGE(KT, 64, false); break; \
     default: return hipErrorInvalidValue;                                                      \
