@@ -42,6 +42,13 @@ __device__ __forceinline__ float group16_max(float v) {
   return fmaxf(v, tri16::dpp<0x140>(v));
 }
 
+__device__ __forceinline__ int group16_min_int(int v) {
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false));
+  return min(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false));
+}
+
 // Elements of a 16-byte chunk of bf16 or fp32 keys as floats.
 template <typename KT>
 __device__ __forceinline__ void chunk_to_f(const uint4& w, float* out);
@@ -109,7 +116,6 @@ __global__ __launch_bounds__(64) void build_kernel(
   __shared__ float sFlip[kItems][kMaxRank];
   __shared__ float sMu[kItems][kDim];
   __shared__ float sLam[kItems][kPage];
-  __shared__ int sOrd[kItems][kPage];
   // quantised basis columns (packed codes, scales) and projections of the scored pages
   __shared__ uint32_t sVw[kScore ? kItems : 1][kScore ? kMaxRank : 1][kScore ? kPage : 1];
   __shared__ float sVs[kScore ? kItems : 1][kScore ? kMaxRank : 1];
@@ -250,7 +256,6 @@ __global__ __launch_bounds__(64) void build_kernel(
     float lam, u[kMaxRank];
     tri16::eig16<kFactors, kMaxRank>(a, li, r, lam, u, &sA[grp][0][0]);
     sLam[grp][li] = fmaxf(lam, 0.0f);
-    sOrd[grp][li] = li;
 #pragma unroll
     for (int l = 0; l < kMaxRank; ++l)
       if (l < r) sU[grp][li][l] = u[l];
@@ -262,9 +267,9 @@ __global__ __launch_bounds__(64) void build_kernel(
   const long out_item = all_pages ? 0 : (long)e * H_kv + h;
   uint8_t* rec = summaries + (blk * H_kv + h) * (long)rec_stride(r, basis);
 
-  // ---- basis columns, one at a time: V[:, l] = D^T u_l / sigma_l.  This lane's
-  //      8 dimensions of the 16 key rows are re-read from global memory (the
-  //      page was just loaded, so they come from cache) and held in registers.
+  // ---- basis columns V[:, l] = D^T u_l / sigma_l.  This lane's 8 dimensions of
+  //      the 16 key rows are re-read from global memory (the page was just
+  //      loaded, so they come from cache) and held in registers.
   constexpr int kSliceVec = 8 * (int)sizeof(KT) / 16;  // 16-byte loads per 8-element slice
   uint4 ks[kPage][kSliceVec];
   {
@@ -277,88 +282,109 @@ __global__ __launch_bounds__(64) void build_kernel(
                           : make_uint4(0, 0, 0, 0);
   }
   float cabs = 0.0f;  // running max |C[li][:]| for the row scale
-  for (int l = 0; l < r; ++l) {
-    const float lam = sLam[grp][l];
-    const bool kept = lam > floor_ && lam > 0.0f;
-    const float sig = kept ? sqrtf(lam) : 1.0f;
-    const int mode = sOrd[grp][l];
-    float v[8];
+  float mu8[8];
 #pragma unroll
-    for (int cc = 0; cc < 8; ++cc) v[cc] = 0.0f;
+  for (int cc = 0; cc < 8; ++cc) mu8[cc] = sMu[grp][8 * li + cc];
+  // four modes at a time: each key row is converted once per pass and
+  // multiplies the four eigenvector components of that row (one LDS broadcast)
+  constexpr int kMG = 4;
+#pragma unroll 1
+  for (int l0 = 0; l0 < r; l0 += kMG) {
+    float vacc[kMG][8];
+#pragma unroll
+    for (int m = 0; m < kMG; ++m)
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) vacc[m][cc] = 0.0f;
+#pragma unroll
     for (int i = 0; i < kPage; ++i) {
-      const float ui = sU[grp][i][mode];
+      const float4 ua = *reinterpret_cast<const float4*>(&sU[grp][i][l0]);
+      const float ui[kMG] = {ua.x, ua.y, ua.z, ua.w};
+      float x[8];
+#pragma unroll
+      for (int u = 0; u < kSliceVec; ++u) chunk_to_f<KT>(ks[i][u], &x[u * (16 / (int)sizeof(KT))]);
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) {
-        const float x = load_elem(reinterpret_cast<const KT*>(&ks[i][0]), cc);
-        v[cc] = fmaf(x - sMu[grp][8 * li + cc], ui, v[cc]);
+        const float dv = x[cc] - mu8[cc];
+#pragma unroll
+        for (int m = 0; m < kMG; ++m) vacc[m][cc] = fmaf(dv, ui[m], vacc[m][cc]);
       }
     }
 #pragma unroll
-    for (int cc = 0; cc < 8; ++cc) v[cc] = kept ? v[cc] / sig : 0.0f;
-    // sign convention: largest |v| (first index on ties) made positive
-    float best = -1.0f;
-    int bidx = 0;
-    float bval = 0.0f;
+    for (int m = 0; m < kMG; ++m) {
+      const int l = l0 + m;
+      if (l >= r) break;
+      const float lam = sLam[grp][l];
+      const bool kept = lam > floor_ && lam > 0.0f;
+      const float isig = kept ? 1.0f / sqrtf(lam) : 0.0f;
+      const float sig = kept ? sqrtf(lam) : 1.0f;
+      float v[8];
 #pragma unroll
-    for (int cc = 0; cc < 8; ++cc) {
-      const float a = fabsf(v[cc]);
-      if (a > best) { best = a; bidx = 8 * li + cc; bval = v[cc]; }
-    }
-    for (int o = 8; o > 0; o >>= 1) {
-      const float ob = __shfl_xor(best, o, 64);
-      const int oi = __shfl_xor(bidx, o, 64);
-      const float ov = __shfl_xor(bval, o, 64);
-      if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; bval = ov; }
-    }
-    const float flip = (bval < 0.0f) ? -1.0f : 1.0f;
-    const float cval = kept ? flip * sU[grp][li][mode] * sig : 0.0f;
-    if (li == 0) sFlip[grp][l] = flip;
-    cabs = fmaxf(cabs, fabsf(cval));
-    if (!active) continue;
-    if (kFactors) {
-      float* bo = basis_out + out_item * (kDim * (long)r);
+      for (int cc = 0; cc < 8; ++cc) v[cc] = vacc[m][cc] * isig;
+      // sign convention: largest |v| (first index on ties) made positive: the
+      // largest magnitude over the item, then the lowest index holding it, with
+      // its sign in the low bit
+      float best = -1.0f;
+      int bidx = 0;
+      float bval = 0.0f;
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) bo[(8 * li + cc) * r + l] = flip * v[cc];
-    } else {
-      if (basis == 0) {  // int4, excess 8, two per byte
-        const float vs = f16_scale(best, 7.0f);
-        uint32_t word = 0;
+      for (int cc = 0; cc < 8; ++cc) {
+        const float a = fabsf(v[cc]);
+        if (a > best) { best = a; bidx = 8 * li + cc; bval = v[cc]; }
+      }
+      const float gbest = group16_max(best);
+      const int key = group16_min_int(best == gbest ? 2 * bidx + (bval < 0.0f ? 1 : 0) : 0x7fffffff);
+      best = gbest;
+      bval = (key & 1) ? -1.0f : 1.0f;
+      const float flip = (bval < 0.0f) ? -1.0f : 1.0f;
+      const float cval = kept ? flip * sU[grp][li][l] * sig : 0.0f;
+      if (li == 0) sFlip[grp][l] = flip;
+      cabs = fmaxf(cabs, fabsf(cval));
+      if (!active) continue;
+      if (kFactors) {
+        float* bo = basis_out + out_item * (kDim * (long)r);
 #pragma unroll
-        for (int cc = 0; cc < 8; ++cc) {
-          const int code = quant(flip * v[cc], vs, 7);
-          word |= (uint32_t)(code + 8) << (4 * cc);
+        for (int cc = 0; cc < 8; ++cc) bo[(8 * li + cc) * r + l] = flip * v[cc];
+      } else {
+        if (basis == 0) {  // int4, excess 8, two per byte
+          const float vs = f16_scale(best, 7.0f);
+          uint32_t word = 0;
+#pragma unroll
+          for (int cc = 0; cc < 8; ++cc) {
+            const int code = quant(flip * v[cc], vs, 7);
+            word |= (uint32_t)(code + 8) << (4 * cc);
+          }
+          *reinterpret_cast<uint32_t*>(rec + 64 * l + 4 * li) = word;
+          if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * l) = f16_bits(vs);
+          if (kScore) {
+            sVw[grp][l][li] = word;
+            if (li == 0) sVs[grp][l] = vs;
+          }
+        } else if (basis == 1) {  // int8, excess 128
+          const float vs = f16_scale(best, 127.0f);
+          uint32_t w[2] = {0u, 0u};
+#pragma unroll
+          for (int cc = 0; cc < 8; ++cc)
+            w[cc >> 2] |= (uint32_t)(quant(flip * v[cc], vs, 127) + 128) << (8 * (cc & 3));
+          *reinterpret_cast<uint2*>(rec + 128 * l + 8 * li) = make_uint2(w[0], w[1]);
+          if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, 1) + 2 * l) = f16_bits(vs);
+        } else {  // bfloat16, round to nearest even; the column scale is 1
+          uint32_t w[4];
+#pragma unroll
+          for (int e2 = 0; e2 < 4; ++e2)
+            w[e2] = bf16_rne_bits(flip * v[2 * e2]) | (bf16_rne_bits(flip * v[2 * e2 + 1]) << 16);
+          *reinterpret_cast<uint4*>(rec + 256 * l + 16 * li) = make_uint4(w[0], w[1], w[2], w[3]);
+          if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, 2) + 2 * l) = f16_bits(1.0f);
         }
-        *reinterpret_cast<uint32_t*>(rec + 64 * l + 4 * li) = word;
-        if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r) + 2 * l) = f16_bits(vs);
-        if (kScore) {
-          sVw[grp][l][li] = word;
-          if (li == 0) sVs[grp][l] = vs;
-        }
-      } else if (basis == 1) {  // int8, excess 128
-        const float vs = f16_scale(best, 127.0f);
-        uint32_t w[2] = {0u, 0u};
-#pragma unroll
-        for (int cc = 0; cc < 8; ++cc)
-          w[cc >> 2] |= (uint32_t)(quant(flip * v[cc], vs, 127) + 128) << (8 * (cc & 3));
-        *reinterpret_cast<uint2*>(rec + 128 * l + 8 * li) = make_uint2(w[0], w[1]);
-        if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, 1) + 2 * l) = f16_bits(vs);
-      } else {  // bfloat16, round to nearest even; the column scale is 1
-        uint32_t w[4];
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2)
-          w[e2] = bf16_rne_bits(flip * v[2 * e2]) | (bf16_rne_bits(flip * v[2 * e2 + 1]) << 16);
-        *reinterpret_cast<uint4*>(rec + 256 * l + 16 * li) = make_uint4(w[0], w[1], w[2], w[3]);
-        if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, 2) + 2 * l) = f16_bits(1.0f);
       }
     }
   }
   __syncthreads();  // sFlip visible to the whole group
   if (!active) return;
-  // C[li][l] = flip_l * U[li][mode_l] * sigma_l (0 for a dropped mode)
+  // C[li][l] = flip_l * U[li][l] * sigma_l (0 for a dropped mode)
   auto coef_value = [&](int l) {
     const float lam = sLam[grp][l];
     const bool kept = lam > floor_ && lam > 0.0f;
-    return kept ? sFlip[grp][l] * sU[grp][li][sOrd[grp][l]] * sqrtf(lam) : 0.0f;
+    return kept ? sFlip[grp][l] * sU[grp][li][l] * sqrtf(lam) : 0.0f;
   };
 
   if (kFactors) {

@@ -47,6 +47,19 @@ __device__ __forceinline__ float row_sum(float v) {
   v += dpp<0x140>(v);
   return v;
 }
+// N independent row sums, stage by stage (each DPP step waits on the previous
+// write of its own operand only)
+template <int N>
+__device__ __forceinline__ void row_sums(float (&v)[N]) {
+#pragma unroll
+  for (int n = 0; n < N; ++n) v[n] += dpp<0xB1>(v[n]);
+#pragma unroll
+  for (int n = 0; n < N; ++n) v[n] += dpp<0x4E>(v[n]);
+#pragma unroll
+  for (int n = 0; n < N; ++n) v[n] += dpp<0x141>(v[n]);
+#pragma unroll
+  for (int n = 0; n < N; ++n) v[n] += dpp<0x140>(v[n]);
+}
 
 template <typename F, int... Ks>
 __device__ __forceinline__ void for_each_int(F& f, std::integer_sequence<int, Ks...>) {
@@ -80,17 +93,19 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
 #pragma unroll
     for (int j = k + 2; j < kN; ++j) sig = fmaf(x[j], x[j], sig);
     const float x0 = x[k + 1];
+    // (hardware square root and reciprocals: the reflector need only be
+    // orthogonal to a few ulp, which its own tau guarantees)
     float t = 0.0f, v0 = 1.0f, beta = x0;
     if (sig > 0.0f) {
-      const float mu = sqrtf(fmaf(x0, x0, sig));
-      v0 = x0 <= 0.0f ? x0 - mu : -sig / (x0 + mu);
-      t = 2.0f * v0 * v0 / (sig + v0 * v0);
+      const float mu = __builtin_amdgcn_sqrtf(fmaf(x0, x0, sig));
+      v0 = x0 <= 0.0f ? x0 - mu : -sig * __builtin_amdgcn_rcpf(x0 + mu);
+      t = 2.0f * v0 * v0 * __builtin_amdgcn_rcpf(fmaf(v0, v0, sig));
       beta = mu;
     }
     e[k] = beta;
     tau[k] = t;
     float v[kN];
-    const float iv0 = 1.0f / v0;
+    const float iv0 = __builtin_amdgcn_rcpf(v0);
     v[k + 1] = 1.0f;
 #pragma unroll
     for (int j = k + 2; j < kN; ++j) v[j] = sig > 0.0f ? x[j] * iv0 : 0.0f;
@@ -133,9 +148,10 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
     lo = fminf(lo, d[t] - el - er);
     hi = fmaxf(hi, d[t] + el + er);
     tn = fmaxf(tn, fabsf(d[t]) + el + er);
-    e2[t] = t > 0 ? e[t - 1] * e[t - 1] : 0.0f;
+    // (the floor moves eigenvalues by at most 1e-19; an all-zero T has a zero-width
+    // interval, so its eigenvalues stay exactly 0)
+    e2[t] = t > 0 ? fmaf(e[t - 1], e[t - 1], 0x1p-126f) : 0.0f;
   }
-  const float pivmin = fmaxf(tn, 1e-30f) * 1e-30f;
   const int ne = kAll ? kN : r;            // eigenvalues wanted: the ne largest
   const int q = kN / ne;                   // lanes per eigenvalue
   const int lq = i / q;
@@ -146,26 +162,28 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
   const int npts = 2 * q;
   const int row0 = threadIdx.x & 48;
   const uint64_t gmask = ((1ull << q) - 1ull) << (row0 + le * q);
+  // the Sturm counts carry rounding of a few ulp of |T|, so the interval is cut to
+  // 2^-22 of its width (2^-24 when every eigenvalue is reported)
   int steps = 0;
-  for (float w = 1.0f; w > 0x1p-28f; w /= (float)(npts + 1)) ++steps;
+  for (float w = 1.0f; w > (kAll ? 0x1p-24f : 0x1p-22f); w /= (float)(npts + 1)) ++steps;
   const float fa = (float)(2 * pi + 1), fb = (float)(2 * pi + 2);
   for (int st = 0; st < steps; ++st) {
     const float h = (hi - lo) / (float)(npts + 1);
     const float xa = fmaf(fa, h, lo), xb = fmaf(fb, h, lo);
     float qa = 1.0f, qb = 1.0f;
-    int ca = 0, cb = 0;
+    uint32_t ca = 0, cb = 0;
 #pragma unroll
     for (int t = 0; t < kN; ++t) {
-      // q_t = (d_t - x) - e_{t-1}^2 / q_{t-1}; the hardware reciprocal's last-bit
-      // error moves only counts at x within rounding of an eigenvalue
-      qa = (d[t] - xa) - e2[t] * __builtin_amdgcn_rcpf(qa);
-      qb = (d[t] - xb) - e2[t] * __builtin_amdgcn_rcpf(qb);
-      if (fabsf(qa) < pivmin) qa = -pivmin;
-      if (fabsf(qb) < pivmin) qb = -pivmin;
-      ca += qa < 0.0f;
-      cb += qb < 0.0f;
+      // q_t = (d_t - x) - e_{t-1}^2 / q_{t-1}, counted by sign bit.  A zero pivot
+      // makes the next one infinite with the opposite sign (one count either
+      // way), and e^2 >= FLT_MIN keeps 0 * inf out.  The hardware reciprocal's
+      // last-bit error moves only counts at x within rounding of an eigenvalue.
+      qa = fmaf(-e2[t], __builtin_amdgcn_rcpf(qa), d[t] - xa);
+      qb = fmaf(-e2[t], __builtin_amdgcn_rcpf(qb), d[t] - xb);
+      ca += __float_as_uint(qa) >> 31;
+      cb += __float_as_uint(qb) >> 31;
     }
-    const uint64_t ma = __ballot(ca <= want), mb = __ballot(cb <= want);
+    const uint64_t ma = __ballot((int)ca <= want), mb = __ballot((int)cb <= want);
     const int nle = __popcll(ma & gmask) + __popcll(mb & gmask);
     const float nlo = nle > 0 ? fmaf((float)nle, h, lo) : lo;
     const float nhi = nle < npts ? fmaf((float)(nle + 1), h, lo) : hi;
@@ -250,13 +268,22 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
   static_for<kN - 2>([&](auto kc) __attribute__((always_inline)) {
     constexpr int k = kN - 3 - decltype(kc)::value;
     const float vk = a[k];
+    float s[kMaxR];
 #pragma unroll
-    for (int l = 0; l < kMaxR; ++l) {
-      if (l < r) {
-        const float s = row_sum(vk * u[l]);
-        u[l] = fmaf(-tau[k] * s, vk, u[l]);
-      }
+    for (int l = 0; l < kMaxR; ++l) s[l] = vk * u[l];
+    if (r <= 8) {
+      float s8[8];
+#pragma unroll
+      for (int l = 0; l < 8; ++l) s8[l] = s[l];
+      row_sums(s8);
+#pragma unroll
+      for (int l = 0; l < 8; ++l) s[l] = s8[l];
+    } else {
+      row_sums(s);
     }
+    const float tk = tau[k];
+#pragma unroll
+    for (int l = 0; l < kMaxR; ++l) u[l] = fmaf(-tk * s[l], vk, u[l]);
   });
 }
 
