@@ -72,9 +72,12 @@ __device__ __forceinline__ float f16_scale(float amax, float qmax) {
   return (float)(_Float16)s;
 }
 
-__device__ __forceinline__ int quant(float x, float s, int qmax) {
-  if (!(s > 0.0f)) return 0;
-  float c = rintf(x / s);
+// 1 / s for a code scale s (0 when s is 0: every code is then 0)
+__device__ __forceinline__ float inv_scale(float s) { return s > 0.0f ? 1.0f / s : 0.0f; }
+// code of x at scale 1 / inv: nearest integer, clamped to +-qmax (x inv may differ
+// from x / s in the last bit, which moves a code only at an exact half)
+__device__ __forceinline__ int quant(float x, float inv, int qmax) {
+  float c = rintf(x * inv);
   c = fminf(fmaxf(c, (float)-qmax), (float)qmax);
   return (int)c;
 }
@@ -347,10 +350,11 @@ __global__ __launch_bounds__(64) void build_kernel(
       } else {
         if (basis == 0) {  // int4, excess 8, two per byte
           const float vs = f16_scale(best, 7.0f);
+          const float ivs = inv_scale(vs);
           uint32_t word = 0;
 #pragma unroll
           for (int cc = 0; cc < 8; ++cc) {
-            const int code = quant(flip * v[cc], vs, 7);
+            const int code = quant(flip * v[cc], ivs, 7);
             word |= (uint32_t)(code + 8) << (4 * cc);
           }
           *reinterpret_cast<uint32_t*>(rec + 64 * l + 4 * li) = word;
@@ -361,10 +365,11 @@ __global__ __launch_bounds__(64) void build_kernel(
           }
         } else if (basis == 1) {  // int8, excess 128
           const float vs = f16_scale(best, 127.0f);
+          const float ivs = inv_scale(vs);
           uint32_t w[2] = {0u, 0u};
 #pragma unroll
           for (int cc = 0; cc < 8; ++cc)
-            w[cc >> 2] |= (uint32_t)(quant(flip * v[cc], vs, 127) + 128) << (8 * (cc & 3));
+            w[cc >> 2] |= (uint32_t)(quant(flip * v[cc], ivs, 127) + 128) << (8 * (cc & 3));
           *reinterpret_cast<uint2*>(rec + 128 * l + 8 * li) = make_uint2(w[0], w[1]);
           if (li == 0) *reinterpret_cast<uint16_t*>(rec + rec_scale_off(r, 1) + 2 * l) = f16_bits(vs);
         } else {  // bfloat16, round to nearest even; the column scale is 1
@@ -400,8 +405,9 @@ __global__ __launch_bounds__(64) void build_kernel(
   float chat[kScore ? kMaxRank : 1];  // decoded row (scored pages)
   {
     const float cs = f16_scale(cabs, 127.0f);
+    const float ics = inv_scale(cs);
     for (int l = 0; l < r; ++l) {
-      const int code = quant(coef_value(l), cs, 127);
+      const int code = quant(coef_value(l), ics, 127);
       rec[rec_coef_off(r, basis) + li * r + l] = (uint8_t)(code + 128);
       if (kScore) {
 #pragma unroll
@@ -417,9 +423,10 @@ __global__ __launch_bounds__(64) void build_kernel(
     for (int cc = 0; cc < 8; ++cc) m = fmaxf(m, fabsf(sMu[grp][8 * li + cc]));
     m = group16_max(m);
     const float ms = f16_scale(m, 127.0f);
+    const float ims = inv_scale(ms);
     float mhat[8];
     for (int cc = 0; cc < 8; ++cc) {
-      const int code = quant(sMu[grp][8 * li + cc], ms, 127);
+      const int code = quant(sMu[grp][8 * li + cc], ims, 127);
       rec[rec_mu_off(r, basis) + 8 * li + cc] = (uint8_t)(code + 128);
       mhat[cc] = (float)code * ms;
     }

@@ -1,17 +1,17 @@
-// Per-page summary construction for pages of B = 16, 32 or 64 tokens (Sec. 4
+// Per-page summary construction for pages of B = 32 or 64 tokens (Sec. 4
 // "Build"; App. D.3 "Page size"): centre the page's B keys, form the B x B Gram of
 // the deviations, find its eigenpairs, keep the r leading nonzero modes, form
 // V = D^T U_r S_r^{-1} and C = U_r S_r, quantise and pack.
 //
-// The symmetric eigenproblem is solved the way a B x B problem is best solved
-// with B lanes, rather than by rotations: Householder reduction to a tridiagonal
-// T (each lane keeps one row of the Gram in registers; the reflector and its
-// update vectors are broadcast through LDS), every eigenvalue of T by bisection on
-// Sturm counts (lane i converges on the i-th largest), the r leading eigenvectors
-// of T by inverse iteration on its LDL^T factorisation (lane l solves for vector
-// l; two rounds, each followed by modified Gram-Schmidt over the r vectors, so a
+// The symmetric eigenproblem is solved with B lanes, one row each: Householder
+// reduction to a tridiagonal T (the rows in LDS; the reflector and its update
+// vectors broadcast through LDS), the wanted eigenvalues of T by multisection on
+// Sturm counts (B / n lanes per eigenvalue), the r leading eigenvectors of T by
+// inverse iteration on its LDL^T factorisation (lane l solves for vector l; two
+// rounds, each followed by modified Gram-Schmidt over the r vectors, so a
 // near-degenerate pair still yields an orthonormal basis of its eigenspace), and
 // the back-transformation through the stored reflectors.  Everything is fp32.
+// Cross-lane sums use DPP within 16-lane rows and row swaps across them.
 //
 // Mapping: one wave per block holding 64 / B items (page, KV head); lane (it, i)
 // owns row i of item it.
@@ -24,7 +24,6 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr float kZeroRel = 1e-6f;
 constexpr float kZeroAbs = 1e-10f;
-constexpr int kBisect = 34;       // bisection steps: the Gershgorin width / 2^34
 constexpr int kInvRounds = 2;     // inverse-iteration rounds (solve + orthogonalise)
 
 template <int B>
@@ -42,14 +41,22 @@ __device__ __forceinline__ float dpp_f(float v) {
 // Sum / max over the B lanes of an item (lane groups of B consecutive lanes):
 // within a 16-lane row by DPP (quad xor 1, quad xor 2, half-row mirror, row
 // mirror), across rows by lane swaps.
+// (a row swap pairs rows 0-1 and 2-3, a half swap the two halves of the wave:
+// the two results summed hold the pair's total in both)
 template <int B>
 __device__ __forceinline__ float group_sum(float v) {
   v += dpp_f<0xB1>(v);
   v += dpp_f<0x4E>(v);
   v += dpp_f<0x141>(v);
   v += dpp_f<0x140>(v);
-  if (B >= 32) v += __shfl_xor(v, 16, 64);
-  if (B >= 64) v += __shfl_xor(v, 32, 64);
+  if (B >= 32) {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  }
+  if (B >= 64) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  }
   return v;
 }
 template <int B>
@@ -58,8 +65,30 @@ __device__ __forceinline__ float group_max(float v) {
   v = fmaxf(v, dpp_f<0x4E>(v));
   v = fmaxf(v, dpp_f<0x141>(v));
   v = fmaxf(v, dpp_f<0x140>(v));
-  if (B >= 32) v = fmaxf(v, __shfl_xor(v, 16, 64));
-  if (B >= 64) v = fmaxf(v, __shfl_xor(v, 32, 64));
+  if (B >= 32) {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  }
+  if (B >= 64) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  }
+  return v;
+}
+template <int B>
+__device__ __forceinline__ int group_min_int(int v) {
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false));
+  if (B >= 32) {
+    const auto p = __builtin_amdgcn_permlane16_swap((uint32_t)v, (uint32_t)v, false, false);
+    v = min((int)p[0], (int)p[1]);
+  }
+  if (B >= 64) {
+    const auto p = __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false);
+    v = min((int)p[0], (int)p[1]);
+  }
   return v;
 }
 
@@ -275,7 +304,7 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   for (int k = 0; k < B - 2; ++k) {
     const float x = arow[k];
     const float sig = group_sum<B>(i > k + 1 ? x * x : 0.0f);
-    const float x0 = __shfl(x, it * B + k + 1, 64);
+    const float x0 = group_sum<B>(i == k + 1 ? x : 0.0f);
     float tau = 0.0f, v0 = 1.0f, beta = x0;
     if (sig > 0.0f) {
       const float mu = sqrtf(fmaf(x0, x0, sig));
@@ -331,14 +360,16 @@ __global__ __launch_bounds__(64) void build_page_kernel(
     sE[it][B - 1] = 0.0f;
   }
   __syncthreads();
-  sE2[it][i] = i > 0 ? sE[it][i - 1] * sE[it][i - 1] : 0.0f;
+  sE2[it][i] = i > 0 ? fmaf(sE[it][i - 1], sE[it][i - 1], 0x1p-126f) : 0.0f;
   __syncthreads();
 
-  // ---- eigenvalues of T by bisection on Sturm counts: lane i converges on the
-  //      i-th largest (the (B - 1 - i)-th smallest)
   float lam;
+  // ---- the wanted eigenvalues of T (the r largest; all B for the factor output)
+  //      by multisection on Sturm counts: q = B / n lanes per eigenvalue, one
+  //      point each per step, so a group cuts its interval into q + 1 parts and
+  //      a wave ballot gives the part that holds the eigenvalue
   {
-    float lo = INFINITY, hi = -INFINITY, tnorm = 0.0f;
+    float lo = INFINITY, hi = -INFINITY;
 #pragma unroll
     for (int t = 0; t < B; ++t) {
       const float el = t > 0 ? fabsf(sE[it][t - 1]) : 0.0f;
@@ -346,31 +377,46 @@ __global__ __launch_bounds__(64) void build_page_kernel(
       const float dd = sD[it][t];
       lo = fminf(lo, dd - el - er);
       hi = fmaxf(hi, dd + el + er);
-      tnorm = fmaxf(tnorm, fabsf(dd) + el + er);
     }
-    const float pivmin = fmaxf(tnorm, 1e-30f) * 1e-30f;
-    const int want = B - 1 - i;  // count(x) <= want  <=>  x <= lambda_i
-    for (int step = 0; step < kBisect; ++step) {
-      const float mid = 0.5f * (lo + hi);
-      int cnt = 0;
+    const int ne = kFactors ? B : r;
+    const int q = B / ne;
+    const int lq = i / q;
+    const bool idle = lq >= ne;            // lanes past ne * q copy the last group
+    const int le = idle ? ne - 1 : lq;     // the eigenvalue (0 = largest)
+    const int pi = idle ? 0 : i - lq * q;  // this lane's point
+    const int want = B - 1 - le;           // count(x) <= want  <=>  x <= lambda_le
+    const uint64_t gmask = (q >= 64 ? ~0ull : ((1ull << q) - 1ull)) << (it * B + le * q);
+    // the Sturm counts carry rounding of a few ulp of |T|: the interval is cut to
+    // 2^-22 of its width (2^-24 for the factor output)
+    int steps = 0;
+    for (float w = 1.0f; w > (kFactors ? 0x1p-24f : 0x1p-22f); w /= (float)(q + 1)) ++steps;
+    for (int st = 0; st < steps; ++st) {
+      const float hstep = (hi - lo) / (float)(q + 1);
+      const float x = fmaf((float)(pi + 1), hstep, lo);
       float qv = 1.0f;
+      uint32_t cnt = 0;
 #pragma unroll
-      for (int q = 0; q < B / 4; ++q) {
-        const float4 d4 = *reinterpret_cast<const float4*>(&sD[it][4 * q]);
-        const float4 e4 = *reinterpret_cast<const float4*>(&sE2[it][4 * q]);
+      for (int qq = 0; qq < B / 4; ++qq) {
+        const float4 d4 = *reinterpret_cast<const float4*>(&sD[it][4 * qq]);
+        const float4 e4 = *reinterpret_cast<const float4*>(&sE2[it][4 * qq]);
         const float dd[4] = {d4.x, d4.y, d4.z, d4.w}, ee[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
         for (int u2 = 0; u2 < 4; ++u2) {
-          // q_t = (d_t - x) - e_{t-1}^2 / q_{t-1}; the hardware reciprocal's last-bit
-          // error moves only counts at x within rounding of an eigenvalue
-          qv = (dd[u2] - mid) - ee[u2] * __builtin_amdgcn_rcpf(qv);
-          if (fabsf(qv) < pivmin) qv = -pivmin;
-          cnt += qv < 0.0f;
+          // q_t = (d_t - x) - e_{t-1}^2 / q_{t-1}, counted by sign bit: a zero
+          // pivot makes the next one infinite with the opposite sign, and
+          // e^2 >= FLT_MIN keeps 0 * inf out
+          qv = fmaf(-ee[u2], __builtin_amdgcn_rcpf(qv), dd[u2] - x);
+          cnt += __float_as_uint(qv) >> 31;
         }
       }
-      if (cnt <= want) lo = mid; else hi = mid;
+      const int nle = __popcll(__ballot((int)cnt <= want) & gmask);
+      const float nlo = nle > 0 ? fmaf((float)nle, hstep, lo) : lo;
+      const float nhi = nle < q ? fmaf((float)(nle + 1), hstep, lo) : hi;
+      lo = nlo;
+      hi = nhi;
     }
-    lam = 0.5f * (lo + hi);
+    const float lam_g = 0.5f * (lo + hi);
+    lam = __shfl(lam_g, it * B + (i < ne ? i : ne - 1) * q, 64);
     sLam[it][i] = lam;
   }
   __syncthreads();
@@ -479,19 +525,46 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   __syncthreads();
 
   // ---- basis columns V[:, l] = D^T u_l / sigma_l over this lane's kCols columns;
-  //      the key rows come back from global memory (cache-resident)
+  //      the key rows come back from global memory (cache-resident), every row's
+  //      slice requested before the first is used
   constexpr int kC = P::kCols;
+  constexpr int kW = kC * (int)sizeof(KT) / 4;  // 32-bit words of a row slice
+  uint32_t ksl[B][kW];
+  {
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(kpage + kC * i);
+    constexpr int kRowW = kDim * (int)sizeof(KT) / 4;
+#pragma unroll
+    for (int t = 0; t < B; ++t) {
+      if constexpr (kW == 4) {
+        const uint4 w = active ? *reinterpret_cast<const uint4*>(src + t * kRowW) : make_uint4(0, 0, 0, 0);
+        ksl[t][0] = w.x; ksl[t][1] = w.y; ksl[t][2] = w.z; ksl[t][3] = w.w;
+      } else if constexpr (kW == 2) {
+        const uint2 w = active ? *reinterpret_cast<const uint2*>(src + t * kRowW) : make_uint2(0, 0);
+        ksl[t][0] = w.x; ksl[t][1] = w.y;
+      } else {
+        ksl[t][0] = active ? src[t * kRowW] : 0u;
+      }
+    }
+  }
+  float mu_c[kC];
+#pragma unroll
+  for (int cc = 0; cc < kC; ++cc) mu_c[cc] = sMu[it][kC * i + cc];
   float vcol[kMaxRank][kC];
 #pragma unroll
   for (int l = 0; l < kMaxRank; ++l)
 #pragma unroll
     for (int cc = 0; cc < kC; ++cc) vcol[l][cc] = 0.0f;
+#pragma unroll
   for (int t = 0; t < B; ++t) {
     float kv[kC];
 #pragma unroll
     for (int cc = 0; cc < kC; ++cc) {
-      const int c = kC * i + cc;
-      kv[cc] = active ? load_elem(kpage, (size_t)t * kDim + c) - sMu[it][c] : 0.0f;
+      float x;
+      if constexpr (sizeof(KT) == 2)
+        x = __uint_as_float((cc & 1) ? (ksl[t][cc >> 1] & 0xffff0000u) : (ksl[t][cc >> 1] << 16));
+      else
+        x = __uint_as_float(ksl[t][cc]);
+      kv[cc] = x - mu_c[cc];
     }
 #pragma unroll
     for (int l = 0; l < kMaxRank; ++l) {
@@ -502,7 +575,9 @@ __global__ __launch_bounds__(64) void build_page_kernel(
       }
     }
   }
-  // sign convention: the largest |V[c][l]| (lowest c on ties) is made positive
+  // sign convention: the largest |V[c][l]| (lowest c on ties) is made positive:
+  // the largest magnitude over the item, then the lowest column holding it, its
+  // sign in the low bit
   float best_abs[kMaxRank];
 #pragma unroll
   for (int l = 0; l < kMaxRank; ++l) {
@@ -518,14 +593,10 @@ __global__ __launch_bounds__(64) void build_page_kernel(
       const float av = fabsf(vcol[l][cc]);
       if (av > best) { best = av; bidx = kC * i + cc; bval = vcol[l][cc]; }
     }
-#pragma unroll
-    for (int o = B / 2; o > 0; o >>= 1) {
-      const float ob = __shfl_xor(best, o, 64);
-      const int oi = __shfl_xor(bidx, o, 64);
-      const float ov = __shfl_xor(bval, o, 64);
-      if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; bval = ov; }
-    }
-    const float flip = bval < 0.0f ? -1.0f : 1.0f;
+    const float gbest = group_max<B>(best);
+    const int key = group_min_int<B>(best == gbest ? 2 * bidx + (bval < 0.0f ? 1 : 0) : 0x7fffffff);
+    best = gbest;
+    const float flip = (key & 1) ? -1.0f : 1.0f;
     if (i == 0) sFlip[it][l] = flip;
 #pragma unroll
     for (int cc = 0; cc < kC; ++cc) vcol[l][cc] *= flip;

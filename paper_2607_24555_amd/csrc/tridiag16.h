@@ -9,9 +9,9 @@
 //     row by A - v w^T - w v^T and keeps v_k[i] in a[k] for the back-transform.
 //  2. Eigenvalues of T by multisection on Sturm counts: the 16 lanes are split
 //     into groups of q = 16 / n lanes for the n eigenvalues wanted, each lane
-//     tests two points per step, so a group cuts its interval into 2q + 1 parts;
+//     tests one point per step, so a group cuts its interval into q + 1 parts;
 //     a wave ballot gives the part that holds the eigenvalue.  Steps continue
-//     until the Gershgorin width is cut by 2^28.
+//     until the Gershgorin width is cut by 2^22 (2^24 when all 16 are wanted).
 //  3. Eigenvectors of T for the r leading eigenvalues by inverse iteration on
 //     T - lambda I = L D L^T (lane l solves for vector l; a pivot below
 //     1.2e-7 |T| is replaced by that value, which only scales the solution),
@@ -59,6 +59,16 @@ __device__ __forceinline__ void row_sums(float (&v)[N]) {
   for (int n = 0; n < N; ++n) v[n] += dpp<0x141>(v[n]);
 #pragma unroll
   for (int n = 0; n < N; ++n) v[n] += dpp<0x140>(v[n]);
+}
+
+// f(std::integral_constant<int, N>) for the smallest N in {2, 4, 8, NMax} with
+// r <= N: loops over the r leading vectors then run at a fixed width
+template <int NMax, typename F>
+__device__ __forceinline__ void with_width(int r, F&& f) {
+  if (r <= 2) f(std::integral_constant<int, 2>{});
+  else if (r <= 4) f(std::integral_constant<int, 4>{});
+  else if (r <= 8) f(std::integral_constant<int, 8>{});
+  else f(std::integral_constant<int, NMax>{});
 }
 
 template <typename F, int... Ks>
@@ -157,34 +167,41 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
   const int lq = i / q;
   const bool idle = lq >= ne;              // lanes past ne * q copy the last group
   const int le = idle ? ne - 1 : lq;       // the eigenvalue (0 = largest)
-  const int pi = idle ? 0 : i - lq * q;    // this lane's pair of points
+  const int pi = idle ? 0 : i - lq * q;    // this lane's first point is kPts * pi
   const int want = kN - 1 - le;            // count(x) <= want  <=>  x <= lambda_le
-  const int npts = 2 * q;
+  constexpr int kPts = 1;                  // points per lane and step
+  const int npts = kPts * q;
   const int row0 = threadIdx.x & 48;
   const uint64_t gmask = ((1ull << q) - 1ull) << (row0 + le * q);
   // the Sturm counts carry rounding of a few ulp of |T|, so the interval is cut to
   // 2^-22 of its width (2^-24 when every eigenvalue is reported)
   int steps = 0;
   for (float w = 1.0f; w > (kAll ? 0x1p-24f : 0x1p-22f); w /= (float)(npts + 1)) ++steps;
-  const float fa = (float)(2 * pi + 1), fb = (float)(2 * pi + 2);
   for (int st = 0; st < steps; ++st) {
     const float h = (hi - lo) / (float)(npts + 1);
-    const float xa = fmaf(fa, h, lo), xb = fmaf(fb, h, lo);
-    float qa = 1.0f, qb = 1.0f;
-    uint32_t ca = 0, cb = 0;
+    float qv[kPts], xv[kPts];
+    uint32_t cnt[kPts];
+#pragma unroll
+    for (int pp = 0; pp < kPts; ++pp) {
+      xv[pp] = fmaf((float)(kPts * pi + pp + 1), h, lo);
+      qv[pp] = 1.0f;
+      cnt[pp] = 0;
+    }
 #pragma unroll
     for (int t = 0; t < kN; ++t) {
       // q_t = (d_t - x) - e_{t-1}^2 / q_{t-1}, counted by sign bit.  A zero pivot
       // makes the next one infinite with the opposite sign (one count either
       // way), and e^2 >= FLT_MIN keeps 0 * inf out.  The hardware reciprocal's
       // last-bit error moves only counts at x within rounding of an eigenvalue.
-      qa = fmaf(-e2[t], __builtin_amdgcn_rcpf(qa), d[t] - xa);
-      qb = fmaf(-e2[t], __builtin_amdgcn_rcpf(qb), d[t] - xb);
-      ca += __float_as_uint(qa) >> 31;
-      cb += __float_as_uint(qb) >> 31;
+#pragma unroll
+      for (int pp = 0; pp < kPts; ++pp) {
+        qv[pp] = fmaf(-e2[t], __builtin_amdgcn_rcpf(qv[pp]), d[t] - xv[pp]);
+        cnt[pp] += __float_as_uint(qv[pp]) >> 31;
+      }
     }
-    const uint64_t ma = __ballot((int)ca <= want), mb = __ballot((int)cb <= want);
-    const int nle = __popcll(ma & gmask) + __popcll(mb & gmask);
+    int nle = 0;
+#pragma unroll
+    for (int pp = 0; pp < kPts; ++pp) nle += __popcll(__ballot((int)cnt[pp] <= want) & gmask);
     const float nlo = nle > 0 ? fmaf((float)nle, h, lo) : lo;
     const float nhi = nle < npts ? fmaf((float)(nle + 1), h, lo) : hi;
     lo = nlo;
@@ -238,15 +255,25 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int l = 0; l < kMaxR; ++l) u[l] = l < r ? scratch[l * kXRow + i] : 0.0f;
+    // (right-looking: once u_m is final it is projected out of every later
+    // vector at once; each vector sees the same operations in the same order
+    // as in the left-looking loop; vectors past r are 0 and stay 0)
+    with_width<kMaxR>(r, [&](auto nc) __attribute__((always_inline)) {
+      constexpr int N = decltype(nc)::value;
+      static_for<N>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        const float nn = row_sum(u[m] * u[m]);
+        u[m] = nn > 0.0f ? u[m] * __builtin_amdgcn_rsqf(nn) : 0.0f;
+        if constexpr (m + 1 < N) {
+          float t[N - 1 - m];
 #pragma unroll
-    for (int l = 0; l < kMaxR; ++l) {
-      if (l < r) {
+          for (int l = m + 1; l < N; ++l) t[l - m - 1] = u[l] * u[m];
+          row_sums(t);
 #pragma unroll
-        for (int m = 0; m < l; ++m) u[l] = fmaf(-row_sum(u[l] * u[m]), u[m], u[l]);
-        const float nn = row_sum(u[l] * u[l]);
-        u[l] = nn > 0.0f ? u[l] * __builtin_amdgcn_rsqf(nn) : 0.0f;
-      }
-    }
+          for (int l = m + 1; l < N; ++l) u[l] = fmaf(-t[l - m - 1], u[m], u[l]);
+        }
+      });
+    });
     if (round == 0) {
       __builtin_amdgcn_wave_barrier();
 #pragma unroll
@@ -268,22 +295,16 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
   static_for<kN - 2>([&](auto kc) __attribute__((always_inline)) {
     constexpr int k = kN - 3 - decltype(kc)::value;
     const float vk = a[k];
-    float s[kMaxR];
-#pragma unroll
-    for (int l = 0; l < kMaxR; ++l) s[l] = vk * u[l];
-    if (r <= 8) {
-      float s8[8];
-#pragma unroll
-      for (int l = 0; l < 8; ++l) s8[l] = s[l];
-      row_sums(s8);
-#pragma unroll
-      for (int l = 0; l < 8; ++l) s[l] = s8[l];
-    } else {
-      row_sums(s);
-    }
     const float tk = tau[k];
+    with_width<kMaxR>(r, [&](auto nc) __attribute__((always_inline)) {
+      constexpr int N = decltype(nc)::value;
+      float s[N];
 #pragma unroll
-    for (int l = 0; l < kMaxR; ++l) u[l] = fmaf(-tk * s[l], vk, u[l]);
+      for (int l = 0; l < N; ++l) s[l] = vk * u[l];
+      row_sums(s);
+#pragma unroll
+      for (int l = 0; l < N; ++l) u[l] = fmaf(-tk * s[l], vk, u[l]);
+    });
   });
 }
 
