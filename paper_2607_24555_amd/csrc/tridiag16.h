@@ -115,10 +115,10 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
     e[k] = beta;
     tau[k] = t;
     float v[kN];
-    const float iv0 = __builtin_amdgcn_rcpf(v0);
+    const float iv0 = sig > 0.0f ? __builtin_amdgcn_rcpf(v0) : 0.0f;
     v[k + 1] = 1.0f;
 #pragma unroll
-    for (int j = k + 2; j < kN; ++j) v[j] = sig > 0.0f ? x[j] * iv0 : 0.0f;
+    for (int j = k + 2; j < kN; ++j) v[j] = x[j] * iv0;
     float vi = 0.0f, p = 0.0f;
 #pragma unroll
     for (int j = k + 1; j < kN; ++j) {
@@ -138,8 +138,8 @@ __device__ __forceinline__ void eig16(float (&a)[kN], const int i, const int r, 
     const float wi = p - kv * vi;
 #pragma unroll
     for (int j = k + 1; j < kN; ++j) {
-      const float wj = pj[j] - kv * v[j];
-      a[j] -= fmaf(vi, wj, wi * v[j]);
+      const float wj = fmaf(-kv, v[j], pj[j]);
+      a[j] = fmaf(-vi, wj, fmaf(-wi, v[j], a[j]));
     }
     a[k] = vi;  // 0 above row k + 1, 1 at row k + 1
   });
