@@ -22,7 +22,10 @@
  *    Device-resident values (page-table entries, sequence lengths) are trusted:
  *    page_table[s][j] must be a valid block for every j < ceil(seq_lens[s]/B),
  *    and seq_lens[s] <= B * max_pages_per_seq (B = page_size).  Entries past a
- *    sequence's last page are never read.
+ *    sequence's last page are never read.  With table checks on
+ *    (locks_set_table_checks) every call that takes a workspace checks them on
+ *    the device instead, clamps what is out of range and reports it in an error
+ *    word inside the workspace.
  *  - Layouts (row-major, innermost last):
  *      q           [num_seqs][num_q_heads][128]          (q_dtype)
  *      k/v cache   [num_blocks][num_kv_heads][B][128]    (kv_dtype, B = page_size)
@@ -343,6 +346,34 @@ int locks_decode_step_static(const locks_cfg_t* cfg, const void* q, const void* 
  * step that may be captured; calling it again is a no-op.  Returns LOCKS_E_HIP
  * if the stream or an event cannot be created. */
 int locks_init(void);
+
+/* Bits of the table-check error word. */
+enum {
+  LOCKS_TABLE_E_LENGTH = 1,  /* some seq_lens[s] < 0 or > B * max_pages_per_seq    */
+  LOCKS_TABLE_E_BLOCK = 2    /* some page_table[s][j], j < ceil(L / B), outside
+                                [0, num_blocks)                                   */
+};
+
+/* Table checks, the device-side guard of the tables' reads, for debugging a
+ * caller's page tables (process-wide; off by default; returns the previous
+ * setting).  While on, every call that takes a workspace (locks_select,
+ * locks_score_pages, locks_sparse_attend, locks_dense_attend and the decode
+ * steps) first runs two small kernels on its stream that copy seq_lens and the
+ * page-table rows into the workspace, clamping each length to
+ * [0, B * max_pages_per_seq] and replacing each out-of-range entry of a sequence's
+ * pages by block 0; the call's other kernels read those copies.  The OR of the
+ * LOCKS_TABLE_E_* bits over the sequences is written to the int32 at byte offset
+ * locks_table_error_offset(cfg) of the workspace, followed by one int32 per
+ * sequence; it holds the last checked call's result until the next call that
+ * uses the workspace (read it after that call completes).  Outputs of a call
+ * with a nonzero word are computed on the clamped tables and are not
+ * meaningful.  The calls without a workspace (builds, KV write, KIVI pass)
+ * are not checked. */
+int locks_set_table_checks(int32_t enable);
+
+/* Byte offset of the table-check error word in the workspace of `cfg`; (size_t)-1
+ * for an invalid configuration. */
+size_t locks_table_error_offset(const locks_cfg_t* cfg);
 
 /* Static description of a status code. */
 const char* locks_strerror(int status);

@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "liblocks.so")
 OBJ = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "build.hip", "build_page.hip", "scan.hip", "select.hip", "attend.hip", "kivi.hip", "append.hip"]
+SOURCES = ["api.hip", "build.hip", "build_page.hip", "scan.hip", "select.hip", "attend.hip", "kivi.hip",
+           "append.hip", "check.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in include/locks.h: argument validation,
 // workspace planning and stream-ordered launches.  No allocation, no
 // synchronisation, no exceptions.
+#include <atomic>
 #include <mutex>
 
 #include "locks_internal.h"
@@ -121,6 +122,27 @@ hipError_t scratch_ptr(void** out) {
   return hipSuccess;
 }
 
+// Table checks (locks_set_table_checks), process-wide.
+std::atomic<int> g_table_checks{0};
+
+// With table checks on: validates page_table / seq_lens into the workspace's
+// checked copies (clamping what is out of range, setting the error word) on `st`
+// and points the two at the copies, which every later launch of the call reads.
+int checked_tables(const locks_cfg_t& c, void* ws, const int32_t*& page_table,
+                   const int32_t*& seq_lens, hipStream_t st) {
+  if (!g_table_checks.load(std::memory_order_relaxed)) return LOCKS_OK;
+  const WsPlan p = plan_workspace(c);
+  char* b = static_cast<char*>(ws);
+  int32_t* pt = reinterpret_cast<int32_t*>(b + p.chk_pt_off);
+  int32_t* sl = reinterpret_cast<int32_t*>(b + p.chk_sl_off);
+  int32_t* err = reinterpret_cast<int32_t*>(b + p.chk_err_off);
+  const int rc = hip_status(launch_check_tables(c, page_table, seq_lens, pt, sl, err, err + 1, st));
+  if (rc) return rc;
+  page_table = pt;
+  seq_lens = sl;
+  return LOCKS_OK;
+}
+
 int check_ws(const locks_cfg_t* c, void* ws, size_t ws_bytes) {
   const WsPlan p = plan_workspace(*c);
   if (!ws || ws_bytes < p.total) return LOCKS_E_WORKSPACE;
@@ -204,6 +226,9 @@ WsPlan plan_workspace(const locks_cfg_t& c) {
   p.attn_off = take(S * Hq * (size_t)p.n_splits * (kDim + 2) * sizeof(float));
   p.slscan_off = take(S * sizeof(int32_t));
   p.partx_off = take(S * Hq * sizeof(float2));
+  p.chk_pt_off = take(S * mp * sizeof(int32_t));
+  p.chk_sl_off = take(S * sizeof(int32_t));
+  p.chk_err_off = take((S + 1) * sizeof(int32_t));
   p.total = off;
   return p;
 }
@@ -299,8 +324,10 @@ int locks_select(const locks_cfg_t* cfg, const void* q, const void* summaries,
     return LOCKS_E_INVAL;
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((rc = checked_tables(*cfg, ws, page_table, seq_lens, st))) return rc;
   return select_impl(cfg, q, summaries, page_table, seq_lens, out_page_ids, out_sel_lse,
-                     out_all_lse, ws, static_cast<hipStream_t>(stream));
+                     out_all_lse, ws, st);
 }
 
 int locks_score_pages(const locks_cfg_t* cfg, const void* q, const void* summaries,
@@ -311,10 +338,12 @@ int locks_score_pages(const locks_cfg_t* cfg, const void* q, const void* summari
   if (!q || !summaries || !page_table || !seq_lens || !out_all_lse) return LOCKS_E_INVAL;
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((rc = checked_tables(*cfg, ws, page_table, seq_lens, st))) return rc;
   const WsPlan p = plan_workspace(*cfg);
   const Ws w = carve(ws, p);
   return hip_status(launch_scan(*cfg, q, summaries, page_table, seq_lens, out_all_lse,
-                                shat_head_major(*cfg), w.part, static_cast<hipStream_t>(stream)));
+                                shat_head_major(*cfg), w.part, st));
 }
 
 int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
@@ -327,12 +356,13 @@ int locks_sparse_attend(const locks_cfg_t* cfg, const void* q, const void* k_cac
     return LOCKS_E_INVAL;
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((rc = checked_tables(*cfg, ws, page_table, seq_lens, st))) return rc;
   const WsPlan p = plan_workspace(*cfg);
   const int pps = sparse_pages_per_split(*cfg);
   const int splits = sparse_splits(*cfg);
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, page_ids,
-                                  pps, splits, carve(ws, p).attn, out, out_lse,
-                                  static_cast<hipStream_t>(stream)));
+                                  pps, splits, carve(ws, p).attn, out, out_lse, st));
 }
 
 int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cache,
@@ -343,10 +373,12 @@ int locks_dense_attend(const locks_cfg_t* cfg, const void* q, const void* k_cach
   if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !out) return LOCKS_E_INVAL;
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((rc = checked_tables(*cfg, ws, page_table, seq_lens, st))) return rc;
   const WsPlan p = plan_workspace(*cfg);
   return hip_status(launch_attend(*cfg, q, k_cache, v_cache, page_table, seq_lens, nullptr,
                                   dense_pages_per_split(*cfg), dense_splits(*cfg), carve(ws, p).attn, out,
-                                  out_lse, static_cast<hipStream_t>(stream)));
+                                  out_lse, st));
 }
 
 int locks_kivi_quantize(const locks_cfg_t* cfg, const locks_kivi_t* kivi, void* k_cache,
@@ -397,6 +429,7 @@ static int decode_step_impl(const locks_cfg_t* cfg, const locks_step_opts_t* opt
   if ((rc = check_ws(cfg, ws, ws_bytes))) return rc;
   if (cfg->num_seqs == 0) return LOCKS_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((rc = checked_tables(*cfg, ws, page_table, seq_lens, st))) return rc;
   // KIVI finalisation of the listed pages, always on the stream that builds them:
   // PRE right before their build, POST right after it; either way before the
   // attention reads them.
@@ -537,6 +570,15 @@ int locks_init(void) {
   std::lock_guard<std::mutex> lock(g_side_mu);
   SideStream* side = nullptr;
   return hip_status(side_stream(&side));
+}
+
+int locks_set_table_checks(int32_t enable) {
+  return g_table_checks.exchange(enable ? 1 : 0);
+}
+
+size_t locks_table_error_offset(const locks_cfg_t* cfg) {
+  if (validate(cfg) != LOCKS_OK) return (size_t)-1;
+  return plan_workspace(*cfg).chk_err_off;
 }
 
 const char* locks_strerror(int status) {

@@ -100,6 +100,9 @@ struct WsPlan {
   size_t attn_off;    // float [S][H_q][splits][d + 2]    split-K partials
   size_t slscan_off;  // int32 [S]                        scan lengths (overlapped builds)
   size_t partx_off;   // float2 [S][H_q]                  extra partials (overlapped builds)
+  size_t chk_pt_off;  // int32 [S][max_pages]             checked page table (table checks)
+  size_t chk_sl_off;  // int32 [S]                        checked sequence lengths
+  size_t chk_err_off; // int32 [1 + S]                    error word, then one word per sequence
   size_t total;
   int n_chunks;       // select chunks per sequence (block-level path)
   int n_splits;       // attention splits per (seq, KV head)
@@ -222,6 +225,11 @@ hipError_t launch_kivi(const locks_cfg_t& c, const locks_kivi_t& kv, void* k_cac
 
 // The newest token of every sequence (token seq_lens[s] - 1, skipped for an empty
 // sequence) copied from k_new / v_new [S][H_kv][128] into the paged caches.
+// Table checks: clamped copies of page_table and seq_lens, the per-sequence error
+// words and their OR (LOCKS_TABLE_E_* bits).
+hipError_t launch_check_tables(const locks_cfg_t& c, const int32_t* page_table,
+                               const int32_t* seq_lens, int32_t* pt_out, int32_t* sl_out,
+                               int32_t* err_word, int32_t* err_rows, hipStream_t st);
 hipError_t launch_append(const locks_cfg_t& c, const void* k_new, const void* v_new,
                          void* k_cache, void* v_cache, const int32_t* page_table,
                          const int32_t* seq_lens, hipStream_t st);

@@ -116,6 +116,8 @@ _SIGS = {
     "locks_init": (ctypes.c_int, []),
     "locks_decode_step_static": (ctypes.c_int, [ctypes.POINTER(_Cfg), _P, _P, _P, _P, _P, _P, _P,
                                                 _I, _P, _P, _P, _P, _P]),
+    "locks_set_table_checks": (ctypes.c_int, [_I]),
+    "locks_table_error_offset": (_SZ, [ctypes.POINTER(_Cfg)]),
     "locks_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "locks_last_hip_error": (ctypes.c_int, []),
 }
@@ -228,6 +230,28 @@ def _check(rc: int):
 def init():
     """locks_init: create the current device's side stream before any capture."""
     _check(lib().locks_init())
+
+
+LOCKS_TABLE_E_LENGTH = 1
+LOCKS_TABLE_E_BLOCK = 2
+
+
+def set_table_checks(enable: bool) -> bool:
+    """locks_set_table_checks: device-side checks of page_table / seq_lens in every
+    call that takes a workspace (clamped copies, error word in the workspace).
+    Returns the previous setting."""
+    return bool(lib().locks_set_table_checks(1 if enable else 0))
+
+
+def table_errors(cfg: Config, ws: torch.Tensor):
+    """The last checked call's error word (LOCKS_TABLE_E_* bits) and the per-sequence
+    words, read from the workspace (waits for the work queued on it)."""
+    c = cfg.c()
+    off = int(lib().locks_table_error_offset(ctypes.byref(c)))
+    if off == ctypes.c_size_t(-1).value:
+        raise LocksError("invalid configuration")
+    words = ws[off:off + 4 * (1 + cfg.num_seqs)].view(torch.int32).cpu()
+    return int(words[0]), [int(x) for x in words[1:]]
 
 
 def summary_payload_bytes(rank: int) -> int:

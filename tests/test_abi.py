@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 21
+    assert len(names) == 23
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGS), "binding and header disagree"
@@ -201,3 +201,19 @@ def test_append_and_step_options_are_checked(lib):
         assert lib.locks_decode_step_ex(ctypes.byref(c), ctypes.byref(o), fake, fake, fake, fake,
                                         fake, fake, None, 0, fake, fake, fake, None, fake, need,
                                         None) == -1
+
+
+def test_table_checks_switch_and_error_offset(lib):
+    """The switch returns the previous setting; the error word sits inside the
+    workspace, after every other region, with one word per sequence behind it."""
+    try:
+        assert B.set_table_checks(True) is False
+        assert B.set_table_checks(True) is True
+    finally:
+        B.set_table_checks(False)
+    c = cfg()
+    off = int(lib.locks_table_error_offset(ctypes.byref(c.c())))
+    ws = B.workspace_bytes(c)
+    assert off % 256 == 0 and off + 4 * (1 + c.num_seqs) <= ws
+    bad = cfg(rank=0)
+    assert lib.locks_table_error_offset(ctypes.byref(bad.c())) == ctypes.c_size_t(-1).value
