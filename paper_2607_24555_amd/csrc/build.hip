@@ -17,6 +17,9 @@ constexpr int kItems = 4;         // items per block
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 constexpr int kRow = 20;          // LDS row stride of A and U: 16-byte aligned, conflict-free
+constexpr int kARows = kPage + 1; // rows per item of A and U: the spare row moves the four
+                                  // items' rows to different banks
+constexpr int kKPad = 16;         // bytes after each key row: consecutive rows start 4 banks apart
 constexpr float kZeroRel = 1e-6f;
 constexpr float kZeroAbs = 1e-10f;
 
@@ -110,12 +113,13 @@ __global__ __launch_bounds__(64) void build_kernel(
   // raw key rows (bf16 or fp32 as stored; deviations are formed on the fly as
   // float(k) - mu, the same fp32 value for every use) share LDS with the Gram A
   // and the eigenvectors U, which are written once the Gram is complete
-  constexpr int kKBytes = kItems * kPage * kDim * (int)sizeof(KT);
-  constexpr int kJBytes = 2 * kItems * kPage * kRow * (int)sizeof(float);
+  constexpr int kKRow = kDim + kKPad / (int)sizeof(KT);  // key row stride (elements)
+  constexpr int kKBytes = kItems * kPage * kKRow * (int)sizeof(KT);
+  constexpr int kJBytes = 2 * kItems * kARows * kRow * (int)sizeof(float);
   __shared__ __align__(16) uint8_t sBuf[kKBytes > kJBytes ? kKBytes : kJBytes];
-  auto& sK = *reinterpret_cast<KT(*)[kItems][kPage][kDim]>(sBuf);
-  auto& sA = *reinterpret_cast<float(*)[kItems][kPage][kRow]>(sBuf);
-  auto& sU = *reinterpret_cast<float(*)[kItems][kPage][kRow]>(sBuf + kJBytes / 2);
+  auto& sK = *reinterpret_cast<KT(*)[kItems][kPage][kKRow]>(sBuf);
+  auto& sA = *reinterpret_cast<float(*)[kItems][kARows][kRow]>(sBuf);
+  auto& sU = *reinterpret_cast<float(*)[kItems][kARows][kRow]>(sBuf + kJBytes / 2);
   __shared__ float sFlip[kItems][kMaxRank];
   __shared__ float sMu[kItems][kDim];
   __shared__ float sLam[kItems][kPage];
