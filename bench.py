@@ -106,8 +106,8 @@ WORKLOADS = {
 
 # HBM traffic of the scan kernel, from two rocprofv3 counter runs of
 #   rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'locks|elementwise' -- \
-#       python bench.py --workload W --steps 4 --warmup 1 --no-dense --no-build \
-#       --no-cpu-baseline --copy-calib-mib 1024
+#       python bench.py --workload W --second none --steps 8 --warmup 2 --no-dense \
+#       --no-build --no-cpu-baseline --no-kivi-pass --copy-calib-mib 1024
 # and the same with WRITE_SIZE (KiB per dispatch; per-workload files under profiles/).
 # Each counter is divided by what it reads for the 1 GiB copy over 1 GiB, so the
 # result is in bytes.  Valid only for the scan sources these hashes name.
@@ -115,11 +115,10 @@ SCAN_SOURCES = ("paper_2607_24555_amd/csrc/scan.hip", "paper_2607_24555_amd/csrc
 SCAN_TRAFFIC = {
     # workload: (sha256 of SCAN_SOURCES, FETCH_SIZE KiB, WRITE_SIZE KiB,
     #            copy FETCH factor, copy WRITE factor, profile file)
-    "1m": ("d263b7a576261335", 55610.2, 9468.7, 0.500015, 1.0, "profiles/scan_1m_hbm_counters.md"),
-    "128k": ("d263b7a576261335", 215102.7, 8729.0, 0.500015, 1.0, "profiles/scan_128k_hbm_counters.md"),
-    "128k-r2": ("d263b7a576261335", 86759.6, 8934.0, 0.500016, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
-    "reasoning": ("d263b7a576261335", 194688.8, 22087.2, 0.500016, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
-    "32k": ("d263b7a576261335", 6774.7, 288.0, 0.500015, 1.0, "profiles/scan_32k_hbm_counters.md"),
+    "1m": ("5cf980d3016741c6", 55831.6, 8942.9, 0.500015, 1.0, "profiles/scan_1m_hbm_counters.md"),
+    "128k": ("5cf980d3016741c6", 215047.4, 8608.2, 0.500015, 1.0, "profiles/scan_128k_hbm_counters.md"),
+    "128k-r2": ("5cf980d3016741c6", 86635.7, 8653.8, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
+    "reasoning": ("5cf980d3016741c6", 194867.6, 21140.2, 0.500015, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
 }
 
 
