@@ -1733,6 +1733,8 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
     constexpr float kLn2 = 0.69314718055994531f;
     const float c0 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
 
+    // (unrolled, so the two tile buffers are named registers, not private memory)
+#pragma unroll
     for (int t = 0; t < Gm::kTiles; ++t) {
       const int page0 = pg * 64 + t * Gm::kTP;
       if (page0 >= n_c) break;
