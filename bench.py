@@ -115,10 +115,10 @@ SCAN_SOURCES = ("paper_2607_24555_amd/csrc/scan.hip", "paper_2607_24555_amd/csrc
 SCAN_TRAFFIC = {
     # workload: (sha256 of SCAN_SOURCES, FETCH_SIZE KiB, WRITE_SIZE KiB,
     #            copy FETCH factor, copy WRITE factor, profile file)
-    "1m": ("5cf980d3016741c6", 55831.6, 8942.9, 0.500015, 1.0, "profiles/scan_1m_hbm_counters.md"),
-    "128k": ("5cf980d3016741c6", 215047.4, 8608.2, 0.500015, 1.0, "profiles/scan_128k_hbm_counters.md"),
-    "128k-r2": ("5cf980d3016741c6", 86635.7, 8653.8, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
-    "reasoning": ("5cf980d3016741c6", 194867.6, 21140.2, 0.500015, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
+    "1m": ("669c498ecc466ecc", 55643.6, 9013.2, 0.500014, 1.0, "profiles/scan_1m_hbm_counters.md"),
+    "128k": ("669c498ecc466ecc", 215121.8, 8609.6, 0.500015, 1.0, "profiles/scan_128k_hbm_counters.md"),
+    "128k-r2": ("669c498ecc466ecc", 86709.8, 8658.3, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
+    "reasoning": ("669c498ecc466ecc", 194761.4, 21138.9, 0.500014, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
 }
 
 
