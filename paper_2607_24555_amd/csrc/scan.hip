@@ -1636,22 +1636,21 @@ template <int R, int B>
 struct PageRegs {
   uint4 vb[PageGeom<R, B>::kSets];
   uint4 tl[PageGeom<R, B>::kTailLoads];
-  int blk;  // lanes 0 .. kTP - 1: block of page page0 + lane (-1: none)
 };
 
+// wave_blk: lane l holds the block of the wave's page l (-1 past the sequence's
+// complete pages), read once per wave; tile t covers the wave's pages
+// t kTP .. t kTP + kTP - 1.
 template <int R, int B>
 __device__ __forceinline__ void issue_page_tile(PageRegs<R, B>& T, const uint8_t* __restrict__ summ,
-                                                const int32_t* __restrict__ pt_row, int page0,
-                                                int n_c, int H_kv, int h, int lane) {
+                                                int wave_blk, int t, int H_kv, int h, int lane) {
   using Gm = PageGeom<R, B>;
   const int col = lane & 15, grp = lane >> 4;
-  const int my_blk = (lane < Gm::kTP && page0 + lane < n_c) ? pt_row[page0 + lane] : -1;
-  T.blk = my_blk;
   const int pp = col / R, l = col % R;
 #pragma unroll
   for (int st = 0; st < Gm::kSets; ++st) {
     const int page = st * Gm::kPPS + pp;
-    const int blk = __shfl(my_blk, page < Gm::kTP ? page : 0, 64);
+    const int blk = __shfl(wave_blk, (t * Gm::kTP + (page < Gm::kTP ? page : 0)) & 63, 64);
     const bool ok = col < Gm::kPPS * R && page < Gm::kTP && blk >= 0;
     T.vb[st] = ok ? *reinterpret_cast<const uint4*>(summ + ((long)blk * H_kv + h) * Gm::kStride +
                                                     64 * l + 16 * grp)
@@ -1661,7 +1660,7 @@ __device__ __forceinline__ void issue_page_tile(PageRegs<R, B>& T, const uint8_t
   for (int u = 0; u < Gm::kTailLoads; ++u) {
     const int c = lane + 64 * u;
     const int page = c / Gm::kTailCh, off = (c % Gm::kTailCh) * 16;
-    const int blk = __shfl(my_blk, page < Gm::kTP ? page : 0, 64);
+    const int blk = __shfl(wave_blk, (t * Gm::kTP + (page < Gm::kTP ? page : 0)) & 63, 64);
     T.tl[u] = (c < Gm::kTP * Gm::kTailCh && blk >= 0)
                   ? *reinterpret_cast<const uint4*>(summ + ((long)blk * H_kv + h) * Gm::kStride +
                                                     64 * R + off)
@@ -1694,8 +1693,9 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
   const int32_t* pt_row = page_table + (long)s * max_pages;
   float run_m = -INFINITY, run_s = 0.0f;  // running normaliser of head col, log2 domain
   if (pg * 64 < n_c) {
+    const int wave_blk = pg * 64 + lane < n_c ? pt_row[pg * 64 + lane] : -1;
     PageRegs<R, B> buf[2];
-    issue_page_tile<R, B>(buf[0], summaries, pt_row, pg * 64, n_c, H_kv, h, lane);
+    issue_page_tile<R, B>(buf[0], summaries, wave_blk, 0, H_kv, h, lane);
 
     // ---- B operands: column = query head, K permuted to match the decoders
     constexpr int kPerm[8] = {0, 4, 1, 5, 2, 6, 3, 7};
@@ -1740,8 +1740,7 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
       if (page0 >= n_c) break;
       PageRegs<R, B>& cur = buf[t & 1];
       if (t + 1 < Gm::kTiles && page0 + Gm::kTP < n_c)
-        issue_page_tile<R, B>(buf[(t + 1) & 1], summaries, pt_row, page0 + Gm::kTP, n_c, H_kv, h,
-                              lane);
+        issue_page_tile<R, B>(buf[(t + 1) & 1], summaries, wave_blk, t + 1, H_kv, h, lane);
 #pragma unroll
       for (int u = 0; u < Gm::kTailLoads; ++u) {
         const int c = lane + 64 * u;
