@@ -1668,7 +1668,11 @@ __device__ __forceinline__ void issue_page_tile(PageRegs<R, B>& T, const uint8_t
   }
 }
 
-template <typename QT, int R, int B>
+// NPG: pages per stage-2 pass (16 / G when the group size G divides 16 and is
+// below 16: the 16 MFMA columns then hold (page, head) pairs, the K axis runs over
+// (page, basis column) and each page's coefficients meet only its own
+// projections; 1: the heads are the columns, any G <= 16).
+template <typename QT, int R, int B, int NPG = 1>
 __global__ __launch_bounds__(256) void scan_page_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q,
     const uint8_t* __restrict__ summaries, const int32_t* __restrict__ page_table,
@@ -1793,65 +1797,121 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
       }
       __builtin_amdgcn_wave_barrier();
 
-      // ---- stage 2, one page at a time: z[token][head] over B / 16 row tiles
-      for (int p = 0; p < Gm::kTP; ++p) {
-        if (page0 + p >= n_c) break;
-        float z[kRT][4];
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-          f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-          for (int kstep = 0; kstep < kKS; ++kstep) {
-            const int l = 4 * kstep + grp;
-            const int tok = 16 * rt + col;
-            const float a = l < R ? (float)((int)sTail[wave][p][tok * R + l] - 128) : 0.0f;
-            const float b = (l < R && col < G) ? sP[wave][p][l < R ? l : 0][col] : 0.0f;
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+      if constexpr (NPG == 1) {
+        // ---- stage 2, one page at a time: z[token][head] over B / 16 row tiles
+        for (int p = 0; p < Gm::kTP; ++p) {
+          if (page0 + p >= n_c) break;
+          float z[kRT][4];
+  #pragma unroll
+          for (int rt = 0; rt < kRT; ++rt) {
+            f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  #pragma unroll
+            for (int kstep = 0; kstep < kKS; ++kstep) {
+              const int l = 4 * kstep + grp;
+              const int tok = 16 * rt + col;
+              const float a = l < R ? (float)((int)sTail[wave][p][tok * R + l] - 128) : 0.0f;
+              const float b = (l < R && col < G) ? sP[wave][p][l < R ? l : 0][col] : 0.0f;
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+            }
+            const uint2 csw = *reinterpret_cast<const uint2*>(
+                &sTail[wave][p][Gm::kSc + 2 * (R + 16 * rt + 4 * grp)]);
+            const h2 cs01 = as_h2(csw.x), cs23 = as_h2(csw.y);
+            const float av = sA[wave][p][col];
+            z[rt][0] = fmaf((float)cs01.x * c0, acc[0], av);
+            z[rt][1] = fmaf((float)cs01.y * c0, acc[1], av);
+            z[rt][2] = fmaf((float)cs23.x * c0, acc[2], av);
+            z[rt][3] = fmaf((float)cs23.y * c0, acc[3], av);
           }
-          const uint2 csw = *reinterpret_cast<const uint2*>(
-              &sTail[wave][p][Gm::kSc + 2 * (R + 16 * rt + 4 * grp)]);
-          const h2 cs01 = as_h2(csw.x), cs23 = as_h2(csw.y);
-          const float av = sA[wave][p][col];
-          z[rt][0] = fmaf((float)cs01.x * c0, acc[0], av);
-          z[rt][1] = fmaf((float)cs01.y * c0, acc[1], av);
-          z[rt][2] = fmaf((float)cs23.x * c0, acc[2], av);
-          z[rt][3] = fmaf((float)cs23.y * c0, acc[3], av);
+          float mx = -INFINITY;
+  #pragma unroll
+          for (int rt = 0; rt < kRT; ++rt)
+            mx = fmaxf(mx, fmaxf(fmaxf(z[rt][0], z[rt][1]), fmaxf(z[rt][2], z[rt][3])));
+          mx = red4_max(mx);
+          float sm = 0.0f;
+  #pragma unroll
+          for (int rt = 0; rt < kRT; ++rt)
+  #pragma unroll
+            for (int jj = 0; jj < 4; ++jj) sm += __builtin_amdgcn_exp2f(z[rt][jj] - mx);
+          sm = red4_sum(sm);
+          const float s2 = mx + __builtin_amdgcn_logf(sm);  // log2-domain page score
+          if (col < G) {
+            if (grp == 0)
+              s_hat[lay.base(s, h) + col * lay.head + (long)(page0 + p) * lay.page] = s2 * kLn2;
+            const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+            if (s2 > run_m) { run_s = fmaf(run_s, e, 1.0f); run_m = s2; }
+            else run_s += e;
+          }
         }
-        float mx = -INFINITY;
+      } else {
+        // ---- stage 2, NPG pages at a time: z[token][(page pc, head gc)]
+        constexpr int kG = 16 / NPG;
+        const int pc = col / kG, gc = col % kG;
 #pragma unroll
-        for (int rt = 0; rt < kRT; ++rt)
-          mx = fmaxf(mx, fmaxf(fmaxf(z[rt][0], z[rt][1]), fmaxf(z[rt][2], z[rt][3])));
-        mx = red4_max(mx);
-        float sm = 0.0f;
+        for (int p0 = 0; p0 < Gm::kTP; p0 += NPG) {
+          if (page0 + p0 >= n_c) break;
+          float z[kRT][4];
 #pragma unroll
-        for (int rt = 0; rt < kRT; ++rt)
+          for (int rt = 0; rt < kRT; ++rt) {
+            f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            const int tok = 16 * rt + col;
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) sm += __builtin_amdgcn_exp2f(z[rt][jj] - mx);
-        sm = red4_sum(sm);
-        const float s2 = mx + __builtin_amdgcn_logf(sm);  // log2-domain page score
-        if (col < G) {
-          if (grp == 0)
-            s_hat[lay.base(s, h) + col * lay.head + (long)(page0 + p) * lay.page] = s2 * kLn2;
-          const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
-          if (s2 > run_m) { run_s = fmaf(run_s, e, 1.0f); run_m = s2; }
-          else run_s += e;
+            for (int pp = 0; pp < NPG; ++pp)
+#pragma unroll
+              for (int kstep = 0; kstep < kKS; ++kstep) {
+                const int l = 4 * kstep + grp;
+                const int la = l < R ? l : 0;
+                const float a = l < R ? (float)((int)sTail[wave][p0 + pp][tok * R + la] - 128) : 0.0f;
+                const float b = (l < R && pc == pp) ? sP[wave][p0 + pp][la][gc] : 0.0f;
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+              }
+            const uint2 csw = *reinterpret_cast<const uint2*>(
+                &sTail[wave][p0 + pc][Gm::kSc + 2 * (R + 16 * rt + 4 * grp)]);
+            const h2 cs01 = as_h2(csw.x), cs23 = as_h2(csw.y);
+            const float av = sA[wave][p0 + pc][gc];
+            z[rt][0] = fmaf((float)cs01.x * c0, acc[0], av);
+            z[rt][1] = fmaf((float)cs01.y * c0, acc[1], av);
+            z[rt][2] = fmaf((float)cs23.x * c0, acc[2], av);
+            z[rt][3] = fmaf((float)cs23.y * c0, acc[3], av);
+          }
+          float mx = -INFINITY;
+#pragma unroll
+          for (int rt = 0; rt < kRT; ++rt)
+            mx = fmaxf(mx, fmaxf(fmaxf(z[rt][0], z[rt][1]), fmaxf(z[rt][2], z[rt][3])));
+          mx = red4_max(mx);
+          float sm = 0.0f;
+#pragma unroll
+          for (int rt = 0; rt < kRT; ++rt)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) sm += __builtin_amdgcn_exp2f(z[rt][jj] - mx);
+          sm = red4_sum(sm);
+          const float s2 = mx + __builtin_amdgcn_logf(sm);  // log2-domain page score
+          if (page0 + p0 + pc < n_c) {
+            if (grp == 0)
+              s_hat[lay.base(s, h) + gc * lay.head + (long)(page0 + p0 + pc) * lay.page] = s2 * kLn2;
+            const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
+            if (s2 > run_m) { run_s = fmaf(run_s, e, 1.0f); run_m = s2; }
+            else run_s += e;
+          }
         }
       }
       __builtin_amdgcn_wave_barrier();
     }
   }
-  // ---- block partial (max, sum exp) per head over its pages (log2 domain)
+  // ---- block partial (max, sum exp) per head over its pages (log2 domain):
+  //      head g's running pairs sit in the columns p G + g, p < NPG, of every wave
   if (lane < 16) sRun[wave][lane] = make_float2(run_m, run_s);
   __syncthreads();
   if (threadIdx.x < G) {
     const int g = threadIdx.x;
     float m = -INFINITY, l = 0.0f;
-    for (int w = 0; w < 4; ++w) m = fmaxf(m, sRun[w][g].x);
+    for (int w = 0; w < 4; ++w)
+      for (int p = 0; p < NPG; ++p) m = fmaxf(m, sRun[w][p * G + g].x);
     if (m > -INFINITY)
-      for (int w = 0; w < 4; ++w) {
-        const float2 v = sRun[w][g];
-        if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
-      }
+      for (int w = 0; w < 4; ++w)
+        for (int p = 0; p < NPG; ++p) {
+          const float2 v = sRun[w][p * G + g];
+          if (v.y > 0.0f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+        }
     partials[(row0 + g) * gridDim.x + blockIdx.x] = make_float2(m, l);
   }
 }
@@ -1871,6 +1931,21 @@ hipError_t dispatch_scan_page(int r, int B, dim3 grid, hipStream_t st, int H_q, 
                          max_pages, q, sum, pt, sl, s_hat, lay, part);                       \
     break;
   if (B != 32 && B != 64) return hipErrorInvalidValue;
+  // four-head groups at the common ranks: four pages per stage-2 pass
+  if (H_q == 4 * H_kv && (r == 2 || r == 4 || r == 8)) {
+#define LOCKS_SCAN_PAGE4(RR)                                                                  \
+    if (r == RR) {                                                                           \
+      if (B == 32)                                                                           \
+        hipLaunchKernelGGL((scan_page_kernel<QT, RR, 32, 4>), grid, dim3(256), 0, st, H_q,   \
+                           H_kv, max_pages, q, sum, pt, sl, s_hat, lay, part);               \
+      else                                                                                   \
+        hipLaunchKernelGGL((scan_page_kernel<QT, RR, 64, 4>), grid, dim3(256), 0, st, H_q,   \
+                           H_kv, max_pages, q, sum, pt, sl, s_hat, lay, part);               \
+      return hipGetLastError();                                                              \
+    }
+    LOCKS_SCAN_PAGE4(2) LOCKS_SCAN_PAGE4(4) LOCKS_SCAN_PAGE4(8)
+#undef LOCKS_SCAN_PAGE4
+  }
   switch (r) {
     LOCKS_SCAN_PAGE_CASE(1) LOCKS_SCAN_PAGE_CASE(2) LOCKS_SCAN_PAGE_CASE(3)
     LOCKS_SCAN_PAGE_CASE(4) LOCKS_SCAN_PAGE_CASE(5) LOCKS_SCAN_PAGE_CASE(6)
