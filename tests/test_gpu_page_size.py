@@ -119,6 +119,9 @@ STEP = {
     "B64-G2-r15-fp32q": (64, 2, 2, 2, [64 * 300 + 33, 17], 15, 1024, "bf16", "fp32"),
     "B32-G4-r8-fp32kv": (32, 2, 4, 2, [32 * 350 + 1, 0], 8, 256, "fp32", "bf16"),
     "B64-b256": (64, 2, 4, 2, [64 * 200 + 11, 64 * 3 + 5], 8, 256, "bf16", "bf16"),
+    # four pages per stage-2 pass (four-head groups) at the other ranks and fp32 q
+    "B32-G4-r2-fp32q": (32, 2, 4, 2, [32 * 300 + 7, 32 * 40], 2, 1024, "bf16", "fp32"),
+    "B64-G4-r4": (64, 2, 4, 2, [64 * 150 + 3, 64 * 30], 4, 1024, "bf16", "bf16"),
 }
 
 
