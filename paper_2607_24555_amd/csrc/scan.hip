@@ -1677,7 +1677,7 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q,
     const uint8_t* __restrict__ summaries, const int32_t* __restrict__ page_table,
     const int32_t* __restrict__ seq_lens, float* __restrict__ s_hat, SHatLayout lay,
-    float2* __restrict__ partials) {
+    float2* __restrict__ partials, int wave_pages) {
   using Gm = PageGeom<R, B>;
   constexpr bool kSplitQ = sizeof(QT) == 4;  // fp32 queries: f16 hi + lo
   constexpr int kKS = (R + 3) / 4;           // stage-2 k-steps
@@ -1692,12 +1692,13 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
   const int h = blockIdx.y, s = blockIdx.z;
   const int G = H_q / H_kv;
   const int n_c = seq_lens[s] / B;
-  const int pg = scan_chunk() * 4 + wave;  // 64-page group of this wave
+  // pages wave_pages (16, 32 or 64) from `base` are this wave's
+  const int base = (scan_chunk() * 4 + wave) * wave_pages;
   const long row0 = (long)s * H_q + (long)h * G;
   const int32_t* pt_row = page_table + (long)s * max_pages;
   float run_m = -INFINITY, run_s = 0.0f;  // running normaliser of head col, log2 domain
-  if (pg * 64 < n_c) {
-    const int wave_blk = pg * 64 + lane < n_c ? pt_row[pg * 64 + lane] : -1;
+  if (base < n_c) {
+    const int wave_blk = lane < wave_pages && base + lane < n_c ? pt_row[base + lane] : -1;
     PageRegs<R, B> buf[2];
     issue_page_tile<R, B>(buf[0], summaries, wave_blk, 0, H_kv, h, lane);
 
@@ -1740,10 +1741,10 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
     // (unrolled, so the two tile buffers are named registers, not private memory)
 #pragma unroll
     for (int t = 0; t < Gm::kTiles; ++t) {
-      const int page0 = pg * 64 + t * Gm::kTP;
-      if (page0 >= n_c) break;
+      const int page0 = base + t * Gm::kTP;
+      if (t * Gm::kTP >= wave_pages || page0 >= n_c) break;
       PageRegs<R, B>& cur = buf[t & 1];
-      if (t + 1 < Gm::kTiles && page0 + Gm::kTP < n_c)
+      if (t + 1 < Gm::kTiles && (t + 1) * Gm::kTP < wave_pages && page0 + Gm::kTP < n_c)
         issue_page_tile<R, B>(buf[(t + 1) & 1], summaries, wave_blk, t + 1, H_kv, h, lane);
 #pragma unroll
       for (int u = 0; u < Gm::kTailLoads; ++u) {
@@ -1918,17 +1919,17 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
 
 
 template <typename QT>
-hipError_t dispatch_scan_page(int r, int B, dim3 grid, hipStream_t st, int H_q, int H_kv,
+hipError_t dispatch_scan_page(int r, int B, int wp, dim3 grid, hipStream_t st, int H_q, int H_kv,
                               int max_pages, const QT* q, const uint8_t* sum, const int32_t* pt,
                               const int32_t* sl, float* s_hat, SHatLayout lay, float2* part) {
 #define LOCKS_SCAN_PAGE_CASE(RR)                                                              \
   case RR:                                                                                   \
     if (B == 32)                                                                             \
       hipLaunchKernelGGL((scan_page_kernel<QT, RR, 32>), grid, dim3(256), 0, st, H_q, H_kv,  \
-                         max_pages, q, sum, pt, sl, s_hat, lay, part);                       \
+                         max_pages, q, sum, pt, sl, s_hat, lay, part, wp);                   \
     else                                                                                     \
       hipLaunchKernelGGL((scan_page_kernel<QT, RR, 64>), grid, dim3(256), 0, st, H_q, H_kv,  \
-                         max_pages, q, sum, pt, sl, s_hat, lay, part);                       \
+                         max_pages, q, sum, pt, sl, s_hat, lay, part, wp);                   \
     break;
   if (B != 32 && B != 64) return hipErrorInvalidValue;
   // four-head groups at the common ranks: four pages per stage-2 pass
@@ -1937,10 +1938,10 @@ hipError_t dispatch_scan_page(int r, int B, dim3 grid, hipStream_t st, int H_q, 
     if (r == RR) {                                                                           \
       if (B == 32)                                                                           \
         hipLaunchKernelGGL((scan_page_kernel<QT, RR, 32, 4>), grid, dim3(256), 0, st, H_q,   \
-                           H_kv, max_pages, q, sum, pt, sl, s_hat, lay, part);               \
+                           H_kv, max_pages, q, sum, pt, sl, s_hat, lay, part, wp);           \
       else                                                                                   \
         hipLaunchKernelGGL((scan_page_kernel<QT, RR, 64, 4>), grid, dim3(256), 0, st, H_q,   \
-                           H_kv, max_pages, q, sum, pt, sl, s_hat, lay, part);               \
+                           H_kv, max_pages, q, sum, pt, sl, s_hat, lay, part, wp);           \
       return hipGetLastError();                                                              \
     }
     LOCKS_SCAN_PAGE4(2) LOCKS_SCAN_PAGE4(4) LOCKS_SCAN_PAGE4(8)
@@ -2049,7 +2050,16 @@ static int r8_steps(const locks_cfg_t& c) {
   return blocks4 < 256 ? 1 : 4;
 }
 
+// Pages per wave of the 32/64-token scan: 64, or 32 / 16 when 64 would leave
+// fewer than two waves per SIMD of the GPU (1,024 SIMDs).
+static int page_wave_pages(const locks_cfg_t& c) {
+  for (int wp = 64; wp > 16; wp /= 2)
+    if ((long)((c.max_pages_per_seq + wp - 1) / wp) * c.num_kv_heads * c.num_seqs >= 2048) return wp;
+  return 16;
+}
+
 int scan_pages_per_block(const locks_cfg_t& c) {
+  if (c.page_size != kPage) return 4 * page_wave_pages(c);
   if (use_r8_kernel(c) || use_r8g4_kernel(c)) return 64 * r8_steps(c);
   return kScanPagesPerBlock;
 }
@@ -2063,11 +2073,13 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
   const int steps = r8_steps(c);
   if (c.page_size != kPage) {
     if (c.q_dtype == LOCKS_BF16)
-      return dispatch_scan_page(c.rank, c.page_size, grid, st, c.num_q_heads, c.num_kv_heads,
+      return dispatch_scan_page(c.rank, c.page_size, page_wave_pages(c), grid, st, c.num_q_heads,
+                                c.num_kv_heads,
                                 c.max_pages_per_seq, static_cast<const uint16_t*>(q),
                                 static_cast<const uint8_t*>(summaries), page_table, seq_lens,
                                 s_hat, lay, partials);
-    return dispatch_scan_page(c.rank, c.page_size, grid, st, c.num_q_heads, c.num_kv_heads,
+    return dispatch_scan_page(c.rank, c.page_size, page_wave_pages(c), grid, st, c.num_q_heads,
+                              c.num_kv_heads,
                               c.max_pages_per_seq, static_cast<const float*>(q),
                               static_cast<const uint8_t*>(summaries), page_table, seq_lens, s_hat,
                               lay, partials);
