@@ -835,6 +835,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   constexpr int G = 16;
   __shared__ __align__(16) uint8_t sTail[4][16][Gm::kTail];
   __shared__ float2 sRun[4][64];
+  __shared__ __align__(16) float sVsc[4][16][R];   // basis column scales x the query scale
+  __shared__ __align__(16) float sCsc[4][16][16];  // coefficient row scales
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
@@ -899,6 +901,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   #pragma unroll
           for (int u = 0; u < Gm::kTailLoads; ++u) tl[u] = bld16(rs, nx.tl[u]);
         }
+        // the step's scales in fp32, once for its four quads: basis column scales
+        // times the query scale, coefficient row scales
+  #pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int e = lane + 64 * u, pgi = e >> 3, l = e & 7;
+          sVsc[wave][pgi][l] = lds_f16(&sTail[wave][pgi][Gm::kSc + 2 * l]) * QD.inv_scale;
+        }
+  #pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = lane + 64 * u, pgi = e >> 4, t2 = e & 15;
+          sCsc[wave][pgi][t2] = lds_f16(&sTail[wave][pgi][Gm::kSc + 2 * (R + t2)]);
+        }
+        __builtin_amdgcn_wave_barrier();
 
         // ---- centroid term: areg[j] = a(page 4 j + grp, head col)
         float areg[4];
@@ -952,8 +967,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
               for (int j = 0; j < 4; ++j) {
                 const int st = 2 * Q + i;
                 const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
-                const float vs = lds_f16(&sTail[wave][page][Gm::kSc + 2 * l]);
-                vals[4 * i + j] = (float)acc[i][j] * (vs * QD.inv_scale);
+                vals[4 * i + j] = (float)acc[i][j] * sVsc[wave][page][l];
               }
           }
           // ---- stage 2 for the quad, then the page LSE in registers
@@ -981,13 +995,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
             acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bh, acc, 0, 0, 0);
             acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, bl, acc, 0, 0, 0);
-            const uint2 csw = *reinterpret_cast<const uint2*>(
-                &sTail[wave][4 * Q + grp][Gm::kSc + 2 * (R + 4 * ps)]);
-            const h2 c01 = as_h2(csw.x), c23 = as_h2(csw.y);
-            z[4 * ps + 0] = (float)c01.x * acc[0];
-            z[4 * ps + 1] = (float)c01.y * acc[1];
-            z[4 * ps + 2] = (float)c23.x * acc[2];
-            z[4 * ps + 3] = (float)c23.y * acc[3];
+            const float4 cs4 = *reinterpret_cast<const float4*>(&sCsc[wave][4 * Q + grp][4 * ps]);
+            z[4 * ps + 0] = cs4.x * acc[0];
+            z[4 * ps + 1] = cs4.y * acc[1];
+            z[4 * ps + 2] = cs4.z * acc[2];
+            z[4 * ps + 3] = cs4.w * acc[3];
           }
           // z are the logits minus the centroid logit a.  The deviations of a
           // page's tokens sum to ~0 (the coefficient columns are orthogonal to
