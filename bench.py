@@ -115,10 +115,10 @@ SCAN_SOURCES = ("paper_2607_24555_amd/csrc/scan.hip", "paper_2607_24555_amd/csrc
 SCAN_TRAFFIC = {
     # workload: (sha256 of SCAN_SOURCES, FETCH_SIZE KiB, WRITE_SIZE KiB,
     #            copy FETCH factor, copy WRITE factor, profile file)
-    "1m": ("669c498ecc466ecc", 55643.6, 9013.2, 0.500014, 1.0, "profiles/scan_1m_hbm_counters.md"),
-    "128k": ("669c498ecc466ecc", 215121.8, 8609.6, 0.500015, 1.0, "profiles/scan_128k_hbm_counters.md"),
-    "128k-r2": ("669c498ecc466ecc", 86709.8, 8658.3, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
-    "reasoning": ("669c498ecc466ecc", 194761.4, 21138.9, 0.500014, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
+    "1m": ("a84df8b8ac672bf6", 55720.5, 8960.9, 0.500016, 1.0, "profiles/scan_1m_hbm_counters.md"),
+    "128k": ("a84df8b8ac672bf6", 215028.0, 8603.3, 0.500014, 1.0, "profiles/scan_128k_hbm_counters.md"),
+    "128k-r2": ("a84df8b8ac672bf6", 86630.4, 8650.4, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
+    "reasoning": ("a84df8b8ac672bf6", 194864.1, 21137.4, 0.500015, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
 }
 
 
