@@ -103,6 +103,22 @@ __device__ __forceinline__ float lds_f16(const uint8_t* p) {
   return (float)*reinterpret_cast<const _Float16*>(p);
 }
 
+// Log-sum-exp, log2 domain, over lanes {l, l ^ 16} (V = 2) or {l, l ^ 16, l ^ 32,
+// l ^ 48} (V = 4); each of those lanes gets the same bits.
+template <int V>
+__device__ __forceinline__ float merge_sub_lse(float v) {
+  auto lse2 = [](float a, float b) {
+    const float mx = fmaxf(a, b);
+    return mx + __builtin_amdgcn_logf(__builtin_amdgcn_exp2f(a - mx) + __builtin_amdgcn_exp2f(b - mx));
+  };
+  if (V == 4) {
+    auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = lse2(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  }
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return lse2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // Reduction over the four lanes {l, l^16, l^32, l^48} with two VALU lane swaps.
 __device__ __forceinline__ float red4_max(float v) {
   auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -765,40 +781,62 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // Byte offsets of what this lane loads from the records of the 16 pages whose
 // blocks lanes 0..15 hold in `blk`: its basis slice of each set and its record
 // tail chunks.  All the lane exchanges of a step are issued together.
-template <int R>
+//
+// Pages of 16 V tokens (V = 2, 4) are scanned as V consecutive 16-token
+// sub-pages.  A step then covers 16 / V pages, so only R / V basis sets are
+// loaded, and the tail of sub-page u is assembled in the 16-token layout: its
+// 16 coefficient rows (16 u .. 16 u + 15), the page's centroid, the basis
+// scales, its 16 coefficient row scales and the centroid scale.
+template <int R, int V = 1>
 struct StepOffs {
-  uint32_t vb[FastGeom<R>::kSets];
+  uint32_t vb[FastGeom<R>::kSets / V];
   uint32_t tl[FastGeom<R>::kTailLoads];
 };
 
-template <int R>
-__device__ __forceinline__ StepOffs<R> step_offsets(int blk, uint32_t blk_bytes, uint32_t head_off,
-                                                    int lane) {
+// Offset inside a record of 16 V-token pages of tail chunk o (16-token layout)
+// of sub-page u.
+template <int R, int V>
+__device__ __forceinline__ uint32_t sub_tail_off(int o, int u) {
+  static_assert(V == 1 || R == 8, "sub-pages assume one 16-byte chunk of basis scales");
+  constexpr int kCoef = 64 * R, kMu = kCoef + 16 * V * R, kSc = kMu + kDim;
+  if (V == 1) return kCoef + 16 * o;
+  if (o < R) return kCoef + 16 * R * u + 16 * o;                  // coefficient rows
+  if (o < R + 8) return kMu + 16 * (o - R);                        // centroid
+  if (o == R + 8) return kSc;                                      // basis scales
+  if (o < R + 11) return kSc + 2 * R + 32 * u + 16 * (o - R - 9);  // coefficient row scales
+  return kSc + 2 * R + 32 * V;                                     // centroid scale
+}
+
+template <int R, int V = 1>
+__device__ __forceinline__ StepOffs<R, V> step_offsets(int blk, uint32_t blk_bytes,
+                                                       uint32_t head_off, int lane) {
   using Gm = FastGeom<R>;
   const int col = lane & 15, grp = lane >> 4;
   const int qs = 4 * (col & 3) + (col >> 2);
-  StepOffs<R> o;
+  StepOffs<R, V> o;
 #pragma unroll
-  for (int st = 0; st < Gm::kSets; ++st) {
-    const int b = __shfl(blk, st * Gm::kPPS + qs / R, 64);
+  for (int st = 0; st < Gm::kSets / V; ++st) {
+    const int b = __shfl(blk, (st * Gm::kPPS + qs / R) * V, 64);
     o.vb[st] = rec_off(b, blk_bytes, head_off) + 64u * (qs % R) + 16u * grp;
   }
 #pragma unroll
   for (int u = 0; u < Gm::kTailLoads; ++u) {
     int c = lane + 64 * u;
     c = c < 16 * Gm::kTailCh ? c : 16 * Gm::kTailCh - 1;
-    const int b = __shfl(blk, c / Gm::kTailCh, 64);
-    o.tl[u] = rec_off(b, blk_bytes, head_off) + 64u * R + (c % Gm::kTailCh) * 16;
+    const int sp = c / Gm::kTailCh;
+    const int b = __shfl(blk, sp, 64);
+    o.tl[u] = rec_off(b, blk_bytes, head_off) + sub_tail_off<R, V>(c % Gm::kTailCh, sp % V);
   }
   return o;
 }
 
-// Physical block of page page0 + (lane & 15); lanes past the end of the
+// Physical block of (sub-)page page0 + (lane & 15); lanes past the end of the
 // sequence take page0's block (a valid record that is loaded but not used).
+template <int V = 1>
 __device__ __forceinline__ int lane_block(const int32_t* __restrict__ pt_row, int page0, int n_c,
                                           int lane) {
   const int pl = page0 + (lane & 15);
-  return pt_row[pl < n_c ? pl : page0];
+  return pt_row[(pl < n_c ? pl : page0) / V];
 }
 
 template <int N>
@@ -825,7 +863,13 @@ struct IntTag {
 // ---------------------------------------------------------------------------
 // 16-page steps per wave (a block covers 4 x 16 x kSteps pages): 4 for large
 // grids, 1 when four steps would leave most compute units idle.
-template <typename QT, int kSteps>
+//
+// Pages of 16 V tokens (V = 2, 4) run as V sub-pages each (see StepOffs): a
+// step's 16 sub-pages are 16 / V pages, stage 1 runs once per page (R / V basis
+// sets per step, in pairs), and the V sub-page LSEs of a page, which sit in
+// lanes l, l ^ 16 (and l ^ 32, l ^ 48), are merged before the page's s_hat is
+// stored and counted in the normaliser.
+template <typename QT, int kSteps, int V = 1>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
     uint32_t summ_bytes, const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
@@ -841,31 +885,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = blockIdx.y, s = blockIdx.z;
-  const int n_c = seq_lens[s] / kPage;
+  const int n_c = seq_lens[s] / (kPage * V) * V;  // sub-pages of the complete pages
   const int pg = scan_chunk() * 4 + wave;
   const long row0 = (long)s * H_q + (long)h * G;
   const int32_t* pt_row = page_table + (long)s * max_pages;
   float run_m = -INFINITY, run_s = 0.0f;
 
   constexpr int kWavePages = 16 * kSteps;
+  constexpr uint32_t kRecStride = rec_stride(R, 0, kPage * V);
+  constexpr int kSetsV = Gm::kSets / V;  // basis sets per step
   if (pg * kWavePages < n_c) {
     const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
-    const uint32_t blk_bytes = (uint32_t)H_kv * (uint32_t)Gm::kStride, head_off = (uint32_t)h * Gm::kStride;
+    const uint32_t blk_bytes = (uint32_t)H_kv * kRecStride, head_off = (uint32_t)h * kRecStride;
     const int first = pg * kWavePages;
     const int n_steps = min(kSteps, (n_c - first + 15) / 16);
-    uint4 vb[Gm::kSets];
+    uint4 vb[kSetsV];
     uint4 tl[Gm::kTailLoads];
     // the record slices of the step whose pages' blocks lanes 0..15 hold in blk
     auto load_step = [&](int blk) {
-      const StepOffs<R> o0 = step_offsets<R>(blk, blk_bytes, head_off, lane);
+      const StepOffs<R, V> o0 = step_offsets<R, V>(blk, blk_bytes, head_off, lane);
 #pragma unroll
-      for (int st = 0; st < Gm::kSets; ++st) vb[st] = bld16(rs, o0.vb[st]);
+      for (int st = 0; st < kSetsV; ++st) vb[st] = bld16(rs, o0.vb[st]);
 #pragma unroll
       for (int u = 0; u < Gm::kTailLoads; ++u) tl[u] = bld16(rs, o0.tl[u]);
     };
     QDigits QD;  // formed once the first step's loads are in flight
     const int a_row = col >> 2, t_row = col & 3;  // A row of this lane: (page, token)
     float* shat_base = s_hat + lay.base(s, h) + (long)col * lay.head;
+    i4v pacc[2];  // stage-1 results of the current pair of basis sets
 
     // kN consecutive steps from page `start` whose first step's slices are
     // loaded (blk_n1: blocks of the second step's pages), fully unrolled so
@@ -877,9 +924,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int t = 0; t < kN; ++t) {
         const int page0 = start + 16 * t;
         const bool more = t + 1 < kN;
-        const int blk_n2 = t + 2 < kN ? lane_block(pt_row, page0 + 32, n_c, lane) : 0;
-        StepOffs<R> nx;
-        if (more) nx = step_offsets<R>(blk_n1, blk_bytes, head_off, lane);
+        const int blk_n2 = t + 2 < kN ? lane_block<V>(pt_row, page0 + 32, n_c, lane) : 0;
+        StepOffs<R, V> nx;
+        if (more) nx = step_offsets<R, V>(blk_n1, blk_bytes, head_off, lane);
         // ---- record tails to LDS; coefficient rows reordered to l = 0,4,1,5,2,6,3,7
   #pragma unroll
         for (int u = 0; u < Gm::kTailLoads; ++u) {
@@ -949,25 +996,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   #pragma unroll
         for (int Q = 0; Q < 4; ++Q) {
           __builtin_amdgcn_sched_barrier(0);
-          // ---- stage 1 (int8 MFMA) for basis sets 2Q, 2Q+1:
-          //      vals[4 i + j] = p(page 4 Q + 2 i + j / 2, l = 4 (j % 2) + grp)
+          // ---- stage 1 (int8 MFMA), basis sets 2 m, 2 m + 1 for pair m = Q / V
+          //      (register j of set st: p(page 2 st + j / 2, l = 4 (j % 2) + grp));
+          //      vals[4 i + j] = p(sub-page 4 Q + 2 i + j / 2, l = 4 (j % 2) + grp)
           float vals[8];
           {
-            i4v a0[2], a1[2], acc[2];
-            nib_operands(vb[2 * Q], a0);
-            nib_operands(vb[2 * Q + 1], a1);
-            proj_horner2(a0, a1, QD, acc[0], acc[1]);
-            if (more) {
-              vb[2 * Q] = bld16(rs, nx.vb[2 * Q]);
-              vb[2 * Q + 1] = bld16(rs, nx.vb[2 * Q + 1]);
+            const int m = Q / V;
+            if (Q % V == 0) {
+              i4v a0[2], a1[2];
+              nib_operands(vb[2 * m], a0);
+              nib_operands(vb[2 * m + 1], a1);
+              proj_horner2(a0, a1, QD, pacc[0], pacc[1]);
+              if (more) {
+                vb[2 * m] = bld16(rs, nx.vb[2 * m]);
+                vb[2 * m + 1] = bld16(rs, nx.vb[2 * m + 1]);
+              }
             }
   #pragma unroll
             for (int i = 0; i < 2; ++i)
   #pragma unroll
               for (int j = 0; j < 4; ++j) {
-                const int st = 2 * Q + i;
-                const int page = 2 * st + j / 2, l = 4 * (j % 2) + grp;
-                vals[4 * i + j] = (float)acc[i][j] * sVsc[wave][page][l];
+                const int sp = 4 * Q + 2 * i + j / 2, pv = sp / V, l = 4 * (j % 2) + grp;
+                vals[4 * i + j] = (float)pacc[pv / 2 - 2 * m][2 * (pv % 2) + j % 2] * sVsc[wave][sp][l];
               }
           }
           // ---- stage 2 for the quad, then the page LSE in registers
@@ -1017,10 +1067,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   #pragma unroll
             for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i] - shift);
           }
-          const float s2 = areg[Q] + shift + __builtin_amdgcn_logf(sm);
-          const int page = page0 + 4 * Q + grp;
-          const bool live = page < n_c;
-          if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
+          float s2 = areg[Q] + shift + __builtin_amdgcn_logf(sm);
+          const int sub = page0 + 4 * Q + grp;
+          const bool live = sub < n_c && grp % V == 0;
+          if (V > 1) s2 = merge_sub_lse<V>(s2);
+          if (live) shat_base[(long)(sub / V) * lay.page] = s2 * 0.69314718055994531f;
           const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
           const bool up = s2 > run_m;
           const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
@@ -1032,15 +1083,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
     };
     if (n_steps == kSteps) {
-      load_step(lane_block(pt_row, first, n_c, lane));
-      const int blk1 = kSteps > 1 ? lane_block(pt_row, first + 16, n_c, lane) : 0;
+      load_step(lane_block<V>(pt_row, first, n_c, lane));
+      const int blk1 = kSteps > 1 ? lane_block<V>(pt_row, first + 16, n_c, lane) : 0;
       QD = q_digits(q + (row0 + col) * kDim, grp);
       run(first, IntTag<kSteps>{}, blk1);
     } else {
       QD = q_digits(q + (row0 + col) * kDim, grp);
 #pragma unroll 1
       for (int t = 0; t < n_steps; ++t) {
-        load_step(lane_block(pt_row, first + 16 * t, n_c, lane));
+        load_step(lane_block<V>(pt_row, first + 16 * t, n_c, lane));
         run(first + 16 * t, IntTag<1>{}, 0);
       }
     }
@@ -1929,6 +1980,22 @@ __global__ __launch_bounds__(256) void scan_page_kernel(
   }
 }
 
+// r = 8, G = 16 over pages of 16 V tokens, V = 2 or 4 (sub-pages of 16 tokens).
+template <typename QT>
+hipError_t dispatch_scan_r8_sub(int V, int steps, dim3 grid, hipStream_t st, int H_q, int H_kv,
+                                int max_pages, const QT* q, const uint8_t* sum,
+                                uint32_t summ_bytes, const int32_t* pt, const int32_t* sl,
+                                float* s_hat, SHatLayout lay, float2* part) {
+#define LOCKS_SCAN_R8_SUB(VV, SS)                                                           \
+  if (V == VV && steps == SS) {                                                            \
+    hipLaunchKernelGGL((scan_r8_kernel<QT, SS, VV>), grid, dim3(256), 0, st, H_q, H_kv,    \
+                       max_pages, q, sum, summ_bytes, pt, sl, s_hat, lay, part);           \
+    return hipGetLastError();                                                              \
+  }
+  LOCKS_SCAN_R8_SUB(2, 1) LOCKS_SCAN_R8_SUB(2, 4) LOCKS_SCAN_R8_SUB(4, 1) LOCKS_SCAN_R8_SUB(4, 4)
+#undef LOCKS_SCAN_R8_SUB
+  return hipErrorInvalidValue;
+}
 
 template <typename QT>
 hipError_t dispatch_scan_page(int r, int B, int wp, dim3 grid, hipStream_t st, int H_q, int H_kv,
@@ -2045,9 +2112,10 @@ hipError_t dispatch_scan(int r, int G, int basis, int steps, dim3 grid, hipStrea
 
 }  // namespace
 
+// r = 8, G = 16 with an int4 basis, at every page size (larger pages as 16-token
+// sub-pages).
 static bool use_r8_kernel(const locks_cfg_t& c) {
-  return c.page_size == kPage && c.basis == LOCKS_BASIS_INT4 && c.rank == 8 &&
-         c.num_q_heads == 16 * c.num_kv_heads;
+  return c.basis == LOCKS_BASIS_INT4 && c.rank == 8 && c.num_q_heads == 16 * c.num_kv_heads;
 }
 
 static bool use_r8g4_kernel(const locks_cfg_t& c) {
@@ -2058,7 +2126,8 @@ static bool use_r8g4_kernel(const locks_cfg_t& c) {
 // 16-page steps per wave of the r = 8 kernels: 4, or 1 when a 4-step grid would
 // have fewer blocks than the GPU has compute units.
 static int r8_steps(const locks_cfg_t& c) {
-  const long blocks4 = (long)((c.max_pages_per_seq + 255) / 256) * c.num_kv_heads * c.num_seqs;
+  const long sub = (long)c.max_pages_per_seq << sub_page_log2(c);
+  const long blocks4 = (sub + 255) / 256 * c.num_kv_heads * c.num_seqs;
   return blocks4 < 256 ? 1 : 4;
 }
 
@@ -2071,8 +2140,9 @@ static int page_wave_pages(const locks_cfg_t& c) {
 }
 
 int scan_pages_per_block(const locks_cfg_t& c) {
+  if (use_r8_kernel(c)) return (64 * r8_steps(c)) >> sub_page_log2(c);
   if (c.page_size != kPage) return 4 * page_wave_pages(c);
-  if (use_r8_kernel(c) || use_r8g4_kernel(c)) return 64 * r8_steps(c);
+  if (use_r8g4_kernel(c)) return 64 * r8_steps(c);
   return kScanPagesPerBlock;
 }
 
@@ -2083,6 +2153,18 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
   const int G = c.num_q_heads / c.num_kv_heads;
   const uint32_t bytes = (uint32_t)summary_store_bytes(c);
   const int steps = r8_steps(c);
+  if (c.page_size != kPage && use_r8_kernel(c)) {
+    const int V = 1 << sub_page_log2(c);
+    if (c.q_dtype == LOCKS_BF16)
+      return dispatch_scan_r8_sub(V, steps, grid, st, c.num_q_heads, c.num_kv_heads,
+                                  c.max_pages_per_seq, static_cast<const uint16_t*>(q),
+                                  static_cast<const uint8_t*>(summaries), bytes, page_table,
+                                  seq_lens, s_hat, lay, partials);
+    return dispatch_scan_r8_sub(V, steps, grid, st, c.num_q_heads, c.num_kv_heads,
+                                c.max_pages_per_seq, static_cast<const float*>(q),
+                                static_cast<const uint8_t*>(summaries), bytes, page_table,
+                                seq_lens, s_hat, lay, partials);
+  }
   if (c.page_size != kPage) {
     if (c.q_dtype == LOCKS_BF16)
       return dispatch_scan_page(c.rank, c.page_size, page_wave_pages(c), grid, st, c.num_q_heads,

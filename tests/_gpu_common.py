@@ -130,15 +130,16 @@ def ids_of(row):
     return [int(x) for x in row if int(x) >= 0]
 
 
-def parse_codes(rec, r):
-    """Integer codes of int4-basis records laid out as include/locks.h documents
-    (test-local parser, independent of the oracle's decoder)."""
+def parse_codes(rec, r, P=16):
+    """Integer codes of int4-basis records of P-token pages laid out as
+    include/locks.h documents (test-local parser, independent of the oracle's
+    decoder)."""
     rec = rec.astype(np.int64)
     v = np.empty((rec.shape[0], 128, r), np.int64)
     for l in range(r):
         b = rec[:, 64 * l:64 * l + 64]
         v[:, 0::2, l] = (b & 15) - 8
         v[:, 1::2, l] = (b >> 4) - 8
-    c = rec[:, 64 * r:80 * r] - 128
-    m = rec[:, 80 * r:80 * r + 128] - 128
+    c = rec[:, 64 * r:(64 + P) * r] - 128
+    m = rec[:, (64 + P) * r:(64 + P) * r + 128] - 128
     return {"vcodes": v, "ccodes": c, "mcodes": m}

@@ -1,7 +1,7 @@
 """Parity at the benchmark's full sizes, in the launch configuration bench.py times:
 the eager fused locks_decode_step over every page of every sequence of the
-GLM-4-9B 1M-token, Llama-3.1-8B 8 x 128K (r = 8 and r = 2) and Qwen3-4B reasoning
-workloads.  The GPU builds every summary; for a few sampled (sequence, KV head)
+GLM-4-9B 1M-token (16-, 32- and 64-token pages), Llama-3.1-8B 8 x 128K (r = 8
+and r = 2) and Qwen3-4B reasoning workloads.  The GPU builds every summary; for a few sampled (sequence, KV head)
 units the oracle builds that unit's summaries itself and computes the whole step
 of that unit (every page scored, the shared table, attention).  On those units:
 GPU-built codes against the oracle's (within +-1, >= 99.9% identical on gapped
@@ -23,6 +23,8 @@ pytestmark = pytest.mark.gpu
 FULL = {
     # name: (workload id, overrides, sampled (seq, KV head) units)
     "glm4-9b-1m": (3, {}, [(0, 1)]),
+    "glm4-9b-1m-B32": (3, {"page_size": 32}, [(0, 0)]),
+    "glm4-9b-1m-B64": (3, {"page_size": 64}, [(0, 1)]),
     "llama-8x128k-r8": (2, {}, [(0, 0), (3, 5), (7, 7)]),
     "llama-8x128k-r2": (2, {"rank": 2}, [(1, 2), (6, 4)]),
     "qwen3-reasoning": (4, {}, [(0, 0), (17, 3), (42, 6), (63, 7)]),
@@ -52,20 +54,20 @@ def test_full_size_step_on_sampled_units(name):
     print(f"[full {name}] generating", flush=True)
     w = make_workload(wid, seed=0, device="cuda", **ov)
     cfg = B.config_for(w.spec, w.num_blocks, w.max_pages)
-    r, G = cfg.rank, cfg.group
+    r, G, P = cfg.rank, cfg.group, cfg.page_size
     store = B.alloc_summaries(cfg)
     B.build_summaries(cfg, w.k_cache, w.page_table, w.seq_lens, store)
     torch.cuda.synchronize()
     ref = {}
     for s, h in units:
         k, v, qg = gather_unit(w, s, h)
-        n_c = k.shape[0] // 16
+        n_c = k.shape[0] // P
         print(f"[full {name}] oracle build of unit ({s}, {h}): {n_c} pages", flush=True)
-        f = O.build_factors(k[:n_c * 16].reshape(n_c, 16, 128), r)
+        f = O.build_factors(k[:n_c * P].reshape(n_c, P, 128), r)
         rec = O.encode(f["mu"], f["V"], f["C"])
         posed = _well_posed(f, r)
         blocks = w.page_table[s, :n_c].long()
-        got, want = parse_codes(store[blocks, h].cpu().numpy(), r), parse_codes(rec, r)
+        got, want = parse_codes(store[blocks, h].cpu().numpy(), r, P), parse_codes(rec, r, P)
         far = np.zeros(n_c, bool)
         for key in want:
             far |= (np.abs(got[key] - want[key]) > 1).reshape(n_c, -1).any(axis=1)
@@ -85,7 +87,7 @@ def test_full_size_step_on_sampled_units(name):
               f"code off by more than 1", flush=True)
         assert same / total >= 0.999
         store[blocks, h] = torch.from_numpy(rec).to(store.device)
-        ref[(s, h)] = (qg, O.decode_step(qg, k, v, rec, r, cfg.budget_tokens), n_c)
+        ref[(s, h)] = (qg, O.decode_step(qg, k, v, rec, r, cfg.budget_tokens, "int4", P), n_c)
 
     ws = B.alloc_workspace(cfg)
     ids, sel, out, lse = B.decode_step(cfg, w.q, w.k_cache, w.v_cache, w.page_table, w.seq_lens,
@@ -107,7 +109,7 @@ def test_full_size_step_on_sampled_units(name):
               f"{len(set(got) & set(rf['ids'])) / len(rf['ids']):.4f}, rel-L2 {worst:.2e}",
               flush=True)
         assert err <= LSE_TOL
-        check_table(got, rf, -(-int(w.spec.seq_lens[s]) // 16), cfg.k)
+        check_table(got, rf, -(-int(w.spec.seq_lens[s]) // P), cfg.k)
         k, v, _ = gather_unit(w, s, h)
-        check_attention_on_table(qg, k, v, got, o, l)
+        check_attention_on_table(qg, k, v, got, o, l, P)
         check_sel_lse(sel[s, hs].double().cpu().numpy(), got, rf["s_hat"], n_c)

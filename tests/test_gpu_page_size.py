@@ -122,6 +122,11 @@ STEP = {
     # four pages per stage-2 pass (four-head groups) at the other ranks and fp32 q
     "B32-G4-r2-fp32q": (32, 2, 4, 2, [32 * 300 + 7, 32 * 40], 2, 1024, "bf16", "fp32"),
     "B64-G4-r4": (64, 2, 4, 2, [64 * 150 + 3, 64 * 30], 4, 1024, "bf16", "bf16"),
+    # r = 8 with sixteen-head groups: 16-token sub-pages whose LSEs are merged per
+    # page; ragged lengths, a sequence without a complete page, fp32 queries
+    "B64-G16-r8": (64, 3, 16, 2, [64 * 700 + 40, 63, 64 * 77], 8, 2048, "bf16", "bf16"),
+    "B32-G16-r8-fp32q": (32, 3, 16, 1, [32 * 900 + 31, 32 * 5, 32 * 260 + 1], 8, 1024, "bf16",
+                         "fp32"),
 }
 
 
