@@ -1136,34 +1136,56 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // The centroid MFMA (once per step) puts page 4 (m % 4) + m / 4 in row m, so
 // register Q of lane (grp, col) holds a(page 4 Q + grp, head col % 4): the
 // centroid of the lanes with grp == col / 4, which keep the result.
+//
+// Pages of 16 V tokens (V = 2, 4) run as V sub-pages of 16 tokens (coefficient
+// rows and row scales 16 u .. 16 u + 15 of sub-page u, the page's basis and
+// centroid); the sub-page LSEs of a page sit in the diagonal lanes 20 a + g,
+// a = 4 Q + sub-page, and are merged with lane exchanges at distance 20 and 40.
 // ---------------------------------------------------------------------------
 
-// Block of page min(page0 + (lane & 15), n_c - 1): always a valid page of the sequence.
+// Block of (sub-)page min(page0 + (lane & 15), n_c - 1): always a valid page of
+// the sequence.
+template <int V = 1>
 __device__ __forceinline__ int lane_block_clamped(const int32_t* __restrict__ pt_row, int page0,
                                                   int n_c, int lane) {
   const int pl = page0 + (lane & 15);
-  return pt_row[pl < n_c ? pl : n_c - 1];
+  return pt_row[(pl < n_c ? pl : n_c - 1) / V];
 }
 
-template <typename QT, int kSteps>
+// Log-sum-exp, log2 domain, of the sub-page values in lanes l, l ^ 20 (V = 2) and
+// l ^ 40, l ^ 60 (V = 4); each of those lanes gets the same bits.
+template <int V>
+__device__ __forceinline__ float merge_diag_lse(float v) {
+  auto lse2 = [](float a, float b) {
+    const float mx = fmaxf(a, b);
+    return mx + __builtin_amdgcn_logf(__builtin_amdgcn_exp2f(a - mx) + __builtin_amdgcn_exp2f(b - mx));
+  };
+  v = lse2(v, __shfl_xor(v, 20, 64));
+  if (V == 4) v = lse2(v, __shfl_xor(v, 40, 64));
+  return v;
+}
+
+template <typename QT, int kSteps, int V = 1>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void scan_r8g4_kernel(
     int H_q, int H_kv, int max_pages, const QT* __restrict__ q, const uint8_t* __restrict__ summ,
     uint32_t summ_bytes, const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     float* __restrict__ s_hat, SHatLayout lay, float2* __restrict__ partials) {
-  constexpr int R = 8, G = 4;
-  constexpr uint32_t kStride = rec_stride(R);
-  constexpr uint32_t kCoef = rec_coef_off(R), kMu = rec_mu_off(R), kSc = rec_scale_off(R);
+  constexpr int R = 8, G = 4, P = kPage * V;
+  constexpr uint32_t kStride = rec_stride(R, 0, P);
+  constexpr uint32_t kCoef = rec_coef_off(R), kMu = rec_mu_off(R, 0, P), kSc = rec_scale_off(R, 0, P);
   __shared__ float2 sRun[4][64];
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = blockIdx.y, s = blockIdx.z;
-  const int n_c = seq_lens[s] / kPage;
+  const int n_c = seq_lens[s] / P * V;  // sub-pages of the complete pages
   const int pg = scan_chunk() * 4 + wave;
   const long row0 = (long)s * H_q + (long)h * G;
   const int32_t* pt_row = page_table + (long)s * max_pages;
   const int ca = col >> 2, g = col & 3;
   const bool diag = grp == ca;
+  // sub-page of the pages this lane reads through ra (4 Q + ca) and rb (4 Q + grp)
+  const uint32_t sub_a = (uint32_t)(ca % V), sub_b = (uint32_t)(grp % V);
   float run_m = -INFINITY, run_s = 0.0f;
 
   constexpr int kWavePages = 16 * kSteps;
@@ -1208,10 +1230,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     auto ld_vb = [&](const Offs& o, int Q, int i) {
       vb[Q][i] = bld16(rs, o.ra[Q] + 64u * (4 * i + g) + 16u * grp);
     };
-    auto ld_cf = [&](const Offs& o, int Q) { cf[Q] = bld8(rs, o.rb[Q] + kCoef + 8u * col); };
-    auto ld_cs = [&](const Offs& o, int Q) { cs[Q] = bld8(rs, o.ra[Q] + kSc + 2u * (R + 4 * grp)); };
+    auto ld_cf = [&](const Offs& o, int Q) {
+      cf[Q] = bld8(rs, o.rb[Q] + kCoef + 8u * (16u * sub_b + col));
+    };
+    auto ld_cs = [&](const Offs& o, int Q) {
+      cs[Q] = bld8(rs, o.ra[Q] + kSc + 2u * (R + 16u * sub_a + 4 * grp));
+    };
     auto ld_vs = [&](const Offs& o, int Q) { vs[Q] = bld16(rs, o.rb[Q] + kSc); };
-    auto ld_ms = [&](const Offs& o, int Q) { msw[Q] = bld4(rs, o.rb[Q] + kSc + 2u * (R + 16)); };
+    auto ld_ms = [&](const Offs& o, int Q) { msw[Q] = bld4(rs, o.rb[Q] + kSc + 2u * (R + P)); };
     auto ld_mu = [&](const Offs& o) {
       mu[0] = bld16(rs, o.rm + kMu + 32u * grp);
       mu[1] = bld16(rs, o.rm + kMu + 32u * grp + 16u);
@@ -1246,7 +1272,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         int blk_after = 0;
         if (pf) {
           on = offsets(blk_next);
-          if (t + 2 < kN) blk_after = lane_block_clamped(pt_row, page0 + 32, n_c, lane);
+          if (t + 2 < kN) blk_after = lane_block_clamped<V>(pt_row, page0 + 32, n_c, lane);
         }
 
         // ---- centroid term: areg[j] = a(page 4 j + grp, head g) / (scale of that page)
@@ -1338,10 +1364,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                  __builtin_amdgcn_exp2f(z[2] - shift) + __builtin_amdgcn_exp2f(z[3] - shift);
             sm = red4_sum(sm);
           }
-          const float s2 = am + shift + __builtin_amdgcn_logf(sm);
-          const int page = page0 + 4 * Q + ca;
-          const bool live = diag && page < n_c;
-          if (live) shat_base[(long)page * lay.page] = s2 * 0.69314718055994531f;
+          float s2 = am + shift + __builtin_amdgcn_logf(sm);
+          const int sub = page0 + 4 * Q + ca;
+          const bool live = diag && sub < n_c && ca % V == 0;
+          if (V > 1) s2 = merge_diag_lse<V>(s2);
+          if (live) shat_base[(long)(sub / V) * lay.page] = s2 * 0.69314718055994531f;
           const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
           const bool up = s2 > run_m;
           const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
@@ -1352,8 +1379,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
     };
     if (n_steps == kSteps) {
-      const int blk0 = lane_block_clamped(pt_row, first, n_c, lane);
-      const int blk1 = kSteps > 1 ? lane_block_clamped(pt_row, first + 16, n_c, lane) : 0;
+      const int blk0 = lane_block_clamped<V>(pt_row, first, n_c, lane);
+      const int blk1 = kSteps > 1 ? lane_block_clamped<V>(pt_row, first + 16, n_c, lane) : 0;
       load_step(blk0);
       form_digits();
       run(first, IntTag<kSteps>{}, blk1);
@@ -1361,7 +1388,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       form_digits();
 #pragma unroll 1
       for (int t = 0; t < n_steps; ++t) {
-        load_step(lane_block_clamped(pt_row, first + 16 * t, n_c, lane));
+        load_step(lane_block_clamped<V>(pt_row, first + 16 * t, n_c, lane));
         run(first + 16 * t, IntTag<1>{}, 0);
       }
     }
@@ -1997,6 +2024,24 @@ hipError_t dispatch_scan_r8_sub(int V, int steps, dim3 grid, hipStream_t st, int
   return hipErrorInvalidValue;
 }
 
+// r = 8, G = 4 over pages of 16 V tokens, V = 2 or 4.
+template <typename QT>
+hipError_t dispatch_scan_r8g4_sub(int V, int steps, dim3 grid, hipStream_t st, int H_q, int H_kv,
+                                  int max_pages, const QT* q, const uint8_t* sum,
+                                  uint32_t summ_bytes, const int32_t* pt, const int32_t* sl,
+                                  float* s_hat, SHatLayout lay, float2* part) {
+#define LOCKS_SCAN_R8G4_SUB(VV, SS)                                                         \
+  if (V == VV && steps == SS) {                                                            \
+    hipLaunchKernelGGL((scan_r8g4_kernel<QT, SS, VV>), grid, dim3(256), 0, st, H_q, H_kv,  \
+                       max_pages, q, sum, summ_bytes, pt, sl, s_hat, lay, part);           \
+    return hipGetLastError();                                                              \
+  }
+  LOCKS_SCAN_R8G4_SUB(2, 1) LOCKS_SCAN_R8G4_SUB(2, 4) LOCKS_SCAN_R8G4_SUB(4, 1)
+  LOCKS_SCAN_R8G4_SUB(4, 4)
+#undef LOCKS_SCAN_R8G4_SUB
+  return hipErrorInvalidValue;
+}
+
 template <typename QT>
 hipError_t dispatch_scan_page(int r, int B, int wp, dim3 grid, hipStream_t st, int H_q, int H_kv,
                               int max_pages, const QT* q, const uint8_t* sum, const int32_t* pt,
@@ -2119,8 +2164,7 @@ static bool use_r8_kernel(const locks_cfg_t& c) {
 }
 
 static bool use_r8g4_kernel(const locks_cfg_t& c) {
-  return c.page_size == kPage && c.basis == LOCKS_BASIS_INT4 && c.rank == 8 &&
-         c.num_q_heads == 4 * c.num_kv_heads;
+  return c.basis == LOCKS_BASIS_INT4 && c.rank == 8 && c.num_q_heads == 4 * c.num_kv_heads;
 }
 
 // 16-page steps per wave of the r = 8 kernels: 4, or 1 when a 4-step grid would
@@ -2140,9 +2184,8 @@ static int page_wave_pages(const locks_cfg_t& c) {
 }
 
 int scan_pages_per_block(const locks_cfg_t& c) {
-  if (use_r8_kernel(c)) return (64 * r8_steps(c)) >> sub_page_log2(c);
+  if (use_r8_kernel(c) || use_r8g4_kernel(c)) return (64 * r8_steps(c)) >> sub_page_log2(c);
   if (c.page_size != kPage) return 4 * page_wave_pages(c);
-  if (use_r8g4_kernel(c)) return 64 * r8_steps(c);
   return kScanPagesPerBlock;
 }
 
@@ -2164,6 +2207,18 @@ hipError_t launch_scan(const locks_cfg_t& c, const void* q, const void* summarie
                                 c.max_pages_per_seq, static_cast<const float*>(q),
                                 static_cast<const uint8_t*>(summaries), bytes, page_table,
                                 seq_lens, s_hat, lay, partials);
+  }
+  if (c.page_size != kPage && use_r8g4_kernel(c)) {
+    const int V = 1 << sub_page_log2(c);
+    if (c.q_dtype == LOCKS_BF16)
+      return dispatch_scan_r8g4_sub(V, steps, grid, st, c.num_q_heads, c.num_kv_heads,
+                                    c.max_pages_per_seq, static_cast<const uint16_t*>(q),
+                                    static_cast<const uint8_t*>(summaries), bytes, page_table,
+                                    seq_lens, s_hat, lay, partials);
+    return dispatch_scan_r8g4_sub(V, steps, grid, st, c.num_q_heads, c.num_kv_heads,
+                                  c.max_pages_per_seq, static_cast<const float*>(q),
+                                  static_cast<const uint8_t*>(summaries), bytes, page_table,
+                                  seq_lens, s_hat, lay, partials);
   }
   if (c.page_size != kPage) {
     if (c.q_dtype == LOCKS_BF16)

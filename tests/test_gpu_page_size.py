@@ -127,6 +127,7 @@ STEP = {
     "B64-G16-r8": (64, 3, 16, 2, [64 * 700 + 40, 63, 64 * 77], 8, 2048, "bf16", "bf16"),
     "B32-G16-r8-fp32q": (32, 3, 16, 1, [32 * 900 + 31, 32 * 5, 32 * 260 + 1], 8, 1024, "bf16",
                          "fp32"),
+    "B64-G4-r8-fp32q": (64, 3, 4, 2, [64 * 400 + 5, 64 * 61, 40], 8, 1024, "bf16", "fp32"),
 }
 
 
@@ -248,11 +249,12 @@ def test_gpu_built_summaries_and_build_list_step(Bp):
 
 
 @pytest.mark.timeout(600)
-def test_full_size_128k_page32():
-    """The 8 x 128K Llama-shaped workload at B = 32 (r = 8, b = 2048): the GPU builds
+@pytest.mark.parametrize("Bp", [32, 64])
+def test_full_size_128k_large_pages(Bp):
+    """The 8 x 128K Llama-shaped workload at B = 32 and 64 (r = 8, b = 2048): the GPU builds
     every summary; on two sampled units with the oracle's bytes installed, every
     page score, the table, the page LSEs and the output."""
-    d = _dev("128k-B32", 32, 8, 4, 8, [131072] * 8, 8, 2048, on_gpu=True)
+    d = _dev(f"128k-B{Bp}", Bp, 8, 4, 8, [131072] * 8, 8, 2048, on_gpu=True)
     cfg = d.cfg
     store = B.alloc_summaries(cfg, d.device)
     B.build_summaries(cfg, d.k, d.pt, d.sl, store)
@@ -270,15 +272,15 @@ def test_full_size_128k_page32():
     Gq = cfg.group
     for (s, h) in units:
         k, v, qg = gather_unit(d.w, s, h)
-        ref = O.decode_step(qg, k, v, recs[(s, h)], 8, 2048, "int4", 32)
-        n = -(-k.shape[0] // 32)
+        ref = O.decode_step(qg, k, v, recs[(s, h)], 8, 2048, "int4", Bp)
+        n = -(-k.shape[0] // Bp)
         hs = slice(h * Gq, (h + 1) * Gq)
         err = float(np.max(np.abs(all_lse[s, hs, :n].double().cpu().numpy() - ref["s_hat"])))
         got = ids_of(ids[s, h].tolist())
         check_table(got, ref, n, cfg.k)
         w = check_attention_on_table(qg, k, v, got, out[s, hs].double().cpu().numpy(),
-                                     lse[s, hs].double().cpu().numpy(), 32)
+                                     lse[s, hs].double().cpu().numpy(), Bp)
         check_sel_lse(sel[s, hs].double().cpu().numpy(), got, ref["s_hat"], n)
-        print(f"[page 32] 128K unit ({s}, {h}): hat s err {err:.2e}, same table "
+        print(f"[page {Bp}] 128K unit ({s}, {h}): hat s err {err:.2e}, same table "
               f"{got == ref['ids']}, rel-L2 {w:.2e}", flush=True)
         assert err <= LSE_TOL
