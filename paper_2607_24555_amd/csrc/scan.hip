@@ -1139,8 +1139,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 //
 // Pages of 16 V tokens (V = 2, 4) run as V sub-pages of 16 tokens (coefficient
 // rows and row scales 16 u .. 16 u + 15 of sub-page u, the page's basis and
-// centroid); the sub-page LSEs of a page sit in the diagonal lanes 20 a + g,
-// a = 4 Q + sub-page, and are merged with lane exchanges at distance 20 and 40.
+// centroid).  At V = 4 a quad is one page, and stage 1 runs once per step for
+// the step's four pages: lane (grp, col) gets p(page grp, l, head g), and three
+// row swaps (16 and 32 lanes) broadcast page u's rows for quad u.  (At V = 2
+// stage 1 stays per quad: sharing it measured slower than the duplicated
+// work.)  The sub-page LSEs of a page sit in the diagonal lanes 20 a + g (a the
+// quad's sub-page) and are merged with lane exchanges at distance 20 and 40.
 // ---------------------------------------------------------------------------
 
 // Block of (sub-)page min(page0 + (lane & 15), n_c - 1): always a valid page of
@@ -1202,9 +1206,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     float* shat_base = s_hat + lay.base(s, h) + (long)g * lay.head;
 
     // record offsets of one step: ra[Q] page 4 Q + ca, rb[Q] page 4 Q + grp,
-    // rm page 4 g + ca (the centroid row of this lane)
+    // rm page 4 g + ca (the centroid row of this lane); when stage 1 is shared
+    // (V = 4), pa[0] and pb[0] are the records of pages ca and grp of the step
+    constexpr int kShare = V == 4 ? 4 : 1;  // quads per stage-1 pass
+    constexpr int kPasses = 4 / kShare;
     struct Offs {
       uint32_t ra[4], rb[4], rm;
+      uint32_t pa[kPasses], pb[kPasses];
     };
     const __amdgpu_buffer_rsrc_t rs = summ_rsrc(summ, summ_bytes);
     const uint32_t blk_bytes = (uint32_t)H_kv * kStride, head_off = (uint32_t)h * kStride;
@@ -1217,18 +1225,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         o.rb[Q] = rec(4 * Q + grp);
       }
       o.rm = rec(4 * g + ca);
+      if constexpr (kShare > 1) {
+#pragma unroll
+        for (int m = 0; m < kPasses; ++m) {
+          o.pa[m] = rec((4 * m + ca) * V);
+          o.pb[m] = rec((4 * m + grp) * V);
+        }
+      }
       return o;
     };
-    uint4 vb[4][2];    // basis rows of quad Q, set i
+    uint4 vb[kPasses][2];  // basis rows of stage-1 pass m (quad m if V = 1), set i
     uint2 cf[4];       // coefficient row `col` of page 4 Q + grp
     uint2 cs[4];       // row scales of tokens 4 grp .. 4 grp + 3 of page 4 Q + ca
-    uint4 vs[4];       // basis column scales of page 4 Q + grp
+    uint4 vs[kPasses];     // basis column scales of the pass's page grp
     uint32_t msw[4];   // centroid scale of page 4 Q + grp (low half)
     uint4 mu[2];       // centroid bytes 32 grp .. 32 grp + 31 of page 4 g + ca
     // loads of one step's registers; in a run the next step's are issued right
     // after the register's last use in the current one
-    auto ld_vb = [&](const Offs& o, int Q, int i) {
-      vb[Q][i] = bld16(rs, o.ra[Q] + 64u * (4 * i + g) + 16u * grp);
+    auto ld_vb = [&](const Offs& o, int m, int i) {
+      vb[m][i] = bld16(rs, (kShare == 1 ? o.ra[m] : o.pa[m]) + 64u * (4 * i + g) + 16u * grp);
     };
     auto ld_cf = [&](const Offs& o, int Q) {
       cf[Q] = bld8(rs, o.rb[Q] + kCoef + 8u * (16u * sub_b + col));
@@ -1236,7 +1251,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     auto ld_cs = [&](const Offs& o, int Q) {
       cs[Q] = bld8(rs, o.ra[Q] + kSc + 2u * (R + 16u * sub_a + 4 * grp));
     };
-    auto ld_vs = [&](const Offs& o, int Q) { vs[Q] = bld16(rs, o.rb[Q] + kSc); };
+    auto ld_vs = [&](const Offs& o, int m) {
+      vs[m] = bld16(rs, (kShare == 1 ? o.rb[m] : o.pb[m]) + kSc);
+    };
     auto ld_ms = [&](const Offs& o, int Q) { msw[Q] = bld4(rs, o.rb[Q] + kSc + 2u * (R + P)); };
     auto ld_mu = [&](const Offs& o) {
       mu[0] = bld16(rs, o.rm + kMu + 32u * grp);
@@ -1249,9 +1266,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       ld_mu(o0);
 #pragma unroll
       for (int Q = 0; Q < 4; ++Q) {
-        ld_vb(o0, Q, 0);
-        ld_vb(o0, Q, 1);
-        ld_vs(o0, Q);
+        if (Q < kPasses) {
+          ld_vb(o0, Q, 0);
+          ld_vb(o0, Q, 1);
+          ld_vs(o0, Q);
+        }
         ld_cf(o0, Q);
         ld_ms(o0, Q);
         ld_cs(o0, Q);
@@ -1302,32 +1321,55 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             areg[j] = fmaf((float)acc[0][j], 65536.0f, (float)(acc[1][j] * 256 + acc[2][j]));
         }
 
+        float bq[kShare][8];  // shared stage 1: the values of the step's quads
 #pragma unroll
         for (int Q = 0; Q < 4; ++Q) {
           __builtin_amdgcn_sched_barrier(0);
           // ---- stage 1: vals[4 i + j] = p(page 4 Q + grp, l = 4 i + j, head g), zero off-diagonal
           float vals[8];
-          i4v acc1[2];
-          {
-            i4v a0[2], a1[2];
-            nib_operands(vb[Q][0], a0);
-            nib_operands(vb[Q][1], a1);
-            proj_horner2(a0, a1, QD, acc1[0], acc1[1]);
-            if (pf) {
-              ld_vb(on, Q, 0);
-              ld_vb(on, Q, 1);
+          if (Q % kShare == 0) {
+            const int m = Q / kShare;
+            i4v acc1[2];
+            {
+              i4v a0[2], a1[2];
+              nib_operands(vb[m][0], a0);
+              nib_operands(vb[m][1], a1);
+              proj_horner2(a0, a1, QD, acc1[0], acc1[1]);
+              if (pf) {
+                ld_vb(on, m, 0);
+                ld_vb(on, m, 1);
+              }
             }
-          }
-          {
-            const uint32_t vsw[4] = {vs[Q].x, vs[Q].y, vs[Q].z, vs[Q].w};
+            const uint32_t vsw[4] = {vs[m].x, vs[m].y, vs[m].z, vs[m].w};
+            const float sc = kShare == 1 ? inv_m : QD.inv_scale;
 #pragma unroll
             for (int l = 0; l < 8; ++l) {
               const int j = l & 3;
               const h2 pr = as_h2(vsw[l >> 1]);
               const float vsc = (float)((l & 1) ? pr.y : pr.x);
-              vals[l] = (float)acc1[l >> 2][j] * (vsc * inv_m);
+              vals[l] = (float)acc1[l >> 2][j] * (vsc * sc);
             }
-            if (pf) ld_vs(on, Q);
+            if (pf) ld_vs(on, m);
+            if constexpr (kShare > 1) {
+              // rows r0..r3 (lanes 16 u ..) hold pages 0..3; the 16-lane swap gives
+              // X = (r0, r0, r2, r2) and Y = (r1, r1, r3, r3), the 32-lane swaps of
+              // X and Y each row everywhere
+#pragma unroll
+              for (int l = 0; l < 8; ++l) {
+                const uint32_t x = __float_as_uint(vals[l]);
+                const auto xy = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+                const auto xx = __builtin_amdgcn_permlane32_swap(xy[0], xy[0], false, false);
+                const auto yy = __builtin_amdgcn_permlane32_swap(xy[1], xy[1], false, false);
+                bq[0][l] = __uint_as_float(xx[0]);
+                bq[1][l] = __uint_as_float(yy[0]);
+                bq[2][l] = __uint_as_float(xx[1]);
+                bq[3][l] = __uint_as_float(yy[1]);
+              }
+            }
+          }
+          if constexpr (kShare > 1) {
+#pragma unroll
+            for (int l = 0; l < 8; ++l) vals[l] = diag ? bq[Q][l] : 0.0f;
           }
           const h8 A = byte8_to_h8(cf[Q].x, cf[Q].y);
           if (pf) ld_cf(on, Q);
