@@ -506,14 +506,18 @@ __device__ __forceinline__ void fast_issue(FastRegs<R>& T, const uint8_t* __rest
   }
 }
 
-__device__ __forceinline__ int sbyte(int x) { return (int)(int8_t)(x & 0xff); }
-
 // Query digits of head gcol for the int8 projection: q is scaled by a power of
 // two to a 20-bit fixed-point integer Q (|Q| < 2^20) and split into three signed
 // 8-bit digits (most significant first).  Element e of MFMA half hh <-> d =
 // 32 grp + 16 hh + perm16[e], the order in which the decoders expand the packed
 // codes.  bias[t] = -8 * sum(digit t) removes the excess-8 offset of the int4
 // codes.
+//
+// The digits are the bytes of U = Q + 0x808080 minus 128: U lies in [0, 2^24),
+// byte i of U is digit i + 128, and the lower two digits land in [-128, 127]
+// (the balanced base-256 digits of Q).  Four elements' bytes are gathered into
+// one digit word per digit by byte permutes, the +128 offsets flipped back by
+// one XOR, and each word's digit sum taken by one signed 4-way dot product.
 struct QDigits {
   i4v bd[3][2];
   int bias[3];
@@ -537,35 +541,37 @@ __device__ __forceinline__ QDigits q_digits(const QT* __restrict__ qrow, int grp
   (void)frexpf(qmax, &ex);  // qmax < 2^ex
   const float qscale = ldexpf(1.0f, 20 - ex);
   D.inv_scale = ldexpf(1.0f, ex - 20) * c0;
-  float bsum[3] = {0.0f, 0.0f, 0.0f};
+  int bsum[3] = {0, 0, 0};
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
     for (int dw = 0; dw < 4; ++dw) {
-      uint32_t w0 = 0, w1 = 0, w2 = 0;
+      uint32_t U[4];
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb) {
         const int e = 4 * dw + bb;
         const int Q = (qmax > 0.0f)
                           ? min(max((int)rintf(qf[16 * hh + kPerm16[e]] * qscale), -0xFFFFF), 0xFFFFF)
                           : 0;
-        const int d2 = sbyte(Q);
-        const int q1 = (Q - d2) >> 8;
-        const int d1 = sbyte(q1);
-        const int d0 = (q1 - d1) >> 8;
-        bsum[0] += (float)d0;
-        bsum[1] += (float)d1;
-        bsum[2] += (float)d2;
-        w0 |= (uint32_t)(d0 & 0xff) << (8 * bb);
-        w1 |= (uint32_t)(d1 & 0xff) << (8 * bb);
-        w2 |= (uint32_t)(d2 & 0xff) << (8 * bb);
+        U[bb] = (uint32_t)(Q + 0x808080);
       }
+      // bytes (U0.b0, U1.b0, U0.b1, U1.b1), (U0.b2, U1.b2, ..) and the same for U2, U3
+      const uint32_t lo01 = __builtin_amdgcn_perm(U[1], U[0], 0x05010400u);
+      const uint32_t lo23 = __builtin_amdgcn_perm(U[3], U[2], 0x05010400u);
+      const uint32_t hi01 = __builtin_amdgcn_perm(U[1], U[0], 0x07030602u);
+      const uint32_t hi23 = __builtin_amdgcn_perm(U[3], U[2], 0x07030602u);
+      const uint32_t w2 = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u) ^ 0x80808080u;
+      const uint32_t w1 = __builtin_amdgcn_perm(lo23, lo01, 0x07060302u) ^ 0x80808080u;
+      const uint32_t w0 = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u) ^ 0x80808080u;
+      bsum[0] = __builtin_amdgcn_sdot4((int)w0, 0x01010101, bsum[0], false);
+      bsum[1] = __builtin_amdgcn_sdot4((int)w1, 0x01010101, bsum[1], false);
+      bsum[2] = __builtin_amdgcn_sdot4((int)w2, 0x01010101, bsum[2], false);
       D.bd[0][hh][dw] = (int)w0;
       D.bd[1][hh][dw] = (int)w1;
       D.bd[2][hh][dw] = (int)w2;
     }
 #pragma unroll
-  for (int t = 0; t < 3; ++t) D.bias[t] = -8 * (int)red4_sum(bsum[t]);
+  for (int t = 0; t < 3; ++t) D.bias[t] = -8 * (int)red4_sum((float)bsum[t]);
   return D;
 }
 
