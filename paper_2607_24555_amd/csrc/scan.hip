@@ -888,7 +888,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   __shared__ __align__(16) float sVsc[4][16][R];   // basis column scales x the query scale
   __shared__ __align__(16) float sCsc[4][16][16];  // coefficient row scales
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int h = blockIdx.y, s = blockIdx.z;
   const int n_c = seq_lens[s] / (kPage * V) * V;  // sub-pages of the complete pages
@@ -917,7 +917,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     };
     QDigits QD;  // formed once the first step's loads are in flight
     const int a_row = col >> 2, t_row = col & 3;  // A row of this lane: (page, token)
-    float* shat_base = s_hat + lay.base(s, h) + (long)col * lay.head;
+    // this lane's page score slot of page group grp / V; the wave-uniform page
+    // offset is added per quad
+    float* shat_lane = s_hat + lay.base(s, h) + (long)col * lay.head + (long)(grp / V) * lay.page;
     i4v pacc[2];  // stage-1 results of the current pair of basis sets
 
     // kN consecutive steps from page `start` whose first step's slices are
@@ -1061,9 +1063,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           // page's tokens sum to ~0 (the coefficient columns are orthogonal to
           // the all-ones vector), so the largest is >= ~0 and sum 2^z is safe
           // without a max; a max-shifted sum is taken only if it is not finite.
-          float sm = 0.0f;
+          float ez[16];
   #pragma unroll
-          for (int i = 0; i < 16; ++i) sm += __builtin_amdgcn_exp2f(z[i]);
+          for (int i = 0; i < 16; ++i) ez[i] = __builtin_amdgcn_exp2f(z[i]);
+  #pragma unroll
+          for (int w = 1; w < 16; w <<= 1)  // pairwise: four dependent adds, not fifteen
+  #pragma unroll
+            for (int i = 0; i < 16; i += 2 * w) ez[i] += ez[i + w];
+          float sm = ez[0];
           float shift = 0.0f;
           if (!(sm > 0.0f && sm < INFINITY)) {
             shift = z[0];
@@ -1077,7 +1084,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           const int sub = page0 + 4 * Q + grp;
           const bool live = sub < n_c && grp % V == 0;
           if (V > 1) s2 = merge_sub_lse<V>(s2);
-          if (live) shat_base[(long)(sub / V) * lay.page] = s2 * 0.69314718055994531f;
+          if (live) shat_lane[(long)((page0 + 4 * Q) / V) * lay.page] = s2 * 0.69314718055994531f;
           const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
           const bool up = s2 > run_m;
           const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
