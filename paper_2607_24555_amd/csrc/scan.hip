@@ -1216,7 +1216,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       QD = q_digits(q + (row0 + g) * kDim, grp);
       inv_m = diag ? QD.inv_scale : 0.0f;
     };
-    float* shat_base = s_hat + lay.base(s, h) + (long)g * lay.head;
+    // this lane's page score slot of page group ca / V; the wave-uniform page
+    // offset is added per quad
+    float* shat_lane = s_hat + lay.base(s, h) + (long)g * lay.head + (long)(ca / V) * lay.page;
 
     // record offsets of one step: ra[Q] page 4 Q + ca, rb[Q] page 4 Q + grp,
     // rm page 4 g + ca (the centroid row of this lane); when stage 1 is shared
@@ -1423,7 +1425,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           const int sub = page0 + 4 * Q + ca;
           const bool live = diag && sub < n_c && ca % V == 0;
           if (V > 1) s2 = merge_diag_lse<V>(s2);
-          if (live) shat_base[(long)(sub / V) * lay.page] = s2 * 0.69314718055994531f;
+          if (live) shat_lane[(long)((page0 + 4 * Q) / V) * lay.page] = s2 * 0.69314718055994531f;
           const float e = __builtin_amdgcn_exp2f(-fabsf(s2 - run_m));
           const bool up = s2 > run_m;
           const float ns = up ? fmaf(run_s, e, 1.0f) : run_s + e;
