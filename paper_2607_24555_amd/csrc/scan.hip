@@ -1152,12 +1152,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 //
 // Pages of 16 V tokens (V = 2, 4) run as V sub-pages of 16 tokens (coefficient
 // rows and row scales 16 u .. 16 u + 15 of sub-page u, the page's basis and
-// centroid).  At V = 4 a quad is one page, and stage 1 runs once per step for
-// the step's four pages: lane (grp, col) gets p(page grp, l, head g), and three
-// row swaps (16 and 32 lanes) broadcast page u's rows for quad u.  (At V = 2
-// stage 1 stays per quad: sharing it measured slower than the duplicated
-// work.)  The sub-page LSEs of a page sit in the diagonal lanes 20 a + g (a the
-// quad's sub-page) and are merged with lane exchanges at distance 20 and 40.
+// centroid).  Stage 1 then runs once per four pages: at V = 4 a quad is one
+// page, lane (grp, col) gets p(page grp of the step, l, head g), and three row
+// swaps (16 and 32 lanes) broadcast page u's rows for quad u; at V = 2 a pass
+// covers two quads, its rows ordered so that one 16-lane swap yields both quads'
+// layouts.  The sub-page LSEs of a page sit in the diagonal lanes 20 a + g (a
+// the quad's sub-page) and are merged with lane exchanges at distance 20 and 40.
 // ---------------------------------------------------------------------------
 
 // Block of (sub-)page min(page0 + (lane & 15), n_c - 1): always a valid page of
@@ -1222,8 +1222,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
     // record offsets of one step: ra[Q] page 4 Q + ca, rb[Q] page 4 Q + grp,
     // rm page 4 g + ca (the centroid row of this lane); when stage 1 is shared
-    // (V = 4), pa[0] and pb[0] are the records of pages ca and grp of the step
-    constexpr int kShare = V == 4 ? 4 : 1;  // quads per stage-1 pass
+    // (V > 1), pa[m] and pb[m] are the records of the pages of pass m in rows
+    // ca and grp: pages 4 m + x at V = 4, pages 4 m + ((x & 1) << 1 | x >> 1) at
+    // V = 2 (rows ordered 0, 2, 1, 3 so that one 16-lane swap splits the pass
+    // into its two quads)
+    constexpr int kShare = V;  // quads per stage-1 pass
     constexpr int kPasses = 4 / kShare;
     struct Offs {
       uint32_t ra[4], rb[4], rm;
@@ -1241,10 +1244,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
       o.rm = rec(4 * g + ca);
       if constexpr (kShare > 1) {
+        auto row_page = [](int x) { return V == 2 ? ((x & 1) << 1 | x >> 1) : x; };
 #pragma unroll
         for (int m = 0; m < kPasses; ++m) {
-          o.pa[m] = rec((4 * m + ca) * V);
-          o.pb[m] = rec((4 * m + grp) * V);
+          o.pa[m] = rec((4 * m + row_page(ca)) * V);
+          o.pb[m] = rec((4 * m + row_page(grp)) * V);
         }
       }
       return o;
@@ -1366,25 +1370,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             }
             if (pf) ld_vs(on, m);
             if constexpr (kShare > 1) {
-              // rows r0..r3 (lanes 16 u ..) hold pages 0..3; the 16-lane swap gives
-              // X = (r0, r0, r2, r2) and Y = (r1, r1, r3, r3), the 32-lane swaps of
-              // X and Y each row everywhere
+              // the 16-lane swap of rows r0..r3 (lanes 16 u ..) gives X = (r0, r0,
+              // r2, r2) and Y = (r1, r1, r3, r3).  V = 4: rows hold pages 0..3 and
+              // the 32-lane swaps of X and Y put each row everywhere.  V = 2: rows
+              // hold pages 4 m + 0, 2, 1, 3, so X is quad 2 m's layout (pages
+              // 4 m, 4 m, 4 m + 1, 4 m + 1) and Y quad 2 m + 1's.
 #pragma unroll
               for (int l = 0; l < 8; ++l) {
                 const uint32_t x = __float_as_uint(vals[l]);
                 const auto xy = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-                const auto xx = __builtin_amdgcn_permlane32_swap(xy[0], xy[0], false, false);
-                const auto yy = __builtin_amdgcn_permlane32_swap(xy[1], xy[1], false, false);
-                bq[0][l] = __uint_as_float(xx[0]);
-                bq[1][l] = __uint_as_float(yy[0]);
-                bq[2][l] = __uint_as_float(xx[1]);
-                bq[3][l] = __uint_as_float(yy[1]);
+                if constexpr (V == 4) {
+                  const auto xx = __builtin_amdgcn_permlane32_swap(xy[0], xy[0], false, false);
+                  const auto yy = __builtin_amdgcn_permlane32_swap(xy[1], xy[1], false, false);
+                  bq[0][l] = __uint_as_float(xx[0]);
+                  bq[1][l] = __uint_as_float(yy[0]);
+                  bq[2][l] = __uint_as_float(xx[1]);
+                  bq[3][l] = __uint_as_float(yy[1]);
+                } else {
+                  bq[0][l] = __uint_as_float(xy[0]);
+                  bq[1][l] = __uint_as_float(xy[1]);
+                }
               }
             }
           }
           if constexpr (kShare > 1) {
 #pragma unroll
-            for (int l = 0; l < 8; ++l) vals[l] = diag ? bq[Q][l] : 0.0f;
+            for (int l = 0; l < 8; ++l) vals[l] = diag ? bq[Q % kShare][l] : 0.0f;
           }
           const h8 A = byte8_to_h8(cf[Q].x, cf[Q].y);
           if (pf) ld_cf(on, Q);
