@@ -115,14 +115,14 @@ SCAN_SOURCES = ("paper_2607_24555_amd/csrc/scan.hip", "paper_2607_24555_amd/csrc
 SCAN_TRAFFIC = {
     # workload: (sha256 of SCAN_SOURCES, FETCH_SIZE KiB, WRITE_SIZE KiB,
     #            copy FETCH factor, copy WRITE factor, profile file)
-    "1m": ("429f9ecd359dba2c", 55275.6, 9033.4, 0.500015, 1.0, "profiles/scan_1m_hbm_counters.md"),
-    "128k": ("429f9ecd359dba2c", 215266.3, 8624.8, 0.500014, 1.0, "profiles/scan_128k_hbm_counters.md"),
-    "128k-r2": ("429f9ecd359dba2c", 86879.7, 8674.7, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
-    "reasoning": ("429f9ecd359dba2c", 194799.3, 21323.0, 0.500014, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
-    "1m-B32": ("429f9ecd359dba2c", 33143.0, 4516.4, 0.500014, 1.0, "profiles/scan_1m-B32_hbm_counters.md"),
-    "1m-B64": ("429f9ecd359dba2c", 21813.0, 2316.9, 0.500015, 1.0, "profiles/scan_1m-B64_hbm_counters.md"),
-    "128k-B32": ("429f9ecd359dba2c", 127554.0, 4371.5, 0.500013, 1.0, "profiles/scan_128k-B32_hbm_counters.md"),
-    "128k-B64": ("429f9ecd359dba2c", 84462.2, 2311.7, 0.500014, 1.0, "profiles/scan_128k-B64_hbm_counters.md"),
+    "1m": ("d72bd2acddea2be2", 55126.2, 8985.9, 0.500016, 1.0, "profiles/scan_1m_hbm_counters.md"),
+    "128k": ("d72bd2acddea2be2", 215269.2, 8618.9, 0.500016, 1.0, "profiles/scan_128k_hbm_counters.md"),
+    "128k-r2": ("d72bd2acddea2be2", 86863.3, 8675.1, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
+    "reasoning": ("d72bd2acddea2be2", 194797.6, 21323.1, 0.500014, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
+    "1m-B32": ("d72bd2acddea2be2", 33145.2, 4518.8, 0.500014, 1.0, "profiles/scan_1m-B32_hbm_counters.md"),
+    "1m-B64": ("d72bd2acddea2be2", 21813.7, 2318.0, 0.500013, 1.0, "profiles/scan_1m-B64_hbm_counters.md"),
+    "128k-B32": ("d72bd2acddea2be2", 127531.1, 4382.0, 0.500015, 1.0, "profiles/scan_128k-B32_hbm_counters.md"),
+    "128k-B64": ("d72bd2acddea2be2", 84462.2, 2312.3, 0.500015, 1.0, "profiles/scan_128k-B64_hbm_counters.md"),
 }
 
 
