@@ -1,8 +1,8 @@
 """locks_decode_step_static -- the fused step on the library's static device scratch,
 for callers that cannot allocate -- against locks_decode_step with a caller
 workspace on the same inputs: two calls in a row, the second on a smaller input,
-then a step with a build list, a HIP-graph capture of the static step, and the
-size limit."""
+32- and 64-token pages, a step with a build list, a HIP-graph capture of the static
+step, and the size limit."""
 import numpy as np
 import pytest
 import torch
@@ -67,6 +67,21 @@ def test_static_step_matches_workspace_step_twice_then_smaller():
     ref2, got2 = _both(d2, store2)
     _same(ref2, got2)
     print("[static] two calls in a row (second smaller) equal the workspace step bit for bit")
+
+
+@pytest.mark.parametrize("Bp,G", [(32, 16), (64, 4)])
+def test_static_step_large_pages(Bp, G):
+    """Pages of 32 and 64 tokens (their scans run as 16-token sub-pages): the static
+    step equals the workspace step bit for bit."""
+    print(f"[static] page {Bp}: S=2 G={G} Hkv=2 r=8 b=2048", flush=True)
+    spec = WorkloadSpec("static-large", 2, 2 * G, 2, [Bp * 900 + 5, Bp * 260], 8, 2048, "bf16",
+                        "bf16", page_size=Bp)
+    d = Dev(build_workload(spec, 35, device="cuda"))
+    store = B.alloc_summaries(d.cfg, d.device)
+    B.build_summaries(d.cfg, d.k, d.pt, d.sl, store)
+    ref, got = _both(d, store)
+    _same(ref, got)
+    print(f"[static] page {Bp}: equal to the workspace step")
 
 
 def test_static_step_with_build_list():
