@@ -32,6 +32,7 @@ struct PG {
   static constexpr int kCols = kDim / B;      // key columns per lane (centroid, basis)
   static constexpr int kPad = B + 4;          // LDS row stride (floats) of the Gram
   static constexpr int kVec = B + 1;          // LDS stride (floats) of a lane's vector
+  static constexpr int kKeyParts = B == 32 ? 2 : 1;  // column parts of the key rows in LDS
 };
 
 template <int C>
@@ -132,7 +133,7 @@ __device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
 template <typename KT>
 __device__ __forceinline__ float key_at(const KT* p, int c) { return load_elem(p, c); }
 
-template <typename KT, int B, bool kFactors>
+template <typename KT, int B, bool kFactors, int kMaxR>
 __global__ __launch_bounds__(64) void build_page_kernel(
     int S, int H_kv, int max_pages, int r, const KT* __restrict__ k_cache,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
@@ -144,13 +145,13 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   // phase-shared LDS: key rows (load, centroid, Gram), then the Gram rows and the
   // reflectors, then U, then the packed record; the inverse-iteration arrays
   // have their own
-  constexpr int kKBytes = kI * B * kDim * (int)sizeof(KT);
+  constexpr int kKBytes = kI * B * (kDim / P::kKeyParts) * (int)sizeof(KT);  // one part of the key rows
   constexpr int kABytes = kI * B * P::kPad * 4;
-  constexpr int kRecBytes = kI * rec_stride(kMaxRank, LOCKS_BASIS_BF16, B);
+  constexpr int kRecBytes = kI * rec_stride(kMaxR, LOCKS_BASIS_BF16, B);
   constexpr int kBig0 = kKBytes > kABytes ? kKBytes : kABytes;
   constexpr int kBig = kBig0 > kRecBytes ? kBig0 : kRecBytes;
   __shared__ __align__(16) uint8_t sBuf[kBig];
-  __shared__ float sInv[3 * kI * kMaxRank * P::kVec];  // [3][kI][kMaxRank][kVec]: M, W, X
+  __shared__ float sInv[3 * kI * kMaxR * P::kVec];  // [3][kI][kMaxR][kVec]: M, W, X
   __shared__ __align__(16) float sMu[kI][kDim];
   __shared__ __align__(16) float sD[kI][B];      // diagonal of T
   __shared__ __align__(16) float sE[kI][B];      // off-diagonal of T (e[k] couples k, k+1)
@@ -159,11 +160,11 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   __shared__ __align__(16) float sV[kI][B];      // reflector broadcast
   __shared__ __align__(16) float sW[kI][B];      // update-vector broadcast
   __shared__ float sLam[kI][B];                  // eigenvalues, descending
-  __shared__ float sFlip[kI][kMaxRank];
-  auto& sK = *reinterpret_cast<KT(*)[kI][B][kDim]>(sBuf);
+  __shared__ float sFlip[kI][kMaxR];
+  auto& sK = *reinterpret_cast<KT(*)[kI][B][kDim / P::kKeyParts]>(sBuf);
   auto& sA = *reinterpret_cast<float(*)[kI][B][P::kPad]>(sBuf);
   auto inv = [&](int which, int it, int l) -> float* {
-    return sInv + ((which * kI + it) * kMaxRank + l) * P::kVec;
+    return sInv + ((which * kI + it) * kMaxR + l) * P::kVec;
   };
 
   const int lane = threadIdx.x;
@@ -192,85 +193,97 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   const long blk = active ? (long)page_table[(long)s * max_pages + j] : 0;
   const KT* kpage = k_cache + (blk * H_kv + h) * (long)B * kDim;
 
-  // ---- key row i to LDS (16-byte loads); its squared norm
-  float energy = 0.0f;
-  {
-    constexpr int kV = 16 / sizeof(KT);
-    const uint4* src = reinterpret_cast<const uint4*>(kpage + (long)i * kDim);
-    uint4 w[kDim / kV];
-#pragma unroll
-    for (int u = 0; u < kDim / kV; ++u) w[u] = active ? src[u] : make_uint4(0, 0, 0, 0);
-    uint4* dst = reinterpret_cast<uint4*>(&sK[it][i][0]);
-#pragma unroll
-    for (int u = 0; u < kDim / kV; ++u) dst[u] = w[u];
-#pragma unroll
-    for (int u = 0; u < kDim / kV; ++u) {
-      float x[kV];
-      chunk_to_f<KT>(w[u], x);
-#pragma unroll
-      for (int e2 = 0; e2 < kV; ++e2) energy = fmaf(x[e2], x[e2], energy);
-    }
-    __syncthreads();
-  }
-  energy = group_sum<B>(energy) * (1.0f / B);
-
-  // ---- centroid of the lane's kCols columns: pairwise sum over the B rows
-  //      (exact when the rows are equal)
-  {
-    constexpr int kC = P::kCols;
-    float v[B][kC];
-#pragma unroll
-    for (int t = 0; t < B; ++t)
-#pragma unroll
-      for (int cc = 0; cc < kC; ++cc) v[t][cc] = key_at(&sK[it][t][0], kC * i + cc);
-#pragma unroll
-    for (int w = B / 2; w > 0; w >>= 1)
-#pragma unroll
-      for (int t = 0; t < w; ++t)
-#pragma unroll
-        for (int cc = 0; cc < kC; ++cc) v[t][cc] = v[t][cc] + v[t + w][cc];
-#pragma unroll
-    for (int cc = 0; cc < kC; ++cc) sMu[it][kC * i + cc] = v[0][cc] * (1.0f / B);
-  }
-  __syncthreads();
-
-  // ---- Gram of the deviations on fp32 MFMA 16x16x4, one 16 x 16 tile at a time:
-  //      lane l supplies row 16 T + l % 16 (A) and 16 U + l % 16 (B) at columns
-  //      32 (l / 16) + m, m = 0..31; register jj then holds G[16 T + 4 (l/16) + jj]
-  //      [16 U + l % 16].  Upper tiles only; the lower triangle is mirrored.
+  // ---- key rows, centroid and Gram in kParts column parts: the LDS holds one
+  //      part of the item's key rows at a time (the squared norm of row i
+  //      accumulates from the registers).  32-token pages take two parts, so the
+  //      key rows need no more LDS than the Gram rows; at 64 tokens the Gram rows
+  //      need more than all the key rows, and one part keeps the registers down.
+  constexpr int kParts = P::kKeyParts;
+  constexpr int kHalf = kDim / kParts;
+  constexpr int kV = 16 / sizeof(KT);
   constexpr int kT = B / 16;
   constexpr int kTiles = kT * (kT + 1) / 2;
+  float energy = 0.0f;
   f4 acc[kI][kTiles];
-  {
-    const int l16 = lane & 15, q4 = lane >> 4;
 #pragma unroll
-    for (int t = 0; t < kI; ++t) {
-      int tile = 0;
+  for (int t = 0; t < kI; ++t)
 #pragma unroll
-      for (int T = 0; T < kT; ++T)
+    for (int tile = 0; tile < kTiles; ++tile) acc[t][tile] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int U = T; U < kT; ++U) {
-          f4 a = f4{0.0f, 0.0f, 0.0f, 0.0f};
-          constexpr int kV = 16 / sizeof(KT);
+  for (int hf = 0; hf < kParts; ++hf) {
+    {
+      const uint4* src = reinterpret_cast<const uint4*>(kpage + (long)i * kDim + hf * kHalf);
+      uint4 w[kHalf / kV];
 #pragma unroll
-          for (int ch = 0; ch < 32 / kV; ++ch) {
-            const int c0 = 32 * q4 + kV * ch;
-            const uint4 wx = *reinterpret_cast<const uint4*>(&sK[t][16 * T + l16][c0]);
-            const uint4 wy = *reinterpret_cast<const uint4*>(&sK[t][16 * U + l16][c0]);
-            float xs[kV], ys[kV];
-            chunk_to_f<KT>(wx, xs);
-            chunk_to_f<KT>(wy, ys);
+      for (int u = 0; u < kHalf / kV; ++u) w[u] = active ? src[u] : make_uint4(0, 0, 0, 0);
+      uint4* dst = reinterpret_cast<uint4*>(&sK[it][i][0]);
 #pragma unroll
-            for (int e2 = 0; e2 < kV; ++e2) {
-              const float m2 = sMu[t][c0 + e2];
-              a = __builtin_amdgcn_mfma_f32_16x16x4f32(xs[e2] - m2, ys[e2] - m2, a, 0, 0, 0);
-            }
-          }
-          acc[t][tile++] = a;
-        }
+      for (int u = 0; u < kHalf / kV; ++u) dst[u] = w[u];
+#pragma unroll
+      for (int u = 0; u < kHalf / kV; ++u) {
+        float x[kV];
+        chunk_to_f<KT>(w[u], x);
+#pragma unroll
+        for (int e2 = 0; e2 < kV; ++e2) energy = fmaf(x[e2], x[e2], energy);
+      }
+      __syncthreads();
     }
+    // centroid of the lane's kHC columns of the part: pairwise sum over the B rows
+    // (exact when the rows are equal)
+    {
+      constexpr int kHC = kHalf / B;
+      float v[B][kHC];
+#pragma unroll
+      for (int t = 0; t < B; ++t)
+#pragma unroll
+        for (int cc = 0; cc < kHC; ++cc) v[t][cc] = key_at(&sK[it][t][0], kHC * i + cc);
+#pragma unroll
+      for (int w = B / 2; w > 0; w >>= 1)
+#pragma unroll
+        for (int t = 0; t < w; ++t)
+#pragma unroll
+          for (int cc = 0; cc < kHC; ++cc) v[t][cc] = v[t][cc] + v[t + w][cc];
+#pragma unroll
+      for (int cc = 0; cc < kHC; ++cc) sMu[it][hf * kHalf + kHC * i + cc] = v[0][cc] * (1.0f / B);
+    }
+    __syncthreads();
+    // Gram of the deviations on fp32 MFMA 16x16x4, one 16 x 16 tile at a time:
+    // lane l supplies row 16 T + l % 16 (A) and 16 U + l % 16 (B) at columns
+    // kGC (l / 16) + m, m < kGC, of the part; register jj then holds
+    // G[16 T + 4 (l/16) + jj][16 U + l % 16].  Upper tiles only; the lower
+    // triangle is mirrored.
+    constexpr int kGC = kHalf / 4;
+    {
+      const int l16 = lane & 15, q4 = lane >> 4;
+#pragma unroll
+      for (int t = 0; t < kI; ++t) {
+        int tile = 0;
+#pragma unroll
+        for (int T = 0; T < kT; ++T)
+#pragma unroll
+          for (int U = T; U < kT; ++U) {
+            f4 a = acc[t][tile];
+#pragma unroll
+            for (int ch = 0; ch < kGC / kV; ++ch) {
+              const int c0 = kGC * q4 + kV * ch;
+              const uint4 wx = *reinterpret_cast<const uint4*>(&sK[t][16 * T + l16][c0]);
+              const uint4 wy = *reinterpret_cast<const uint4*>(&sK[t][16 * U + l16][c0]);
+              float xs[kV], ys[kV];
+              chunk_to_f<KT>(wx, xs);
+              chunk_to_f<KT>(wy, ys);
+#pragma unroll
+              for (int e2 = 0; e2 < kV; ++e2) {
+                const float m2 = sMu[t][hf * kHalf + c0 + e2];
+                a = __builtin_amdgcn_mfma_f32_16x16x4f32(xs[e2] - m2, ys[e2] - m2, a, 0, 0, 0);
+              }
+            }
+            acc[t][tile++] = a;
+          }
+      }
+    }
+    __syncthreads();  // the next part (or the Gram rows) takes the key rows' LDS
   }
-  __syncthreads();  // key rows are no longer read: the Gram takes their LDS
+  energy = group_sum<B>(energy) * (1.0f / B);
   {
     const int l16 = lane & 15, q4 = lane >> 4;
 #pragma unroll
@@ -479,11 +492,11 @@ __global__ __launch_bounds__(64) void build_page_kernel(
     __syncthreads();
     // modified Gram-Schmidt over the vectors in eigenvalue order; lane i holds
     // component i
-    float xr[kMaxRank];
+    float xr[kMaxR];
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l) xr[l] = l < r ? inv(2, it, l)[i] : 0.0f;
+    for (int l = 0; l < kMaxR; ++l) xr[l] = l < r ? inv(2, it, l)[i] : 0.0f;
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l) {
+    for (int l = 0; l < kMaxR; ++l) {
       if (l < r) {
 #pragma unroll
         for (int m = 0; m < l; ++m) {
@@ -495,21 +508,21 @@ __global__ __launch_bounds__(64) void build_page_kernel(
       }
     }
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l)
+    for (int l = 0; l < kMaxR; ++l)
       if (l < r) inv(2, it, l)[i] = xr[l];
     __syncthreads();
   }
 
   // ---- back-transformation: u_l = H_0 H_1 ... H_{B-3} x_l, lane i component i
-  float u[kMaxRank];
+  float u[kMaxR];
 #pragma unroll
-  for (int l = 0; l < kMaxRank; ++l) u[l] = l < r ? inv(2, it, l)[i] : 0.0f;
+  for (int l = 0; l < kMaxR; ++l) u[l] = l < r ? inv(2, it, l)[i] : 0.0f;
   // (column k of row i holds v_k[i] for i > k + 1)
   for (int k = B - 3; k >= 0; --k) {
     const float vi = i == k + 1 ? 1.0f : (i > k + 1 ? arow[k] : 0.0f);
     const float tau = sTau[it][k];
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l) {
+    for (int l = 0; l < kMaxR; ++l) {
       if (l < r) {
         const float d = group_sum<B>(vi * u[l]);
         u[l] = fmaf(-tau * d, vi, u[l]);
@@ -517,10 +530,10 @@ __global__ __launch_bounds__(64) void build_page_kernel(
     }
   }
   __syncthreads();  // the reflectors are no longer read: U takes their LDS
-  float* sU = reinterpret_cast<float*>(sBuf);  // [kI][B][kMaxRank + 1]
-  auto U_at = [&](int t, int row, int l) -> float& { return sU[(t * B + row) * (kMaxRank + 1) + l]; };
+  float* sU = reinterpret_cast<float*>(sBuf);  // [kI][B][kMaxR + 1]
+  auto U_at = [&](int t, int row, int l) -> float& { return sU[(t * B + row) * (kMaxR + 1) + l]; };
 #pragma unroll
-  for (int l = 0; l < kMaxRank; ++l)
+  for (int l = 0; l < kMaxR; ++l)
     if (l < r) U_at(it, i, l) = u[l];
   __syncthreads();
 
@@ -549,9 +562,9 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   float mu_c[kC];
 #pragma unroll
   for (int cc = 0; cc < kC; ++cc) mu_c[cc] = sMu[it][kC * i + cc];
-  float vcol[kMaxRank][kC];
+  float vcol[kMaxR][kC];
 #pragma unroll
-  for (int l = 0; l < kMaxRank; ++l)
+  for (int l = 0; l < kMaxR; ++l)
 #pragma unroll
     for (int cc = 0; cc < kC; ++cc) vcol[l][cc] = 0.0f;
 #pragma unroll
@@ -567,7 +580,7 @@ __global__ __launch_bounds__(64) void build_page_kernel(
       kv[cc] = x - mu_c[cc];
     }
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l) {
+    for (int l = 0; l < kMaxR; ++l) {
       if (l < r) {
         const float ul = U_at(it, t, l);
 #pragma unroll
@@ -578,9 +591,9 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   // sign convention: the largest |V[c][l]| (lowest c on ties) is made positive:
   // the largest magnitude over the item, then the lowest column holding it, its
   // sign in the low bit
-  float best_abs[kMaxRank];
+  float best_abs[kMaxR];
 #pragma unroll
-  for (int l = 0; l < kMaxRank; ++l) {
+  for (int l = 0; l < kMaxR; ++l) {
     best_abs[l] = 0.0f;
     if (l >= r) continue;
     const bool kl = kept(l);
@@ -604,9 +617,9 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   }
   __syncthreads();
   // coefficient row i: C[i][l] = flip_l u_l[i] sigma_l (0 for a dropped mode)
-  float crow[kMaxRank];
+  float crow[kMaxR];
 #pragma unroll
-  for (int l = 0; l < kMaxRank; ++l)
+  for (int l = 0; l < kMaxR; ++l)
     crow[l] = (l < r && kept(l)) ? sFlip[it][l] * u[l] * sqrtf(sLam[it][l]) : 0.0f;
 
   if (kFactors) {
@@ -615,14 +628,14 @@ __global__ __launch_bounds__(64) void build_page_kernel(
 #pragma unroll
     for (int cc = 0; cc < kC; ++cc) mu_out[out_item * kDim + kC * i + cc] = sMu[it][kC * i + cc];
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l) {
+    for (int l = 0; l < kMaxR; ++l) {
       if (l >= r) continue;
 #pragma unroll
       for (int cc = 0; cc < kC; ++cc)
         basis_out[(out_item * kDim + kC * i + cc) * r + l] = vcol[l][cc];
     }
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l)
+    for (int l = 0; l < kMaxR; ++l)
       if (l < r) coef_out[(out_item * B + i) * r + l] = crow[l];
     sigma2_out[out_item * B + i] = fmaxf(sLam[it][i], 0.0f);
     return;
@@ -633,7 +646,7 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   uint8_t* sRec = sBuf + it * stride;
   const int scale_off = rec_scale_off(r, basis, B);
 #pragma unroll
-  for (int l = 0; l < kMaxRank; ++l) {
+  for (int l = 0; l < kMaxR; ++l) {
     if (l >= r) continue;
     if (basis == LOCKS_BASIS_INT4) {
       const float vs = f16_scale(best_abs[l], 7.0f);
@@ -661,11 +674,11 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   {
     float cabs = 0.0f;
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l) cabs = fmaxf(cabs, fabsf(crow[l]));
+    for (int l = 0; l < kMaxR; ++l) cabs = fmaxf(cabs, fabsf(crow[l]));
     const float cs = f16_scale(cabs, 127.0f);
     const int coef_off = rec_coef_off(r, basis);
 #pragma unroll
-    for (int l = 0; l < kMaxRank; ++l)
+    for (int l = 0; l < kMaxR; ++l)
       if (l < r) sRec[coef_off + i * r + l] = (uint8_t)(quant(crow[l], cs, 127) + 128);
     *reinterpret_cast<uint16_t*>(sRec + scale_off + 2 * (r + i)) = f16_bits(cs);
   }
@@ -703,11 +716,15 @@ hipError_t launch_build_page(const locks_cfg_t& c, const void* k_cache, const in
   const long blocks = (items + per - 1) / per;
   if (blocks > 0x7fffffffL) return hipErrorInvalidConfiguration;
   const dim3 grid((unsigned)blocks), block(64);
-#define LOCKS_BUILD_PAGE(KT, BP, F)                                                            \
-  hipLaunchKernelGGL((build_page_kernel<KT, BP, F>), grid, block, 0, st, c.num_seqs,            \
+  // ranks up to 8 take the instance whose rank-sized arrays (LDS and registers)
+  // hold 8 vectors: its smaller LDS fits more waves per compute unit
+#define LOCKS_BUILD_PAGE_R(KT, BP, F, MR)                                                      \
+  hipLaunchKernelGGL((build_page_kernel<KT, BP, F, MR>), grid, block, 0, st, c.num_seqs,        \
                      c.num_kv_heads, c.max_pages_per_seq, c.rank, static_cast<const KT*>(k_cache), \
                      page_table, seq_lens, build_list, n_items, (int)all_pages,                \
                      (uint8_t*)summaries, mu, basis, coef, sigma2, c.basis)
+#define LOCKS_BUILD_PAGE(KT, BP, F)                                                            \
+  if (c.rank <= 8) LOCKS_BUILD_PAGE_R(KT, BP, F, 8); else LOCKS_BUILD_PAGE_R(KT, BP, F, kMaxRank)
 #define LOCKS_BUILD_PAGE_B(KT)                                                                 \
   switch (c.page_size) {                                                                       \
     case 32: if (factors) LOCKS_BUILD_PAGE(KT, 32, true); else LOCKS_BUILD_PAGE(KT, 32, false); break; \
@@ -721,6 +738,7 @@ hipError_t launch_build_page(const locks_cfg_t& c, const void* k_cache, const in
   }
 #undef LOCKS_BUILD_PAGE_B
 #undef LOCKS_BUILD_PAGE
+#undef LOCKS_BUILD_PAGE_R
   return hipGetLastError();
 }
 
