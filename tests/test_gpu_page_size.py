@@ -128,6 +128,8 @@ STEP = {
     "B32-G16-r8-fp32q": (32, 3, 16, 1, [32 * 900 + 31, 32 * 5, 32 * 260 + 1], 8, 1024, "bf16",
                          "fp32"),
     "B64-G4-r8-fp32q": (64, 3, 4, 2, [64 * 400 + 5, 64 * 61, 40], 8, 1024, "bf16", "fp32"),
+    "B64-G16-r8-fp32q": (64, 2, 16, 2, [64 * 500 + 17, 64 * 90], 8, 2048, "bf16", "fp32"),
+    "B32-G4-r8-fp32q": (32, 3, 4, 2, [32 * 640 + 9, 32 * 33, 31], 8, 1024, "bf16", "fp32"),
 }
 
 
