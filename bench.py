@@ -117,7 +117,7 @@ SCAN_TRAFFIC = {
     #            copy FETCH factor, copy WRITE factor, profile file)
     "1m": ("d72bd2acddea2be2", 55126.2, 8985.9, 0.500016, 1.0, "profiles/scan_1m_hbm_counters.md"),
     "128k": ("d72bd2acddea2be2", 215269.2, 8618.9, 0.500016, 1.0, "profiles/scan_128k_hbm_counters.md"),
-    "128k-r2": ("d72bd2acddea2be2", 86863.3, 8675.1, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
+    "128k-r2": ("d72bd2acddea2be2", 86822.1, 8668.3, 0.500014, 1.0, "profiles/scan_128k-r2_hbm_counters.md"),
     "reasoning": ("d72bd2acddea2be2", 194797.6, 21323.1, 0.500014, 1.0, "profiles/scan_reasoning_hbm_counters.md"),
     "1m-B32": ("d72bd2acddea2be2", 33145.2, 4518.8, 0.500014, 1.0, "profiles/scan_1m-B32_hbm_counters.md"),
     "1m-B64": ("d72bd2acddea2be2", 21813.7, 2318.0, 0.500013, 1.0, "profiles/scan_1m-B64_hbm_counters.md"),
