@@ -134,7 +134,7 @@ template <typename KT>
 __device__ __forceinline__ float key_at(const KT* p, int c) { return load_elem(p, c); }
 
 template <typename KT, int B, bool kFactors, int kMaxR>
-__global__ __launch_bounds__(64) void build_page_kernel(
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void build_page_kernel(
     int S, int H_kv, int max_pages, int r, const KT* __restrict__ k_cache,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ build_list, int n_items, int all_pages,
@@ -312,7 +312,8 @@ __global__ __launch_bounds__(64) void build_page_kernel(
   //      = 1) and updates the trailing block by the rank-2 form A - v w^T - w v^T;
   //      v is then kept in column k of the rows below k + 1 for the
   //      back-transformation.  Entries of v, p and w at indices <= k are zero, so
-  //      every lane runs the same full-row loops.
+  //      every lane runs the same row loops over the 4-column groups from the one
+  //      holding column k + 1 on (the skipped products are exact zeros).
   float* arow = &sA[it][i][0];
   for (int k = 0; k < B - 2; ++k) {
     const float x = arow[k];
@@ -334,9 +335,10 @@ __global__ __launch_bounds__(64) void build_page_kernel(
     sV[it][i] = vi;
     __builtin_amdgcn_wave_barrier();
     // p = tau A v over the trailing block
+    const int q0 = (k + 1) >> 2;
     float p = 0.0f;
-#pragma unroll
-    for (int q = 0; q < B / 4; ++q) {
+#pragma unroll 4
+    for (int q = q0; q < B / 4; ++q) {
       const float4 r4 = *reinterpret_cast<const float4*>(arow + 4 * q);
       const float4 v4 = *reinterpret_cast<const float4*>(&sV[it][4 * q]);
       p = fmaf(r4.x, v4.x, p);
@@ -349,15 +351,15 @@ __global__ __launch_bounds__(64) void build_page_kernel(
     const float wi = p - kc * vi;
     sW[it][i] = wi;
     __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int q = 0; q < B / 4; ++q) {
+#pragma unroll 4
+    for (int q = q0; q < B / 4; ++q) {
       float4 r4 = *reinterpret_cast<const float4*>(arow + 4 * q);
       const float4 v4 = *reinterpret_cast<const float4*>(&sV[it][4 * q]);
       const float4 w4 = *reinterpret_cast<const float4*>(&sW[it][4 * q]);
-      r4.x -= fmaf(vi, w4.x, wi * v4.x);
-      r4.y -= fmaf(vi, w4.y, wi * v4.y);
-      r4.z -= fmaf(vi, w4.z, wi * v4.z);
-      r4.w -= fmaf(vi, w4.w, wi * v4.w);
+      r4.x = fmaf(-vi, w4.x, fmaf(-wi, v4.x, r4.x));
+      r4.y = fmaf(-vi, w4.y, fmaf(-wi, v4.y, r4.y));
+      r4.z = fmaf(-vi, w4.z, fmaf(-wi, v4.z, r4.z));
+      r4.w = fmaf(-vi, w4.w, fmaf(-wi, v4.w, r4.w));
       *reinterpret_cast<float4*>(arow + 4 * q) = r4;
     }
     __builtin_amdgcn_wave_barrier();
