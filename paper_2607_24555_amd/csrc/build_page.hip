@@ -493,21 +493,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void bu
     }
     __syncthreads();
     // modified Gram-Schmidt over the vectors in eigenvalue order; lane i holds
-    // component i
+    // component i.  Vectors past r are zero and stay zero, so every loop runs at
+    // the full width without a branch and the lane reductions can overlap.
     float xr[kMaxR];
 #pragma unroll
     for (int l = 0; l < kMaxR; ++l) xr[l] = l < r ? inv(2, it, l)[i] : 0.0f;
 #pragma unroll
     for (int l = 0; l < kMaxR; ++l) {
-      if (l < r) {
 #pragma unroll
-        for (int m = 0; m < l; ++m) {
-          const float d = group_sum<B>(xr[l] * xr[m]);
-          xr[l] = fmaf(-d, xr[m], xr[l]);
-        }
-        const float nn = group_sum<B>(xr[l] * xr[l]);
-        xr[l] = nn > 0.0f ? xr[l] * __builtin_amdgcn_rsqf(nn) : 0.0f;
+      for (int m = 0; m < l; ++m) {
+        const float d = group_sum<B>(xr[l] * xr[m]);
+        xr[l] = fmaf(-d, xr[m], xr[l]);
       }
+      const float nn = group_sum<B>(xr[l] * xr[l]);
+      xr[l] = nn > 0.0f ? xr[l] * __builtin_amdgcn_rsqf(nn) : 0.0f;
     }
 #pragma unroll
     for (int l = 0; l < kMaxR; ++l)
@@ -520,16 +519,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void bu
 #pragma unroll
   for (int l = 0; l < kMaxR; ++l) u[l] = l < r ? inv(2, it, l)[i] : 0.0f;
   // (column k of row i holds v_k[i] for i > k + 1)
+  // (vectors past r are zero and stay zero: no branch, the kMaxR reductions overlap)
   for (int k = B - 3; k >= 0; --k) {
     const float vi = i == k + 1 ? 1.0f : (i > k + 1 ? arow[k] : 0.0f);
     const float tau = sTau[it][k];
+    float dd[kMaxR];
 #pragma unroll
-    for (int l = 0; l < kMaxR; ++l) {
-      if (l < r) {
-        const float d = group_sum<B>(vi * u[l]);
-        u[l] = fmaf(-tau * d, vi, u[l]);
-      }
-    }
+    for (int l = 0; l < kMaxR; ++l) dd[l] = group_sum<B>(vi * u[l]);
+#pragma unroll
+    for (int l = 0; l < kMaxR; ++l) u[l] = fmaf(-tau * dd[l], vi, u[l]);
   }
   __syncthreads();  // the reflectors are no longer read: U takes their LDS
   float* sU = reinterpret_cast<float*>(sBuf);  // [kI][B][kMaxR + 1]
